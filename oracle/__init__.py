@@ -1,0 +1,184 @@
+"""CPU oracle for the MoE decode step under an expert budget -- TEST INFRASTRUCTURE.
+
+Only the tests, ``__graft_entry__.smoke()`` and the benchmark's CPU-baseline
+leg may import this package.  The arithmetic lives in ``moe_oracle.c`` (plain
+C, fp64); this module builds it with gcc and marshals numpy arrays into it.
+It shares no code with the HIP library.
+"""
+from __future__ import annotations
+
+import ctypes as C
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "moe_oracle.c")
+_LIB = os.path.join(_HERE, "libmoe_oracle.so")
+
+F32, BF16, INT4G128 = 0, 1, 2
+OK, ERR_ARG, ERR_RANGE, ERR_NONFINITE, ERR_BUDGET = 0, -1, -2, -3, -4
+HIT, MISS, PREFETCH = 0, 1, 2
+
+EVENT_DTYPE = np.dtype([("t", "<i4"), ("layer", "<i4"), ("expert", "<i4"),
+                        ("kind", "<i4"), ("slot", "<i4"), ("victim_key", "<i4")])
+
+
+def build() -> str:
+    """Compile ``libmoe_oracle.so`` (gcc -O2, OpenMP over output rows)."""
+    tmp = _LIB + ".tmp"
+    subprocess.run(["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
+                    "-o", tmp, _SRC, "-lm"], check=True)
+    os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib() -> C.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+            build()
+        _lib = C.CDLL(_LIB)
+        P, I32, SZ, D = C.c_void_p, C.c_int, C.c_size_t, C.POINTER(C.c_double)
+        _lib.oracle_router_logits.argtypes = [P, P, I32, I32, I32, I32, P]
+        _lib.oracle_topk_softmax.argtypes = [P, I32, I32, I32, P, P]
+        _lib.oracle_expert_forward.argtypes = [P, I32, I32, P, I32, P]
+        _lib.oracle_moe_ffn.argtypes = [P, I32, I32, I32, I32, I32, P, P, P, SZ, I32, P, P]
+        _lib.oracle_expert_bytes.argtypes = [I32, I32, I32]
+        _lib.oracle_expert_bytes.restype = SZ
+        _lib.oracle_expert_weight.argtypes = [P, I32, I32, I32, I32, I32, I32]
+        _lib.oracle_expert_weight.restype = C.c_double
+        _lib.oracle_lru_new.argtypes = [I32, I32, I32, I32]
+        _lib.oracle_lru_new.restype = P
+        _lib.oracle_lru_free.argtypes = [P]
+        _lib.oracle_lru_lookup.argtypes = [P, I32, I32, P, I32, I32]
+        _lib.oracle_lru_n_events.argtypes = [P]
+        _lib.oracle_lru_n_events.restype = SZ
+        _lib.oracle_lru_events.argtypes = [P, SZ, P, SZ]
+        _lib.oracle_lru_events.restype = SZ
+        _lib.oracle_lru_stats.argtypes = [P, P]
+        _lib.oracle_lru_slot_of.argtypes = [P, I32, I32]
+        _lib.oracle_lru_occupancy.argtypes = [P]
+        del D
+    return _lib
+
+
+def _p(a: np.ndarray) -> int:
+    return a.ctypes.data
+
+
+def _c(a, dtype) -> np.ndarray:
+    return np.ascontiguousarray(a, dtype=dtype)
+
+
+def threads_used() -> int:
+    """OpenMP threads the oracle's parallel loops run on."""
+    n = os.environ.get("OMP_NUM_THREADS")
+    return int(n) if n else (len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count())
+
+
+def expert_bytes(H: int, I: int, dtype: int) -> int:
+    return int(lib().oracle_expert_bytes(H, I, dtype))
+
+
+def expert_weight(blob: np.ndarray, H: int, I: int, dtype: int, which: str, r: int, c: int) -> float:
+    """Dequantised weight (r, c) of matrix ``which`` ('gu' or 'd') of an expert blob."""
+    b = _c(blob, np.uint8)
+    return float(lib().oracle_expert_weight(_p(b), dtype, H, I, 0 if which == "gu" else 1, r, c))
+
+
+def router_logits(x: np.ndarray, w_router: np.ndarray, w_dtype: int) -> np.ndarray:
+    """fp64 logits ``[T x E]`` of fp32 ``x [T x H]`` against ``w_router [E x H]`` (f32 or bf16 bits)."""
+    x = _c(x, np.float32)
+    w = _c(w_router, np.float32 if w_dtype == F32 else np.uint16)
+    T, H = x.shape
+    E = w.shape[0]
+    z = np.empty((T, E), dtype=np.float64)
+    st = lib().oracle_router_logits(_p(x), _p(w), w_dtype, T, H, E, _p(z))
+    if st != OK:
+        raise ValueError(f"oracle_router_logits status {st}")
+    return z
+
+
+def topk_softmax(z: np.ndarray, k: int):
+    """Top-k ids (rank order) and fp64 softmax weights of fp32 logits ``z [T x E]``.
+
+    Returns (ids int32 [T x k], weights float64 [T x k], status)."""
+    z = _c(z, np.float32)
+    T, E = z.shape
+    ids = np.empty((T, k), dtype=np.int32)
+    w = np.empty((T, k), dtype=np.float64)
+    st = lib().oracle_topk_softmax(_p(z), T, E, k, _p(ids), _p(w))
+    return ids, w, st
+
+
+def expert_forward(x: np.ndarray, blob: np.ndarray, H: int, I: int, dtype: int) -> np.ndarray:
+    x = _c(x, np.float32).reshape(H)
+    b = _c(blob, np.uint8)
+    y = np.empty(H, dtype=np.float64)
+    st = lib().oracle_expert_forward(_p(x), H, I, _p(b), dtype, _p(y))
+    if st != OK:
+        raise ValueError(f"oracle_expert_forward status {st}")
+    return y
+
+
+def moe_ffn(x: np.ndarray, ids: np.ndarray, w: np.ndarray, experts: np.ndarray, H: int, I: int,
+            dtype: int, shared: np.ndarray | None = None) -> np.ndarray:
+    """fp64 ``y [T x H]`` = weighted sum of the selected experts (+ shared expert).
+
+    ``experts`` is ``[E x expert_bytes]`` uint8 (one blob per routed expert)."""
+    x = _c(x, np.float32)
+    T = x.shape[0]
+    ids = _c(ids, np.int32).reshape(T, -1)
+    k = ids.shape[1]
+    w = _c(w, np.float64).reshape(T, k)
+    ex = np.ascontiguousarray(experts, dtype=np.uint8)
+    E, stride = ex.shape
+    sh = None if shared is None else _c(shared, np.uint8)
+    y = np.empty((T, H), dtype=np.float64)
+    st = lib().oracle_moe_ffn(_p(x), T, H, I, E, k, _p(ids), _p(w), _p(ex), stride, dtype,
+                              None if sh is None else _p(sh), _p(y))
+    if st != OK:
+        raise ValueError(f"oracle_moe_ffn status {st}")
+    return y
+
+
+class LRU:
+    """LRU expert-slot table (the oracle's residency state machine)."""
+
+    def __init__(self, capacity: int, L: int, E: int, preload: bool = False):
+        self._h = lib().oracle_lru_new(capacity, L, E, int(preload))
+        if not self._h:
+            raise ValueError("oracle_lru_new: invalid arguments")
+        self.C, self.L, self.E = capacity, L, E
+
+    def __del__(self):
+        h, self._h = getattr(self, "_h", None), None
+        if h:
+            lib().oracle_lru_free(h)
+
+    def lookup(self, t: int, layer: int, ids, prefetch: bool = False) -> int:
+        a = _c(np.atleast_1d(ids), np.int32)
+        return lib().oracle_lru_lookup(self._h, t, layer, _p(a), a.size, int(prefetch))
+
+    def events(self, first: int = 0) -> np.ndarray:
+        n = int(lib().oracle_lru_n_events(self._h))
+        out = np.empty(max(0, n - first), dtype=EVENT_DTYPE)
+        if out.size:
+            lib().oracle_lru_events(self._h, first, _p(out), out.size)
+        return out
+
+    def stats(self) -> dict:
+        s = np.zeros(4, dtype=np.uint64)
+        lib().oracle_lru_stats(self._h, _p(s))
+        return dict(hits=int(s[0]), misses=int(s[1]), prefetches=int(s[2]), evictions=int(s[3]))
+
+    def slot_of(self, layer: int, expert: int) -> int:
+        return int(lib().oracle_lru_slot_of(self._h, layer, expert))
+
+    def occupancy(self) -> int:
+        return int(lib().oracle_lru_occupancy(self._h))

@@ -1,0 +1,431 @@
+"""Pins of the CPU oracle against facts that do not come from the oracle itself.
+
+Hand-derived golden cases (tests/golden/), brute force on small inputs,
+textbook special cases and invariants.  CPU only.
+"""
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+import scipy.special
+
+import oracle
+import synth
+from blobs import decode_blob, make_blob, swiglu_dense
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+def _golden_lines(name):
+    with open(os.path.join(GOLDEN, name)) as f:
+        return [ln.split() for ln in f if ln.strip() and not ln.startswith("#")]
+
+
+def _kv(lines):
+    return {ln[0]: ln[1:] for ln in lines}
+
+
+# ------------------------------------------------------------- routing ---
+def test_golden_topk_softmax():
+    g = _kv(_golden_lines("topk_softmax.txt"))
+    z = np.array([float(v) for v in g["logits"]], np.float32)[None]
+    ids, w, st = oracle.topk_softmax(z, int(g["k"][0]))
+    assert st == oracle.OK
+    assert ids[0].tolist() == [int(v) for v in g["ids"]]
+    np.testing.assert_allclose(w[0], [float(v) for v in g["weights"]], rtol=1e-15, atol=0)
+
+
+def _sorted_topk(z, k):
+    return sorted(range(z.size), key=lambda e: (-float(z[e]), e))[:k]
+
+
+@pytest.mark.parametrize("E,k", [(4, 1), (4, 2), (16, 2), (16, 16), (128, 8), (256, 8)])
+def test_topk_matches_full_sort_with_ties(E, k):
+    rng = np.random.default_rng(E * 100 + k)
+    # few distinct values -> many ties; include both signed zeros
+    vals = np.array([-2.0, -0.0, 0.0, 0.5, 1.0, 3.0], np.float32)
+    z = vals[rng.integers(0, vals.size, size=(40, E))]
+    ids, w, st = oracle.topk_softmax(z, k)
+    assert st == oracle.OK
+    for t in range(z.shape[0]):
+        assert ids[t].tolist() == _sorted_topk(z[t], k)
+
+
+def test_topk_k1_is_argmax_weight_one():
+    z = np.random.default_rng(1).standard_normal((64, 32)).astype(np.float32)
+    z[3, [4, 9]] = 10.0  # tie: np.argmax keeps the first
+    ids, w, _ = oracle.topk_softmax(z, 1)
+    assert ids[:, 0].tolist() == np.argmax(z, axis=1).tolist()
+    assert (w == 1.0).all()
+
+
+def test_topk_kE_is_plain_softmax():
+    z = np.random.default_rng(2).standard_normal((16, 12)).astype(np.float32) * 3
+    ids, w, _ = oracle.topk_softmax(z, 12)
+    for t in range(16):
+        ref = scipy.special.softmax(z[t].astype(np.float64))
+        np.testing.assert_allclose(w[t], ref[ids[t]], rtol=1e-13)
+
+
+def test_topk_invariants():
+    z = np.random.default_rng(3).standard_normal((200, 128)).astype(np.float32)
+    k = 8
+    ids, w, _ = oracle.topk_softmax(z, k)
+    assert ((ids >= 0) & (ids < 128)).all()
+    assert all(len(set(r)) == k for r in ids.tolist())
+    assert (np.diff(w, axis=1) <= 0).all()
+    assert np.abs(w.sum(axis=1) - 1.0).max() <= k * 2.0 ** -52
+    # the selected logits dominate the rest
+    for t in range(200):
+        rest = np.delete(z[t], ids[t])
+        assert z[t, ids[t]].min() >= rest.max()
+
+
+@pytest.mark.parametrize("bad", [np.nan, np.inf, -np.inf])
+def test_topk_nonfinite_is_error(bad):
+    z = np.zeros((3, 8), np.float32)
+    z[1, 5] = bad
+    ids, w, st = oracle.topk_softmax(z, 2)
+    assert st == oracle.ERR_NONFINITE
+    assert ids[1].tolist() == [-1, -1]
+    assert ids[0].tolist() == [0, 1] and ids[2].tolist() == [0, 1]
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16])
+def test_router_logits_exact_on_integers(dtype):
+    rng = np.random.default_rng(4)
+    E, H, T = 16, 256, 5
+    wi = rng.integers(-8, 9, size=(E, H))
+    xi = rng.integers(-8, 9, size=(T, H))
+    w = wi.astype(np.float32) if dtype == synth.F32 else synth.bf16_bits(wi.astype(np.float32))
+    z = oracle.router_logits(xi.astype(np.float32), w, dtype)
+    assert (z == (xi @ wi.T).astype(np.float64)).all()
+
+
+# ---------------------------------------------------------- expert FFN ---
+def test_golden_swiglu_expert():
+    lines = _golden_lines("swiglu_expert.txt")
+    H = int(next(l for l in lines if l[0] == "H")[1])
+    I = int(next(l for l in lines if l[0] == "I")[1])
+    gu = np.zeros((2 * I, H), np.float32)
+    d = np.zeros((H, I), np.float32)
+    x = np.zeros(H, np.float32)
+    y_ref = np.zeros(H)
+    for l in lines:
+        if l[0] == "weights":
+            (gu if l[1] == "gu" else d)[int(l[2]), int(l[3])] = float(l[4])
+        elif l[0] == "x":
+            x[int(l[1])] = float(l[2])
+        elif l[0] == "y":
+            y_ref[int(l[1])] = float(l[2])
+    for dtype in (synth.F32, synth.BF16):
+        y = oracle.expert_forward(x, make_blob(gu, d, dtype), H, I, dtype)
+        np.testing.assert_allclose(y, y_ref, rtol=1e-15, atol=0)
+
+
+def _random_experts(rng, E, H, I, dtype, scale=0.05):
+    blobs = [make_blob(rng.standard_normal((2 * I, H)) * scale, rng.standard_normal((H, I)) * scale, dtype)
+             for _ in range(E)]
+    return np.stack(blobs)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16, synth.INT4G128])
+@pytest.mark.parametrize("shared", [False, True])
+def test_ffn_matches_dense_all_experts_masked(dtype, shared):
+    """Dense evaluation of every expert, weights masked to the top-k."""
+    rng = np.random.default_rng(10 + dtype)
+    E, H, I, T, k = 6, 128, 256, 3, 2
+    ex = _random_experts(rng, E, H, I, dtype)
+    sh = _random_experts(rng, 1, H, I, dtype)[0] if shared else None
+    x = rng.standard_normal((T, H)).astype(np.float32)
+    z = rng.standard_normal((T, E)).astype(np.float32)
+    ids, w, _ = oracle.topk_softmax(z, k)
+    y = oracle.moe_ffn(x, ids, w, ex, H, I, dtype, sh)
+    dense = np.stack([swiglu_dense(x, *decode_blob(ex[e], H, I, dtype)) for e in range(E)], axis=1)
+    mask = np.zeros((T, E))
+    mask[np.arange(T)[:, None], ids] = w
+    ref = np.einsum("te,teh->th", mask, dense)
+    if shared:
+        ref += swiglu_dense(x, *decode_blob(sh, H, I, dtype))
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-14)
+
+
+def test_ffn_single_expert_is_plain_swiglu():
+    rng = np.random.default_rng(11)
+    H, I = 256, 128
+    gu = rng.standard_normal((2 * I, H)).astype(np.float32) * 0.05
+    d = rng.standard_normal((H, I)).astype(np.float32) * 0.05
+    x = rng.standard_normal((1, H)).astype(np.float32)
+    y = oracle.moe_ffn(x, np.array([[0]]), np.array([[1.0]]), make_blob(gu, d, synth.F32)[None], H, I, synth.F32)
+    g = x.astype(np.float64) @ gu[0::2].T.astype(np.float64)
+    u = x.astype(np.float64) @ gu[1::2].T.astype(np.float64)
+    ref = (g * scipy.special.expit(g) * u) @ d.T.astype(np.float64)
+    np.testing.assert_allclose(y, ref, rtol=1e-12, atol=1e-15)
+
+
+def test_ffn_zero_up_rows_give_zero():
+    rng = np.random.default_rng(12)
+    H, I = 128, 128
+    gu = rng.standard_normal((2 * I, H)).astype(np.float32)
+    gu[1::2] = 0.0
+    d = rng.standard_normal((H, I)).astype(np.float32)
+    y = oracle.expert_forward(rng.standard_normal(H).astype(np.float32), make_blob(gu, d, synth.BF16), H, I,
+                              synth.BF16)
+    assert (y == 0.0).all()
+
+
+def test_ffn_identical_experts_independent_of_routing():
+    rng = np.random.default_rng(13)
+    E, H, I, T, k = 8, 128, 128, 4, 3
+    one = _random_experts(rng, 1, H, I, synth.BF16)[0]
+    ex = np.stack([one] * E)
+    x = rng.standard_normal((T, H)).astype(np.float32)
+    ys = []
+    for s in range(3):
+        z = np.random.default_rng(100 + s).standard_normal((T, E)).astype(np.float32)
+        ids, w, _ = oracle.topk_softmax(z, k)
+        ys.append(oracle.moe_ffn(x, ids, w, ex, H, I, synth.BF16))
+    single = np.stack([oracle.expert_forward(x[t], one, H, I, synth.BF16) for t in range(T)])
+    for y in ys:
+        np.testing.assert_allclose(y, single, rtol=1e-12, atol=1e-15)
+
+
+def test_layer_permutation_equivariance():
+    """Relabelling experts (router rows and blobs together) leaves the layer output unchanged."""
+    rng = np.random.default_rng(14)
+    E, H, I, T, k = 8, 128, 128, 5, 3
+    ex = _random_experts(rng, E, H, I, synth.BF16)
+    wr = synth.bf16_bits(rng.standard_normal((E, H)).astype(np.float32) * 0.1)
+    x = rng.standard_normal((T, H)).astype(np.float32)
+    perm = rng.permutation(E)
+
+    def layer(wr_, ex_):
+        z = oracle.router_logits(x, wr_, synth.BF16).astype(np.float32)
+        ids, w, _ = oracle.topk_softmax(z, k)
+        return oracle.moe_ffn(x, ids, w, ex_, H, I, synth.BF16)
+
+    np.testing.assert_allclose(layer(wr, ex), layer(wr[perm], ex[perm]), rtol=1e-12, atol=1e-15)
+
+
+def test_ffn_rejects_out_of_range_ids():
+    ex = np.zeros((2, synth.expert_bytes(128, 128, synth.BF16)), np.uint8)
+    with pytest.raises(ValueError):
+        oracle.moe_ffn(np.zeros((1, 128), np.float32), np.array([[2]]), np.array([[1.0]]), ex, 128, 128, synth.BF16)
+
+
+# ---------------------------------------------------------------- int4 ---
+def test_int4_nibble_table_and_scales():
+    table = {int(a): int(b) for a, b in _golden_lines("int4_nibbles.txt")}
+    H = I = 128
+    blob = np.zeros(synth.expert_bytes(H, I, synth.INT4G128), np.uint8)
+    lay = synth.blob_layout(H, I, synth.INT4G128)
+    oq, _, _ = lay["gu_q"]
+    os_, _, _ = lay["gu_s"]
+    # row 3 of W_gu: element c holds nibble c % 16; group 0 scale 0.5, group 0 of row 4 scale -3
+    for c in range(H):
+        nib = c % 16
+        byte = oq + 3 * (H // 2) + c // 2
+        blob[byte] |= nib if c % 2 == 0 else nib << 4
+    blob[os_ + 2 * 3:os_ + 2 * 4] = synth.bf16_bits(np.array([0.5], np.float32)).view(np.uint8)
+    for c in range(H):
+        assert oracle.expert_weight(blob, H, I, synth.INT4G128, "gu", 3, c) == 0.5 * table[c % 16]
+    blob[oq + 4 * (H // 2)] = 0x9F  # low nibble 15 -> -1, high nibble 9 -> -7
+    blob[os_ + 2 * 4:os_ + 2 * 5] = synth.bf16_bits(np.array([-3.0], np.float32)).view(np.uint8)
+    assert oracle.expert_weight(blob, H, I, synth.INT4G128, "gu", 4, 0) == 3.0
+    assert oracle.expert_weight(blob, H, I, synth.INT4G128, "gu", 4, 1) == 21.0
+
+
+def test_int4_roundtrip_and_quantizer_bound():
+    rng = np.random.default_rng(15)
+    H, I = 256, 128
+    gu = rng.standard_normal((2 * I, H)).astype(np.float32) * 0.02
+    d = rng.standard_normal((H, I)).astype(np.float32) * 0.02
+    blob = make_blob(gu, d, synth.INT4G128)
+    dgu, dd = decode_blob(blob, H, I, synth.INT4G128)
+    for which, m, dm in (("gu", gu, dgu), ("d", d, dd)):
+        rows, cols = m.shape
+        for r, c in zip(rng.integers(0, rows, 200), rng.integers(0, cols, 200)):
+            assert oracle.expert_weight(blob, H, I, synth.INT4G128, which, int(r), int(c)) == dm[r, c]
+        # quantizer: every group's error is at most half a step (plus the bf16 scale rounding)
+        s = np.abs(m).reshape(rows, cols // 128, 128).max(axis=2) / 7.0
+        err = np.abs(m - dm).reshape(rows, cols // 128, 128).max(axis=2)
+        assert (err <= 0.5 * s * (1 + 2.0 ** -7) + 1e-3 * s).all()
+
+
+# ----------------------------------------------------------------- LRU ---
+def _events_tuples(ev):
+    return [tuple(int(v) for v in e) for e in ev]
+
+
+def test_golden_lru_textbook():
+    lines = _golden_lines("lru_textbook.txt")
+    kv = {l[0]: l[1:] for l in lines if not l[0].lstrip("-").isdigit()}
+    C, E = int(kv["capacity"][0]), int(kv["experts"][0])
+    ref = [int(v) for v in kv["reference"]]
+    c = oracle.LRU(C, 1, E)
+    for t, e in enumerate(ref):
+        assert c.lookup(t, 0, [e]) == oracle.OK
+    assert c.stats()["misses"] == int(kv["faults"][0])
+    expect = [tuple(int(v) for v in l) for l in lines if l[0].lstrip("-").isdigit()]
+    assert _events_tuples(c.events()) == expect
+
+
+def test_golden_lru_step_sets():
+    lines = _golden_lines("lru_step_sets.txt")
+    kv = {l[0]: l[1:] for l in lines if l[0] in ("capacity", "experts")}
+    c = oracle.LRU(int(kv["capacity"][0]), 1, int(kv["experts"][0]))
+    for l in lines:
+        if l[0] == "op":
+            arrow = l.index("->")
+            t, layer, ids = int(l[2]), int(l[3]), [int(v) for v in l[4:arrow]]
+            assert c.lookup(t, layer, ids, prefetch=(l[1] == "prefetch")) == int(l[arrow + 1])
+    expect = [tuple(int(v) for v in l[1:]) for l in lines if l[0] == "ev"]
+    assert _events_tuples(c.events()) == expect
+
+
+def _random_trace(rng, steps, L, E, n):
+    return [(int(rng.integers(0, L)), rng.integers(0, E, size=n)) for _ in range(steps)]
+
+
+def _step_stack_hits(trace, C):
+    """Brute force: hit iff (distinct keys used in later steps) + (keys of its
+    last step with a larger id) < C."""
+    hits = []
+    last_step = {}
+    step_sets = []
+    for s, (layer, ids) in enumerate(trace):
+        R = sorted(set(int(i) for i in ids))
+        out = []
+        for e in R:
+            key = (layer, e)
+            if key not in last_step:
+                out.append(False)
+                continue
+            s0 = last_step[key]
+            newer = set()
+            for s1 in range(s0 + 1, s):
+                newer |= step_sets[s1]
+            # keys of step s0 stamped after `key`: the same layer, a larger id
+            newer |= {kk for kk in step_sets[s0] if kk[1] > e}
+            out.append(len(newer) < C)
+        for e in R:
+            last_step[(layer, e)] = s
+        step_sets.append({(layer, e) for e in R})
+        hits.append(out)
+    return hits
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_lru_hits_match_step_stack_distance(seed):
+    rng = np.random.default_rng(200 + seed)
+    L, E, n = 2, 12, int(rng.integers(1, 5))
+    trace = _random_trace(rng, 120, L, E, n)
+    for C in range(n, 3 * E):
+        c = oracle.LRU(C, L, E)
+        got = []
+        for t, (layer, ids) in enumerate(trace):
+            first = len(c.events())
+            assert c.lookup(t, layer, ids) == oracle.OK
+            got.append([int(ev["kind"]) == oracle.HIT for ev in c.events(first)])
+        assert got == _step_stack_hits(trace, C), f"C={C}"
+
+
+def _recency_list_model(trace, C):
+    """Brute force with an explicit recency list (most recent last) and a slot array."""
+    recency, slots, events = [], [None] * C, []
+    for t, (layer, ids) in enumerate(trace):
+        R = sorted(set(int(i) for i in ids))
+        step_keys = {(layer, e) for e in R}
+        for e in R:
+            key = (layer, e)
+            if key in recency:
+                recency.remove(key)
+                recency.append(key)
+                events.append((t, layer, e, 0, slots.index(key), -1))
+                continue
+            if None in slots:
+                s, victim = slots.index(None), -1
+            else:
+                vk = next(kk for kk in recency if kk not in step_keys)
+                s, victim = slots.index(vk), vk[0] * 1000 + vk[1]
+                recency.remove(vk)
+            slots[s] = key
+            recency.append(key)
+            events.append((t, layer, e, 1, s, victim))
+    return events
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_lru_slots_and_victims_match_recency_list(seed):
+    rng = np.random.default_rng(300 + seed)
+    L, E = 3, 1000
+    trace = [(int(rng.integers(0, L)), rng.integers(0, 10, size=int(rng.integers(1, 4)))) for _ in range(300)]
+    for C in (3, 4, 7, 12):
+        c = oracle.LRU(C, L, E)
+        for t, (layer, ids) in enumerate(trace):
+            c.lookup(t, layer, ids)
+        assert _events_tuples(c.events()) == _recency_list_model(trace, C)
+
+
+def test_lru_cyclic_trace_misses_every_time():
+    C = 5
+    c = oracle.LRU(C, 1, C + 1)
+    for t in range(10 * (C + 1)):
+        c.lookup(t, 0, [t % (C + 1)])
+    assert c.stats() == dict(hits=0, misses=10 * (C + 1), prefetches=0, evictions=10 * (C + 1) - C)
+
+
+def test_lru_compulsory_misses_only_when_everything_fits():
+    rng = np.random.default_rng(16)
+    trace = _random_trace(rng, 500, 4, 16, 8)
+    distinct = {(l, int(e)) for l, ids in trace for e in ids}
+    c = oracle.LRU(len(distinct), 4, 16)
+    for t, (l, ids) in enumerate(trace):
+        c.lookup(t, l, ids)
+    st = c.stats()
+    assert st["misses"] == len(distinct) and st["evictions"] == 0
+
+
+def test_lru_inclusion_and_counts():
+    rng = np.random.default_rng(17)
+    L, E, n = 3, 32, 8
+    trace = _random_trace(rng, 400, L, E, n)
+    lookups = sum(len(set(ids.tolist())) for _, ids in trace)
+    prev_hits = None
+    prev_miss = None
+    for C in range(n, L * E + 1, 5):
+        c = oracle.LRU(C, L, E)
+        occ = []
+        for t, (l, ids) in enumerate(trace):
+            c.lookup(t, l, ids)
+            occ.append(c.occupancy())
+        st = c.stats()
+        assert st["hits"] + st["misses"] == lookups
+        assert max(occ) <= C
+        hits = {(int(e["t"]), int(e["expert"])) for e in c.events() if e["kind"] == oracle.HIT}
+        if prev_hits is not None:
+            assert prev_hits <= hits and st["misses"] <= prev_miss
+        prev_hits, prev_miss = hits, st["misses"]
+
+
+def test_lru_preload_all_resident():
+    L, E = 2, 5
+    c = oracle.LRU(L * E, L, E, preload=True)
+    assert [c.slot_of(l, e) for l in range(L) for e in range(E)] == list(range(L * E))
+    for t in range(20):
+        c.lookup(t, t % L, [(t * 3) % E, (t * 7 + 1) % E])
+    assert c.stats()["misses"] == 0
+
+
+def test_lru_errors():
+    c = oracle.LRU(2, 2, 4)
+    assert c.lookup(0, 0, [4]) == oracle.ERR_RANGE
+    assert c.lookup(0, 0, [-1]) == oracle.ERR_RANGE
+    assert c.lookup(0, 2, [0]) == oracle.ERR_ARG
+    assert c.lookup(0, 0, [0, 1, 2]) == oracle.ERR_BUDGET
+    assert c.lookup(0, 0, [1, 1, 0, 1]) == oracle.OK  # duplicates count once
+    assert c.occupancy() == 2 and len(c.events()) == 2
+    with pytest.raises(ValueError):
+        oracle.LRU(0, 1, 1)
