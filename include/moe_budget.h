@@ -1,0 +1,282 @@
+/*
+ * moe_budget.h -- C ABI of the MI355X (gfx950) library for one Mixture-of-Experts
+ * decode step under a fixed HBM budget for expert weights.
+ *
+ * The step (paper sec. 4, Fig. 1): the routing result (hidden state h and the
+ * routing vector r) picks a subset of experts (sec. 3); a lookup table maps
+ * each sub-module (expert) id to a slot of a fixed-size slot group on the
+ * accelerator; sub-modules missing from the slots are brought in from the
+ * host tier ("selective load") after making room ("evict"); execution stays
+ * within a memory budget (sec. 5, memory-constrained execution).  Residency
+ * follows least-recently-used replacement, the conventional policy sec. 4
+ * contrasts with its own rotation scheme (which the paper does not define).
+ *
+ * Conventions for every call:
+ *  - Return value: MOE_OK (0) or a negative MOE_ERR_* code; moe_last_error()
+ *    returns a thread-local message for the last failure of the calling
+ *    thread.  Nothing aborts or throws across this boundary.
+ *  - Pointers named "device" are HIP device memory of the current device, owned
+ *    by the caller; "host" pointers are host memory owned by the caller.  The
+ *    library owns only what it allocates itself (cache slot pools, its copy
+ *    stream and events, per-device error flags, stack workspaces).
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Device
+ *    work is enqueued asynchronously on it unless a call says otherwise.
+ *  - Errors found on the device (expert id out of range, non-finite logits,
+ *    expert not resident) are raised in per-device sticky flags; read and
+ *    clear them with moe_sync_check().
+ *
+ * Expert blob layout (one contiguous blob per expert; the residency unit):
+ *    W_gu [2I x H] row-major, rows interleaved: row 2i = gate row i,
+ *                  row 2i+1 = up row i;
+ *    W_d  [H x I]  row-major.
+ *  MOE_INT4G128 stores each matrix as packed nibbles [rows x K/2] (even
+ *  element in the low nibble, two's complement q in [-8, 7]) followed by its
+ *  bf16 scales [rows x K/128]; the weight is scale * q.  The blob is
+ *  [gu nibbles | gu scales | d nibbles | d scales].
+ *  Bytes per expert: 3*H*I*4 (f32), 3*H*I*2 (bf16), 3*H*I/2 + 3*H*I/64 (int4).
+ */
+#ifndef MOE_BUDGET_H
+#define MOE_BUDGET_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* Exported entry points (the library is built with hidden default visibility). */
+#define MOE_API __attribute__((visibility("default")))
+
+/* ---- status codes ---- */
+#define MOE_OK 0
+#define MOE_ERR_INVALID_ARG (-1)  /* bad size, null pointer, unsupported shape */
+#define MOE_ERR_RANGE (-2)        /* expert id outside [0, E) */
+#define MOE_ERR_NONFINITE (-3)    /* NaN or +-inf router logit */
+#define MOE_ERR_BUDGET (-4)       /* budget below one expert, or a step needs more experts than fit */
+#define MOE_ERR_NOT_PINNED (-5)   /* host store is not page-locked (hipHostMalloc) memory */
+#define MOE_ERR_HIP (-6)          /* a HIP runtime call failed */
+#define MOE_ERR_COPY (-7)         /* a host-to-device fill failed; the slot stays unmapped */
+#define MOE_ERR_NOT_RESIDENT (-8) /* the expert FFN found an expert with no slot */
+
+/* ---- weight storage types ---- */
+#define MOE_F32 0
+#define MOE_BF16 1
+#define MOE_INT4G128 2
+
+/* ---- moe_expert_ffn_grouped flags ---- */
+#define MOE_ACCUMULATE 1 /* y_out += MoE output (fused residual add) instead of y_out = output */
+
+/* ---- residency ---- */
+#define MOE_POLICY_LRU 0
+#define MOE_CACHE_PRELOAD 1  /* start with every expert resident at slot layer*E + expert */
+#define MOE_CACHE_HOST_SIM 2 /* no device: slots live in host memory and fills are memcpy */
+
+#define MOE_EVENT_HIT 0
+#define MOE_EVENT_MISS 1
+#define MOE_EVENT_PREFETCH 2
+
+/* Limits of the decode kernels. */
+#define MOE_MAX_EXPERTS 256   /* router top-k holds at most 4 logits per lane of a 64-wide wave */
+#define MOE_MAX_TOPK 16
+#define MOE_MAX_DECODE_TOKENS 16
+
+/* ======================================================================= */
+/* Library / device                                                        */
+/* ======================================================================= */
+
+/* Make `device` current for the calling thread and set up its error flags.
+ * Other calls set up the current device on first use; calling this first
+ * keeps that set-up out of timed regions. */
+MOE_API int moe_init(int device);
+
+/* Message of the calling thread's last failed call ("" if none). Owned by the
+ * library; valid until the thread's next failing call. */
+MOE_API const char *moe_last_error(void);
+
+/* Synchronise `stream`, then read and clear the current device's sticky error
+ * flags.  Returns MOE_ERR_RANGE, MOE_ERR_NONFINITE or MOE_ERR_NOT_RESIDENT
+ * (first set, in that order) or MOE_OK. */
+MOE_API int moe_sync_check(void *stream);
+
+/* ======================================================================= */
+/* Routing (paper sec. 3: tokens pass through a subset of experts; Fig. 1:   */
+/* the routing result (h, r) drives the slot lookup)                         */
+/* ======================================================================= */
+
+/* Router logits and softmax-renormalised top-k for T tokens.
+ *   x          device fp32 [T x H], or NULL to rank `logit_bias` alone
+ *   w_router   device [E x H] row-major, w_dtype MOE_F32 or MOE_BF16
+ *   logit_bias device fp32 [T x E] added to W_r x, or NULL
+ *   logits     device fp32 [T x E] out: z = W_r x (+ bias), fp32 accumulation
+ *   ids        device int32 [T x k] out: the k largest z of each token ranked by
+ *              (z descending, expert id ascending)
+ *   weights    device fp32 [T x k] out: exp(z_j - z_0) / sum_j' exp(z_j' - z_0)
+ * Limits: 1 <= k <= min(E, MOE_MAX_TOPK), E <= MOE_MAX_EXPERTS, H % 128 == 0.
+ * A token with a non-finite logit gets ids -1 and weights 0 and raises
+ * MOE_ERR_NONFINITE in the device flags.  T == 0 is a no-op. */
+MOE_API int moe_route_topk(const float *x, const void *w_router, int w_dtype, int T, int H, int E, int k,
+                   const float *logit_bias, float *logits, int32_t *ids, float *weights,
+                   void *stream);
+
+/* ======================================================================= */
+/* Expert FFN with weighted combine (north-star "fused SwiGLU expert FFN")   */
+/* ======================================================================= */
+
+/* Device workspace bytes moe_expert_ffn_grouped needs for T tokens. */
+MOE_API size_t moe_ffn_workspace_bytes(int T, int k, int I);
+
+/* y[t] = sum_j weights[t,j] * FFN_{ids[t,j]}(x[t]) + FFN_shared(x[t]), with
+ * FFN(x) = W_d (silu(W_g x) * (W_u x)), fp32 accumulation, for T <= 16 tokens.
+ *   x          device fp32 [T x H]
+ *   ids        device int32 [T x k] (as written by moe_route_topk)
+ *   weights    device fp32 [T x k]
+ *   slot_of    device int32 [E]: slot of each expert of this layer (-1 = absent),
+ *              or NULL for slot = expert id
+ *   pool       device base of the slots; slot s starts at pool + s * expert_bytes
+ *              (expert_bytes must be a multiple of 256)
+ *   shared_w   device blob of the layer's shared expert (weight 1), or NULL
+ *   y_out      device fp32 [T x H]; may alias x when flags has MOE_ACCUMULATE
+ *   workspace  device, >= moe_ffn_workspace_bytes(T, k, I) bytes, 256-aligned
+ * Each selected expert's weights are read once per call however many of the T
+ * tokens chose it.  Ids out of range or without a slot raise MOE_ERR_RANGE /
+ * MOE_ERR_NOT_RESIDENT in the device flags and contribute nothing. */
+MOE_API int moe_expert_ffn_grouped(const float *x, int T, int H, int I, int E, int k, const int32_t *ids,
+                           const float *weights, const int32_t *slot_of, const void *pool,
+                           size_t expert_bytes, int w_dtype, const void *shared_w, float *y_out,
+                           void *workspace, size_t workspace_bytes, int flags, void *stream);
+
+/* y_out[t,h] (+)= sum_j weights[t,j] * y_partial[t,j,h] (rank order) + y_shared[t,h].
+ *   y_partial device fp32 [T x k x H]; y_shared device fp32 [T x H] or NULL;
+ *   flags MOE_ACCUMULATE adds into y_out. */
+MOE_API int moe_combine(const float *y_partial, const float *weights, const float *y_shared, int T, int k,
+                int H, float *y_out, int flags, void *stream);
+
+/* ======================================================================= */
+/* Expert residency: LRU slot table in HBM, misses filled from pinned host   */
+/* memory (paper Fig. 1: host tier, slot group, lookup table sub-module id  */
+/* -> slot, selective load, evict; sec. 4: LRU as the conventional policy)  */
+/* ======================================================================= */
+
+typedef struct moe_cache moe_cache;
+
+typedef struct {
+    int n_layers;              /* L */
+    int n_experts;             /* E routed experts per layer */
+    size_t expert_bytes;       /* bytes of one expert blob; multiple of 256 */
+    size_t budget_bytes;       /* HBM budget for expert weights */
+    size_t reserved_bytes;     /* part of the budget held by always-resident weights (shared experts) */
+    const void *host_base;     /* pinned host store; expert (l, e) at host_base + l*host_layer_stride + e*host_expert_stride */
+    size_t host_layer_stride;  /* 0 lets layers alias one host copy (keys stay distinct) */
+    size_t host_expert_stride;
+    int policy;                /* MOE_POLICY_LRU */
+    int flags;                 /* MOE_CACHE_PRELOAD | MOE_CACHE_HOST_SIM */
+} moe_cache_desc;
+
+typedef struct {
+    uint64_t lookups;     /* expert lookups (unique ids per call) */
+    uint64_t hits;
+    uint64_t misses;
+    uint64_t prefetches;  /* speculative inserts */
+    uint64_t evictions;
+    uint64_t h2d_bytes;   /* bytes filled from the host store */
+    int32_t capacity;     /* slots: floor((budget - reserved) / expert_bytes) */
+    int32_t occupancy;    /* slots holding an expert */
+} moe_cache_stats;
+
+/* One residency decision.  victim_key = layer * E + expert of the evicted
+ * entry, or -1. */
+typedef struct {
+    int32_t step, layer, expert, kind, slot, victim_key;
+} moe_cache_event;
+
+/* Create a cache: allocates capacity * expert_bytes of HBM for the slots, a
+ * copy stream and its events, and the device slot table int32 [L x E].
+ * MOE_ERR_BUDGET if capacity < 1 (or < L*E with MOE_CACHE_PRELOAD);
+ * MOE_ERR_NOT_PINNED if host_base is not hipHostMalloc memory.  PRELOAD fills
+ * every slot synchronously before returning.  With MOE_CACHE_HOST_SIM no HIP
+ * call is made: slots are host memory and `dev_slot_of` is a host array. */
+MOE_API int expert_cache_create(const moe_cache_desc *desc, moe_cache **out);
+
+/* Wait for the cache's copies and free everything it owns. */
+MOE_API int expert_cache_destroy(moe_cache *c);
+
+/* Demand lookup of the experts one step needs at `layer` (host call).
+ *   ids_host  host int32 [n]; the step's set is the ascending unique ids
+ *   slots_out host int32 [n] or NULL: slot of each ids_host[i]
+ *   hit_out   host uint8 [n] or NULL: 1 if ids_host[i] was resident
+ * Each id in ascending order takes one recency stamp: a resident id is a hit;
+ * a missing one takes the lowest free slot, else evicts the least recently
+ * used slot whose expert is not in this step's set.  Fills are queued on the
+ * cache's copy stream, each after the last recorded reader of its victim
+ * slot; the changed slot-table entries are written on `compute_stream`, which
+ * is then made to wait for the fills.  MOE_ERR_BUDGET (no state change) if
+ * the set is larger than the capacity; MOE_ERR_RANGE for ids outside [0, E). */
+MOE_API int expert_cache_lookup(moe_cache *c, int step, int layer, const int32_t *ids_host, int n,
+                        int32_t *slots_out, uint8_t *hit_out, void *compute_stream);
+
+/* Speculative insert: non-resident ids are placed like misses (counted as
+ * prefetches, logged with MOE_EVENT_PREFETCH) and their fills queued; resident
+ * ids are left untouched (no recency refresh).  Does not wait on anything;
+ * the next lookup on a compute stream orders the fills before its use.
+ * Errors as for expert_cache_lookup. */
+MOE_API int expert_cache_prefetch(moe_cache *c, int step, int layer, const int32_t *ids_host, int n);
+
+/* Record, on `compute_stream`, the point after which the slots returned by
+ * the last lookup are no longer read (call after enqueueing the FFN).  A
+ * lookup that finds unreleased slots releases them on the stream of the
+ * previous lookup first. */
+MOE_API int expert_cache_release(moe_cache *c, void *compute_stream);
+
+/* Device slot table int32 [L x E] (-1 = absent; a host array under
+ * HOST_SIM) and the slot pool base.  Owned by the cache. */
+MOE_API int expert_cache_slot_table(moe_cache *c, const int32_t **dev_slot_of, const void **pool);
+
+MOE_API int expert_cache_stats(moe_cache *c, moe_cache_stats *out);
+
+/* Copy events [first, first + cap) of the decision log into buf; *n_out =
+ * number copied. */
+MOE_API int expert_cache_trace(moe_cache *c, size_t first, moe_cache_event *buf, size_t cap,
+                       size_t *n_out);
+
+/* ======================================================================= */
+/* Decode stack driver: for each layer, route -> (lookup) -> FFN with fused  */
+/* residual x += MoE(x); attention is the identity                          */
+/* ======================================================================= */
+
+typedef struct moe_stack moe_stack;
+
+typedef struct {
+    int n_layers, H, I, E, k;
+    int w_dtype;                    /* expert storage type */
+    int router_dtype;               /* MOE_F32 or MOE_BF16 */
+    const void *const *router_w;    /* host array [L] of device [E x H] router weights */
+    const void *const *shared_w;    /* host array [L] of device shared-expert blobs, or NULL */
+    moe_cache *cache;               /* residency of the routed experts */
+    int max_tokens;                 /* largest T passed to moe_stack_decode_step (<= 16) */
+} moe_stack_desc;
+
+MOE_API int moe_stack_create(const moe_stack_desc *desc, moe_stack **out);
+MOE_API int moe_stack_destroy(moe_stack *s);
+
+/* One decode step over every layer, in place on x (device fp32 [T x H]):
+ * x <- x + MoE_l(x) for l = 0..L-1.  logit_bias is device fp32 [L x T x E]
+ * added to each layer's router logits, or NULL.  Unless the cache was created
+ * with PRELOAD, each layer copies its ids to the host (one synchronisation per
+ * layer), runs the lookup, then enqueues the FFN and releases the slots.
+ * ids_out (device int32 [L x T x k]) and weights_out (device fp32 [L x T x k])
+ * receive each layer's routing when non-NULL. */
+MOE_API int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *logit_bias,
+                          int32_t *ids_out, float *weights_out, void *stream);
+
+/* Mean device time (ms) and count of the kernels the stack enqueued since the
+ * last call, measured with HIP events around each launch when timing is on:
+ *   which 0 = router+top-k, 1 = expert gate/up + SwiGLU, 2 = expert down + combine. */
+MOE_API int moe_stack_set_timing(moe_stack *s, int on);
+MOE_API int moe_stack_kernel_time(moe_stack *s, int which, double *mean_ms, uint64_t *count);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MOE_BUDGET_H */

@@ -1,0 +1,60 @@
+// Internal declarations shared by the library's translation units (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+struct moe_cache;
+
+namespace moe {
+
+// Sticky device error bits (OR-ed by kernels into the per-device flag word).
+enum : int { kErrRange = 1, kErrNonfinite = 2, kErrNotResident = 4 };
+
+// Bytes of one expert blob and the byte offset of W_d inside it.
+size_t expert_blob_bytes(int H, int I, int dtype);
+size_t down_offset(int H, int I, int dtype);
+
+// Workspace carve-up of moe_expert_ffn_grouped.
+struct FfnWorkspace {
+    float *act;       // [(T*k + T) x I] SwiGLU activations, one row per (token, rank) pair + shared
+    int *groups;      // grouping table (T > 1 only)
+};
+size_t ffn_workspace_bytes(int T, int k, int I);
+FfnWorkspace ffn_workspace(void *base, int T, int k, int I);
+
+// Kernel launchers (all asynchronous on `s`).  Shapes are validated by the caller.
+hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int T, int H, int E,
+                                const float *bias, float *logits, hipStream_t s);
+hipError_t launch_topk_softmax(const float *logits, int T, int E, int k, int32_t *ids, float *weights,
+                               int *err_flags, hipStream_t s);
+// Optional events recorded around the two expert kernels (for per-kernel timing).
+struct FfnEvents {
+    hipEvent_t gu_begin, gu_end, dn_end;
+};
+hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, const int32_t *ids,
+                             const float *weights, const int32_t *slot_of, const void *pool,
+                             size_t expert_bytes, int dtype, const void *shared_w, float *y,
+                             bool accumulate, const FfnWorkspace &ws, int *err_flags, hipStream_t s,
+                             const FfnEvents *ev = nullptr);
+hipError_t launch_combine(const float *y_partial, const float *weights, const float *y_shared, int T,
+                          int k, int H, float *y, bool accumulate, hipStream_t s);
+hipError_t launch_slot_update(int32_t *table, const int32_t *index, const int32_t *value, int n,
+                              hipStream_t s);
+
+bool ffn_shape_supported(int H, int I, int dtype);
+bool router_shape_supported(int H, int dtype);
+
+// Error reporting across the C ABI: records a thread-local message, returns `code`.
+int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail_hip(hipError_t e, const char *what);
+void clear_error();
+
+// Slot stride of a cache's pool.
+size_t cache_expert_bytes(const struct ::moe_cache *c);
+
+// Sticky error-flag word of the current device (set up on first use).
+int *device_error_flags();
+
+}  // namespace moe

@@ -1,0 +1,455 @@
+// residency.cpp -- expert slot table in HBM with least-recently-used replacement.
+//
+// The paper's residency picture (sec. 4, Fig. 1): every sub-module (expert)
+// lives in the host tier; the accelerator holds a fixed group of slots; a
+// lookup table maps sub-module id to slot; missing sub-modules are brought in
+// by a selective load after an eviction makes room; the whole runs inside a
+// memory budget (sec. 5).  Replacement here is LRU at step granularity: a
+// step's ascending unique experts take one recency stamp each, and a miss
+// evicts the least recently used slot whose expert the same step does not need.
+//
+// Device ordering (per cache):
+//   copy stream : [wait last reader of each victim] [H2D fills] [slot-table update] -> fill event
+//   compute     : waits on the fill event, then the caller enqueues the FFN, then release()
+//                 records the slots' last-reader event.
+// Events come from a ring; an entry is synchronised before it is re-recorded,
+// so a slot whose reader entry was recycled has provably finished being read.
+#include <stdarg.h>
+#include <string.h>
+
+#include <algorithm>
+#include <functional>
+#include <queue>
+#include <vector>
+
+#include "internal.h"
+#include "../../include/moe_budget.h"
+
+namespace {
+
+struct EvRef {
+    int idx = -1;
+    uint64_t gen = 0;
+};
+
+class EventRing {
+  public:
+    explicit EventRing(int n = 512) : ev_(n), gen_(n, 0) {}
+    hipError_t init() {
+        for (auto &e : ev_) {
+            hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableTiming);
+            if (r != hipSuccess) return r;
+        }
+        return hipSuccess;
+    }
+    void destroy() {
+        for (auto &e : ev_)
+            if (e) (void)hipEventDestroy(e);
+    }
+    hipError_t record(hipStream_t s, EvRef *out) {
+        const int i = next_;
+        next_ = (next_ + 1) % int(ev_.size());
+        if (gen_[i]) {
+            hipError_t r = hipEventSynchronize(ev_[i]);  // the old record must be complete before reuse
+            if (r != hipSuccess) return r;
+        }
+        ++gen_[i];
+        out->idx = i;
+        out->gen = gen_[i];
+        return hipEventRecord(ev_[i], s);
+    }
+    // True while the referenced record may still be outstanding.
+    bool live(const EvRef &r) const { return r.idx >= 0 && gen_[r.idx] == r.gen; }
+    hipEvent_t event(const EvRef &r) const { return ev_[r.idx]; }
+
+  private:
+    std::vector<hipEvent_t> ev_;
+    std::vector<uint64_t> gen_;
+    int next_ = 0;
+};
+
+}  // namespace
+
+struct moe_cache {
+    moe_cache_desc d{};
+    int L = 0, E = 0, C = 0;
+    bool sim = false;
+
+    std::vector<int32_t> key_of_slot;  // layer*E + expert, -1 = free
+    std::vector<int32_t> slot_of_key;  // host mirror of the device table [L*E]
+    std::vector<int32_t> prev, next;   // recency list over slots, head = least recent
+    int head = -1, tail = -1;
+    std::priority_queue<int, std::vector<int>, std::greater<int>> free_slots;
+    std::vector<uint64_t> step_mark;   // == epoch while the key is in the current step's set
+    uint64_t epoch = 0;
+
+    uint8_t *pool = nullptr;            // device (or host under sim) slots
+    int32_t *dev_slot_of = nullptr;     // device (or host under sim) table [L*E]
+    hipStream_t copy = nullptr;
+    EventRing ring;
+    std::vector<EvRef> reader;          // last recorded reader of each slot
+    std::vector<int> unreleased;        // slots handed out by the last lookup
+    hipStream_t last_compute = nullptr;
+    bool have_last_compute = false;
+    EvRef prefetch_done;                // copy-stream point after the latest prefetch's fills
+
+    std::vector<moe_cache_event> log;
+    moe_cache_stats st{};
+};
+
+namespace {
+
+void unlink(moe_cache *c, int s) {
+    const int p = c->prev[s], n = c->next[s];
+    if (p >= 0) c->next[p] = n; else c->head = n;
+    if (n >= 0) c->prev[n] = p; else c->tail = p;
+    c->prev[s] = c->next[s] = -1;
+}
+
+void push_recent(moe_cache *c, int s) {
+    c->prev[s] = c->tail;
+    c->next[s] = -1;
+    if (c->tail >= 0) c->next[c->tail] = s; else c->head = s;
+    c->tail = s;
+}
+
+int check_ids(moe_cache *c, int layer, const int32_t *ids, int n, std::vector<int32_t> *R) {
+    if (!c) return moe::fail(MOE_ERR_INVALID_ARG, "cache is NULL");
+    if (layer < 0 || layer >= c->L) return moe::fail(MOE_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, c->L);
+    if (n < 0 || (n > 0 && !ids)) return moe::fail(MOE_ERR_INVALID_ARG, "bad id list (n=%d)", n);
+    for (int i = 0; i < n; ++i)
+        if (ids[i] < 0 || ids[i] >= c->E)
+            return moe::fail(MOE_ERR_RANGE, "expert id %d outside [0, %d)", ids[i], c->E);
+    R->assign(ids, ids + n);
+    std::sort(R->begin(), R->end());
+    R->erase(std::unique(R->begin(), R->end()), R->end());
+    if (int(R->size()) > c->C)
+        return moe::fail(MOE_ERR_BUDGET, "step needs %zu experts but only %d slots fit the budget", R->size(), c->C);
+    return MOE_OK;
+}
+
+// Records the pending last-reader event for slots of the previous lookup.
+int release_pending(moe_cache *c, hipStream_t s) {
+    if (c->unreleased.empty()) return MOE_OK;
+    if (!c->sim) {
+        EvRef r;
+        hipError_t e = c->ring.record(s, &r);
+        if (e != hipSuccess) return moe::fail_hip(e, "recording slot release");
+        for (int slot : c->unreleased) c->reader[slot] = r;
+    }
+    c->unreleased.clear();
+    return MOE_OK;
+}
+
+const uint8_t *host_blob(const moe_cache *c, int layer, int expert) {
+    return static_cast<const uint8_t *>(c->d.host_base) + size_t(layer) * c->d.host_layer_stride +
+           size_t(expert) * c->d.host_expert_stride;
+}
+
+// Insert (layer, e) at a free or victim slot and queue its fill.  Returns the
+// slot, or -1 with the error recorded.
+int place_and_fill(moe_cache *c, int layer, int e, int32_t *victim, std::vector<int32_t> *chg_idx,
+                   std::vector<int32_t> *chg_val, int *status) {
+    int s;
+    *victim = -1;
+    if (!c->free_slots.empty()) {
+        s = c->free_slots.top();
+        c->free_slots.pop();
+    } else {
+        s = c->head;
+        while (s >= 0 && c->step_mark[c->key_of_slot[s]] == c->epoch) s = c->next[s];
+        if (s < 0) {  // unreachable while |R| <= C
+            *status = moe::fail(MOE_ERR_BUDGET, "no evictable slot");
+            return -1;
+        }
+        *victim = c->key_of_slot[s];
+        c->slot_of_key[*victim] = -1;
+        chg_idx->push_back(*victim);
+        chg_val->push_back(-1);
+        unlink(c, s);
+        ++c->st.evictions;
+    }
+    const int32_t key = layer * c->E + e;
+    uint8_t *dst = c->pool + size_t(s) * c->d.expert_bytes;
+    const uint8_t *src = host_blob(c, layer, e);
+    if (c->sim) {
+        memcpy(dst, src, c->d.expert_bytes);
+    } else {
+        if (c->ring.live(c->reader[s])) {
+            hipError_t r = hipStreamWaitEvent(c->copy, c->ring.event(c->reader[s]), 0);
+            if (r != hipSuccess) *status = moe::fail_hip(r, "ordering fill after last reader");
+        }
+        hipError_t r = hipMemcpyAsync(dst, src, c->d.expert_bytes, hipMemcpyHostToDevice, c->copy);
+        if (r != hipSuccess) {
+            // the slot stays unmapped so that a retry misses again
+            c->free_slots.push(s);
+            c->key_of_slot[s] = -1;
+            *status = moe::fail(MOE_ERR_COPY, "fill of expert (%d, %d) failed: %s", layer, e,
+                                hipGetErrorString(r));
+            return -1;
+        }
+    }
+    c->key_of_slot[s] = key;
+    c->slot_of_key[key] = s;
+    chg_idx->push_back(key);
+    chg_val->push_back(s);
+    push_recent(c, s);
+    c->st.h2d_bytes += c->d.expert_bytes;
+    return s;
+}
+
+// Applies slot-table changes (last value per entry wins) after the fills on the
+// copy stream and returns the event marking the end of that work.
+int publish(moe_cache *c, std::vector<int32_t> &idx, std::vector<int32_t> &val, EvRef *done) {
+    std::vector<int32_t> ui, uv;
+    for (size_t i = 0; i < idx.size(); ++i) {
+        bool later = false;
+        for (size_t j = i + 1; j < idx.size(); ++j)
+            if (idx[j] == idx[i]) later = true;
+        if (!later) {
+            ui.push_back(idx[i]);
+            uv.push_back(val[i]);
+        }
+    }
+    if (c->sim) {
+        for (size_t i = 0; i < ui.size(); ++i) c->dev_slot_of[ui[i]] = uv[i];
+        return MOE_OK;
+    }
+    hipError_t e = moe::launch_slot_update(c->dev_slot_of, ui.data(), uv.data(), int(ui.size()), c->copy);
+    if (e != hipSuccess) return moe::fail_hip(e, "slot-table update");
+    e = c->ring.record(c->copy, done);
+    if (e != hipSuccess) return moe::fail_hip(e, "recording fill event");
+    return MOE_OK;
+}
+
+int lookup_impl(moe_cache *c, int step, int layer, const int32_t *ids, int n, bool prefetch,
+                int32_t *slots_out, uint8_t *hit_out, hipStream_t compute) {
+    std::vector<int32_t> R;
+    int st = check_ids(c, layer, ids, n, &R);
+    if (st != MOE_OK) return st;
+    moe::clear_error();
+    if (c->have_last_compute) {
+        st = release_pending(c, c->last_compute);
+        if (st != MOE_OK) return st;
+    }
+    ++c->epoch;
+    for (int e : R) c->step_mark[layer * c->E + e] = c->epoch;
+    std::vector<int32_t> chg_idx, chg_val;
+    std::vector<uint8_t> hit_of(R.size(), 0);
+    st = MOE_OK;
+    for (size_t r = 0; r < R.size(); ++r) {
+        const int e = R[r];
+        const int32_t key = layer * c->E + e;
+        int s = c->slot_of_key[key];
+        if (s >= 0) {
+            if (prefetch) continue;  // a prefetch leaves resident experts untouched
+            unlink(c, s);
+            push_recent(c, s);
+            ++c->st.hits;
+            ++c->st.lookups;
+            hit_of[r] = 1;
+            c->log.push_back({step, layer, e, MOE_EVENT_HIT, s, -1});
+            continue;
+        }
+        int32_t victim;
+        s = place_and_fill(c, layer, e, &victim, &chg_idx, &chg_val, &st);
+        if (s < 0) break;
+        if (prefetch) {
+            ++c->st.prefetches;
+        } else {
+            ++c->st.misses;
+            ++c->st.lookups;
+        }
+        c->log.push_back({step, layer, e, prefetch ? MOE_EVENT_PREFETCH : MOE_EVENT_MISS, s, victim});
+    }
+    if (!chg_idx.empty()) {
+        EvRef done;
+        int pst = publish(c, chg_idx, chg_val, &done);
+        if (pst != MOE_OK && st == MOE_OK) st = pst;
+        if (!c->sim && pst == MOE_OK) {
+            if (prefetch) {
+                c->prefetch_done = done;
+            } else {
+                hipError_t e = hipStreamWaitEvent(compute, c->ring.event(done), 0);
+                if (e != hipSuccess && st == MOE_OK) st = moe::fail_hip(e, "ordering compute after fills");
+            }
+        }
+    }
+    if (!prefetch) {
+        // earlier prefetches' fills (and table updates) must land before this step's compute
+        if (!c->sim && c->ring.live(c->prefetch_done)) {
+            hipError_t e = hipStreamWaitEvent(compute, c->ring.event(c->prefetch_done), 0);
+            if (e != hipSuccess && st == MOE_OK) st = moe::fail_hip(e, "ordering compute after prefetch");
+            c->prefetch_done = EvRef{};
+        }
+        for (int e : R) {
+            const int s = c->slot_of_key[layer * c->E + e];
+            if (s >= 0) c->unreleased.push_back(s);
+        }
+        c->last_compute = compute;
+        c->have_last_compute = true;
+        for (int i = 0; i < n; ++i) {
+            const size_t r = size_t(std::lower_bound(R.begin(), R.end(), ids[i]) - R.begin());
+            if (slots_out) slots_out[i] = c->slot_of_key[layer * c->E + ids[i]];
+            if (hit_out) hit_out[i] = hit_of[r];
+        }
+    }
+    return st;
+}
+
+}  // namespace
+
+size_t moe::cache_expert_bytes(const moe_cache *c) { return c->d.expert_bytes; }
+
+extern "C" {
+
+int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
+    if (!d || !out) return moe::fail(MOE_ERR_INVALID_ARG, "NULL descriptor or output");
+    *out = nullptr;
+    if (d->n_layers < 1 || d->n_experts < 1 || d->expert_bytes == 0)
+        return moe::fail(MOE_ERR_INVALID_ARG, "n_layers, n_experts and expert_bytes must be positive");
+    if (d->expert_bytes % 256)
+        return moe::fail(MOE_ERR_INVALID_ARG, "expert_bytes (%zu) must be a multiple of 256", d->expert_bytes);
+    if (d->policy != MOE_POLICY_LRU) return moe::fail(MOE_ERR_INVALID_ARG, "unknown policy %d", d->policy);
+    if (!d->host_base) return moe::fail(MOE_ERR_INVALID_ARG, "host_base is NULL");
+    if (d->reserved_bytes > d->budget_bytes)
+        return moe::fail(MOE_ERR_BUDGET, "reserved bytes exceed the budget");
+    const size_t cap = (d->budget_bytes - d->reserved_bytes) / d->expert_bytes;
+    const size_t keys = size_t(d->n_layers) * d->n_experts;
+    if (cap < 1) return moe::fail(MOE_ERR_BUDGET, "budget holds no expert slot");
+    const bool preload = d->flags & MOE_CACHE_PRELOAD;
+    if (preload && cap < keys)
+        return moe::fail(MOE_ERR_BUDGET, "preload needs %zu slots, the budget holds %zu", keys, cap);
+    if (keys > size_t(INT32_MAX)) return moe::fail(MOE_ERR_INVALID_ARG, "too many experts");
+
+    auto *c = new moe_cache();
+    c->d = *d;
+    c->L = d->n_layers;
+    c->E = d->n_experts;
+    c->C = int(std::min(cap, preload ? keys : cap));
+    c->sim = d->flags & MOE_CACHE_HOST_SIM;
+    c->key_of_slot.assign(c->C, -1);
+    c->slot_of_key.assign(keys, -1);
+    c->prev.assign(c->C, -1);
+    c->next.assign(c->C, -1);
+    c->step_mark.assign(keys, 0);
+    c->reader.assign(c->C, EvRef{});
+    c->st.capacity = c->C;
+
+    auto cleanup = [&](int code) {
+        expert_cache_destroy(c);
+        return code;
+    };
+    const size_t pool_bytes = size_t(c->C) * d->expert_bytes;
+    if (c->sim) {
+        c->pool = static_cast<uint8_t *>(malloc(pool_bytes));
+        c->dev_slot_of = static_cast<int32_t *>(malloc(sizeof(int32_t) * keys));
+        if (!c->pool || !c->dev_slot_of) return cleanup(moe::fail(MOE_ERR_INVALID_ARG, "host allocation failed"));
+        for (size_t i = 0; i < keys; ++i) c->dev_slot_of[i] = -1;
+    } else {
+        hipPointerAttribute_t attr;
+        hipError_t e = hipPointerGetAttributes(&attr, d->host_base);
+        if (e != hipSuccess || attr.type != hipMemoryTypeHost) {
+            (void)hipGetLastError();
+            delete c;
+            return moe::fail(MOE_ERR_NOT_PINNED, "host store is not page-locked memory");
+        }
+        if ((e = hipMalloc(&c->pool, pool_bytes)) != hipSuccess)
+            return cleanup(moe::fail_hip(e, "allocating the slot pool"));
+        if ((e = hipMalloc(&c->dev_slot_of, sizeof(int32_t) * keys)) != hipSuccess)
+            return cleanup(moe::fail_hip(e, "allocating the slot table"));
+        if ((e = hipMemset(c->dev_slot_of, 0xff, sizeof(int32_t) * keys)) != hipSuccess)
+            return cleanup(moe::fail_hip(e, "clearing the slot table"));
+        if ((e = hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking)) != hipSuccess)
+            return cleanup(moe::fail_hip(e, "creating the copy stream"));
+        if ((e = c->ring.init()) != hipSuccess) return cleanup(moe::fail_hip(e, "creating events"));
+    }
+    if (preload) {
+        for (int l = 0; l < c->L; ++l)
+            for (int e = 0; e < c->E; ++e) {
+                const int s = l * c->E + e;
+                uint8_t *dst = c->pool + size_t(s) * d->expert_bytes;
+                if (c->sim) {
+                    memcpy(dst, host_blob(c, l, e), d->expert_bytes);
+                } else {
+                    hipError_t r = hipMemcpyAsync(dst, host_blob(c, l, e), d->expert_bytes,
+                                                  hipMemcpyHostToDevice, c->copy);
+                    if (r != hipSuccess) return cleanup(moe::fail_hip(r, "preloading experts"));
+                }
+                c->key_of_slot[s] = s;
+                c->slot_of_key[s] = s;
+                push_recent(c, s);
+            }
+        if (c->sim) {
+            for (size_t i = 0; i < keys; ++i) c->dev_slot_of[i] = int32_t(i);
+        } else {
+            hipError_t r = hipMemcpyAsync(c->dev_slot_of, c->slot_of_key.data(), sizeof(int32_t) * keys,
+                                          hipMemcpyHostToDevice, c->copy);
+            if (r == hipSuccess) r = hipStreamSynchronize(c->copy);
+            if (r != hipSuccess) return cleanup(moe::fail_hip(r, "preloading experts"));
+        }
+    } else {
+        for (int s = 0; s < c->C; ++s) c->free_slots.push(s);
+    }
+    *out = c;
+    return MOE_OK;
+}
+
+int expert_cache_destroy(moe_cache *c) {
+    if (!c) return MOE_OK;
+    if (c->sim) {
+        free(c->pool);
+        free(c->dev_slot_of);
+    } else {
+        if (c->copy) (void)hipStreamSynchronize(c->copy);
+        if (c->have_last_compute) (void)hipStreamSynchronize(c->last_compute);
+        c->ring.destroy();
+        if (c->copy) (void)hipStreamDestroy(c->copy);
+        if (c->pool) (void)hipFree(c->pool);
+        if (c->dev_slot_of) (void)hipFree(c->dev_slot_of);
+    }
+    delete c;
+    return MOE_OK;
+}
+
+int expert_cache_lookup(moe_cache *c, int step, int layer, const int32_t *ids_host, int n,
+                        int32_t *slots_out, uint8_t *hit_out, void *compute_stream) {
+    return lookup_impl(c, step, layer, ids_host, n, false, slots_out, hit_out,
+                       static_cast<hipStream_t>(compute_stream));
+}
+
+int expert_cache_prefetch(moe_cache *c, int step, int layer, const int32_t *ids_host, int n) {
+    return lookup_impl(c, step, layer, ids_host, n, true, nullptr, nullptr, nullptr);
+}
+
+int expert_cache_release(moe_cache *c, void *compute_stream) {
+    if (!c) return moe::fail(MOE_ERR_INVALID_ARG, "cache is NULL");
+    return release_pending(c, static_cast<hipStream_t>(compute_stream));
+}
+
+int expert_cache_slot_table(moe_cache *c, const int32_t **dev_slot_of, const void **pool) {
+    if (!c) return moe::fail(MOE_ERR_INVALID_ARG, "cache is NULL");
+    if (dev_slot_of) *dev_slot_of = c->dev_slot_of;
+    if (pool) *pool = c->pool;
+    return MOE_OK;
+}
+
+int expert_cache_stats(moe_cache *c, moe_cache_stats *out) {
+    if (!c || !out) return moe::fail(MOE_ERR_INVALID_ARG, "NULL argument");
+    *out = c->st;
+    int occ = 0;
+    for (int32_t k : c->key_of_slot) occ += k >= 0;
+    out->occupancy = occ;
+    return MOE_OK;
+}
+
+int expert_cache_trace(moe_cache *c, size_t first, moe_cache_event *buf, size_t cap, size_t *n_out) {
+    if (!c || !n_out || (cap && !buf)) return moe::fail(MOE_ERR_INVALID_ARG, "NULL argument");
+    size_t n = 0;
+    if (first < c->log.size()) n = std::min(cap, c->log.size() - first);
+    if (n) memcpy(buf, c->log.data() + first, n * sizeof(moe_cache_event));
+    *n_out = n;
+    return MOE_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,309 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, on MI355X.
+
+Tolerances: router logits normwise 1e-5 per token; top-k ids bit-exact given
+the GPU's own fp32 logits; weights |w - w_ref| <= 1e-5 * max(1, |w_ref|);
+expert FFN output normwise max|y - y_ref| / max|y_ref| per token <= 1e-5 (fp32
+weights), 1e-2 (bf16), 3e-2 (int4) against the fp64 oracle on the same stored
+weights; residency event logs byte-equal to the oracle replaying the same calls.
+"""
+import numpy as np
+import pytest
+import torch
+
+import oracle
+import paper_2605_29135_amd as moe
+import synth
+
+pytestmark = pytest.mark.gpu
+
+TOL = {synth.F32: 1e-5, synth.BF16: 1e-2, synth.INT4G128: 3e-2}
+DEV = torch.device("cuda:0")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _init():
+    moe.moe_init(0)
+    yield
+    torch.cuda.synchronize()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def normwise(y, ref):
+    y = np.atleast_2d(y).astype(np.float64)
+    ref = np.atleast_2d(ref)
+    return float(np.max(np.abs(y - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-30)))
+
+
+def check_route(x, wr, rdtype, k, bias=None):
+    """Run moe_route_topk and check it against the oracle; returns (ids, weights) on the host."""
+    logits, ids, w = moe.moe_route_topk(None if x is None else dev(x), None if wr is None else dev(wr), rdtype, k,
+                                        E=(wr.shape[0] if wr is not None else bias.shape[1]),
+                                        logit_bias=None if bias is None else dev(bias))
+    moe.moe_sync_check()
+    z = logits.cpu().numpy()
+    if x is not None:
+        zref = oracle.router_logits(x, wr, rdtype) + (0 if bias is None else bias)
+        assert normwise(z, zref) <= 1e-5
+    o_ids, o_w, st = oracle.topk_softmax(z, k)
+    assert st == oracle.OK
+    g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
+    assert (g_ids == o_ids).all()
+    assert (np.abs(g_w - o_w) <= 1e-5 * np.maximum(1.0, np.abs(o_w))).all()
+    return g_ids, g_w
+
+
+# ----------------------------------------------------------------- route ---
+@pytest.mark.parametrize("cfg,T", [(1, 1), (2, 1), (3, 1), (3, 4), (3, 16), (2, 37)])
+def test_route_parity_configs(cfg, T):
+    wl = synth.workload(cfg)
+    wr = synth.router_weights(wl, 0)
+    for step in range(3):
+        x = synth.hidden_states(wl, step, T=T)
+        check_route(x, wr, wl.router_dtype, wl.k)
+
+
+def test_route_with_mask_bias_selects_the_drawn_sets():
+    wl = synth.workload(3, T=16)
+    wr = synth.router_weights(wl, 0)
+    sets = synth.routing_sets(wl, steps=4, T=16)
+    for t in range(4):
+        bias = synth.mask_logits(wl, sets[t, 0])
+        ids, _ = check_route(synth.hidden_states(wl, t, T=16), wr, wl.router_dtype, wl.k, bias)
+        assert (np.sort(ids, axis=1) == sets[t, 0]).all()
+
+
+@pytest.mark.parametrize("E,k", [(16, 16), (256, 1), (256, 16), (64, 3), (130, 5)])
+def test_route_ties_and_edge_k(E, k):
+    rng = np.random.default_rng(E + k)
+    vals = np.array([-1.0, -0.0, 0.0, 0.25, 2.0], np.float32)
+    bias = vals[rng.integers(0, vals.size, size=(9, E))]
+    check_route(None, None, synth.F32, k, bias)
+    H = 256
+    x = rng.standard_normal((9, H)).astype(np.float32)
+    wr = synth.bf16_bits(rng.standard_normal((E, H)).astype(np.float32) * 0.05)
+    check_route(x, wr, synth.BF16, k, bias)
+
+
+def test_route_nonfinite_raises_and_marks_token():
+    bias = np.zeros((3, 32), np.float32)
+    bias[1, 7] = np.nan
+    _, ids, w = moe.moe_route_topk(None, None, synth.F32, 4, E=32, logit_bias=dev(bias))
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_sync_check()
+    assert ei.value.code == -3
+    assert (ids.cpu().numpy()[1] == -1).all() and (w.cpu().numpy()[1] == 0).all()
+    assert (ids.cpu().numpy()[0] == [0, 1, 2, 3]).all()
+    moe.moe_sync_check()  # flags were cleared
+
+
+def test_route_rejects_bad_arguments():
+    x = torch.zeros((1, 256), device=DEV)
+    w = torch.zeros((300, 256), device=DEV)
+    with pytest.raises(moe.MoeError):
+        moe.moe_route_topk(x, w, synth.F32, 8)  # E > 256
+    with pytest.raises(moe.MoeError):
+        moe.moe_route_topk(x, w[:16], synth.F32, 17)  # k > E
+    moe.moe_route_topk(x[:0], w[:16], synth.F32, 2)  # T = 0 is a no-op
+
+
+# ------------------------------------------------------------------- FFN ---
+_EXPERTS = {}
+
+
+def _experts(wl):
+    """Layer 0's routed experts [E x expert_bytes] and shared blob (cached per workload shape)."""
+    key = (wl.cfg_id, wl.H, wl.E, wl.I, wl.L, wl.dtype, wl.shared)
+    if key not in _EXPERTS:
+        _EXPERTS.clear()
+        ex = synth.layer_experts(wl, 0)
+        sh = synth.expert_blob(wl, 0, None) if wl.shared else None
+        _EXPERTS[key] = (ex, sh)
+    return _EXPERTS[key]
+
+
+def check_ffn(wl, x, ids, w, ex, sh, slot_perm=None, accumulate=False):
+    E, eb = ex.shape
+    if slot_perm is not None:  # expert e lives in slot slot_perm[e]
+        pool_np = np.empty_like(ex)
+        pool_np[slot_perm] = ex
+        slot_of = dev(slot_perm.astype(np.int32))
+    else:
+        pool_np, slot_of = ex, None
+    pool = dev(pool_np.reshape(-1))
+    xd = dev(x)
+    base = np.random.default_rng(0).standard_normal(x.shape).astype(np.float32)
+    y = dev(base) if accumulate else None
+    y = moe.moe_expert_ffn_grouped(xd, dev(ids), dev(w), pool, eb, wl.dtype, wl.I, wl.E, slot_of=slot_of,
+                                   shared_w=None if sh is None else dev(sh), y_out=y, accumulate=accumulate)
+    moe.moe_sync_check()
+    ref = oracle.moe_ffn(x, ids, w.astype(np.float64), ex, wl.H, wl.I, wl.dtype, sh)
+    got = y.cpu().numpy() - (base if accumulate else 0)
+    err = normwise(got, ref)
+    assert err <= TOL[wl.dtype], err
+    return err
+
+
+@pytest.mark.parametrize("cfg,T", [(1, 1), (2, 1), (3, 1), (3, 4), (3, 16), (5, 1), (5, 4)])
+def test_ffn_parity_configs(cfg, T):
+    wl = synth.workload(cfg, T=T, L=1)
+    ex, sh = _experts(wl)
+    wr = synth.router_weights(wl, 0)
+    for step in range(2):
+        x = synth.hidden_states(wl, step, T=T)
+        ids, w = check_route(x, wr, wl.router_dtype, wl.k)
+        check_ffn(wl, x, ids, w, ex, sh)
+
+
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16, synth.INT4G128])
+def test_ffn_grouping_duplicates_slots_and_accumulate(dtype):
+    """Tokens sharing experts, a permuted slot table, ragged shapes and the fused residual."""
+    H = 2048 if dtype == synth.INT4G128 else 384
+    wl = synth.Workload("ragged", H=H, E=24, k=6, I=384, dtype=dtype, router_dtype=synth.F32, shared=True,
+                        cfg_id=90 + dtype)
+    ex, sh = _experts(wl)
+    rng = np.random.default_rng(dtype)
+    for T in (2, 7, 16):
+        x = rng.standard_normal((T, wl.H)).astype(np.float32)
+        ids = np.stack([rng.choice(6, size=6, replace=False) for _ in range(T)]).astype(np.int32)  # heavy overlap
+        w = rng.random((T, 6)).astype(np.float32)
+        check_ffn(wl, x, ids, w, ex, sh, slot_perm=rng.permutation(wl.E))
+        check_ffn(wl, x, ids, w, ex, None, accumulate=True)
+
+
+def test_ffn_invalid_ids_raise_and_contribute_nothing():
+    wl = synth.Workload("bad-ids", H=256, E=8, k=2, I=128, dtype=synth.BF16, cfg_id=95)
+    ex, _ = _experts(wl)
+    x = np.random.default_rng(1).standard_normal((2, 256)).astype(np.float32)
+    w = np.array([[0.6, 0.4], [0.5, 0.5]], np.float32)
+    for T1 in (1, 2):
+        ids = np.array([[3, 9], [1, 2]], np.int32)[:T1]
+        y = moe.moe_expert_ffn_grouped(dev(x[:T1]), dev(ids), dev(w[:T1]), dev(ex.reshape(-1)), wl.expert_bytes,
+                                       wl.dtype, wl.I, wl.E)
+        with pytest.raises(moe.MoeError) as ei:
+            moe.moe_sync_check()
+        assert ei.value.code == -2
+        ref = oracle.moe_ffn(x[:1], np.array([[3]]), np.array([[0.6]]), ex, wl.H, wl.I, wl.dtype)
+        assert normwise(y.cpu().numpy()[:1], ref) <= 1e-2
+    slot_of = dev(np.array([0, 1, 2, -1, 4, 5, 6, 7], np.int32))
+    moe.moe_expert_ffn_grouped(dev(x[:1]), dev(np.array([[3, 1]], np.int32)), dev(w[:1]), dev(ex.reshape(-1)),
+                               wl.expert_bytes, wl.dtype, wl.I, wl.E, slot_of=slot_of)
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_sync_check()
+    assert ei.value.code == -8
+
+
+def test_combine_parity():
+    rng = np.random.default_rng(3)
+    T, k, H = 5, 8, 2048
+    yp = rng.standard_normal((T, k, H)).astype(np.float32)
+    w = rng.random((T, k)).astype(np.float32)
+    ys = rng.standard_normal((T, H)).astype(np.float32)
+    y = moe.moe_combine(dev(yp), dev(w), dev(ys))
+    ref = np.einsum("tk,tkh->th", w.astype(np.float64), yp.astype(np.float64)) + ys
+    assert normwise(y.cpu().numpy(), ref) <= 1e-6
+    base = dev(ys)
+    moe.moe_combine(dev(yp), dev(w), None, y_out=base, accumulate=True)
+    assert normwise(base.cpu().numpy(), ref) <= 1e-6
+
+
+# ------------------------------------------------------- budgeted stack ---
+def _pinned_store(wl, layers_alias=False):
+    L_store = 1 if layers_alias else wl.L
+    buf = moe.PinnedBuffer(L_store * wl.E * wl.expert_bytes)
+    st = buf.array.reshape(L_store, wl.E * wl.expert_bytes)
+    for l in range(L_store):
+        synth.layer_experts(wl, l, st[l])
+    return buf
+
+
+def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=None, T=1):
+    """Decode `steps` steps through the stack; check events exactly and outputs within tolerance."""
+    buf = _pinned_store(wl, layers_alias)
+    eb = wl.expert_bytes
+    cache = moe.ExpertCache(wl.L, wl.E, eb, capacity * eb + (wl.L * eb if wl.shared else 0), buf.ptr,
+                            0 if layers_alias else wl.E * eb, eb, reserved_bytes=wl.L * eb if wl.shared else 0)
+    routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
+    shared = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)] if wl.shared else None
+    stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T)
+    sets = synth.routing_sets(wl, steps=steps, T=T)
+    o = oracle.LRU(capacity, wl.L, wl.E)
+    check_steps = set(range(steps) if check_steps is None else check_steps)
+    host_layers = {}
+    for t in range(steps):
+        x0 = synth.hidden_states(wl, t, T=T)
+        bias = np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)])
+        x = dev(x0)
+        ids = torch.empty((wl.L, T, wl.k), dtype=torch.int32, device=DEV)
+        w = torch.empty((wl.L, T, wl.k), dtype=torch.float32, device=DEV)
+        stack.decode_step(t, x, dev(bias), ids, w)
+        moe.moe_sync_check()
+        g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
+        for l in range(wl.L):
+            assert (np.sort(g_ids[l], axis=1) == sets[t, l]).all()
+            assert o.lookup(t, l, g_ids[l].reshape(-1)) == oracle.OK
+        if t in check_steps:
+            # oracle chain in fp64 from the same input, routed by the GPU's ids and weights
+            xr = x0.astype(np.float64)
+            for l in range(wl.L):
+                lsrc = 0 if layers_alias else l
+                if lsrc not in host_layers:
+                    host_layers[lsrc] = synth.layer_experts(wl, lsrc)
+                sh = synth.expert_blob(wl, l, None) if wl.shared else None
+                xr = xr + oracle.moe_ffn(xr.astype(np.float32), g_ids[l], g_w[l], host_layers[lsrc], wl.H, wl.I,
+                                         wl.dtype, sh)
+            assert normwise(x.cpu().numpy() - x0, xr - x0) <= TOL[wl.dtype]
+    ev = cache.trace()
+    oev = o.events()
+    assert len(ev) == len(oev)
+    assert (ev.view(np.int32).reshape(-1, 6) == oev.view(np.int32).reshape(-1, 6)).all()
+    s = cache.stats()
+    assert s["occupancy"] <= capacity and s["misses"] == o.stats()["misses"]
+    stack.close()
+    cache.close()
+    buf.close()
+    return s
+
+
+def test_budgeted_stack_small_evicting():
+    wl = synth.Workload("small stack", H=512, E=32, k=4, I=256, L=4, dtype=synth.BF16, routing="zipf_overlap",
+                        cfg_id=97)
+    s = run_stack_and_check(wl, steps=40, capacity=24)
+    assert s["evictions"] > 0
+
+
+def test_budgeted_stack_tokens_and_shared_int4():
+    wl = synth.Workload("int4 stack", H=2048, E=64, k=8, I=256, L=3, dtype=synth.INT4G128, shared=True,
+                        routing="zipf_overlap", cfg_id=98)
+    s = run_stack_and_check(wl, steps=12, capacity=40, T=4, check_steps=[0, 5, 11])
+    assert s["evictions"] > 0
+
+
+def test_budgeted_stack_full_size_config4_sampled():
+    """The benchmark's configuration (40 layers, 6 GiB budget -> 682 slots), layers aliasing one host copy."""
+    wl = synth.workload(4)
+    s = run_stack_and_check(wl, steps=6, capacity=wl.capacity(), layers_alias=True, check_steps=[0, 5])
+    assert s["capacity"] == 682 and s["misses"] > 0
+
+
+def test_full_size_config2_every_output():
+    wl = synth.workload(2)
+    ex, _ = _experts(wl)
+    wr = synth.router_weights(wl, 0)
+    pool = dev(ex.reshape(-1))
+    for step in range(4):
+        x = synth.hidden_states(wl, step)
+        ids, w = check_route(x, wr, wl.router_dtype, wl.k)
+        y = moe.moe_expert_ffn_grouped(dev(x), dev(ids), dev(w), pool, wl.expert_bytes, wl.dtype, wl.I, wl.E)
+        moe.moe_sync_check()
+        ref = oracle.moe_ffn(x, ids, w.astype(np.float64), ex, wl.H, wl.I, wl.dtype)
+        assert normwise(y.cpu().numpy(), ref) <= TOL[wl.dtype]
+
+
+def test_cache_rejects_pageable_host_memory():
+    host = np.zeros(4 * 256, np.uint8)
+    with pytest.raises(moe.MoeError) as ei:
+        moe.ExpertCache(1, 4, 256, 2 * 256, host.ctypes.data, 0, 256)
+    assert ei.value.code == -5
