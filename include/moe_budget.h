@@ -64,6 +64,9 @@ extern "C" {
 #define MOE_BF16 1
 #define MOE_INT4G128 2
 
+/* ---- moe_route_topk flags ---- */
+#define MOE_ROUTE_RMSNORM 1 /* route on the RMS-normalised input (pre-norm of the MoE block) */
+
 /* ---- moe_expert_ffn_grouped flags ---- */
 #define MOE_ACCUMULATE 1 /* y_out += MoE output (fused residual add) instead of y_out = output */
 
@@ -107,17 +110,20 @@ MOE_API int moe_sync_check(void *stream);
 /* Router logits and softmax-renormalised top-k for T tokens.
  *   x          device fp32 [T x H], or NULL to rank `logit_bias` alone
  *   w_router   device [E x H] row-major, w_dtype MOE_F32 or MOE_BF16
- *   logit_bias device fp32 [T x E] added to W_r x, or NULL
- *   logits     device fp32 [T x E] out: z = W_r x (+ bias), fp32 accumulation
+ *   logit_bias device fp32 [T x E] added to the router output, or NULL
+ *   logits     device fp32 [T x E] out: z = W_r h (+ bias), fp32 accumulation,
+ *              where h = x, or with MOE_ROUTE_RMSNORM h = x / sqrt(mean(x^2) + 1e-6)
  *   ids        device int32 [T x k] out: the k largest z of each token ranked by
  *              (z descending, expert id ascending)
  *   weights    device fp32 [T x k] out: exp(z_j - z_0) / sum_j' exp(z_j' - z_0)
+ *   x_norm     device fp32 [T x H] out (MOE_ROUTE_RMSNORM only, may be NULL):
+ *              the normalised h, the input of the block's experts
  * Limits: 1 <= k <= min(E, MOE_MAX_TOPK), E <= MOE_MAX_EXPERTS, H % 128 == 0.
  * A token with a non-finite logit gets ids -1 and weights 0 and raises
  * MOE_ERR_NONFINITE in the device flags.  T == 0 is a no-op. */
 MOE_API int moe_route_topk(const float *x, const void *w_router, int w_dtype, int T, int H, int E, int k,
-                   const float *logit_bias, float *logits, int32_t *ids, float *weights,
-                   void *stream);
+                           const float *logit_bias, float *logits, int32_t *ids, float *weights, int flags,
+                           float *x_norm, void *stream);
 
 /* ======================================================================= */
 /* Expert FFN with weighted combine (north-star "fused SwiGLU expert FFN")   */
@@ -240,8 +246,8 @@ MOE_API int expert_cache_trace(moe_cache *c, size_t first, moe_cache_event *buf,
                        size_t *n_out);
 
 /* ======================================================================= */
-/* Decode stack driver: for each layer, route -> (lookup) -> FFN with fused  */
-/* residual x += MoE(x); attention is the identity                          */
+/* Decode stack driver: for each layer, pre-norm + route -> (lookup) -> FFN */
+/* with fused residual x += MoE(rmsnorm(x)); attention is the identity       */
 /* ======================================================================= */
 
 typedef struct moe_stack moe_stack;
@@ -260,7 +266,7 @@ MOE_API int moe_stack_create(const moe_stack_desc *desc, moe_stack **out);
 MOE_API int moe_stack_destroy(moe_stack *s);
 
 /* One decode step over every layer, in place on x (device fp32 [T x H]):
- * x <- x + MoE_l(x) for l = 0..L-1.  logit_bias is device fp32 [L x T x E]
+ * x <- x + MoE_l(rmsnorm(x)) for l = 0..L-1 (unit-gain RMS norm, eps 1e-6).  logit_bias is device fp32 [L x T x E]
  * added to each layer's router logits, or NULL.  Unless the cache was created
  * with PRELOAD, each layer copies its ids to the host (one synchronisation per
  * layer), runs the lookup, then enqueues the FFN and releases the slots.

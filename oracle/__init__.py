@@ -44,6 +44,7 @@ def lib() -> C.CDLL:
             build()
         _lib = C.CDLL(_LIB)
         P, I32, SZ, D = C.c_void_p, C.c_int, C.c_size_t, C.POINTER(C.c_double)
+        _lib.oracle_rmsnorm.argtypes = [P, I32, I32, C.c_double, P]
         _lib.oracle_router_logits.argtypes = [P, P, I32, I32, I32, I32, P]
         _lib.oracle_topk_softmax.argtypes = [P, I32, I32, I32, P, P]
         _lib.oracle_expert_forward.argtypes = [P, I32, I32, P, I32, P]
@@ -89,6 +90,20 @@ def expert_weight(blob: np.ndarray, H: int, I: int, dtype: int, which: str, r: i
     """Dequantised weight (r, c) of matrix ``which`` ('gu' or 'd') of an expert blob."""
     b = _c(blob, np.uint8)
     return float(lib().oracle_expert_weight(_p(b), dtype, H, I, 0 if which == "gu" else 1, r, c))
+
+
+RMS_EPS = 1e-6
+
+
+def rmsnorm(x: np.ndarray, eps: float = RMS_EPS) -> np.ndarray:
+    """fp64 ``x / sqrt(mean(x^2) + eps)`` per row of fp32 ``x [T x H]``."""
+    x = _c(np.atleast_2d(x), np.float32)
+    T, H = x.shape
+    h = np.empty((T, H), dtype=np.float64)
+    st = lib().oracle_rmsnorm(_p(x), T, H, eps, _p(h))
+    if st != OK:
+        raise ValueError(f"oracle_rmsnorm status {st}")
+    return h
 
 
 def router_logits(x: np.ndarray, w_router: np.ndarray, w_dtype: int) -> np.ndarray:

@@ -13,6 +13,8 @@
  *     Qwen3-class MoE of the paper's Table 2: silu(W_g x) * (W_u x), then W_d.
  *   - combine: y = sum over the k selected experts, in rank order, of weight
  *     times expert output, plus the shared expert with weight 1.
+ *   - stacking: each MoE block reads the RMS-normalised residual stream
+ *     (unit gain) and adds its output back: x <- x + MoE(rmsnorm(x)).
  *   - residency (paper sec. 4 and Fig. 1: a host tier holds every sub-module,
  *     the accelerator holds slots, a lookup table maps sub-module id to slot,
  *     selective load brings sub-modules in and evict makes room; sec. 4 names
@@ -121,6 +123,26 @@ size_t oracle_expert_bytes(int H, int I, int dtype)
     if (dtype == OR_INT4G128)
         return (size_t)3 * H * I / 2 + (size_t)3 * H * I / 128 * 2;
     return (size_t)3 * H * I * (dtype == OR_F32 ? 4 : 2);
+}
+
+/* ---------------------------------------------------------- pre-norm --- */
+
+/* h[t,:] = x[t,:] / sqrt(mean_i x[t,i]^2 + eps): the RMS normalisation a
+ * pre-norm decoder (such as the Qwen3-class model of the paper's Table 2)
+ * applies to the input of each MoE block, with unit gain. */
+int oracle_rmsnorm(const float *x, int T, int H, double eps, double *h)
+{
+    if (T < 0 || H <= 0)
+        return OR_ERR_ARG;
+    for (int t = 0; t < T; t++) {
+        double ss = 0.0;
+        for (int i = 0; i < H; i++)
+            ss += (double)x[(size_t)t * H + i] * (double)x[(size_t)t * H + i];
+        double inv = 1.0 / sqrt(ss / H + eps);
+        for (int i = 0; i < H; i++)
+            h[(size_t)t * H + i] = (double)x[(size_t)t * H + i] * inv;
+    }
+    return OR_OK;
 }
 
 /* ------------------------------------------------------------ routing --- */

@@ -21,6 +21,7 @@ ERR_NAMES = {-1: "INVALID_ARG", -2: "RANGE", -3: "NONFINITE", -4: "BUDGET", -5: 
              -6: "HIP", -7: "COPY", -8: "NOT_RESIDENT"}
 MOE_F32, MOE_BF16, MOE_INT4G128 = 0, 1, 2
 MOE_ACCUMULATE = 1
+MOE_ROUTE_RMSNORM = 1
 MOE_POLICY_LRU = 0
 MOE_CACHE_PRELOAD, MOE_CACHE_HOST_SIM = 1, 2
 EVENT_HIT, EVENT_MISS, EVENT_PREFETCH = 0, 1, 2
@@ -69,7 +70,7 @@ def lib() -> C.CDLL:
         P, I, SZ, U64P = C.c_void_p, C.c_int, C.c_size_t, C.POINTER(C.c_uint64)
         sig = {
             "moe_init": [I], "moe_last_error": [], "moe_sync_check": [P],
-            "moe_route_topk": [P, P, I, I, I, I, I, P, P, P, P, P],
+            "moe_route_topk": [P, P, I, I, I, I, I, P, P, P, P, I, P, P],
             "moe_ffn_workspace_bytes": [I, I, I],
             "moe_expert_ffn_grouped": [P, I, I, I, I, I, P, P, P, P, SZ, I, P, P, P, SZ, I, P],
             "moe_combine": [P, P, P, I, I, I, P, I, P],
@@ -139,8 +140,11 @@ def moe_sync_check(stream=None) -> None:
 
 
 def moe_route_topk(x, w_router, w_dtype: int, k: int, *, E: int | None = None, logit_bias=None,
-                   logits=None, ids=None, weights=None, stream=None):
-    """Router logits and top-k; returns (logits [T x E], ids [T x k], weights [T x k])."""
+                   logits=None, ids=None, weights=None, rmsnorm: bool = False, x_norm=None, stream=None):
+    """Router logits and top-k; returns (logits [T x E], ids [T x k], weights [T x k]).
+
+    With ``rmsnorm`` the router reads x / rms(x) and, if ``x_norm`` is given,
+    stores that normalised input there."""
     import torch
     src = x if x is not None else logit_bias
     T = src.shape[0]
@@ -153,7 +157,8 @@ def moe_route_topk(x, w_router, w_dtype: int, k: int, *, E: int | None = None, l
     _check(lib().moe_route_topk(_dev(x, "x", torch.float32), _dev(w_router, "w_router"), w_dtype, T, H, E, k,
                                 _dev(logit_bias, "logit_bias", torch.float32),
                                 _dev(logits, "logits", torch.float32), _dev(ids, "ids", torch.int32),
-                                _dev(weights, "weights", torch.float32), _stream(stream)), "moe_route_topk")
+                                _dev(weights, "weights", torch.float32), MOE_ROUTE_RMSNORM if rmsnorm else 0,
+                                _dev(x_norm, "x_norm", torch.float32), _stream(stream)), "moe_route_topk")
     return logits, ids, weights
 
 

@@ -99,8 +99,8 @@ int moe_sync_check(void *stream) {
 }
 
 int moe_route_topk(const float *x, const void *w_router, int w_dtype, int T, int H, int E, int k,
-                   const float *logit_bias, float *logits, int32_t *ids, float *weights,
-                   void *stream) {
+                   const float *logit_bias, float *logits, int32_t *ids, float *weights, int flags,
+                   float *x_norm, void *stream) {
     if (T < 0 || E < 1 || E > MOE_MAX_EXPERTS || k < 1 || k > E || k > MOE_MAX_TOPK)
         return fail(MOE_ERR_INVALID_ARG, "route: need T >= 0, 1 <= k <= min(E, %d), E <= %d (T=%d E=%d k=%d)",
                     MOE_MAX_TOPK, MOE_MAX_EXPERTS, T, E, k);
@@ -111,17 +111,19 @@ int moe_route_topk(const float *x, const void *w_router, int w_dtype, int T, int
         if (!moe::router_shape_supported(H, w_dtype))
             return fail(MOE_ERR_INVALID_ARG, "route: unsupported H=%d / dtype %d (H %% 128 == 0, f32 or bf16)",
                         H, w_dtype);
-        if (!aligned16(x) || !aligned16(w_router))
-            return fail(MOE_ERR_INVALID_ARG, "route: x and w_router must be 16-byte aligned");
+        if (!aligned16(x) || !aligned16(w_router) || (x_norm && !aligned16(x_norm)))
+            return fail(MOE_ERR_INVALID_ARG, "route: x, w_router and x_norm must be 16-byte aligned");
     } else if (!logit_bias) {
         return fail(MOE_ERR_INVALID_ARG, "route: x and logit_bias are both NULL");
     }
-    int *flags = moe::device_error_flags();
-    if (!flags) return fail(MOE_ERR_HIP, "device error flags unavailable");
+    int *eflags = moe::device_error_flags();
+    if (!eflags) return fail(MOE_ERR_HIP, "device error flags unavailable");
     auto s = static_cast<hipStream_t>(stream);
-    hipError_t e = moe::launch_router_logits(x, w_router, w_dtype, T, H, E, logit_bias, logits, s);
+    const bool norm = flags & MOE_ROUTE_RMSNORM;
+    hipError_t e = moe::launch_router_logits(x, w_router, w_dtype, T, H, E, logit_bias, logits, norm,
+                                             norm ? x_norm : nullptr, s);
     if (e != hipSuccess) return fail_hip(e, "route: router logits launch");
-    return finish_launch(moe::launch_topk_softmax(logits, T, E, k, ids, weights, flags, s), "route: top-k launch");
+    return finish_launch(moe::launch_topk_softmax(logits, T, E, k, ids, weights, eflags, s), "route: top-k launch");
 }
 
 size_t moe_ffn_workspace_bytes(int T, int k, int I) {

@@ -26,7 +26,7 @@ FfnWorkspace ffn_workspace(void *base, int T, int k, int I);
 
 // Kernel launchers (all asynchronous on `s`).  Shapes are validated by the caller.
 hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int T, int H, int E,
-                                const float *bias, float *logits, hipStream_t s);
+                                const float *bias, float *logits, bool norm, float *h_out, hipStream_t s);
 hipError_t launch_topk_softmax(const float *logits, int T, int E, int k, int32_t *ids, float *weights,
                                int *err_flags, hipStream_t s);
 // Optional events recorded around the two expert kernels (for per-kernel timing).

@@ -17,6 +17,7 @@ constexpr int kWave = 64;
 constexpr int kBlock = 256;  // 4 waves per workgroup
 constexpr int kDownRows = 2; // output rows per wave in the down projection
 constexpr int kDownSlots = 4; // 16-byte chunks per lane per pass of the down projection
+constexpr float kRmsEps = 1e-6f;
 
 enum : int { F32 = MOE_F32, BF16 = MOE_BF16, INT4 = MOE_INT4G128 };
 
@@ -82,35 +83,69 @@ __device__ __forceinline__ float chunk_dot(uint4 w, const float *xv) {
 }
 
 // --------------------------------------------------------------- router ---
-// z[t, e] = W_r[e, :] . x[t, :] (+ bias[t, e]); one wave per (token, expert row).
-template <int DT, int NCH>
+// z[t, e] = W_r[e, :] . h_t (+ bias[t, e]) with h_t = x_t, or with NORM
+// h_t = x_t / sqrt(mean(x_t^2) + eps); one wave per (token, expert row).  Each
+// wave holds the whole token row (one 16-byte column chunk per lane and
+// pass), so it forms the norm itself; wave 0 of the token's first block
+// stores h_t for the expert FFN.
+template <int DT, int NCH, bool NORM>
 __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__restrict__ x,
                                                                const uint8_t *__restrict__ w, int H,
                                                                int E, const float *__restrict__ bias,
-                                                               float *__restrict__ logits) {
+                                                               float *__restrict__ logits,
+                                                               float *__restrict__ h_out) {
     constexpr int EPC = Fmt<DT>::EPC;
     const int lane = threadIdx.x & (kWave - 1);
-    const int e = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
+    const int wave = threadIdx.x / kWave;
+    const int e = blockIdx.x * (kBlock / kWave) + wave;
     const int t = blockIdx.y;
-    if (e >= E) return;
-    const uint8_t *row = w + size_t(e) * row_bytes_of(DT, H);
     const float *xt = x + size_t(t) * H;
+    const uint8_t *row = w + size_t(e < E ? e : 0) * row_bytes_of(DT, H);
     uint4 wv[NCH];
+    float xv[NCH][EPC];
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         const int col0 = (c * kWave + lane) * EPC;
-        wv[c] = col0 < H ? load16(row + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
+        wv[c] = (col0 < H && e < E) ? load16(row + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
     }
-    float acc = 0.f;
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         const int col0 = (c * kWave + lane) * EPC;
         if (col0 < H) {
-            float xv[EPC];
-            load_x<DT>(xt, col0, xv);
-            acc += chunk_dot<DT>(wv[c], xv);
+            load_x<DT>(xt, col0, xv[c]);
+        } else {
+#pragma unroll
+            for (int q = 0; q < EPC; ++q) xv[c][q] = 0.f;
         }
     }
+    if constexpr (NORM) {
+        float ss = 0.f;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+#pragma unroll
+            for (int q = 0; q < EPC; ++q) ss = fmaf(xv[c][q], xv[c][q], ss);
+        const float inv = rsqrtf(wave_sum(ss) / float(H) + kRmsEps);
+#pragma unroll
+        for (int c = 0; c < NCH; ++c)
+#pragma unroll
+            for (int q = 0; q < EPC; ++q) xv[c][q] *= inv;
+        if (h_out && blockIdx.x == 0 && wave == 0) {
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                const int col0 = (c * kWave + lane) * EPC;
+                if (col0 < H) {
+                    float4 *o = reinterpret_cast<float4 *>(h_out + size_t(t) * H + col0);
+#pragma unroll
+                    for (int q = 0; q < EPC / 4; ++q)
+                        o[q] = make_float4(xv[c][4 * q], xv[c][4 * q + 1], xv[c][4 * q + 2], xv[c][4 * q + 3]);
+                }
+            }
+        }
+    }
+    if (e >= E) return;
+    float acc = 0.f;
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) acc += chunk_dot<DT>(wv[c], xv[c]);
     acc = wave_sum(acc);
     if (lane == 0) logits[size_t(t) * E + e] = acc + (bias ? bias[size_t(t) * E + e] : 0.f);
 }
@@ -541,7 +576,7 @@ bool router_shape_supported(int H, int dtype) {
 }
 
 hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int T, int H, int E,
-                                const float *bias, float *logits, hipStream_t s) {
+                                const float *bias, float *logits, bool norm, float *h_out, hipStream_t s) {
     if (T == 0) return hipSuccess;
     if (!x) {
         if (bias == logits) return hipSuccess;
@@ -552,7 +587,10 @@ hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int 
     const int nch = chunks_per_row(H, w_dtype);
 #define ROUTER_CASE(DT, N)                                                                          \
     if (w_dtype == DT && nch == N) {                                                                \
-        router_logits_kernel<DT, N><<<grid, kBlock, 0, s>>>(x, wp, H, E, bias, logits);             \
+        if (norm)                                                                                   \
+            router_logits_kernel<DT, N, true><<<grid, kBlock, 0, s>>>(x, wp, H, E, bias, logits, h_out); \
+        else                                                                                        \
+            router_logits_kernel<DT, N, false><<<grid, kBlock, 0, s>>>(x, wp, H, E, bias, logits, nullptr); \
         return hipGetLastError();                                                                   \
     }
     ROUTER_CASE(F32, 1) ROUTER_CASE(F32, 2) ROUTER_CASE(F32, 4) ROUTER_CASE(F32, 8)

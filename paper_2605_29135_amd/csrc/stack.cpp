@@ -1,5 +1,5 @@
-// stack.cpp -- decode step over a stack of MoE layers: x <- x + MoE_l(x), l = 0..L-1
-// (attention is the identity).  Under a budget each layer brings its ids to
+// stack.cpp -- decode step over a stack of MoE layers: x <- x + MoE_l(rmsnorm(x)),
+// l = 0..L-1 (attention is the identity; the pre-norm is fused into the router).  Under a budget each layer brings its ids to
 // the host, runs the slot lookup, then enqueues the expert FFN and releases
 // the slots; with every expert resident the whole step stays on the device.
 #include <string.h>
@@ -83,6 +83,7 @@ struct moe_stack {
     bool budgeted = false;
     size_t expert_bytes = 0;
     float *logits = nullptr;    // device [Tmax x E]
+    float *h = nullptr;         // device [Tmax x H]: RMS-normalised input of the current layer
     int32_t *ids = nullptr;     // device [Tmax x k]
     float *weights = nullptr;   // device [Tmax x k]
     int32_t *ids_host = nullptr;  // pinned [Tmax x k]
@@ -100,6 +101,7 @@ int moe_stack_destroy(moe_stack *s) {
     if (!s) return MOE_OK;
     (void)hipDeviceSynchronize();
     if (s->logits) (void)hipFree(s->logits);
+    if (s->h) (void)hipFree(s->h);
     if (s->ids) (void)hipFree(s->ids);
     if (s->weights) (void)hipFree(s->weights);
     if (s->ids_host) (void)hipHostFree(s->ids_host);
@@ -146,6 +148,7 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
         return code;
     };
     if ((e = hipMalloc(&s->logits, sizeof(float) * T * d->E)) != hipSuccess) return bail(e, "stack buffers");
+    if ((e = hipMalloc(&s->h, sizeof(float) * T * d->H)) != hipSuccess) return bail(e, "stack buffers");
     if ((e = hipMalloc(&s->ids, sizeof(int32_t) * T * d->k)) != hipSuccess) return bail(e, "stack buffers");
     if ((e = hipMalloc(&s->weights, sizeof(float) * T * d->k)) != hipSuccess) return bail(e, "stack buffers");
     if ((e = hipHostMalloc(&s->ids_host, sizeof(int32_t) * T * d->k, 0)) != hipSuccess) return bail(e, "stack buffers");
@@ -176,7 +179,8 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
         const float *bias = logit_bias ? logit_bias + size_t(l) * T * d.E : nullptr;
         hipEvent_t *rt = s->timing ? s->route_timer.next() : nullptr;
         if (rt) (void)hipEventRecord(rt[0], strm);
-        hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, bias, s->logits, strm);
+        hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, bias, s->logits,
+                                                 true, s->h, strm);
         if (e == hipSuccess) e = moe::launch_topk_softmax(s->logits, T, d.E, d.k, ids, w, eflags, strm);
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: routing");
         if (rt) (void)hipEventRecord(rt[1], strm);
@@ -193,7 +197,7 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
             fe = {ft[0], ft[1], ft[2]};
             fep = &fe;
         }
-        e = moe::launch_expert_ffn(x, T, d.H, d.I, d.E, d.k, ids, w, s->slot_table + size_t(l) * d.E, s->pool,
+        e = moe::launch_expert_ffn(s->h, T, d.H, d.I, d.E, d.k, ids, w, s->slot_table + size_t(l) * d.E, s->pool,
                                    s->expert_bytes, d.w_dtype, s->shared_w.empty() ? nullptr : s->shared_w[l], x,
                                    true, ws, eflags, strm, fep);
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: expert FFN");

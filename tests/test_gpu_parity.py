@@ -37,15 +37,21 @@ def normwise(y, ref):
     return float(np.max(np.abs(y - ref).max(axis=1) / np.maximum(np.abs(ref).max(axis=1), 1e-30)))
 
 
-def check_route(x, wr, rdtype, k, bias=None):
+def check_route(x, wr, rdtype, k, bias=None, norm=False):
     """Run moe_route_topk and check it against the oracle; returns (ids, weights) on the host."""
+    h = torch.empty(x.shape, dtype=torch.float32, device=DEV) if (norm and x is not None) else None
     logits, ids, w = moe.moe_route_topk(None if x is None else dev(x), None if wr is None else dev(wr), rdtype, k,
                                         E=(wr.shape[0] if wr is not None else bias.shape[1]),
-                                        logit_bias=None if bias is None else dev(bias))
+                                        logit_bias=None if bias is None else dev(bias), rmsnorm=norm, x_norm=h)
     moe.moe_sync_check()
     z = logits.cpu().numpy()
     if x is not None:
-        zref = oracle.router_logits(x, wr, rdtype) + (0 if bias is None else bias)
+        xin = x
+        if norm:
+            href = oracle.rmsnorm(x)
+            assert normwise(h.cpu().numpy(), href) <= 1e-6
+            xin = href.astype(np.float32)
+        zref = oracle.router_logits(xin, wr, rdtype) + (0 if bias is None else bias)
         assert normwise(z, zref) <= 1e-5
     o_ids, o_w, st = oracle.topk_softmax(z, k)
     assert st == oracle.OK
@@ -57,12 +63,13 @@ def check_route(x, wr, rdtype, k, bias=None):
 
 # ----------------------------------------------------------------- route ---
 @pytest.mark.parametrize("cfg,T", [(1, 1), (2, 1), (3, 1), (3, 4), (3, 16), (2, 37)])
-def test_route_parity_configs(cfg, T):
+@pytest.mark.parametrize("norm", [False, True])
+def test_route_parity_configs(cfg, T, norm):
     wl = synth.workload(cfg)
     wr = synth.router_weights(wl, 0)
     for step in range(3):
-        x = synth.hidden_states(wl, step, T=T)
-        check_route(x, wr, wl.router_dtype, wl.k)
+        x = synth.hidden_states(wl, step, T=T) * np.float32(1.0 + step)
+        check_route(x, wr, wl.router_dtype, wl.k, norm=norm)
 
 
 def test_route_with_mask_bias_selects_the_drawn_sets():
@@ -245,15 +252,16 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
             assert (np.sort(g_ids[l], axis=1) == sets[t, l]).all()
             assert o.lookup(t, l, g_ids[l].reshape(-1)) == oracle.OK
         if t in check_steps:
-            # oracle chain in fp64 from the same input, routed by the GPU's ids and weights
+            # oracle chain in fp64 from the same input, routed by the GPU's ids and weights:
+            # x <- x + MoE(rmsnorm(x)) per layer
             xr = x0.astype(np.float64)
             for l in range(wl.L):
                 lsrc = 0 if layers_alias else l
                 if lsrc not in host_layers:
                     host_layers[lsrc] = synth.layer_experts(wl, lsrc)
                 sh = synth.expert_blob(wl, l, None) if wl.shared else None
-                xr = xr + oracle.moe_ffn(xr.astype(np.float32), g_ids[l], g_w[l], host_layers[lsrc], wl.H, wl.I,
-                                         wl.dtype, sh)
+                hr = oracle.rmsnorm(xr.astype(np.float32)).astype(np.float32)
+                xr = xr + oracle.moe_ffn(hr, g_ids[l], g_w[l], host_layers[lsrc], wl.H, wl.I, wl.dtype, sh)
             assert normwise(x.cpu().numpy() - x0, xr - x0) <= TOL[wl.dtype]
     ev = cache.trace()
     oev = o.events()

@@ -104,6 +104,29 @@ def test_router_logits_exact_on_integers(dtype):
     assert (z == (xi @ wi.T).astype(np.float64)).all()
 
 
+def test_rmsnorm_closed_forms():
+    H = 128
+    x = np.zeros((3, H), np.float32)
+    x[0, :2] = [3.0, 4.0]          # mean square 25/128
+    x[1, :] = -2.5                 # constant row
+    x[2, 5] = 1e-3                 # tiny row: eps dominates
+    h = oracle.rmsnorm(x, eps=1e-6)
+    np.testing.assert_allclose(h[0, :2], np.array([3.0, 4.0]) / math.sqrt(25 / 128 + 1e-6), rtol=1e-15)
+    assert (h[0, 2:] == 0).all()
+    np.testing.assert_allclose(h[1], -2.5 / math.sqrt(6.25 + 1e-6), rtol=1e-15)
+    v = float(np.float32(1e-3))
+    np.testing.assert_allclose(h[2, 5], v / math.sqrt(v * v / 128 + 1e-6), rtol=1e-15)
+
+
+def test_rmsnorm_invariants():
+    rng = np.random.default_rng(5)
+    x = rng.standard_normal((6, 2048)).astype(np.float32) * 3
+    h = oracle.rmsnorm(x)
+    np.testing.assert_allclose((h ** 2).mean(axis=1), 1.0, rtol=1e-6)   # unit RMS (eps is tiny)
+    np.testing.assert_allclose(oracle.rmsnorm(x * np.float32(4.0)), h, rtol=1e-6)  # positive scale drops out
+    np.testing.assert_allclose(oracle.rmsnorm(-x), -h, rtol=1e-15)
+
+
 # ---------------------------------------------------------- expert FFN ---
 def test_golden_swiglu_expert():
     lines = _golden_lines("swiglu_expert.txt")
