@@ -275,11 +275,15 @@ MOE_API int moe_stack_destroy(moe_stack *s);
 MOE_API int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *logit_bias,
                           int32_t *ids_out, float *weights_out, void *stream);
 
-/* Mean device time (ms) and count of the kernels the stack enqueued since the
- * last call, measured with HIP events around each launch when timing is on:
- *   which 0 = router+top-k, 1 = expert gate/up + SwiGLU, 2 = expert down + combine. */
-MOE_API int moe_stack_set_timing(moe_stack *s, int on);
-MOE_API int moe_stack_kernel_time(moe_stack *s, int which, double *mean_ms, uint64_t *count);
+/* Mean device time (ms) of one launch of kernel `which` (0 = router logits and
+ * top-k, 1 = expert gate/up + SwiGLU, 2 = expert down + combine).  Each
+ * layer's launch of the last decode step is re-issued with the same
+ * arguments, in step order, captured into one HIP graph on a private stream
+ * (ordered after `stream`); the graph is replayed n times between two HIP
+ * events (multi-token steps under a budget replay only the last layer, whose
+ * slots are still current).  Outputs go to scratch buffers: the residual
+ * stream and the residency state are untouched.  Synchronous. */
+MOE_API int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *mean_ms);
 
 #ifdef __cplusplus
 }

@@ -85,8 +85,7 @@ def lib() -> C.CDLL:
             "moe_stack_create": [C.POINTER(StackDesc), C.POINTER(P)],
             "moe_stack_destroy": [P],
             "moe_stack_decode_step": [P, I, P, I, P, P, P, P],
-            "moe_stack_set_timing": [P, I],
-            "moe_stack_kernel_time": [P, I, C.POINTER(C.c_double), U64P],
+            "moe_stack_kernel_time": [P, I, I, P, C.POINTER(C.c_double)],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -306,14 +305,12 @@ class MoeStack:
                "moe_stack_decode_step")
         return x
 
-    def set_timing(self, on: bool):
-        _check(lib().moe_stack_set_timing(self._h, int(on)), "moe_stack_set_timing")
-
-    def kernel_time(self, which: int):
-        """(mean ms, count) of kernel `which` (0 route, 1 gate/up, 2 down) since the last read."""
-        ms, n = C.c_double(), C.c_uint64()
-        _check(lib().moe_stack_kernel_time(self._h, which, C.byref(ms), C.byref(n)), "moe_stack_kernel_time")
-        return ms.value, n.value
+    def kernel_time(self, which: int, n: int = 200, stream=None) -> float:
+        """Mean ms of one launch of kernel `which` (0 route, 1 gate/up, 2 down), re-launched n times
+        back to back with the last step's last-layer arguments."""
+        ms = C.c_double()
+        _check(lib().moe_stack_kernel_time(self._h, which, n, _stream(stream), C.byref(ms)), "moe_stack_kernel_time")
+        return ms.value
 
 
 class PinnedBuffer:

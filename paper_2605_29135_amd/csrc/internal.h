@@ -29,15 +29,23 @@ hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int 
                                 const float *bias, float *logits, bool norm, float *h_out, hipStream_t s);
 hipError_t launch_topk_softmax(const float *logits, int T, int E, int k, int32_t *ids, float *weights,
                                int *err_flags, hipStream_t s);
-// Optional events recorded around the two expert kernels (for per-kernel timing).
-struct FfnEvents {
-    hipEvent_t gu_begin, gu_end, dn_end;
+
+// Which expert kernels launch_expert_ffn enqueues (grouping goes with gate/up).
+enum : int { kFfnGateUp = 1, kFfnDown = 2, kFfnBoth = 3 };
+
+// Slots of a single-token step known on the host (after a residency lookup):
+// off[j] = byte offset from the pool of the expert of rank j.  n = k when
+// valid, 0 when the kernels must read ids and the slot table on the device.
+struct FfnPlan {
+    int n = 0;
+    long long off[16];
 };
+
 hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, const int32_t *ids,
                              const float *weights, const int32_t *slot_of, const void *pool,
                              size_t expert_bytes, int dtype, const void *shared_w, float *y,
                              bool accumulate, const FfnWorkspace &ws, int *err_flags, hipStream_t s,
-                             const FfnEvents *ev = nullptr);
+                             const FfnPlan *plan = nullptr, int parts = kFfnBoth);
 hipError_t launch_combine(const float *y_partial, const float *weights, const float *y_shared, int T,
                           int k, int H, float *y, bool accumulate, hipStream_t s);
 hipError_t launch_slot_update(int32_t *table, const int32_t *index, const int32_t *value, int n,
@@ -51,8 +59,9 @@ int fail(int code, const char *fmt, ...) __attribute__((format(printf, 2, 3)));
 int fail_hip(hipError_t e, const char *what);
 void clear_error();
 
-// Slot stride of a cache's pool.
+// Slot stride of a cache's pool; whether it was preloaded (slot = layer * E + expert, never evicted).
 size_t cache_expert_bytes(const struct ::moe_cache *c);
+bool cache_preloaded(const struct ::moe_cache *c);
 
 // Sticky error-flag word of the current device (set up on first use).
 int *device_error_flags();

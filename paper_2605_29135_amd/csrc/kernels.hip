@@ -31,10 +31,22 @@ __host__ __device__ constexpr size_t row_bytes_of(int DT, int cols) {
     return DT == INT4 ? size_t(cols) / 2 : size_t(cols) * (DT == F32 ? 4 : 2);
 }
 
+template <int CTRL>
+__device__ __forceinline__ float dpp(float v) {
+    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+
+// Sum over the 64 lanes, returned in every lane: DPP quad swaps (xor 1, xor 2),
+// half-row and row mirrors give each 16-lane row its total; four readlanes add the rows.
 __device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-    for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off, kWave);
-    return v;
+    v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
+    v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
+    v += dpp<0x141>(v);  // row_half_mirror
+    v += dpp<0x140>(v);  // row_mirror
+    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
+           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)) +
+           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
+           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
 }
 
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t b16) { return __uint_as_float(b16 << 16); }
@@ -82,6 +94,119 @@ __device__ __forceinline__ float chunk_dot(uint4 w, const float *xv) {
     return acc;
 }
 
+// ---------------------------------------------------------------- top-k ---
+// Order-preserving 32-bit key of a finite float (-0 ranks with +0).
+__device__ __forceinline__ uint32_t order_key(float z) {
+    uint32_t u = __float_as_uint(z);
+    if (u == 0x80000000u) u = 0u;
+    return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
+struct TopkScratch {  // per wave, in LDS
+    uint32_t key[MOE_MAX_TOPK];
+    int32_t id[MOE_MAX_TOPK];
+    float z[MOE_MAX_TOPK];
+    int32_t rid[MOE_MAX_TOPK];
+    float rz[MOE_MAX_TOPK];
+};
+
+__device__ __forceinline__ void wave_lds_sync() {
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+}
+
+// Top-k of one token's E (<= 256) logits by one wave: ids ranked by (z desc, id
+// asc) and the softmax over the k selected.  A bisection over the 32 key bits
+// (ballot + popcount per bit) finds the k-th largest key; keys above it are
+// selected and ties at it are filled in ascending id; the k selected are then
+// ranked against each other.  COHERENT reads logits written by other
+// workgroups of the same launch.
+template <bool COHERENT>
+__device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wout, int *err, TopkScratch *sc) {
+    const int lane = threadIdx.x & (kWave - 1);
+    float v[4];
+    uint32_t key[4];
+    bool live[4];
+    bool bad = false;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        const int e = lane + kWave * m;
+        live[m] = e < E;
+        if constexpr (COHERENT)
+            v[m] = live[m] ? __hip_atomic_load(z + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0.f;
+        else
+            v[m] = live[m] ? z[e] : 0.f;
+        if (live[m] && !isfinite(v[m])) bad = true;
+        key[m] = order_key(v[m]);
+    }
+    if (__any(bad)) {
+        if (lane < k) {
+            ids[lane] = -1;
+            wout[lane] = 0.f;
+        }
+        if (lane == 0) atomicOr(err, kErrNonfinite);
+        return;
+    }
+    uint32_t kth = 0;
+    for (int b = 31; b >= 0; --b) {
+        const uint32_t cand = kth | (1u << b);
+        int cnt = 0;
+#pragma unroll
+        for (int m = 0; m < 4; ++m) cnt += __popcll(__ballot(live[m] && key[m] >= cand));
+        if (cnt >= k) kth = cand;
+    }
+    int above = 0;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) above += __popcll(__ballot(live[m] && key[m] > kth));
+    const int need = k - above;  // ties at the threshold to take, lowest ids first
+    const uint64_t below = __lanemask_lt();
+    int eq_seen = 0, placed = 0;
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        const bool eq = live[m] && key[m] == kth;
+        const uint64_t eqm = __ballot(eq);
+        const bool sel = (live[m] && key[m] > kth) || (eq && eq_seen + __popcll(eqm & below) < need);
+        const uint64_t selm = __ballot(sel);
+        if (sel) {
+            const int pos = placed + __popcll(selm & below);
+            sc->key[pos] = key[m];
+            sc->id[pos] = lane + kWave * m;
+            sc->z[pos] = v[m];
+        }
+        eq_seen += __popcll(eqm);
+        placed += __popcll(selm);
+    }
+    wave_lds_sync();
+    if (lane < k) {
+        const uint32_t mk = sc->key[lane];
+        const int mi = sc->id[lane];
+        int r = 0;
+        for (int j = 0; j < k; ++j) r += (sc->key[j] > mk) || (sc->key[j] == mk && sc->id[j] < mi);
+        sc->rid[r] = mi;
+        sc->rz[r] = sc->z[lane];
+    }
+    wave_lds_sync();
+    if (lane < k) {
+        const float z0 = sc->rz[0];
+        float sum = 0.f;
+        for (int j = 0; j < k; ++j) sum += expf(sc->rz[j] - z0);  // rank order
+        ids[lane] = sc->rid[lane];
+        wout[lane] = expf(sc->rz[lane] - z0) / sum;
+    }
+}
+
+// One wave per token.
+__global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__restrict__ logits, int T,
+                                                              int E, int k, int32_t *__restrict__ ids,
+                                                              float *__restrict__ wout, int *err) {
+    __shared__ TopkScratch sc[kBlock / kWave];
+    const int wave = threadIdx.x / kWave;
+    const int t = blockIdx.x * (kBlock / kWave) + wave;
+    if (t >= T) return;
+    topk_wave<false>(logits + size_t(t) * E, E, k, ids + size_t(t) * k, wout + size_t(t) * k, err, &sc[wave]);
+}
+
 // --------------------------------------------------------------- router ---
 // z[t, e] = W_r[e, :] . h_t (+ bias[t, e]) with h_t = x_t, or with NORM
 // h_t = x_t / sqrt(mean(x_t^2) + eps); one wave per (token, expert row).  Each
@@ -104,12 +229,7 @@ __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__re
     uint4 wv[NCH];
     float xv[NCH][EPC];
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) {
-        const int col0 = (c * kWave + lane) * EPC;
-        wv[c] = (col0 < H && e < E) ? load16(row + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int c = 0; c < NCH; ++c) {
+    for (int c = 0; c < NCH; ++c) {  // x first: waiting for it never waits for the weight loads
         const int col0 = (c * kWave + lane) * EPC;
         if (col0 < H) {
             load_x<DT>(xt, col0, xv[c]);
@@ -117,6 +237,11 @@ __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__re
 #pragma unroll
             for (int q = 0; q < EPC; ++q) xv[c][q] = 0.f;
         }
+    }
+#pragma unroll
+    for (int c = 0; c < NCH; ++c) {
+        const int col0 = (c * kWave + lane) * EPC;
+        wv[c] = (col0 < H && e < E) ? load16(row + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
     }
     if constexpr (NORM) {
         float ss = 0.f;
@@ -142,77 +267,12 @@ __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__re
             }
         }
     }
-    if (e >= E) return;
-    float acc = 0.f;
+    if (e < E) {
+        float acc = 0.f;
 #pragma unroll
-    for (int c = 0; c < NCH; ++c) acc += chunk_dot<DT>(wv[c], xv[c]);
-    acc = wave_sum(acc);
-    if (lane == 0) logits[size_t(t) * E + e] = acc + (bias ? bias[size_t(t) * E + e] : 0.f);
-}
-
-// ---------------------------------------------------------------- top-k ---
-// One wave per token: each lane holds up to 4 logits (E <= 256); k rounds of a
-// wave-wide arg-max ordered by (value desc, id asc), then softmax over the k.
-__global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__restrict__ logits, int T,
-                                                              int E, int k, int32_t *__restrict__ ids,
-                                                              float *__restrict__ wout, int *err) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int t = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
-    if (t >= T) return;
-    const float *z = logits + size_t(t) * E;
-    float v[4];
-    bool live[4];
-    bool bad = false;
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        const int e = lane + kWave * m;
-        live[m] = e < E;
-        v[m] = live[m] ? z[e] : 0.f;
-        if (live[m] && !isfinite(v[m])) bad = true;
-    }
-    if (__any(bad)) {
-        if (lane < k) {
-            ids[size_t(t) * k + lane] = -1;
-            wout[size_t(t) * k + lane] = 0.f;
-        }
-        if (lane == 0) atomicOr(err, kErrNonfinite);
-        return;
-    }
-    int my_id = -1;
-    float my_v = 0.f, z0 = 0.f;
-    for (int j = 0; j < k; ++j) {
-        // lane-local best; ids grow with m, so strict '>' keeps the lower id on ties
-        float bv = -INFINITY;
-        int bi = INT_MAX;
-#pragma unroll
-        for (int m = 0; m < 4; ++m)
-            if (live[m] && (bi == INT_MAX || v[m] > bv)) {
-                bv = v[m];
-                bi = lane + kWave * m;
-            }
-#pragma unroll
-        for (int off = kWave / 2; off > 0; off >>= 1) {
-            const float ov = __shfl_xor(bv, off, kWave);
-            const int oi = __shfl_xor(bi, off, kWave);
-            if (ov > bv || (ov == bv && oi < bi)) {
-                bv = ov;
-                bi = oi;
-            }
-        }
-#pragma unroll
-        for (int m = 0; m < 4; ++m)
-            if (bi == lane + kWave * m) live[m] = false;
-        if (lane == j) {
-            my_id = bi;
-            my_v = bv;
-        }
-        if (j == 0) z0 = bv;
-    }
-    const float s = lane < k ? expf(my_v - z0) : 0.f;
-    const float sum = wave_sum(s);
-    if (lane < k) {
-        ids[size_t(t) * k + lane] = my_id;
-        wout[size_t(t) * k + lane] = s / sum;
+        for (int c = 0; c < NCH; ++c) acc += chunk_dot<DT>(wv[c], xv[c]);
+        acc = wave_sum(acc);
+        if (lane == 0) logits[size_t(t) * E + e] = acc + (bias ? bias[size_t(t) * E + e] : 0.f);
     }
 }
 
@@ -300,7 +360,7 @@ __global__ __launch_bounds__(kBlock) void group_pairs_kernel(const int32_t *__re
 }
 
 // -------------------------------------------------------------- gate/up ---
-// act[p, i] = silu(W_g[i] . x_t) * (W_u[i] . x_t) for every pair p of one
+// act[p, i] = w_p * silu(W_g[i] . x_t) * (W_u[i] . x_t) for every pair p of one
 // expert group.  One wave per row pair (gate row 2i, up row 2i+1): the pair's
 // weights are loaded once into registers and applied to each token of the
 // group.  ONE_TOKEN: T == 1, groups are the k ranks (+ shared), no table.
@@ -308,7 +368,8 @@ template <int DT, int NCH, bool ONE_TOKEN>
 __global__ __launch_bounds__(kBlock) void gateup_kernel(
     const float *__restrict__ x, int T, int H, int I, int E, int k, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ slot_of, const uint8_t *__restrict__ pool, size_t expert_bytes,
-    const uint8_t *__restrict__ shared_w, int *groups, float *__restrict__ act, int *err) {
+    const uint8_t *__restrict__ shared_w, const float *__restrict__ weights, int *groups,
+    float *__restrict__ act, int *err, FfnPlan plan) {
     constexpr int EPC = Fmt<DT>::EPC;
     const int lane = threadIdx.x & (kWave - 1);
     const int g = blockIdx.y;
@@ -316,7 +377,9 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     int pstart = 0, pcount = 1, single = 0;
     const int *pairs = nullptr;
     if constexpr (ONE_TOKEN) {
-        if (g < k) {
+        if (g < k && plan.n) {
+            blob = pool + plan.off[g];  // slots known on the host: no device lookups
+        } else if (g < k) {
             const int e = ids[g];
             if (e < 0 || e >= E) {
                 if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, kErrRange);
@@ -342,6 +405,26 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     }
     const int i = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
     if (i >= I) return;
+    const int P = T * k;
+    // The first pair's activations are loaded before the weight stream: loads
+    // retire in issue order, so waiting for x never waits for the weights.
+    float xv[NCH][EPC];
+    float wp0;  // combine weight of the first pair (1 for the shared expert)
+    {
+        const int p0 = ONE_TOKEN ? single : pairs[pstart];
+        wp0 = p0 < P ? weights[p0] : 1.f;
+        const float *xt = x + size_t(p0 < P ? p0 / k : p0 - P) * H;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int col0 = (c * kWave + lane) * EPC;
+            if (col0 < H) {
+                load_x<DT>(xt, col0, xv[c]);
+            } else {
+#pragma unroll
+                for (int q = 0; q < EPC; ++q) xv[c][q] = 0.f;
+            }
+        }
+    }
     const size_t rb = row_bytes_of(DT, H);
     const uint8_t *gate = blob + size_t(2 * i) * rb;
     const uint8_t *up = gate + rb;
@@ -360,35 +443,38 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
             su[c] = in ? bf16_bits_to_float(sc[size_t(2 * i + 1) * groups_per_row + col0 / 128]) : 0.f;
         }
     }
-    const int P = T * k;
     for (int q = 0; q < pcount; ++q) {
         const int p = ONE_TOKEN ? single : pairs[pstart + q];
-        const int t = p < P ? p / k : p - P;
-        const float *xt = x + size_t(t) * H;
+        if (q > 0) {
+            const float *xt = x + size_t(p < P ? p / k : p - P) * H;
+#pragma unroll
+            for (int c = 0; c < NCH; ++c) {
+                const int col0 = (c * kWave + lane) * EPC;
+                if (col0 < H) load_x<DT>(xt, col0, xv[c]);
+            }
+        }
         float ga = 0.f, ua = 0.f;
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            const int col0 = (c * kWave + lane) * EPC;
-            if (col0 < H) {
-                float xv[EPC];
-                load_x<DT>(xt, col0, xv);
-                float dg = chunk_dot<DT>(wg[c], xv), du = chunk_dot<DT>(wu[c], xv);
-                if constexpr (DT == INT4) {
-                    dg *= sg[c];
-                    du *= su[c];
-                }
-                ga += dg;
-                ua += du;
+            float dg = chunk_dot<DT>(wg[c], xv[c]), du = chunk_dot<DT>(wu[c], xv[c]);
+            if constexpr (DT == INT4) {
+                dg *= sg[c];
+                du *= su[c];
             }
+            ga += dg;
+            ua += du;
         }
         ga = wave_sum(ga);
         ua = wave_sum(ua);
-        if (lane == 0) act[size_t(p) * I + i] = ga / (1.f + expf(-ga)) * ua;
+        // the pair's combine weight is folded in here
+        const float wp = q == 0 ? wp0 : (p < P ? weights[p] : 1.f);
+        if (lane == 0) act[size_t(p) * I + i] = wp * (ga / (1.f + expf(-ga)) * ua);
     }
 }
 
 // ------------------------------------------------------ down + combine ---
-// y[t, h] (+)= sum_j w[t,j] * (W_d^{e_tj}[h, :] . act[t*k + j]) + W_d^shared[h, :] . act[T*k + t].
+// y[t, h] (+)= sum_j W_d^{e_tj}[h, :] . act[t*k + j] + W_d^shared[h, :] . act[T*k + t], where the
+// gate/up kernel has already scaled act[t*k + j] by the combine weight w[t, j].
 // One block per (row tile, token); the token's k (+1) down rows for output h
 // form one virtual row of (k+1) * I elements that the wave streams in 16-byte
 // chunks; the combine weight is folded into the activations held in registers,
@@ -396,37 +482,30 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
 template <int DT>
 __global__ __launch_bounds__(kBlock) void down_combine_kernel(
     int T, int H, int I, int E, int k, const int32_t *__restrict__ ids,
-    const float *__restrict__ weights, const int32_t *__restrict__ slot_of,
-    const uint8_t *__restrict__ pool, size_t expert_bytes, const uint8_t *__restrict__ shared_w,
-    size_t d_off, const float *__restrict__ act, float *__restrict__ y, int accumulate) {
+    const int32_t *__restrict__ slot_of, const uint8_t *__restrict__ pool, size_t expert_bytes,
+    const uint8_t *__restrict__ shared_w, size_t d_off, const float *__restrict__ act,
+    float *__restrict__ y, int accumulate) {
     constexpr int EPC = Fmt<DT>::EPC;
-    __shared__ const uint8_t *ent_ptr[MOE_MAX_TOPK + 1];
-    __shared__ float ent_w[MOE_MAX_TOPK + 1];
+    // entry j: slot (-2 shared expert, -1 skipped) and activation row
+    __shared__ int ent_slot[MOE_MAX_TOPK + 1];
     __shared__ int ent_p[MOE_MAX_TOPK + 1];
     const int t = blockIdx.y;
     const int NE = k + (shared_w != nullptr);
     if (threadIdx.x < NE) {
         const int j = threadIdx.x;
-        const uint8_t *ptr = nullptr;
-        float wj = 0.f;
-        int p;
+        int sl = -1, p;
         if (j < k) {
             p = t * k + j;
             const int e = ids[p];
             if (e >= 0 && e < E) {
-                const int s = slot_of ? slot_of[e] : e;
-                if (s >= 0) {
-                    ptr = pool + size_t(s) * expert_bytes;
-                    wj = weights[p];
-                }
+                sl = slot_of ? slot_of[e] : e;
+                if (sl < 0) sl = -1;
             }
         } else {
             p = T * k + t;
-            ptr = shared_w;
-            wj = 1.f;
+            sl = -2;
         }
-        ent_ptr[j] = ptr;
-        ent_w[j] = wj;
+        ent_slot[j] = sl;
         ent_p[j] = p;
     }
     __syncthreads();
@@ -450,20 +529,18 @@ __global__ __launch_bounds__(kBlock) void down_combine_kernel(
         for (int s = 0; s < kDownSlots; ++s) {
             const int gch = base + s * kWave + lane;
             ok[s] = false;
-            rp[s] = nullptr;
-            sp[s] = nullptr;
+            rp[s] = pool;  // (a global pointer, so the loads below stay global loads)
+            sp[s] = reinterpret_cast<const uint16_t *>(pool);
             if (gch < total) {
                 const int j = gch / cpr, c = gch - j * cpr;
-                const uint8_t *blob = ent_ptr[j];
-                if (blob) {
+                const int sl = ent_slot[j];
+                if (sl != -1) {
+                    const uint8_t *blob = sl == -2 ? shared_w : pool + size_t(sl) * expert_bytes;
                     ok[s] = true;
                     rp[s] = blob + d_off + size_t(c) * 16;
                     if constexpr (DT == INT4)
                         sp[s] = reinterpret_cast<const uint16_t *>(blob + d_sc) + (c * EPC) / 128;
                     load_x<DT>(act + size_t(ent_p[j]) * I, c * EPC, av[s]);
-                    const float wj = ent_w[j];
-#pragma unroll
-                    for (int q = 0; q < EPC; ++q) av[s][q] *= wj;
                 }
             }
         }
@@ -491,6 +568,130 @@ __global__ __launch_bounds__(kBlock) void down_combine_kernel(
             float *o = y + size_t(t) * H + h;
             *o = accumulate ? *o + v : v;
         }
+    }
+}
+
+// The same down + combine with every chunk of a wave's output row issued at
+// once (NS 16-byte chunks per lane, NS * 64 >= (k+1) * I / elements-per-chunk).
+// The token's activations (combine weights already folded in by the gate/up
+// kernel) are contiguous rows t*k .. t*k+k-1 plus the shared row T*k + t: each
+// thread issues its staging loads first, then the weight loads go out back to
+// back without branches (an invalid chunk loads from the pool base and is
+// masked), and only then are the staged values written to LDS.
+// One output row per wave, four per block, one block per (row tile, token).
+template <int DT, int NS>
+__global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
+    int T, int H, int I, int E, int k, const int32_t *__restrict__ ids,
+    const int32_t *__restrict__ slot_of, const uint8_t *__restrict__ pool, size_t expert_bytes,
+    const uint8_t *__restrict__ shared_w, size_t d_off, const float *__restrict__ act,
+    float *__restrict__ y, int accumulate, FfnPlan plan) {
+    constexpr int EPC = Fmt<DT>::EPC;
+    // float4 staging loads per thread: (k+1) I <= NS * 64 * EPC = SM * 4 * 256
+    constexpr int SM = (NS * EPC + 15) / 16;
+    extern __shared__ float4 aw4[];  // [(k+1) x I / 4] activations of this token
+    // Entry j: byte offset of its blob from `pool` (the shared expert's too, so
+    // that every address derives from a kernel argument and stays a global
+    // load) and whether it contributes.
+    __shared__ long long ent_off[MOE_MAX_TOPK + 1];
+    __shared__ int ent_ok[MOE_MAX_TOPK + 1];
+    const int t = blockIdx.y;
+    const int NE = k + (shared_w != nullptr);
+    // 1. staging loads (independent of everything else)
+    const int n4 = NE * I / 4, routed4 = k * I / 4;
+    const float4 *src_routed = reinterpret_cast<const float4 *>(act) + size_t(t) * routed4;
+    const float4 *src_shared = reinterpret_cast<const float4 *>(act) + (size_t(T) * k + t) * (I / 4) - routed4;
+    float4 stage[SM];
+#pragma unroll
+    for (int m = 0; m < SM; ++m) {
+        const int i = threadIdx.x + m * kBlock;
+        stage[m] = i < n4 ? (i < routed4 ? src_routed[i] : src_shared[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    // 2. where the entries live
+    if (threadIdx.x < NE) {
+        const int j = threadIdx.x;
+        int ok = 0;
+        long long off = 0;
+        if (j < k) {
+            if (plan.n) {
+                ok = 1;
+                off = plan.off[j];
+            } else {
+                const int e = ids[t * k + j];
+                if (e >= 0 && e < E) {
+                    const int sl = slot_of ? slot_of[e] : e;
+                    if (sl >= 0) {
+                        ok = 1;
+                        off = (long long)sl * (long long)expert_bytes;
+                    }
+                }
+            }
+        } else {
+            ok = 1;
+            off = (long long)(shared_w - pool);
+        }
+        ent_off[j] = off;
+        ent_ok[j] = ok;
+    }
+    __syncthreads();
+    // 3. weight loads of this wave's output row
+    const int lane = threadIdx.x & (kWave - 1);
+    const int h = min(blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave), H - 1);
+    const size_t rb = row_bytes_of(DT, I);
+    const unsigned cpr = unsigned(rb / 16);  // chunks per expert row
+    const unsigned total = unsigned(NE) * cpr;
+    const size_t row_off = d_off + size_t(h) * rb;
+    const size_t sc_off = d_off + size_t(H) * rb + size_t(h) * (I / 128) * 2;  // int4: this row's scales
+    uint4 wv[NS];
+    float sv[NS];
+    bool ok[NS];
+    unsigned j = unsigned(lane) / cpr, c = unsigned(lane) - j * cpr;  // chunk lane + 64 s = entry j, column chunk c
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        const bool in = unsigned(s * kWave + lane) < total;
+        const unsigned jj = in ? j : 0u;
+        ok[s] = in && ent_ok[jj];
+        const uint8_t *blob = pool + (ok[s] ? ent_off[jj] : 0);
+        wv[s] = load16(ok[s] ? blob + row_off + size_t(c) * 16 : pool);
+        if constexpr (DT == INT4)
+            sv[s] = bf16_bits_to_float(*reinterpret_cast<const uint16_t *>(
+                ok[s] ? blob + sc_off + size_t(c * EPC / 128) * 2 : pool));
+        c += kWave;
+        while (c >= cpr) {
+            c -= cpr;
+            ++j;
+        }
+    }
+    // 4. staged activations to LDS; chunk g of the virtual row covers aw[g * EPC, +EPC)
+#pragma unroll
+    for (int m = 0; m < SM; ++m) {
+        const int i = threadIdx.x + m * kBlock;
+        if (i < n4) aw4[i] = stage[m];
+    }
+    __syncthreads();
+    float acc = 0.f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+        if (ok[s]) {
+            const int g = s * kWave + lane;
+            float av[EPC];
+#pragma unroll
+            for (int q = 0; q < EPC / 4; ++q) {
+                const float4 a4 = aw4[g * (EPC / 4) + q];
+                av[4 * q] = a4.x;
+                av[4 * q + 1] = a4.y;
+                av[4 * q + 2] = a4.z;
+                av[4 * q + 3] = a4.w;
+            }
+            float d = chunk_dot<DT>(wv[s], av);
+            if constexpr (DT == INT4) d *= sv[s];
+            acc += d;
+        }
+    }
+    const float v = wave_sum(acc);
+    const int hrow = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
+    if (lane == 0 && hrow < H) {
+        float *o = y + size_t(t) * H + hrow;
+        *o = accumulate ? *o + v : v;
     }
 }
 
@@ -531,6 +732,13 @@ int chunks_per_row(int H, int dtype) {
     for (int n : {1, 2, 4, 8})
         if (need <= n) return n;
     return -1;
+}
+
+// Launch with each argument converted to the kernel's parameter type.
+template <typename... Params, typename... Args>
+hipError_t launch(void (*kernel)(Params...), dim3 grid, dim3 block, size_t shmem, hipStream_t s, Args... args) {
+    kernel<<<grid, block, shmem, s>>>(static_cast<Params>(args)...);
+    return hipGetLastError();
 }
 
 }  // namespace
@@ -585,14 +793,11 @@ hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int 
     const dim3 grid((E + 3) / 4, T);
     const auto *wp = static_cast<const uint8_t *>(w);
     const int nch = chunks_per_row(H, w_dtype);
+    float *hp = norm ? h_out : nullptr;
 #define ROUTER_CASE(DT, N)                                                                          \
-    if (w_dtype == DT && nch == N) {                                                                \
-        if (norm)                                                                                   \
-            router_logits_kernel<DT, N, true><<<grid, kBlock, 0, s>>>(x, wp, H, E, bias, logits, h_out); \
-        else                                                                                        \
-            router_logits_kernel<DT, N, false><<<grid, kBlock, 0, s>>>(x, wp, H, E, bias, logits, nullptr); \
-        return hipGetLastError();                                                                   \
-    }
+    if (w_dtype == DT && nch == N)                                                                  \
+        return norm ? launch(router_logits_kernel<DT, N, true>, grid, kBlock, 0, s, x, wp, H, E, bias, logits, hp) \
+                    : launch(router_logits_kernel<DT, N, false>, grid, kBlock, 0, s, x, wp, H, E, bias, logits, hp);
     ROUTER_CASE(F32, 1) ROUTER_CASE(F32, 2) ROUTER_CASE(F32, 4) ROUTER_CASE(F32, 8)
     ROUTER_CASE(BF16, 1) ROUTER_CASE(BF16, 2) ROUTER_CASE(BF16, 4) ROUTER_CASE(BF16, 8)
 #undef ROUTER_CASE
@@ -610,57 +815,69 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
                              const float *weights, const int32_t *slot_of, const void *pool,
                              size_t expert_bytes, int dtype, const void *shared_w, float *y,
                              bool accumulate, const FfnWorkspace &ws, int *err_flags, hipStream_t s,
-                             const FfnEvents *ev) {
+                             const FfnPlan *plan, int parts) {
+    FfnPlan pl1;
+    if (plan && T == 1 && plan->n == k) pl1 = *plan;
     if (T == 0) return hipSuccess;
     const bool one = T == 1;
     const int has_shared = shared_w != nullptr;
     const auto *pl = static_cast<const uint8_t *>(pool);
     const auto *sw = static_cast<const uint8_t *>(shared_w);
-    if (!one) {
+    if (!one && (parts & kFfnGateUp)) {
         group_pairs_kernel<<<1, kBlock, 0, s>>>(ids, T, k, E, slot_of, has_shared, ws.groups, err_flags);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (ev) (void)hipEventRecord(ev->gu_begin, s);
     const int groups = one ? k + has_shared : (T * k < E ? T * k : E) + has_shared;
     const dim3 ggrid((I + 3) / 4, groups);
     const int nch = chunks_per_row(H, dtype);
-    bool launched = false;
+    bool launched = !(parts & kFfnGateUp);
 #define GU_CASE(DT, N)                                                                              \
     if (!launched && dtype == DT && nch == N) {                                                     \
-        if (one)                                                                                    \
-            gateup_kernel<DT, N, true><<<ggrid, kBlock, 0, s>>>(x, T, H, I, E, k, ids, slot_of, pl,  \
-                                                                expert_bytes, sw, ws.groups,        \
-                                                                ws.act, err_flags);                 \
-        else                                                                                        \
-            gateup_kernel<DT, N, false><<<ggrid, kBlock, 0, s>>>(x, T, H, I, E, k, ids, slot_of, pl, \
-                                                                 expert_bytes, sw, ws.groups,       \
-                                                                 ws.act, err_flags);                \
+        e = one ? launch(gateup_kernel<DT, N, true>, ggrid, kBlock, 0, s, x, T, H, I, E, k, ids, \
+                         slot_of, pl, expert_bytes, sw, weights, ws.groups, ws.act, err_flags, pl1) \
+                : launch(gateup_kernel<DT, N, false>, ggrid, kBlock, 0, s, x, T, H, I, E, k, ids, \
+                         slot_of, pl, expert_bytes, sw, weights, ws.groups, ws.act, err_flags, FfnPlan{}); \
         launched = true;                                                                            \
     }
+    hipError_t e = hipSuccess;
     GU_CASE(F32, 1) GU_CASE(F32, 2) GU_CASE(F32, 4) GU_CASE(F32, 8)
     GU_CASE(BF16, 1) GU_CASE(BF16, 2) GU_CASE(BF16, 4) GU_CASE(BF16, 8)
     GU_CASE(INT4, 1) GU_CASE(INT4, 2) GU_CASE(INT4, 4) GU_CASE(INT4, 8)
 #undef GU_CASE
     if (!launched) return hipErrorInvalidValue;
-    hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    if (ev) (void)hipEventRecord(ev->gu_end, s);
-    const dim3 dgrid((H + 4 * kDownRows - 1) / (4 * kDownRows), T);
+    if (!(parts & kFfnDown)) return hipSuccess;
     const size_t doff = down_offset(H, I, dtype);
     const int acc = accumulate ? 1 : 0;
+    const int NE = k + has_shared;
+    const int epc = dtype == F32 ? 4 : dtype == BF16 ? 8 : 32;
+    const int need = (NE * (I / epc) + kWave - 1) / kWave;
+    const size_t lds = sizeof(float) * size_t(NE) * I;
+    int ns = 0;
+    for (int n : {1, 2, 3, 4, 6, 8, 9, 12, 16})
+        if (!ns && need <= n) ns = n;
+    if (ns && lds <= 64 * 1024) {
+        const dim3 grid((H + 3) / 4, T);
+#define DN_CASE(DT, N)                                                                               \
+        if (dtype == DT && ns == N)                                                                  \
+            return launch(down_combine_lds_kernel<DT, N>, grid, kBlock, lds, s, T, H, I, E, k, ids, \
+                          slot_of, pl, expert_bytes, sw, doff, ws.act, y, acc, pl1);
+#define DN_ALL(N) DN_CASE(F32, N) DN_CASE(BF16, N) DN_CASE(INT4, N)
+        DN_ALL(1) DN_ALL(2) DN_ALL(3) DN_ALL(4) DN_ALL(6) DN_ALL(8) DN_ALL(9) DN_ALL(12) DN_ALL(16)
+#undef DN_ALL
+#undef DN_CASE
+        return hipErrorInvalidValue;
+    }
+    const dim3 dgrid((H + 4 * kDownRows - 1) / (4 * kDownRows), T);
     if (dtype == F32)
-        down_combine_kernel<F32><<<dgrid, kBlock, 0, s>>>(T, H, I, E, k, ids, weights, slot_of, pl,
-                                                           expert_bytes, sw, doff, ws.act, y, acc);
-    else if (dtype == BF16)
-        down_combine_kernel<BF16><<<dgrid, kBlock, 0, s>>>(T, H, I, E, k, ids, weights, slot_of, pl,
-                                                            expert_bytes, sw, doff, ws.act, y, acc);
-    else
-        down_combine_kernel<INT4><<<dgrid, kBlock, 0, s>>>(T, H, I, E, k, ids, weights, slot_of, pl,
-                                                            expert_bytes, sw, doff, ws.act, y, acc);
-    e = hipGetLastError();
-    if (ev) (void)hipEventRecord(ev->dn_end, s);
-    return e;
+        return launch(down_combine_kernel<F32>, dgrid, kBlock, 0, s, T, H, I, E, k, ids, slot_of, pl,
+                      expert_bytes, sw, doff, ws.act, y, acc);
+    if (dtype == BF16)
+        return launch(down_combine_kernel<BF16>, dgrid, kBlock, 0, s, T, H, I, E, k, ids, slot_of, pl,
+                      expert_bytes, sw, doff, ws.act, y, acc);
+    return launch(down_combine_kernel<INT4>, dgrid, kBlock, 0, s, T, H, I, E, k, ids, slot_of, pl,
+                  expert_bytes, sw, doff, ws.act, y, acc);
 }
 
 hipError_t launch_combine(const float *y_partial, const float *weights, const float *y_shared, int T,

@@ -300,6 +300,7 @@ int lookup_impl(moe_cache *c, int step, int layer, const int32_t *ids, int n, bo
 }  // namespace
 
 size_t moe::cache_expert_bytes(const moe_cache *c) { return c->d.expert_bytes; }
+bool moe::cache_preloaded(const moe_cache *c) { return c->d.flags & MOE_CACHE_PRELOAD; }
 
 extern "C" {
 

@@ -11,66 +11,15 @@
 
 namespace {
 
-// Device time of consecutive spans on one stream: each entry is N+1 events
-// (span i runs from event i to event i+1) taken from a ring; an entry's spans
-// are folded into running sums when the entry is reused or on read-out.
-template <int N>
-class SpanTimer {
-  public:
-    static constexpr int kEntries = 1024;
-    hipError_t init() {
-        for (auto &en : entries_)
-            for (auto &ev : en.ev) {
-                hipError_t e = hipEventCreate(&ev);
-                if (e != hipSuccess) return e;
-            }
-        return hipSuccess;
-    }
-    void destroy() {
-        for (auto &en : entries_)
-            for (auto &ev : en.ev)
-                if (ev) (void)hipEventDestroy(ev);
-    }
-    // Events of the next entry, or nullptr if folding its old spans failed.
-    hipEvent_t *next() {
-        Entry &en = entries_[next_];
-        next_ = (next_ + 1) % kEntries;
-        if (en.used && !fold(en)) return nullptr;
-        en.used = true;
-        return en.ev;
-    }
-    bool flush() {
-        for (auto &en : entries_)
-            if (en.used && !fold(en)) return false;
-        return true;
-    }
-    void read(int span, double *mean_ms, uint64_t *count) {
-        *mean_ms = n_[span] ? sum_ms_[span] / double(n_[span]) : 0.0;
-        *count = n_[span];
-        sum_ms_[span] = 0.0;
-        n_[span] = 0;
-    }
-
-  private:
-    struct Entry {
-        hipEvent_t ev[N + 1] = {};
-        bool used = false;
-    };
-    bool fold(Entry &en) {
-        if (hipEventSynchronize(en.ev[N]) != hipSuccess) return false;
-        for (int i = 0; i < N; ++i) {
-            float ms = 0.f;
-            if (hipEventElapsedTime(&ms, en.ev[i], en.ev[i + 1]) != hipSuccess) return false;
-            sum_ms_[i] += ms;
-            ++n_[i];
-        }
-        en.used = false;
-        return true;
-    }
-    Entry entries_[kEntries];
-    int next_ = 0;
-    double sum_ms_[N] = {};
-    uint64_t n_[N] = {};
+// Arguments of the last layer's launches, for re-launching them in isolation.
+struct LastLayer {
+    bool valid = false;
+    int T = 0, layer = 0;
+    const int32_t *ids = nullptr;
+    const float *weights = nullptr;
+    const int32_t *slot_of = nullptr;
+    const uint8_t *pool = nullptr;
+    moe::FfnPlan plan;
 };
 
 }  // namespace
@@ -87,12 +36,13 @@ struct moe_stack {
     int32_t *ids = nullptr;     // device [Tmax x k]
     float *weights = nullptr;   // device [Tmax x k]
     int32_t *ids_host = nullptr;  // pinned [Tmax x k]
+    int32_t *slots_host = nullptr; // [Tmax x k] slot of each id after the lookup
     void *ws = nullptr;
     size_t ws_bytes = 0;
     hipEvent_t ids_ready = nullptr;
-    bool timing = false;
-    SpanTimer<1> route_timer;   // router logits + top-k
-    SpanTimer<2> ffn_timer;     // span 0: gate/up + SwiGLU, span 1: down + combine
+    float *scratch_x = nullptr;  // device [Tmax x H] scratch input/output of kernel re-launches
+    float *scratch_y = nullptr;  // device [Tmax x H]
+    std::vector<LastLayer> last;  // per layer, arguments of the last decode step
 };
 
 extern "C" {
@@ -105,10 +55,11 @@ int moe_stack_destroy(moe_stack *s) {
     if (s->ids) (void)hipFree(s->ids);
     if (s->weights) (void)hipFree(s->weights);
     if (s->ids_host) (void)hipHostFree(s->ids_host);
+    delete[] s->slots_host;
     if (s->ws) (void)hipFree(s->ws);
     if (s->ids_ready) (void)hipEventDestroy(s->ids_ready);
-    s->route_timer.destroy();
-    s->ffn_timer.destroy();
+    if (s->scratch_x) (void)hipFree(s->scratch_x);
+    if (s->scratch_y) (void)hipFree(s->scratch_y);
     delete s;
     return MOE_OK;
 }
@@ -134,7 +85,9 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
     s->d.router_w = nullptr;
     s->d.shared_w = nullptr;
     expert_cache_slot_table(d->cache, &s->slot_table, &s->pool);
-    s->budgeted = cs.capacity < d->n_layers * d->E;
+    // a preloaded cache never misses: the step stays on the device; otherwise
+    // every layer looks its experts up on the host
+    s->budgeted = !moe::cache_preloaded(d->cache);
     s->expert_bytes = moe::cache_expert_bytes(d->cache);
     if (s->expert_bytes < moe::expert_blob_bytes(d->H, d->I, d->w_dtype)) {
         delete s;
@@ -152,12 +105,14 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
     if ((e = hipMalloc(&s->ids, sizeof(int32_t) * T * d->k)) != hipSuccess) return bail(e, "stack buffers");
     if ((e = hipMalloc(&s->weights, sizeof(float) * T * d->k)) != hipSuccess) return bail(e, "stack buffers");
     if ((e = hipHostMalloc(&s->ids_host, sizeof(int32_t) * T * d->k, 0)) != hipSuccess) return bail(e, "stack buffers");
+    s->slots_host = new int32_t[size_t(T) * d->k];
+    s->last.assign(d->n_layers, LastLayer{});
     s->ws_bytes = moe::ffn_workspace_bytes(T, d->k, d->I);
     if ((e = hipMalloc(&s->ws, s->ws_bytes)) != hipSuccess) return bail(e, "stack workspace");
     if ((e = hipEventCreateWithFlags(&s->ids_ready, hipEventDisableTiming)) != hipSuccess)
         return bail(e, "stack event");
-    if ((e = s->route_timer.init()) != hipSuccess || (e = s->ffn_timer.init()) != hipSuccess)
-        return bail(e, "stack timing events");
+    if ((e = hipMalloc(&s->scratch_x, sizeof(float) * T * d->H)) != hipSuccess) return bail(e, "stack buffers");
+    if ((e = hipMalloc(&s->scratch_y, sizeof(float) * T * d->H)) != hipSuccess) return bail(e, "stack buffers");
     *out = s;
     moe::clear_error();
     return MOE_OK;
@@ -177,29 +132,35 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
         int32_t *ids = ids_out ? ids_out + size_t(l) * T * d.k : s->ids;
         float *w = weights_out ? weights_out + size_t(l) * T * d.k : s->weights;
         const float *bias = logit_bias ? logit_bias + size_t(l) * T * d.E : nullptr;
-        hipEvent_t *rt = s->timing ? s->route_timer.next() : nullptr;
-        if (rt) (void)hipEventRecord(rt[0], strm);
         hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, bias, s->logits,
                                                  true, s->h, strm);
         if (e == hipSuccess) e = moe::launch_topk_softmax(s->logits, T, d.E, d.k, ids, w, eflags, strm);
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: routing");
-        if (rt) (void)hipEventRecord(rt[1], strm);
         if (s->budgeted) {
             e = hipMemcpyAsync(s->ids_host, ids, sizeof(int32_t) * T * d.k, hipMemcpyDeviceToHost, strm);
             if (e == hipSuccess) e = hipEventRecord(s->ids_ready, strm);
             if (e == hipSuccess) e = hipEventSynchronize(s->ids_ready);
             if (e != hipSuccess) return moe::fail_hip(e, "stack step: ids to host");
-            int st = expert_cache_lookup(d.cache, step, l, s->ids_host, T * d.k, nullptr, nullptr, strm);
+            int st = expert_cache_lookup(d.cache, step, l, s->ids_host, T * d.k, s->slots_host, nullptr, strm);
             if (st != MOE_OK) return st;
         }
-        moe::FfnEvents fe{}, *fep = nullptr;
-        if (hipEvent_t *ft = s->timing ? s->ffn_timer.next() : nullptr) {
-            fe = {ft[0], ft[1], ft[2]};
-            fep = &fe;
+        // Where this layer's experts live: after a lookup the host knows every
+        // slot (T == 1 passes them to the kernels directly); preloaded slots are
+        // layer * E + expert, so the layer's pool starts at slot layer * E.
+        moe::FfnPlan plan;
+        const int32_t *slot_of = s->slot_table + size_t(l) * d.E;
+        const uint8_t *pool = static_cast<const uint8_t *>(s->pool);
+        if (s->budgeted && T == 1) {
+            plan.n = d.k;
+            for (int j = 0; j < d.k; ++j) plan.off[j] = (long long)s->slots_host[j] * (long long)s->expert_bytes;
+        } else if (!s->budgeted) {
+            pool += size_t(l) * d.E * s->expert_bytes;
+            slot_of = nullptr;
         }
-        e = moe::launch_expert_ffn(s->h, T, d.H, d.I, d.E, d.k, ids, w, s->slot_table + size_t(l) * d.E, s->pool,
-                                   s->expert_bytes, d.w_dtype, s->shared_w.empty() ? nullptr : s->shared_w[l], x,
-                                   true, ws, eflags, strm, fep);
+        e = moe::launch_expert_ffn(s->h, T, d.H, d.I, d.E, d.k, ids, w, slot_of, pool, s->expert_bytes, d.w_dtype,
+                                   s->shared_w.empty() ? nullptr : s->shared_w[l], x, true, ws, eflags, strm,
+                                   plan.n ? &plan : nullptr);
+        s->last[l] = LastLayer{true, T, l, ids, w, slot_of, pool, plan};
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: expert FFN");
         if (s->budgeted) {
             int st = expert_cache_release(d.cache, strm);
@@ -210,21 +171,71 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
     return MOE_OK;
 }
 
-int moe_stack_set_timing(moe_stack *s, int on) {
-    if (!s) return moe::fail(MOE_ERR_INVALID_ARG, "stack is NULL");
-    s->timing = on != 0;
-    return MOE_OK;
-}
-
-int moe_stack_kernel_time(moe_stack *s, int which, double *mean_ms, uint64_t *count) {
-    if (!s || !mean_ms || !count || which < 0 || which > 2)
+int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *mean_ms) {
+    if (!s || !mean_ms || which < 0 || which > 2 || n < 1)
         return moe::fail(MOE_ERR_INVALID_ARG, "kernel_time: bad argument");
-    bool ok = which == 0 ? s->route_timer.flush() : s->ffn_timer.flush();
-    if (!ok) return moe::fail(MOE_ERR_HIP, "kernel_time: reading events failed");
-    if (which == 0)
-        s->route_timer.read(0, mean_ms, count);
-    else
-        s->ffn_timer.read(which - 1, mean_ms, count);
+    for (const LastLayer &ll : s->last)
+        if (!ll.valid) return moe::fail(MOE_ERR_INVALID_ARG, "kernel_time: no decode step has run yet");
+    auto strm = static_cast<hipStream_t>(stream);
+    int *eflags = moe::device_error_flags();
+    if (!eflags) return moe::fail(MOE_ERR_HIP, "device error flags unavailable");
+    const auto &d = s->d;
+    const int L = d.n_layers, T = s->last[0].T;
+    const moe::FfnWorkspace ws = moe::ffn_workspace(s->ws, T, d.k, d.I);
+    // Every layer's launch of the last step, in step order, captured into one
+    // graph on a private stream (so that host launch overhead does not starve
+    // the device) and replayed n times.  The last layer's normalised input
+    // feeds every launch; results go to scratch.
+    hipStream_t cs = nullptr;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    hipEvent_t a = nullptr, b = nullptr;
+    hipError_t e = hipMemcpyAsync(s->scratch_x, s->h, sizeof(float) * T * d.H, hipMemcpyDeviceToDevice, strm);
+    if (e == hipSuccess) e = hipEventCreate(&a);
+    if (e == hipSuccess) e = hipEventCreate(&b);
+    if (e == hipSuccess) e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+    if (e == hipSuccess) e = hipEventRecord(a, strm);
+    if (e == hipSuccess) e = hipStreamWaitEvent(cs, a, 0);
+    auto enqueue = [&](const LastLayer &ll) -> hipError_t {
+        const int l = ll.layer;
+        if (which == 0) {
+            hipError_t r = moe::launch_router_logits(s->scratch_x, s->router_w[l], d.router_dtype, T, d.H, d.E, nullptr,
+                                                     s->logits, true, s->scratch_y, cs);
+            return r == hipSuccess ? moe::launch_topk_softmax(s->logits, T, d.E, d.k, s->ids, s->weights, eflags, cs)
+                                   : r;
+        }
+        return moe::launch_expert_ffn(s->scratch_x, T, d.H, d.I, d.E, d.k, ll.ids, ll.weights, ll.slot_of, ll.pool,
+                                      s->expert_bytes, d.w_dtype, s->shared_w.empty() ? nullptr : s->shared_w[l],
+                                      s->scratch_y, false, ws, eflags, cs, ll.plan.n ? &ll.plan : nullptr,
+                                      which == 1 ? moe::kFfnGateUp : moe::kFfnDown);
+    };
+    // Multi-token steps under a budget read the device slot table, where an
+    // earlier layer's experts may have been evicted since: replay only the
+    // last layer then (T == 1 steps carry their slots with them).
+    const int l0 = (s->budgeted && T > 1) ? L - 1 : 0;
+    if (e == hipSuccess) e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+    if (e == hipSuccess) {
+        for (int l = l0; l < L && e == hipSuccess; ++l) e = enqueue(s->last[l]);
+        hipError_t e2 = hipStreamEndCapture(cs, &graph);
+        if (e == hipSuccess) e = e2;
+    }
+    if (e == hipSuccess) e = hipGraphInstantiate(&exec, graph, nullptr, nullptr, 0);
+    if (e == hipSuccess) e = hipGraphLaunch(exec, cs);  // warm
+    if (e == hipSuccess) e = hipEventRecord(a, cs);
+    for (int i = 0; i < n && e == hipSuccess; ++i) e = hipGraphLaunch(exec, cs);
+    if (e == hipSuccess) e = hipEventRecord(b, cs);
+    if (e == hipSuccess) e = hipEventSynchronize(b);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, a, b);
+    if (cs) (void)hipStreamSynchronize(cs);
+    if (exec) (void)hipGraphExecDestroy(exec);
+    if (graph) (void)hipGraphDestroy(graph);
+    if (cs) (void)hipStreamDestroy(cs);
+    if (a) (void)hipEventDestroy(a);
+    if (b) (void)hipEventDestroy(b);
+    if (e != hipSuccess) return moe::fail_hip(e, "kernel_time");
+    *mean_ms = double(ms) / (double(n) * (L - l0));
+    moe::clear_error();
     return MOE_OK;
 }
 

@@ -263,6 +263,11 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
                 hr = oracle.rmsnorm(xr.astype(np.float32)).astype(np.float32)
                 xr = xr + oracle.moe_ffn(hr, g_ids[l], g_w[l], host_layers[lsrc], wl.H, wl.I, wl.dtype, sh)
             assert normwise(x.cpu().numpy() - x0, xr - x0) <= TOL[wl.dtype]
+    n_ev = len(cache.trace())
+    for which in range(3):  # re-launch timing leaves the residency state alone
+        assert stack.kernel_time(which, 5) > 0
+    moe.moe_sync_check()
+    assert len(cache.trace()) == n_ev
     ev = cache.trace()
     oev = o.events()
     assert len(ev) == len(oev)
