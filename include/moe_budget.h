@@ -152,6 +152,29 @@ MOE_API int moe_expert_ffn_grouped(const float *x, int T, int H, int I, int E, i
                            size_t expert_bytes, int w_dtype, const void *shared_w, float *y_out,
                            void *workspace, size_t workspace_bytes, int flags, void *stream);
 
+/* Device workspace bytes moe_prefill_grouped needs. */
+MOE_API size_t moe_prefill_workspace_bytes(int T, int k, int E, int H, int I);
+
+/* Prompt evaluation (prefill; its rate is reported beside decode in the
+ * table of sec. 8.1): the routed expert FFN of the sec. 4 step, over a whole
+ * prompt chunk at once.
+ * The expert FFN of moe_expert_ffn_grouped for a prefill chunk of any T, as
+ * grouped GEMMs on the matrix cores: the T*k (token, rank) pairs are grouped by
+ * expert on the device (the shared expert takes all T tokens), each group's
+ * rows run through x W_gu^T -> SwiGLU -> W_d^T in 64-row tiles with bf16 MFMA
+ * and fp32 accumulation, and each token's outputs are summed in rank order
+ * with its weights (the moe_combine kernel).  The inputs and the SwiGLU
+ * activations are rounded to bf16 for the matrix cores, and int4 weights are
+ * dequantised to bf16 (scale * q rounded once); fp32 weights are rounded to
+ * bf16 too.  Arguments as for moe_expert_ffn_grouped; H, I multiples of 128,
+ * E <= MOE_MAX_EXPERTS; workspace >= moe_prefill_workspace_bytes(T, k, E, H, I).
+ * Pairs with an id out of range or without a slot raise the device flag and
+ * contribute nothing. */
+MOE_API int moe_prefill_grouped(const float *x, int T, int H, int I, int E, int k, const int32_t *ids,
+                                const float *weights, const int32_t *slot_of, const void *pool,
+                                size_t expert_bytes, int w_dtype, const void *shared_w, float *y_out,
+                                void *workspace, size_t workspace_bytes, int flags, void *stream);
+
 /* y_out[t,h] (+)= sum_j weights[t,j] * y_partial[t,j,h] (rank order) + y_shared[t,h].
  *   y_partial device fp32 [T x k x H]; y_shared device fp32 [T x H] or NULL;
  *   flags MOE_ACCUMULATE adds into y_out. */

@@ -74,6 +74,8 @@ def lib() -> C.CDLL:
             "moe_ffn_workspace_bytes": [I, I, I],
             "moe_expert_ffn_grouped": [P, I, I, I, I, I, P, P, P, P, SZ, I, P, P, P, SZ, I, P],
             "moe_combine": [P, P, P, I, I, I, P, I, P],
+            "moe_prefill_workspace_bytes": [I, I, I, I, I],
+            "moe_prefill_grouped": [P, I, I, I, I, I, P, P, P, P, SZ, I, P, P, P, SZ, I, P],
             "expert_cache_create": [C.POINTER(CacheDesc), C.POINTER(P)],
             "expert_cache_destroy": [P],
             "expert_cache_lookup": [P, I, I, P, I, P, P, P],
@@ -93,6 +95,7 @@ def lib() -> C.CDLL:
             fn.restype = I
         L.moe_last_error.restype = C.c_char_p
         L.moe_ffn_workspace_bytes.restype = SZ
+        L.moe_prefill_workspace_bytes.restype = SZ
         _lib = L
     return _lib
 
@@ -182,6 +185,30 @@ def moe_expert_ffn_grouped(x, ids, weights, pool, expert_bytes: int, w_dtype: in
         expert_bytes, w_dtype, _dev(shared_w, "shared_w"), _dev(y_out, "y_out", torch.float32),
         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
         MOE_ACCUMULATE if accumulate else 0, _stream(stream)), "moe_expert_ffn_grouped")
+    return y_out
+
+
+def moe_prefill_workspace_bytes(T: int, k: int, E: int, H: int, I: int) -> int:
+    return int(lib().moe_prefill_workspace_bytes(T, k, E, H, I))
+
+
+def moe_prefill_grouped(x, ids, weights, pool, expert_bytes: int, w_dtype: int, I: int, E: int, *,
+                        slot_of=None, shared_w=None, y_out=None, workspace=None, accumulate: bool = False,
+                        stream=None):
+    """Prefill-chunk expert FFN (grouped bf16 MFMA GEMMs); returns y_out [T x H]."""
+    import torch
+    T, H = x.shape
+    k = ids.shape[1]
+    y_out = torch.empty((T, H), dtype=torch.float32, device=x.device) if y_out is None else y_out
+    nws = moe_prefill_workspace_bytes(T, k, E, H, I)
+    if workspace is None:
+        workspace = torch.empty(max(nws, 256), dtype=torch.uint8, device=x.device)
+    _check(lib().moe_prefill_grouped(
+        _dev(x, "x", torch.float32), T, H, I, E, k, _dev(ids, "ids", torch.int32),
+        _dev(weights, "weights", torch.float32), _dev(slot_of, "slot_of", torch.int32), _dev(pool, "pool"),
+        expert_bytes, w_dtype, _dev(shared_w, "shared_w"), _dev(y_out, "y_out", torch.float32),
+        _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
+        MOE_ACCUMULATE if accumulate else 0, _stream(stream)), "moe_prefill_grouped")
     return y_out
 
 

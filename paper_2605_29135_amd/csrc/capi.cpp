@@ -162,6 +162,41 @@ int moe_expert_ffn_grouped(const float *x, int T, int H, int I, int E, int k, co
                          "ffn launch");
 }
 
+size_t moe_prefill_workspace_bytes(int T, int k, int E, int H, int I) {
+    if (T < 0 || k < 1 || E < 1 || H < 1 || I < 1) return 0;
+    return moe::prefill_workspace_bytes(T, k, E, H, I);
+}
+
+int moe_prefill_grouped(const float *x, int T, int H, int I, int E, int k, const int32_t *ids, const float *weights,
+                        const int32_t *slot_of, const void *pool, size_t expert_bytes, int w_dtype,
+                        const void *shared_w, float *y_out, void *workspace, size_t workspace_bytes, int flags,
+                        void *stream) {
+    if (T < 0 || k < 1 || k > MOE_MAX_TOPK || E < 1 || E > MOE_MAX_EXPERTS || k > E)
+        return fail(MOE_ERR_INVALID_ARG, "prefill: need T >= 0, 1 <= k <= min(E, %d), E <= %d (T=%d E=%d k=%d)",
+                    MOE_MAX_TOPK, MOE_MAX_EXPERTS, T, E, k);
+    if (!moe::ffn_shape_supported(H, I, w_dtype))
+        return fail(MOE_ERR_INVALID_ARG, "prefill: unsupported H=%d I=%d dtype=%d", H, I, w_dtype);
+    if (expert_bytes < moe::expert_blob_bytes(H, I, w_dtype) || expert_bytes % 256)
+        return fail(MOE_ERR_INVALID_ARG, "prefill: expert_bytes %zu must be >= %zu and a multiple of 256", expert_bytes,
+                    moe::expert_blob_bytes(H, I, w_dtype));
+    if (T == 0) return MOE_OK;
+    if (size_t(T) * k > size_t(INT32_MAX) / 2) return fail(MOE_ERR_INVALID_ARG, "prefill: T*k too large");
+    if (!x || !ids || !weights || !pool || !y_out || !workspace)
+        return fail(MOE_ERR_INVALID_ARG, "prefill: NULL pointer argument");
+    if (!aligned16(x) || !aligned16(pool) || (shared_w && !aligned16(shared_w)) || !aligned16(workspace))
+        return fail(MOE_ERR_INVALID_ARG, "prefill: x, pool, shared_w and workspace must be 16-byte aligned");
+    if (workspace_bytes < moe::prefill_workspace_bytes(T, k, E, H, I))
+        return fail(MOE_ERR_INVALID_ARG, "prefill: workspace of %zu bytes, need %zu", workspace_bytes,
+                    moe::prefill_workspace_bytes(T, k, E, H, I));
+    int *eflags = moe::device_error_flags();
+    if (!eflags) return fail(MOE_ERR_HIP, "device error flags unavailable");
+    const moe::PrefillWorkspace ws = moe::prefill_workspace(workspace, T, k, E, H, I);
+    return finish_launch(moe::launch_prefill_ffn(x, T, H, I, E, k, ids, weights, slot_of, pool, expert_bytes, w_dtype,
+                                                 shared_w, y_out, flags & MOE_ACCUMULATE, ws, eflags,
+                                                 static_cast<hipStream_t>(stream)),
+                         "prefill launch");
+}
+
 int moe_combine(const float *y_partial, const float *weights, const float *y_shared, int T, int k,
                 int H, float *y_out, int flags, void *stream) {
     if (T < 0 || k < 0 || H < 0) return fail(MOE_ERR_INVALID_ARG, "combine: negative size");

@@ -51,6 +51,25 @@ hipError_t launch_combine(const float *y_partial, const float *weights, const fl
 hipError_t launch_slot_update(int32_t *table, const int32_t *index, const int32_t *value, int n,
                               hipStream_t s);
 
+// Prefill (any T): pairs grouped by expert, grouped bf16 MFMA GEMMs, rank-order combine.
+struct PrefillWorkspace {
+    int *hdr;      // [0] = tiles
+    int *g_slot;   // [E + 1] slot of each group (-2 = shared expert)
+    int *g_off;    // [E + 2] start of each group in `sorted`
+    int *tile_g;   // [max tiles] group of each 64-row tile
+    int *tile_r0;  // [max tiles] first row of each tile within its group
+    int *sorted;   // [T*k + T] pair ids grouped by expert
+    float *act;    // [(T*k + T) x I] SwiGLU activations per pair
+    float *y_part; // [T*k x H] expert outputs per routed pair
+    float *y_shared; // [T x H] shared expert outputs
+};
+size_t prefill_workspace_bytes(int T, int k, int E, int H, int I);
+PrefillWorkspace prefill_workspace(void *base, int T, int k, int E, int H, int I);
+hipError_t launch_prefill_ffn(const float *x, int T, int H, int I, int E, int k, const int32_t *ids,
+                              const float *weights, const int32_t *slot_of, const void *pool, size_t expert_bytes,
+                              int dtype, const void *shared_w, float *y, bool accumulate, const PrefillWorkspace &ws,
+                              int *err_flags, hipStream_t s);
+
 bool ffn_shape_supported(int H, int I, int dtype);
 bool router_shape_supported(int H, int dtype);
 

@@ -8,91 +8,18 @@
 #include <math.h>
 
 #include "internal.h"
+#include "device_common.h"
 #include "../../include/moe_budget.h"
 
 namespace moe {
 namespace {
 
-constexpr int kWave = 64;
-constexpr int kBlock = 256;  // 4 waves per workgroup
+using namespace dev;
+
+
 constexpr int kDownRows = 2; // output rows per wave in the down projection
 constexpr int kDownSlots = 4; // 16-byte chunks per lane per pass of the down projection
 constexpr float kRmsEps = 1e-6f;
-
-enum : int { F32 = MOE_F32, BF16 = MOE_BF16, INT4 = MOE_INT4G128 };
-
-// Elements held by one 16-byte chunk, and bytes per element of the dense types.
-template <int DT> struct Fmt;
-template <> struct Fmt<F32> { static constexpr int EPC = 4; };
-template <> struct Fmt<BF16> { static constexpr int EPC = 8; };
-template <> struct Fmt<INT4> { static constexpr int EPC = 32; };
-
-__host__ __device__ constexpr size_t row_bytes_of(int DT, int cols) {
-    return DT == INT4 ? size_t(cols) / 2 : size_t(cols) * (DT == F32 ? 4 : 2);
-}
-
-template <int CTRL>
-__device__ __forceinline__ float dpp(float v) {
-    return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
-}
-
-// Sum over the 64 lanes, returned in every lane: DPP quad swaps (xor 1, xor 2),
-// half-row and row mirrors give each 16-lane row its total; four readlanes add the rows.
-__device__ __forceinline__ float wave_sum(float v) {
-    v += dpp<0xB1>(v);   // quad_perm [1,0,3,2]
-    v += dpp<0x4E>(v);   // quad_perm [2,3,0,1]
-    v += dpp<0x141>(v);  // row_half_mirror
-    v += dpp<0x140>(v);  // row_mirror
-    return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 0)) +
-           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 16)) +
-           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 32)) +
-           __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
-}
-
-__device__ __forceinline__ float bf16_bits_to_float(uint32_t b16) { return __uint_as_float(b16 << 16); }
-
-__device__ __forceinline__ uint4 load16(const uint8_t *p) { return *reinterpret_cast<const uint4 *>(p); }
-
-// EPC consecutive fp32 values of x starting at col0 (16-byte aligned).
-template <int DT>
-__device__ __forceinline__ void load_x(const float *__restrict__ x, int col0, float *xv) {
-    const float4 *p = reinterpret_cast<const float4 *>(x + col0);
-#pragma unroll
-    for (int i = 0; i < Fmt<DT>::EPC / 4; ++i) {
-        float4 v = p[i];
-        xv[4 * i + 0] = v.x;
-        xv[4 * i + 1] = v.y;
-        xv[4 * i + 2] = v.z;
-        xv[4 * i + 3] = v.w;
-    }
-}
-
-// Dot product of one 16-byte weight chunk with EPC fp32 values.  int4 returns
-// the unscaled sum of q * x (the caller applies the group scale).
-template <int DT>
-__device__ __forceinline__ float chunk_dot(uint4 w, const float *xv) {
-    const uint32_t d[4] = {w.x, w.y, w.z, w.w};
-    float acc = 0.f;
-    if constexpr (DT == F32) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) acc = fmaf(__uint_as_float(d[i]), xv[i], acc);
-    } else if constexpr (DT == BF16) {
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            acc = fmaf(__uint_as_float(d[i] << 16), xv[2 * i], acc);
-            acc = fmaf(__uint_as_float(d[i] & 0xffff0000u), xv[2 * i + 1], acc);
-        }
-    } else {
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                int q = __builtin_amdgcn_sbfe(d[i], 4 * e, 4);  // signed nibble e, low nibble first
-                acc = fmaf(float(q), xv[8 * i + e], acc);
-            }
-    }
-    return acc;
-}
 
 // ---------------------------------------------------------------- top-k ---
 // Order-preserving 32-bit key of a finite float (-0 ranks with +0).

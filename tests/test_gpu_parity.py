@@ -320,3 +320,89 @@ def test_cache_rejects_pageable_host_memory():
     with pytest.raises(moe.MoeError) as ei:
         moe.ExpertCache(1, 4, 256, 2 * 256, host.ctypes.data, 0, 256)
     assert ei.value.code == -5
+
+
+# --------------------------------------------------------------- prefill ---
+# The grouped MFMA path rounds the token rows and the SwiGLU activations to bf16
+# for the matrix cores (int4 weights are dequantised to bf16): per product the
+# relative rounding is <= 2**-8, which over H ~ 2e3 random-sign terms stays far
+# inside the bf16 / int4 tolerances below.
+PREFILL_TOL = {synth.BF16: 1e-2, synth.INT4G128: 3e-2}
+
+
+def run_prefill(wl, x, ids, w, ex, sh, slot_perm=None):
+    E, eb = ex.shape
+    if slot_perm is not None:
+        pool_np = np.empty_like(ex)
+        pool_np[slot_perm] = ex
+        slot_of = dev(slot_perm.astype(np.int32))
+    else:
+        pool_np, slot_of = ex, None
+    y = moe.moe_prefill_grouped(dev(x), dev(ids), dev(w), dev(pool_np.reshape(-1)), eb, wl.dtype, wl.I, wl.E,
+                                slot_of=slot_of, shared_w=None if sh is None else dev(sh))
+    moe.moe_sync_check()
+    return y.cpu().numpy()
+
+
+@pytest.mark.parametrize("dtype", [synth.BF16, synth.INT4G128])
+@pytest.mark.parametrize("shared", [False, True])
+def test_prefill_parity_small_ragged(dtype, shared):
+    H = 2048 if dtype == synth.INT4G128 else 256
+    wl = synth.Workload("prefill-small", H=H, E=16, k=4, I=256, dtype=dtype, router_dtype=synth.F32, shared=shared,
+                        cfg_id=80 + dtype)
+    ex, sh = _experts(wl)
+    rng = np.random.default_rng(7 + dtype)
+    for T in (1, 37, 130):
+        x = rng.standard_normal((T, wl.H)).astype(np.float32)
+        z = rng.standard_normal((T, wl.E)).astype(np.float32)
+        z[:, 3] += 2.0  # one popular expert: its group spans several 64-row tiles
+        ids, w, _ = oracle.topk_softmax(z, wl.k)
+        w = w.astype(np.float32)
+        y = run_prefill(wl, x, ids, w, ex, sh, slot_perm=rng.permutation(wl.E))
+        ref = oracle.moe_ffn(x, ids, w.astype(np.float64), ex, wl.H, wl.I, wl.dtype, sh)
+        assert normwise(y, ref) <= PREFILL_TOL[dtype]
+
+
+def test_prefill_config5_chunk():
+    """Config 5's 2048-token chunk (E 256, top-8, int4-g128, shared expert) routed by its router."""
+    wl = synth.workload(5, L=1)
+    ex, sh = _experts(wl)
+    wr = synth.router_weights(wl, 0)
+    x = synth.prefill_states(wl)
+    _, ids_d, w_d = moe.moe_route_topk(dev(x), dev(wr), wl.router_dtype, wl.k, rmsnorm=False)
+    ids, w = ids_d.cpu().numpy(), w_d.cpu().numpy()
+    counts = np.bincount(ids.reshape(-1), minlength=wl.E)
+    assert counts.max() > 64  # some groups span more than one tile
+    y = run_prefill(wl, x, ids, w, ex, sh)
+    # every token against the decode kernel (fp32 activations), 16 tokens per call
+    pool = dev(ex.reshape(-1))
+    ws = torch.empty(moe.moe_ffn_workspace_bytes(16, wl.k, wl.I), dtype=torch.uint8, device=DEV)
+    y_dec = np.empty_like(y)
+    shd = dev(sh)
+    for t0 in range(0, wl.prefill, 16):
+        yd = moe.moe_expert_ffn_grouped(dev(x[t0:t0 + 16]), ids_d[t0:t0 + 16].contiguous(),
+                                        w_d[t0:t0 + 16].contiguous(), pool, wl.expert_bytes, wl.dtype, wl.I, wl.E,
+                                        shared_w=shd, workspace=ws)
+        y_dec[t0:t0 + 16] = yd.cpu().numpy()
+    moe.moe_sync_check()
+    assert normwise(y, y_dec) <= PREFILL_TOL[wl.dtype]
+    # sampled tokens against the oracle
+    sample = np.random.default_rng(0).choice(wl.prefill, 12, replace=False)
+    ref = oracle.moe_ffn(x[sample], ids[sample], w[sample].astype(np.float64), ex, wl.H, wl.I, wl.dtype, sh)
+    assert normwise(y[sample], ref) <= PREFILL_TOL[wl.dtype]
+
+
+def test_prefill_invalid_ids_contribute_nothing():
+    wl = synth.Workload("prefill-bad", H=256, E=8, k=2, I=128, dtype=synth.BF16, cfg_id=96)
+    ex, _ = _experts(wl)
+    x = np.random.default_rng(2).standard_normal((3, 256)).astype(np.float32)
+    ids = np.array([[3, 9], [1, 2], [5, -1]], np.int32)
+    w = np.full((3, 2), 0.5, np.float32)
+    y = moe.moe_prefill_grouped(dev(x), dev(ids), dev(w), dev(ex.reshape(-1)), wl.expert_bytes, wl.dtype, wl.I, wl.E)
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_sync_check()
+    assert ei.value.code == -2
+    ok_ids = np.array([[3], [1], [5]], np.int32)
+    ref = oracle.moe_ffn(x, ok_ids, np.full((3, 1), 0.5), ex, wl.H, wl.I, wl.dtype)
+    ref[1] += 0.5 * oracle.expert_forward(x[1], ex[2], wl.H, wl.I, wl.dtype)
+    assert normwise(y.cpu().numpy(), ref) <= PREFILL_TOL[wl.dtype]
