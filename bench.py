@@ -68,6 +68,78 @@ def pcie_ceiling_gbps(torch, moe, chunk: int, total: int) -> float:
     return best
 
 
+def hbm_ceiling(torch, moe, launch_bytes: int, n_launch: int = 40, stream_bytes: int = 4 << 30):
+    """HBM read rate of the library's streaming probe (the expert kernels' 16-byte nontemporal loads):
+    one pass over `stream_bytes`, and `n_launch` launches of `launch_bytes` each over distinct memory
+    (so the 256 MB last-level cache cannot serve repeats), replayed from a graph so that host launch
+    cost is out of the picture.  Also runs one 256 MiB device copy: the known-size kernels the HBM
+    byte counters are calibrated against."""
+    launch_bytes = (launch_bytes // 16) * 16
+    total = max(stream_bytes, launch_bytes * n_launch)
+    buf = torch.zeros(total, dtype=torch.uint8, device="cuda")
+    sink = torch.zeros(1, dtype=torch.float32, device="cuda")
+    cp_src = torch.ones(256 << 20, dtype=torch.uint8, device="cuda")
+    cp_dst = torch.empty_like(cp_src)
+    cp_dst.copy_(cp_src)
+    ev = lambda: torch.cuda.Event(enable_timing=True)
+    best_stream = 0.0
+    for _ in range(3):
+        a, b = ev(), ev()
+        a.record()
+        moe.moe_hbm_read_probe(buf[:stream_bytes], sink)
+        b.record()
+        b.synchronize()
+        best_stream = max(best_stream, stream_bytes / (a.elapsed_time(b) * 1e-3) / 1e9)
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(n_launch):
+            moe.moe_hbm_read_probe(buf[i * launch_bytes:(i + 1) * launch_bytes], sink)
+    g.replay()
+    torch.cuda.synchronize()
+    a, b = ev(), ev()
+    reps = 5
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    b.synchronize()
+    us = a.elapsed_time(b) * 1e3 / (reps * n_launch)
+    del g, buf, cp_src, cp_dst
+    return {"stream_GBps": best_stream, "stream_bytes": stream_bytes,
+            "launch_GBps": launch_bytes / (us * 1e-6) / 1e9, "launch_us": us, "launch_bytes": launch_bytes,
+            "method": f"moe_hbm_read_probe: one {stream_bytes >> 30} GiB pass; {n_launch} launches of "
+                      f"{launch_bytes} B over distinct memory replayed from a graph"}
+
+
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cfg4_gateup_hbm_traffic.txt")
+GATEUP_SOURCES = [os.path.join(ROOT, "paper_2605_29135_amd", "csrc", f) for f in ("kernels.hip", "device_common.h")]
+
+
+def gateup_source_hash() -> str:
+    import hashlib
+    h = hashlib.sha256()
+    for f in GATEUP_SOURCES:
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def measured_traffic():
+    """HBM bytes per gate/up launch from the committed counter summary (FETCH_SIZE + WRITE_SIZE, each
+    calibrated by a known-size kernel), or None when the kernel source changed since they were taken."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None, "no counter summary"
+    kv = {}
+    with open(TRAFFIC_FILE) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                key, val = line.split(":", 1)
+                kv[key.strip()] = val.strip()
+    if kv.get("kernel_source_sha256") != gateup_source_hash():
+        return None, "kernel source changed since the counters were taken"
+    return float(kv["hbm_bytes_per_launch"]), TRAFFIC_FILE[len(ROOT) + 1:]
+
+
 def cpu_baseline(wl, store, steps, bias_np, x_np, budget_s):
     """The oracle on the host cores: whole tokens through every layer, no budget."""
     import oracle
@@ -192,6 +264,9 @@ def main():
                 "tokens_per_s_bound": ceil * 1e9 / h2d_per_tok if h2d_per_tok else None,
                 "ceiling_method": "hipMemcpyAsync from hipHostMalloc memory, 64 MiB and expert-size chunks"}
 
+    hbm = hbm_ceiling(torch, moe, gu_bytes)
+    traffic, traffic_src = measured_traffic()
+
     # ---- oracle on the host cores (bounded sample of the timed tokens), with a parity check
     sample = list(range(args.warmup, n_steps))
     cpu_tps, outs, cpu_dt = cpu_baseline(wl, lambda l: store[0 if alias else l], sample, bias_np
@@ -227,7 +302,10 @@ def main():
                      "bytes_per_launch": gu_bytes, "mean_launch_us": gu_ms * 1e3,
                      "timing": f"the last step's {L} launches (one per layer, same arguments) in one HIP graph, "
                                f"replayed {args.replays}x between HIP events",
-                     "traffic": None},
+                     "traffic": traffic, "traffic_source": traffic_src,
+                     "practical_ceiling_GBps": hbm["launch_GBps"],
+                     "frac_of_practical": gu_gbps / hbm["launch_GBps"] if gu_gbps else None},
+        "hbm_ceiling": hbm,
         "kernels": {"route_us": rt_ms * 1e3, "gateup_us": gu_ms * 1e3, "down_us": dn_ms * 1e3,
                     "down_GBps": dn_gbps, "down_bytes_per_launch": dn_bytes,
                     "ffn_GBps": (gu_bytes + dn_bytes) / ((gu_ms + dn_ms) * 1e-3) / 1e9 if gu_ms else None},

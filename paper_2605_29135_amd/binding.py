@@ -88,6 +88,7 @@ def lib() -> C.CDLL:
             "moe_stack_destroy": [P],
             "moe_stack_decode_step": [P, I, P, I, P, P, P, P],
             "moe_stack_kernel_time": [P, I, I, P, C.POINTER(C.c_double)],
+            "moe_hbm_read_probe": [P, SZ, P, P],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -210,6 +211,14 @@ def moe_prefill_grouped(x, ids, weights, pool, expert_bytes: int, w_dtype: int, 
         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
         MOE_ACCUMULATE if accumulate else 0, _stream(stream)), "moe_prefill_grouped")
     return y_out
+
+
+def moe_hbm_read_probe(buf, sink, stream=None):
+    """Stream the device tensor `buf` once with the expert kernels' 16-byte loads (measurement aid)."""
+    import torch
+    nbytes = buf.numel() * buf.element_size()
+    _check(lib().moe_hbm_read_probe(_dev(buf, "buf"), nbytes, _dev(sink, "sink", torch.float32), _stream(stream)),
+           "moe_hbm_read_probe")
 
 
 def moe_combine(y_partial, weights, y_shared=None, y_out=None, accumulate: bool = False, stream=None):

@@ -46,6 +46,16 @@ __device__ __forceinline__ float bf16_bits_to_float(uint32_t b16) { return __uin
 
 __device__ __forceinline__ uint4 load16(const uint8_t *p) { return *reinterpret_cast<const uint4 *>(p); }
 
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte load with the nontemporal hint, for expert weights that are read once
+// per call: a streamed read of tens of MB then does not displace what the next
+// kernels reuse, and reaches a higher fraction of HBM bandwidth.
+__device__ __forceinline__ uint4 load16_stream(const uint8_t *p) {
+    const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 // EPC consecutive fp32 values of x starting at col0 (16-byte aligned).
 template <int DT>
 __device__ __forceinline__ void load_x(const float *__restrict__ x, int col0, float *xv) {

@@ -50,6 +50,7 @@ hipError_t launch_combine(const float *y_partial, const float *weights, const fl
                           int k, int H, float *y, bool accumulate, hipStream_t s);
 hipError_t launch_slot_update(int32_t *table, const int32_t *index, const int32_t *value, int n,
                               hipStream_t s);
+hipError_t launch_hbm_read(const void *buf, size_t bytes, float *sink, hipStream_t s);
 
 // Prefill (any T): pairs grouped by expert, grouped bf16 MFMA GEMMs, rank-order combine.
 struct PrefillWorkspace {

@@ -361,8 +361,8 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     for (int c = 0; c < NCH; ++c) {
         const int col0 = (c * kWave + lane) * EPC;
         const bool in = col0 < H;
-        wg[c] = in ? load16(gate + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
-        wu[c] = in ? load16(up + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
+        wg[c] = in ? load16_stream(gate + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
+        wu[c] = in ? load16_stream(up + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
         if constexpr (DT == INT4) {
             const uint16_t *sc = reinterpret_cast<const uint16_t *>(blob + size_t(I) * H);
             const int groups_per_row = H / 128;
@@ -476,7 +476,7 @@ __global__ __launch_bounds__(kBlock) void down_combine_kernel(
         for (int r = 0; r < kDownRows; ++r)
 #pragma unroll
             for (int s = 0; s < kDownSlots; ++s)
-                wv[r][s] = (ok[s] && h0 + r < H) ? load16(rp[s] + size_t(h0 + r) * rb) : make_uint4(0, 0, 0, 0);
+                wv[r][s] = (ok[s] && h0 + r < H) ? load16_stream(rp[s] + size_t(h0 + r) * rb) : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int r = 0; r < kDownRows; ++r)
 #pragma unroll
@@ -578,7 +578,7 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
         const unsigned jj = in ? j : 0u;
         ok[s] = in && ent_ok[jj];
         const uint8_t *blob = pool + (ok[s] ? ent_off[jj] : 0);
-        wv[s] = load16(ok[s] ? blob + row_off + size_t(c) * 16 : pool);
+        wv[s] = load16_stream(ok[s] ? blob + row_off + size_t(c) * 16 : pool);
         if constexpr (DT == INT4)
             sv[s] = bf16_bits_to_float(*reinterpret_cast<const uint16_t *>(
                 ok[s] ? blob + sc_off + size_t(c * EPC / 128) * 2 : pool));
@@ -813,6 +813,38 @@ hipError_t launch_combine(const float *y_partial, const float *weights, const fl
     if (n == 0) return hipSuccess;
     combine_kernel<<<unsigned((n + kBlock - 1) / kBlock), kBlock, 0, s>>>(y_partial, weights, y_shared, T,
                                                                           k, H, y, accumulate ? 1 : 0);
+    return hipGetLastError();
+}
+
+namespace {
+// Streams n16 16-byte words once: each wave reads kReadLoads consecutive 1 KiB
+// pieces (lane-contiguous 16-byte loads with the nontemporal hint, all issued
+// before any is consumed), as the expert kernels read weight rows.
+constexpr int kReadLoads = 8;
+__global__ __launch_bounds__(kBlock) void hbm_read_kernel(const uint8_t *__restrict__ buf, size_t n16,
+                                                          float *__restrict__ sink) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const size_t wave = size_t(blockIdx.x) * (kBlock / kWave) + threadIdx.x / kWave;
+    const size_t first = wave * (kReadLoads * kWave) + lane;
+    uint4 v[kReadLoads];
+#pragma unroll
+    for (int i = 0; i < kReadLoads; ++i) {
+        const size_t w = first + size_t(i) * kWave;
+        v[i] = w < n16 ? load16_stream(buf + w * 16) : make_uint4(0u, 0u, 0u, 0u);
+    }
+    uint32_t acc = 0;
+#pragma unroll
+    for (int i = 0; i < kReadLoads; ++i) acc ^= v[i].x ^ v[i].y ^ v[i].z ^ v[i].w;
+    if (acc == 0x7fc00001u) sink[0] = __uint_as_float(acc);  // keeps the loads; a benign race if it fires
+}
+}  // namespace
+
+hipError_t launch_hbm_read(const void *buf, size_t bytes, float *sink, hipStream_t s) {
+    const size_t n16 = bytes / 16;
+    if (n16 == 0) return hipSuccess;
+    const size_t per_block = size_t(kReadLoads) * kBlock;  // 16-byte words per block
+    const size_t blocks = (n16 + per_block - 1) / per_block;
+    hbm_read_kernel<<<unsigned(blocks), kBlock, 0, s>>>(static_cast<const uint8_t *>(buf), n16, sink);
     return hipGetLastError();
 }
 
