@@ -163,10 +163,11 @@ MOE_API size_t moe_prefill_workspace_bytes(int T, int k, int E, int H, int I);
  * expert on the device (the shared expert takes all T tokens), each group's
  * rows run through x W_gu^T -> SwiGLU -> W_d^T in 64-row tiles with bf16 MFMA
  * and fp32 accumulation, and each token's outputs are summed in rank order
- * with its weights (the moe_combine kernel).  The inputs and the SwiGLU
- * activations are rounded to bf16 for the matrix cores, and int4 weights are
- * dequantised to bf16 (scale * q rounded once); fp32 weights are rounded to
- * bf16 too.  Arguments as for moe_expert_ffn_grouped; H, I multiples of 128,
+ * with its weights (the moe_combine kernel).  x and the SwiGLU activations are
+ * rounded to bf16 (round to nearest even) for the matrix cores, and int4
+ * weights are dequantised to bf16 (scale * q, rounded once).
+ * w_dtype MOE_BF16 or MOE_INT4G128 (MOE_ERR_INVALID_ARG otherwise); other
+ * arguments as for moe_expert_ffn_grouped; H, I multiples of 128,
  * E <= MOE_MAX_EXPERTS; workspace >= moe_prefill_workspace_bytes(T, k, E, H, I).
  * Pairs with an id out of range or without a slot raise the device flag and
  * contribute nothing. */

@@ -176,6 +176,8 @@ int moe_prefill_grouped(const float *x, int T, int H, int I, int E, int k, const
                     MOE_MAX_TOPK, MOE_MAX_EXPERTS, T, E, k);
     if (!moe::ffn_shape_supported(H, I, w_dtype))
         return fail(MOE_ERR_INVALID_ARG, "prefill: unsupported H=%d I=%d dtype=%d", H, I, w_dtype);
+    if (!moe::prefill_dtype_supported(w_dtype))
+        return fail(MOE_ERR_INVALID_ARG, "prefill: weights must be MOE_BF16 or MOE_INT4G128 (dtype=%d)", w_dtype);
     if (expert_bytes < moe::expert_blob_bytes(H, I, w_dtype) || expert_bytes % 256)
         return fail(MOE_ERR_INVALID_ARG, "prefill: expert_bytes %zu must be >= %zu and a multiple of 256", expert_bytes,
                     moe::expert_blob_bytes(H, I, w_dtype));

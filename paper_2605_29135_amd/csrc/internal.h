@@ -54,16 +54,20 @@ hipError_t launch_hbm_read(const void *buf, size_t bytes, float *sink, hipStream
 
 // Prefill (any T): pairs grouped by expert, grouped bf16 MFMA GEMMs, rank-order combine.
 struct PrefillWorkspace {
-    int *hdr;      // [0] = tiles
-    int *g_slot;   // [E + 1] slot of each group (-2 = shared expert)
-    int *g_off;    // [E + 2] start of each group in `sorted`
-    int *tile_g;   // [max tiles] group of each 64-row tile
-    int *tile_r0;  // [max tiles] first row of each tile within its group
-    int *sorted;   // [T*k + T] pair ids grouped by expert
-    float *act;    // [(T*k + T) x I] SwiGLU activations per pair
-    float *y_part; // [T*k x H] expert outputs per routed pair
-    float *y_shared; // [T x H] shared expert outputs
+    int *hdr;           // [0] = tiles
+    int *g_slot;        // [E + 1] slot of each group (-2 = shared expert)
+    int *g_off;         // [E + 2] start of each group in `sorted`
+    int *tile_g;        // [max tiles] group of each 64-row tile
+    int *tile_r0;       // [max tiles] first row of each tile within its group
+    int *sorted;        // [T*k + T] pair ids grouped by expert
+    uint16_t *xb;       // [T x H] bf16 copy of x (int4: each 8-group in the order 0,4,1,5,2,6,3,7)
+    uint16_t *act;      // [(T*k + T) x I] bf16 SwiGLU activations, rows in `sorted` order (same 8-group order)
+    float *y_part;      // [T*k x H] expert outputs per routed pair
+    float *y_shared;    // [T x H] shared expert outputs
+    float *sx;          // int4: [T x H/128] sums of xb over each quantisation group
+    float *sa;          // int4: [(T*k + T) x I/128] sums of act over each quantisation group
 };
+bool prefill_dtype_supported(int dtype);
 size_t prefill_workspace_bytes(int T, int k, int E, int H, int I);
 PrefillWorkspace prefill_workspace(void *base, int T, int k, int E, int H, int I);
 hipError_t launch_prefill_ffn(const float *x, int T, int H, int I, int E, int k, const int32_t *ids,

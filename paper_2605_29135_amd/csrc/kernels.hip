@@ -20,6 +20,7 @@ using namespace dev;
 constexpr int kDownRows = 2; // output rows per wave in the down projection
 constexpr int kDownSlots = 4; // 16-byte chunks per lane per pass of the down projection
 constexpr float kRmsEps = 1e-6f;
+constexpr int kRouterMfmaMinTokens = 16;  // from this many tokens on, bf16 routers run on the matrix cores
 
 // ---------------------------------------------------------------- top-k ---
 // Order-preserving 32-bit key of a finite float (-0 ranks with +0).
@@ -200,6 +201,102 @@ __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__re
         for (int c = 0; c < NCH; ++c) acc += chunk_dot<DT>(wv[c], xv[c]);
         acc = wave_sum(acc);
         if (lane == 0) logits[size_t(t) * E + e] = acc + (bias ? bias[size_t(t) * E + e] : 0.f);
+    }
+}
+
+// ------------------------------------------------- router on the matrix cores ---
+// For many tokens (a prefill chunk) the router is a [T x H] x [H x E] product.
+// Each x value is split exactly into three bf16 terms x = x1 + x2 + x3
+// (x1 = bf16(x), x2 = bf16(x - x1), x3 = bf16(x - x1 - x2): 24 mantissa bits in
+// all), so with bf16 router weights every MFMA product is exact and the fp32
+// result differs from a sequential fp32 dot product only in summation order.
+typedef __bf16 rbf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 rbf16x2 __attribute__((ext_vector_type(2)));
+typedef float rfloatx2 __attribute__((ext_vector_type(2)));
+typedef float rfloatx4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ uint32_t rpack2(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(rfloatx2{lo, hi}, rbf16x2));
+}
+
+// Eight fp32 values -> three bf16x8 terms whose sum is exact.
+__device__ __forceinline__ void split3(const float *v, rbf16x8 &t1, rbf16x8 &t2, rbf16x8 &t3) {
+    uint32_t a[4], b[4], c[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float x0 = v[2 * e], x1 = v[2 * e + 1];
+        a[e] = rpack2(x0, x1);
+        const float r0 = x0 - __uint_as_float(a[e] << 16), r1 = x1 - __uint_as_float(a[e] & 0xffff0000u);
+        b[e] = rpack2(r0, r1);
+        const float q0 = r0 - __uint_as_float(b[e] << 16), q1 = r1 - __uint_as_float(b[e] & 0xffff0000u);
+        c[e] = rpack2(q0, q1);
+    }
+    t1 = __builtin_bit_cast(rbf16x8, make_uint4(a[0], a[1], a[2], a[3]));
+    t2 = __builtin_bit_cast(rbf16x8, make_uint4(b[0], b[1], b[2], b[3]));
+    t3 = __builtin_bit_cast(rbf16x8, make_uint4(c[0], c[1], c[2], c[3]));
+}
+
+constexpr int kRouterTileT = 64;  // tokens per block (16 per wave)
+constexpr int kRouterTileE = 32;  // experts per block (two 16-column MFMA blocks)
+
+// h = x / sqrt(mean(x^2) + eps), one wave per token.
+__global__ __launch_bounds__(kBlock) void rmsnorm_rows_kernel(const float *__restrict__ x, int T, int H,
+                                                              float *__restrict__ h) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int t = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
+    if (t >= T) return;
+    const float4 *xr = reinterpret_cast<const float4 *>(x + size_t(t) * H);
+    float ss = 0.f;
+    for (int c = lane; c < H / 4; c += kWave) {
+        const float4 v = xr[c];
+        ss = fmaf(v.x, v.x, fmaf(v.y, v.y, fmaf(v.z, v.z, fmaf(v.w, v.w, ss))));
+    }
+    const float inv = rsqrtf(wave_sum(ss) / float(H) + kRmsEps);
+    float4 *hr = reinterpret_cast<float4 *>(h + size_t(t) * H);
+    for (int c = lane; c < H / 4; c += kWave) {
+        const float4 v = xr[c];
+        hr[c] = make_float4(v.x * inv, v.y * inv, v.z * inv, v.w * inv);
+    }
+}
+
+// logits[t, e] = sum_i W[e, i] x[t, i] (+ bias[t, e]); W bf16 [E x H], H % 32 == 0.
+// Wave w of a block takes tokens t0 + 16w .. +15; lane (lr = l % 16, lg = l / 16)
+// supplies x[t0 + 16w + lr][k + 8lg .. +7] and W[e0 + 16j + lr][k + 8lg .. +7].
+__global__ __launch_bounds__(kBlock) void router_mfma_kernel(const float *__restrict__ x,
+                                                             const uint16_t *__restrict__ w, int T, int H,
+                                                             int E, const float *__restrict__ bias,
+                                                             float *__restrict__ logits) {
+    const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
+    const int lr = lane % 16, lg = lane / 16;
+    const int t0 = blockIdx.y * kRouterTileT + wave * 16, e0 = blockIdx.x * kRouterTileE;
+    const float *xr = x + size_t(min(t0 + lr, T - 1)) * H + 8 * lg;
+    const uint16_t *wr0 = w + size_t(min(e0 + lr, E - 1)) * H + 8 * lg;
+    const uint16_t *wr1 = w + size_t(min(e0 + 16 + lr, E - 1)) * H + 8 * lg;
+    rfloatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < H; k += 32) {
+        const float4 xa = *reinterpret_cast<const float4 *>(xr + k);
+        const float4 xb = *reinterpret_cast<const float4 *>(xr + k + 4);
+        const rbf16x8 b0 = __builtin_bit_cast(rbf16x8, *reinterpret_cast<const uint4 *>(wr0 + k));
+        const rbf16x8 b1 = __builtin_bit_cast(rbf16x8, *reinterpret_cast<const uint4 *>(wr1 + k));
+        const float v[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
+        rbf16x8 a1, a2, a3;
+        split3(v, a1, a2, a3);
+        // smallest terms first
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, b0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, b1, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b1, acc1, 0, 0, 0);
+        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b0, acc0, 0, 0, 0);
+        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc1, 0, 0, 0);
+    }
+    // lane holds C[t = t0 + 4lg + q][e = e0 + 16j + lr]
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+        const int t = t0 + 4 * lg + q;
+        if (t >= T) continue;
+        const int ea = e0 + lr, eb = e0 + 16 + lr;
+        if (ea < E) logits[size_t(t) * E + ea] = acc0[q] + (bias ? bias[size_t(t) * E + ea] : 0.f);
+        if (eb < E) logits[size_t(t) * E + eb] = acc1[q] + (bias ? bias[size_t(t) * E + eb] : 0.f);
     }
 }
 
@@ -716,6 +813,19 @@ hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int 
     if (!x) {
         if (bias == logits) return hipSuccess;
         return hipMemcpyAsync(logits, bias, sizeof(float) * size_t(T) * E, hipMemcpyDeviceToDevice, s);
+    }
+    if (w_dtype == BF16 && T >= kRouterMfmaMinTokens && (!norm || h_out)) {
+        // many tokens: (pre-norm, then) the router product on the matrix cores
+        const float *src = x;
+        if (norm) {
+            rmsnorm_rows_kernel<<<(T + 3) / 4, kBlock, 0, s>>>(x, T, H, h_out);
+            const hipError_t e = hipGetLastError();
+            if (e != hipSuccess) return e;
+            src = h_out;
+        }
+        const dim3 g((E + kRouterTileE - 1) / kRouterTileE, (T + kRouterTileT - 1) / kRouterTileT);
+        router_mfma_kernel<<<g, kBlock, 0, s>>>(src, static_cast<const uint16_t *>(w), T, H, E, bias, logits);
+        return hipGetLastError();
     }
     const dim3 grid((E + 3) / 4, T);
     const auto *wp = static_cast<const uint8_t *>(w);

@@ -1,93 +1,123 @@
 // prefill.hip -- MoE FFN over a prefill chunk on gfx950: the (token, rank)
-// pairs are grouped by expert, then each expert's tokens run through grouped
+// pairs are grouped by expert, then each expert's rows run through grouped
 // GEMMs on bf16 MFMA (v_mfma_f32_16x16x32_bf16, fp32 accumulation).
 //
-// An expert sees ~T*k/E tokens of a chunk (64 at T = 2048, k = 8, E = 256), so
+// An expert sees ~T*k/E rows of a chunk (64 at T = 2048, k = 8, E = 256), so
 // its weights are read once for all of them: this is the one place in the path
-// that is a dense contraction.  Activations are rounded to bf16 as they are
-// staged in LDS; int4 weights are dequantised to bf16 there.
+// that is a dense contraction.  Layout of the work:
+//   plan    one block groups the pairs by expert (histogram, scan, 64-row
+//           tiles, scatter); the other blocks round x to bf16 once.
+//   gate/up C = x W_gu^T per 64 x 256 tile; the epilogue writes the bf16
+//           SwiGLU activation in grouped row order.
+//   down    C = act W_d^T per 64 x 256 tile; one fp32 output row per pair.
+//   combine each token's rows summed in rank order with its weights.
+// In both GEMMs the A rows (activations, shared by the block's four waves)
+// are staged through double-buffered LDS, while each wave loads its own 64
+// weight rows straight into registers in the matrix-core lane layout and
+// dequantises int4 there: a weight is used by exactly one wave, so staging it
+// in LDS would only add traffic.
 #include "internal.h"
 #include "device_common.h"
+
+#include <algorithm>
 
 namespace moe {
 namespace {
 
 using namespace dev;
 
-constexpr int kTileM = 64;      // pair rows per tile
-constexpr int kTileN = 64;      // output columns per tile (gate/up: W_gu rows; down: output h)
-constexpr int kTileK = 64;      // reduction elements staged per LDS round
-constexpr int kLdsStride = 72;  // bf16 per LDS row (64 + 8 padding: 16-lane reads hit distinct banks)
-constexpr int kAlignThreads = 1024;
+constexpr int kTileM = 64;        // pair rows per tile
+constexpr int kWaveN = 64;        // output columns per wave
+constexpr int kTileN = 4 * kWaveN;  // output columns per block
+constexpr int kPlanThreads = 1024;
+constexpr int kXcds = 8;          // gfx950 dispatches consecutive workgroups round-robin over 8 XCDs
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float floatx2 __attribute__((ext_vector_type(2)));
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ uint32_t bf16_rne(float f) {
-    const uint32_t u = __float_as_uint(f);
-    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
-}
-__device__ __forceinline__ uint32_t pack_bf16(float lo, float hi) { return bf16_rne(lo) | (bf16_rne(hi) << 16); }
-
-// Sixteen consecutive fp32 values of a row -> eight packed bf16 pairs.
-__device__ __forceinline__ void f32x16_to_bf16(const float *p, uint4 out[2]) {
-    const float4 *q = reinterpret_cast<const float4 *>(p);
-    const float4 a = q[0], b = q[1], c = q[2], d = q[3];
-    out[0] = make_uint4(pack_bf16(a.x, a.y), pack_bf16(a.z, a.w), pack_bf16(b.x, b.y), pack_bf16(b.z, b.w));
-    out[1] = make_uint4(pack_bf16(c.x, c.y), pack_bf16(c.z, c.w), pack_bf16(d.x, d.y), pack_bf16(d.z, d.w));
+// Two floats -> packed bf16 pair (round to nearest even; one v_cvt_pk_bf16_f32).
+__device__ __forceinline__ uint32_t pack2(float lo, float hi) {
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, bf16x2));
 }
 
-// Sixteen consecutive weights of row r, columns col .. col+15, of a dense
-// [rows x K] matrix at `m` -> eight packed bf16 pairs (bf16 copied, f32 rounded).
-template <int DT>
-__device__ __forceinline__ void weights16_to_bf16(const uint8_t *m, int K, int r, int col, uint4 out[2]) {
-    static_assert(DT == BF16 || DT == F32, "int4 rows are dequantised by dequant16");
-    if constexpr (DT == BF16) {
-        const uint4 *q = reinterpret_cast<const uint4 *>(m + (size_t(r) * K + col) * 2);
-        out[0] = q[0];
-        out[1] = q[1];
-    } else {
-        f32x16_to_bf16(reinterpret_cast<const float *>(m) + size_t(r) * K + col, out);
-    }
-}
-
-// Raw 16 nibbles (two dwords) times one scale -> eight packed bf16 pairs.
-__device__ __forceinline__ void dequant16(uint2 nib, float s, uint4 out[2]) {
-    uint32_t w[8];
+// Eight signed nibbles of one dword (element e in bits 4e..4e+3) times a scale -> four packed bf16 pairs.
+__device__ __forceinline__ bf16x8 dequant8(uint32_t v, float s) {
+    uint32_t w[4];
 #pragma unroll
-    for (int d = 0; d < 2; ++d) {
-        const uint32_t v = d == 0 ? nib.x : nib.y;
-#pragma unroll
-        for (int e = 0; e < 8; e += 2) {
-            const float lo = float(int(__builtin_amdgcn_sbfe(v, 4 * e, 4))) * s;  // builtin returns the source's (unsigned) type
-            const float hi = float(int(__builtin_amdgcn_sbfe(v, 4 * e + 4, 4))) * s;
-            w[d * 4 + e / 2] = pack_bf16(lo, hi);
-        }
+    for (int e = 0; e < 4; ++e) {
+        // the builtin returns the type of its source (unsigned): convert to int before widening
+        const float lo = float(int(__builtin_amdgcn_sbfe(v, 8 * e, 4))) * s;
+        const float hi = float(int(__builtin_amdgcn_sbfe(v, 8 * e + 4, 4))) * s;
+        w[e] = pack2(lo, hi);
     }
-    out[0] = make_uint4(w[0], w[1], w[2], w[3]);
-    out[1] = make_uint4(w[4], w[5], w[6], w[7]);
+    return __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
 }
 
-// ------------------------------------------------------------------ align ---
+// int4 -> bf16 with the offset form used by the grouped GEMM: for the eight
+// nibbles of one dword (element e in bits 4e..4e+3, two's complement q), the
+// bf16 pattern 0x4300 | (r ^ 8) is exactly 128 + (q + 8) = 136 + q.  Two bit
+// operations give a pair: ((v >> 4e) & 0x000F000F) ^ 0x43084308 holds elements
+// e and e + 4, so the eight values come out in the order 0,4,1,5,2,6,3,7 (the
+// A operand is stored in the same order).  The scale and the -136 offset are
+// applied to the fp32 MFMA result of the whole quantisation group.
+__device__ __forceinline__ bf16x8 int4_offset8(uint32_t v) {
+    const uint32_t w0 = v & 0x000F000Fu, w1 = (v >> 4) & 0x000F000Fu, w2 = (v >> 8) & 0x000F000Fu,
+                   w3 = (v >> 12) & 0x000F000Fu;
+    return __builtin_bit_cast(bf16x8, make_uint4(w0 ^ 0x43084308u, w1 ^ 0x43084308u, w2 ^ 0x43084308u,
+                                                 w3 ^ 0x43084308u));
+}
+
+// Position of element e (0..7) of an 8-element group in the order 0,4,1,5,2,6,3,7.
+__device__ __forceinline__ int perm8_pos(int e) { return e < 4 ? 2 * e : 2 * e - 7; }
+
+// ------------------------------------------------------------------- plan ---
 // Groups: 0..E-1 routed experts, E the shared expert (all T tokens).  Output:
-// hdr[0] = tiles; g_slot[g]; g_off[g] (start of group g in `sorted`);
-// tiles (group, first row) of up to 64 rows; sorted pair ids (routed pair
-// p = t*k + j, shared pair T*k + t).  Pairs with a bad id or no slot raise
-// the flag and their partial output rows are zeroed.
-__global__ __launch_bounds__(kAlignThreads) void prefill_align_kernel(const int32_t *__restrict__ ids, int T,
-                                                                      int k, int E, const int32_t *__restrict__ slot_of,
-                                                                      int has_shared, PrefillWorkspace ws, int H,
-                                                                      int *err) {
-    __shared__ int cnt[MOE_MAX_EXPERTS + 1], cur[MOE_MAX_EXPERTS + 1], off[MOE_MAX_EXPERTS + 2];
-    __shared__ int slot[MOE_MAX_EXPERTS + 1];
-    const int P = T * k, G = E + 1;
-    for (int g = threadIdx.x; g < G; g += kAlignThreads) {
+// hdr[0] = tiles; g_slot[g]; g_off[g] (start of group g in `sorted`); tiles
+// (group, first row) of up to 64 rows; sorted pair ids (routed pair p = t*k+j,
+// shared pair T*k + t).  Pairs with a bad id or no slot raise the flag and
+// their output rows are zeroed.  Blocks 1.. write xb = bf16(x).
+__global__ __launch_bounds__(kPlanThreads) void prefill_plan_kernel(const int32_t *__restrict__ ids, int T, int k,
+                                                                    int E, const int32_t *__restrict__ slot_of,
+                                                                    int has_shared, const float *__restrict__ x,
+                                                                    int H, int offset_form, PrefillWorkspace ws,
+                                                                    int *err) {
+    if (blockIdx.x > 0) {
+        // 8 elements per thread; 16 consecutive threads hold one 128-element group (H % 128 == 0)
+        const size_t n8 = size_t(T) * H / 8;
+        const size_t stride = size_t(gridDim.x - 1) * kPlanThreads;
+        for (size_t i = size_t(blockIdx.x - 1) * kPlanThreads + threadIdx.x; i < n8; i += stride) {
+            const float4 a = reinterpret_cast<const float4 *>(x)[2 * i];
+            const float4 b = reinterpret_cast<const float4 *>(x)[2 * i + 1];
+            if (offset_form) {
+                const uint32_t p0 = pack2(a.x, b.x), p1 = pack2(a.y, b.y), p2 = pack2(a.z, b.z), p3 = pack2(a.w, b.w);
+                reinterpret_cast<uint4 *>(ws.xb)[i] = make_uint4(p0, p1, p2, p3);
+                // group sum of the bf16 values the matrix cores see
+                float sum = 0.f;
+                const uint32_t pk[4] = {p0, p1, p2, p3};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) sum += __uint_as_float(pk[e] << 16) + __uint_as_float(pk[e] & 0xffff0000u);
+#pragma unroll
+                for (int d = 1; d < 16; d <<= 1) sum += __shfl_xor(sum, d);
+                if ((threadIdx.x & 15) == 0) ws.sx[i / 16] = sum;
+            } else {
+                reinterpret_cast<uint4 *>(ws.xb)[i] =
+                    make_uint4(pack2(a.x, a.y), pack2(a.z, a.w), pack2(b.x, b.y), pack2(b.z, b.w));
+            }
+        }
+        return;
+    }
+    __shared__ int cnt[MOE_MAX_EXPERTS + 1], cur[MOE_MAX_EXPERTS + 1], slot[MOE_MAX_EXPERTS + 1];
+    __shared__ int off[MOE_MAX_EXPERTS + 2], toff[MOE_MAX_EXPERTS + 2];
+    const int P = T * k, G = E + 1, tid = threadIdx.x;
+    for (int g = tid; g < G; g += kPlanThreads) {
         cnt[g] = 0;
         cur[g] = 0;
         slot[g] = g == E ? -2 : (slot_of ? slot_of[g] : g);
     }
     __syncthreads();
-    for (int p = threadIdx.x; p < P; p += kAlignThreads) {
+    for (int p = tid; p < P; p += kPlanThreads) {
         const int e = ids[p];
         const bool in = e >= 0 && e < E;
         if (!in || slot[e] < 0) {
@@ -98,150 +128,289 @@ __global__ __launch_bounds__(kAlignThreads) void prefill_align_kernel(const int3
         atomicAdd(&cnt[e], 1);
     }
     __syncthreads();
-    if (threadIdx.x == 0) {
-        cnt[E] = has_shared ? T : 0;
-        off[0] = 0;
-        int nt = 0;
-        for (int g = 0; g < G; ++g) {
-            off[g + 1] = off[g] + cnt[g];
-            for (int r0 = 0; r0 < cnt[g]; r0 += kTileM) {
-                ws.tile_g[nt] = g;
-                ws.tile_r0[nt] = r0;
-                ++nt;
+    if (tid == 0) cnt[E] = has_shared ? T : 0;
+    __syncthreads();
+    // exclusive scans of the group sizes and of their tile counts, by wave 0 in chunks of 64
+    if (tid < kWave) {
+        int carry = 0, tcarry = 0;
+        for (int g0 = 0; g0 < G; g0 += kWave) {
+            const int g = g0 + tid;
+            const int c = g < G ? cnt[g] : 0;
+            int v = c, tv = (c + kTileM - 1) / kTileM;
+            const int c_t = tv;
+            for (int d = 1; d < kWave; d <<= 1) {
+                const int y = __shfl_up(v, d), ty = __shfl_up(tv, d);
+                if (tid >= d) {
+                    v += y;
+                    tv += ty;
+                }
             }
+            if (g < G) {
+                off[g] = carry + v - c;
+                toff[g] = tcarry + tv - c_t;
+            }
+            carry += __shfl(v, kWave - 1);
+            tcarry += __shfl(tv, kWave - 1);
         }
-        ws.hdr[0] = nt;
+        if (tid == 0) {
+            off[G] = carry;
+            toff[G] = tcarry;
+            ws.hdr[0] = tcarry;
+        }
     }
     __syncthreads();
-    for (int g = threadIdx.x; g <= G; g += kAlignThreads) {
+    for (int g = tid; g <= G; g += kPlanThreads) {
         ws.g_off[g] = off[g];
-        if (g < G) ws.g_slot[g] = slot[g];
+        if (g < G) {
+            ws.g_slot[g] = slot[g];
+            for (int i = 0, t = toff[g]; t < toff[g + 1]; ++i, ++t) {
+                ws.tile_g[t] = g;
+                ws.tile_r0[t] = i * kTileM;
+            }
+        }
     }
-    for (int p = threadIdx.x; p < P; p += kAlignThreads) {
+    for (int p = tid; p < P; p += kPlanThreads) {
         const int e = ids[p];
         if (e < 0 || e >= E || slot[e] < 0) continue;
         ws.sorted[off[e] + atomicAdd(&cur[e], 1)] = p;
     }
     if (has_shared)
-        for (int t = threadIdx.x; t < T; t += kAlignThreads) ws.sorted[off[E] + t] = P + t;
+        for (int t = tid; t < T; t += kPlanThreads) ws.sorted[off[E] + t] = P + t;
 }
 
 // ------------------------------------------------------------ grouped GEMM ---
-// One 64 x 64 output tile per block of 4 waves (2 x 2 waves of 32 x 32, each
-// 2 x 2 MFMA 16x16 blocks).  Rows are pairs of one group; the A operand is
-// the pair's input row (gate/up: x of its token; down: its SwiGLU activation),
-// the B operand rows of the group's expert matrix.  Global loads of the next
-// K round are issued before the MFMAs of the current one.
-//   DOWN = false: C = x W_gu^T, epilogue act[p, i] = silu(C[:, 2i]) * C[:, 2i+1]
-//   DOWN = true:  C = act W_d^T, epilogue y_part[p, h] (routed) / y_shared[t, h]
+// Reduction depth per round: int4 takes one quantisation group (128), so a
+// column's weights of a round share one scale; bf16 takes 64.  Lane l of a
+// wave owns output column (l % 16) of each of its four 16-column blocks and the
+// k range [SEG*(l/16), SEG*(l/16) + SEG) of the round; MFMA step s uses the
+// eight k at offset 8s of that range, from A and B alike.
+template <int DT>
+struct Round {
+    static constexpr int BK = DT == INT4 ? 128 : 64;
+    static constexpr int SEG = BK / 4;        // k per lane group, and per staging thread of A
+    static constexpr int STEPS = BK / 32;     // MFMA k-steps per round
+    static constexpr int LDS = BK + 8;        // bf16 per LDS row: 16 rows read at one offset hit distinct banks
+    static constexpr int A16 = SEG / 8;       // 16-byte A loads per staging thread
+    static constexpr int B16 = DT == INT4 ? 1 : SEG / 8;  // 16-byte weight loads per lane and column block
+};
+
+// int4: per round, tmp = A (136 + Q)^T on the matrix cores, then
+//   acc += s_n * (tmp - 136 * S_m)
+// with s_n the column's scale and S_m the row's sum of A over the group (read
+// from ws.sx for x, ws.sa for the activations).  bf16: acc += A W^T directly.
 template <int DT, bool DOWN>
-__global__ __launch_bounds__(kBlock) void prefill_gemm_kernel(const float *__restrict__ x, int T, int H, int I, int k,
+__global__ __launch_bounds__(kBlock, 2) void prefill_gemm_kernel(int T, int H, int I, int k,
                                                               const uint8_t *__restrict__ pool, size_t expert_bytes,
                                                               const uint8_t *__restrict__ shared_w, size_t d_off,
-                                                              PrefillWorkspace ws) {
-    __shared__ __align__(16) uint16_t As[kTileM * kLdsStride];
-    __shared__ __align__(16) uint16_t Bs[kTileN * kLdsStride];
-    __shared__ int arow[kTileM];  // pair id of each tile row (-1 = padding)
-    const int tile = blockIdx.y;
-    if (tile >= ws.hdr[0]) return;
+                                                              int nblk_n, PrefillWorkspace ws) {
+    using R = Round<DT>;
+    constexpr bool kOffset = DT == INT4;
+    __shared__ __align__(16) uint16_t As[2][kTileM * R::LDS];
+    __shared__ __align__(16) float Ss[2][kTileM];  // int4: group sums of the tile rows
+    __shared__ float Sred[4][kTileM];              // int4 gate/up epilogue: per-wave activation sums
+    __shared__ int arow[kTileM];                   // pair id of each tile row (-1 = padding)
+    // XCD-aware order: the blocks of one tile (and neighbouring tiles of a group) share an XCD's L2
+    const int nwork = ws.hdr[0] * nblk_n;
+    const int chunk = (nwork + kXcds - 1) / kXcds;
+    const int idx = blockIdx.x / kXcds;
+    if (idx >= chunk) return;
+    const int work = (blockIdx.x % kXcds) * chunk + idx;
+    if (work >= nwork) return;
+    const int tile = work / nblk_n, nb = work % nblk_n;
+
     const int P = T * k;
     const int g = ws.tile_g[tile];
     const int base = ws.g_off[g] + ws.tile_r0[tile];
     const int rows = min(kTileM, ws.g_off[g + 1] - base);
     const int sl = ws.g_slot[g];
     const uint8_t *blob = sl == -2 ? shared_w : pool + size_t(sl) * expert_bytes;
-    // B matrix: gate/up [2I x H] at the blob start; down [H x I] at d_off
-    const int K = DOWN ? I : H;
-    const uint8_t *bmat = DOWN ? blob + d_off : blob;
-    const int brows = DOWN ? H : 2 * I;
-    const uint16_t *bscale = reinterpret_cast<const uint16_t *>(bmat + size_t(brows) * K / 2);  // int4 only
-    const int n0 = blockIdx.x * kTileN;
+    const int K = DOWN ? I : H, N = DOWN ? H : 2 * I;
+    const int KG = K / 128;                            // quantisation groups per row
+    const uint8_t *bmat = DOWN ? blob + d_off : blob;  // gate/up [2I x H] at the blob start, down [H x I]
+    const uint16_t *bscale = reinterpret_cast<const uint16_t *>(bmat + size_t(N) * K / 2);  // int4 only
     const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int lr = lane % 16, lg = lane / 16;
+    const int wn0 = nb * kTileN + wave * kWaveN;
+    const bool active = wn0 < N;  // N is a multiple of 64: a wave's columns are all in range or all out
+    // The main loop has no branches: padding rows load row 0 of the tile and an out-of-range wave
+    // loads weight row N-1; neither result is stored.  (A branch around a load leaves the compiler
+    // unable to count outstanding loads, and it then waits for all of them.)
+
     if (tid < kTileM) arow[tid] = tid < rows ? ws.sorted[base + tid] : -1;
     __syncthreads();
-    // staging assignment: thread -> row tid/4, 16 columns at (tid%4)*16
-    const int sr = tid / 4, sc = (tid % 4) * 16;
-    const int p_s = arow[sr];
-    const float *arow_ptr = nullptr;
-    if (p_s >= 0) {
-        if (DOWN)
-            arow_ptr = ws.act + size_t(p_s) * I;
-        else
-            arow_ptr = x + size_t(p_s < P ? p_s / k : p_s - P) * H;
+
+    // A staging: thread -> row tid / 4, SEG columns at (tid % 4) * SEG of each round
+    const int sr = tid / 4, sc = (tid % 4) * R::SEG;
+    const int ar = sr < rows ? sr : 0;
+    const uint16_t *asrc;
+    if constexpr (DOWN) {
+        asrc = ws.act + size_t(base + ar) * I;
+    } else {
+        const int p = arow[ar];
+        asrc = ws.xb + size_t(p < P ? p / k : p - P) * H;
     }
-    uint4 ra[2], rb[2];
-    uint2 rnib = make_uint2(0u, 0u);
-    float rscale = 0.f;
-    auto fetch = [&](int k0) {
-        if (arow_ptr)
-            f32x16_to_bf16(arow_ptr + k0 + sc, ra);
-        else
-            ra[0] = ra[1] = make_uint4(0u, 0u, 0u, 0u);
-        const int br = n0 + sr;
-        if constexpr (DT == INT4) {
-            rnib = *reinterpret_cast<const uint2 *>(bmat + (size_t(br) * K + k0 + sc) / 2);
-            rscale = bf16_bits_to_float(bscale[size_t(br) * (K / 128) + (k0 + sc) / 128]);
+    // group sums: thread tid < 64 stages row tid's sum of the next round
+    const float *ssrc = nullptr;
+    if constexpr (kOffset) {
+        const int rr = tid < rows ? tid : 0;
+        if constexpr (DOWN) {
+            ssrc = ws.sa + size_t(base + rr) * KG;
         } else {
-            weights16_to_bf16<DT>(bmat, K, br, k0 + sc, rb);
+            const int p = arow[tid < kTileM ? rr : 0];
+            ssrc = ws.sx + size_t(p < P ? p / k : p - P) * KG;
         }
-    };
-    floatx4 acc[2][2];
+    }
+
+    floatx4 acc[4][4];
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
-    const int wm = wave / 2, wn = wave % 2;
-    fetch(0);
-    for (int k0 = 0; k0 < K; k0 += kTileK) {
-        if constexpr (DT == INT4) dequant16(rnib, rscale, rb);
-        uint4 *as = reinterpret_cast<uint4 *>(As + sr * kLdsStride + sc);
-        uint4 *bs = reinterpret_cast<uint4 *>(Bs + sr * kLdsStride + sc);
-        as[0] = ra[0];
-        as[1] = ra[1];
-        bs[0] = rb[0];
-        bs[1] = rb[1];
-        __syncthreads();
-        if (k0 + kTileK < K) fetch(k0 + kTileK);  // next round's loads overlap the MFMAs
+        for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+
+    u32x4 ra[R::A16];       // next round's A segment of this thread
+    uint4 rb[4][R::B16];    // next round's weights of this lane, one entry per 16-column block
+    uint32_t rsb[4] = {0u, 0u, 0u, 0u};  // their raw bf16 scale bits (widened at use: no wait after the load)
+    float rS = 0.f;         // next round's group sum of row tid (int4, tid < 64)
+    // 32-bit byte offsets of this lane's weight rows (and scale rows) within the expert matrix
+    uint32_t boff[4], soff[4];
 #pragma unroll
-        for (int ks = 0; ks < kTileK; ks += 32) {
-            bf16x8 a[2], b[2];
+    for (int j = 0; j < 4; ++j) {
+        const uint32_t n = uint32_t(min(wn0 + 16 * j + lr, N - 1));
+        boff[j] = DT == INT4 ? n * uint32_t(K / 2) + uint32_t(R::SEG * lg / 2) : (n * uint32_t(K) + uint32_t(R::SEG * lg)) * 2u;
+        soff[j] = n * uint32_t(KG);
+    }
+    const int rounds = K / R::BK;
+    // Software pipeline: iteration r issues round r+1's loads, multiplies round r out of LDS and
+    // registers, then stores round r+1's A into the other LDS buffer.
+    for (int r = -1; r < rounds; ++r) {
+        uint4 cb[4][R::B16];
+        float cs[4];
 #pragma unroll
-            for (int i = 0; i < 2; ++i) {
-                a[i] = *reinterpret_cast<const bf16x8 *>(As + (wm * 32 + i * 16 + lane % 16) * kLdsStride + ks + (lane / 16) * 8);
-                b[i] = *reinterpret_cast<const bf16x8 *>(Bs + (wn * 32 + i * 16 + lane % 16) * kLdsStride + ks + (lane / 16) * 8);
+        for (int j = 0; j < 4; ++j) {
+            cs[j] = bf16_bits_to_float(rsb[j]);
+#pragma unroll
+            for (int i = 0; i < R::B16; ++i) cb[j][i] = rb[j][i];
+        }
+        if (r + 1 < rounds) {
+            const int k0 = (r + 1) * R::BK;
+#pragma unroll
+            for (int i = 0; i < R::A16; ++i) ra[i] = *reinterpret_cast<const u32x4 *>(asrc + k0 + sc + 8 * i);
+            if constexpr (kOffset) {
+                if (tid < kTileM) rS = ssrc[r + 1];
             }
 #pragma unroll
-            for (int i = 0; i < 2; ++i)
+            for (int j = 0; j < 4; ++j) {
+                if constexpr (DT == INT4) {
+                    rb[j][0] = *reinterpret_cast<const uint4 *>(bmat + boff[j] + uint32_t(k0 / 2));
+                    rsb[j] = bscale[soff[j] + uint32_t(k0 / 128)];
+                } else {
 #pragma unroll
-                for (int j = 0; j < 2; ++j) acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+                    for (int i = 0; i < R::B16; ++i)
+                        rb[j][i] = *reinterpret_cast<const uint4 *>(bmat + boff[j] + uint32_t(k0 * 2 + 16 * i));
+                }
+            }
+        }
+        if (r >= 0) {
+            const int buf = r & 1;
+            floatx4 tmp[4][4];
+#pragma unroll
+            for (int s = 0; s < R::STEPS; ++s) {
+                bf16x8 a[4];
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+                    a[i] = *reinterpret_cast<const bf16x8 *>(&As[buf][(16 * i + lr) * R::LDS + R::SEG * lg + 8 * s]);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    if constexpr (kOffset) {
+                        const uint32_t d = s == 0 ? cb[j][0].x : s == 1 ? cb[j][0].y : s == 2 ? cb[j][0].z : cb[j][0].w;
+                        const bf16x8 b = int4_offset8(d);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            tmp[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                a[i], b, s == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : tmp[i][j], 0, 0, 0);
+                    } else {
+                        const bf16x8 b = __builtin_bit_cast(bf16x8, cb[j][s]);
+#pragma unroll
+                        for (int i = 0; i < 4; ++i)
+                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b, acc[i][j], 0, 0, 0);
+                    }
+                }
+            }
+            if constexpr (kOffset) {
+                // rows of this lane: m = 16i + 4lg + q
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const float4 sv = *reinterpret_cast<const float4 *>(&Ss[buf][16 * i + 4 * lg]);
+                    const float svq[4] = {sv.x, sv.y, sv.z, sv.w};
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const float off = -136.f * cs[j];
+#pragma unroll
+                        for (int q = 0; q < 4; ++q) acc[i][j][q] = fmaf(cs[j], tmp[i][j][q], fmaf(off, svq[q], acc[i][j][q]));
+                    }
+                }
+            }
+        }
+        if (r + 1 < rounds) {
+            u32x4 *dst = reinterpret_cast<u32x4 *>(&As[(r + 1) & 1][sr * R::LDS + sc]);
+#pragma unroll
+            for (int i = 0; i < R::A16; ++i) dst[i] = ra[i];
+            if constexpr (kOffset) {
+                if (tid < kTileM) Ss[(r + 1) & 1][tid] = rS;
+            }
         }
         __syncthreads();
     }
-    // epilogue: lane holds C[m = (lane/16)*4 + q][n = lane%16] of each 16x16 block
+
+    // epilogue: lane holds C[m = 16i + 4*lg + q][n = wn0 + 16j + lr]
+    float rowsum[4][4];  // int4 gate/up: this lane's bf16 activations summed per row
 #pragma unroll
-    for (int i = 0; i < 2; ++i)
+    for (int i = 0; i < 4; ++i)
 #pragma unroll
-        for (int j = 0; j < 2; ++j)
+        for (int q = 0; q < 4; ++q) {
+            rowsum[i][q] = 0.f;
+            const int m = 16 * i + 4 * lg + q;
+            const int p = arow[m];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                const int m = wm * 32 + i * 16 + (lane / 16) * 4 + q;
-                const int n = n0 + wn * 32 + j * 16 + lane % 16;
+            for (int j = 0; j < 4; ++j) {
+                const int n = wn0 + 16 * j + lr;
                 const float v = acc[i][j][q];
-                const int p = arow[m];
                 if constexpr (DOWN) {
-                    if (p >= 0) {
+                    if (active && p >= 0) {
                         float *o = p < P ? ws.y_part + size_t(p) * H : ws.y_shared + size_t(p - P) * H;
                         o[n] = v;
                     }
                 } else {
                     // W_gu rows 2i (gate) and 2i+1 (up) sit in neighbouring lanes
                     const float partner = dpp<0xB1>(v);
-                    if ((n & 1) == 0 && p >= 0) {
-                        const float gte = v, up = partner;
-                        ws.act[size_t(p) * I + n / 2] = gte / (1.f + expf(-gte)) * up;
+                    if ((lr & 1) == 0 && active && p >= 0) {
+                        const float a = v * __builtin_amdgcn_rcpf(1.f + __expf(-v)) * partner;
+                        const uint32_t ab = pack2(a, 0.f) & 0xffffu;
+                        const int c = n / 2;
+                        const int pos = kOffset ? (c & ~7) + perm8_pos(c & 7) : c;
+                        ws.act[size_t(base + m) * I + pos] = uint16_t(ab);
+                        rowsum[i][q] += __uint_as_float(ab << 16);
                     }
                 }
             }
+        }
+    if constexpr (kOffset && !DOWN) {
+        // group sums of the activations for the down GEMM: this block's 256 gate/up columns are
+        // the 128 activation columns of down group nb
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                float v = rowsum[i][q];
+                v += __shfl_xor(v, 1);
+                v += __shfl_xor(v, 2);
+                v += __shfl_xor(v, 4);
+                v += __shfl_xor(v, 8);
+                if (lr == 0) Sred[wave][16 * i + 4 * lg + q] = v;
+            }
+        __syncthreads();
+        if (tid < rows) ws.sa[size_t(base + tid) * (I / 128) + nb] = Sred[0][tid] + Sred[1][tid] + Sred[2][tid] + Sred[3][tid];
+    }
 }
 
 template <typename... Params, typename... Args>
@@ -256,15 +425,18 @@ int max_tiles(int T, int k, int E) { return (T * k + T + kTileM - 1) / kTileM + 
 
 }  // namespace
 
+bool prefill_dtype_supported(int dtype) { return dtype == BF16 || dtype == INT4; }
+
 size_t prefill_workspace_bytes(int T, int k, int E, int H, int I) {
-    const size_t P = size_t(T) * k, mt = size_t(max_tiles(T, k, E));
+    const size_t P = size_t(T) * k, R = P + T, mt = size_t(max_tiles(T, k, E));
     return align256(sizeof(int) * 16) + align256(sizeof(int) * (E + 1)) + align256(sizeof(int) * (E + 2)) +
-           2 * align256(sizeof(int) * mt) + align256(sizeof(int) * (P + T)) + align256(sizeof(float) * (P + T) * I) +
-           align256(sizeof(float) * P * H) + align256(sizeof(float) * size_t(T) * H);
+           2 * align256(sizeof(int) * mt) + align256(sizeof(int) * R) + align256(2 * size_t(T) * H) +
+           align256(2 * R * I) + align256(sizeof(float) * P * H) + align256(sizeof(float) * size_t(T) * H) +
+           align256(sizeof(float) * size_t(T) * (H / 128)) + align256(sizeof(float) * R * (I / 128));
 }
 
 PrefillWorkspace prefill_workspace(void *base, int T, int k, int E, int H, int I) {
-    const size_t P = size_t(T) * k, mt = size_t(max_tiles(T, k, E));
+    const size_t P = size_t(T) * k, R = P + T, mt = size_t(max_tiles(T, k, E));
     char *c = static_cast<char *>(base);
     PrefillWorkspace w;
     auto take = [&](size_t n) {
@@ -277,10 +449,13 @@ PrefillWorkspace prefill_workspace(void *base, int T, int k, int E, int H, int I
     w.g_off = reinterpret_cast<int *>(take(sizeof(int) * (E + 2)));
     w.tile_g = reinterpret_cast<int *>(take(sizeof(int) * mt));
     w.tile_r0 = reinterpret_cast<int *>(take(sizeof(int) * mt));
-    w.sorted = reinterpret_cast<int *>(take(sizeof(int) * (P + T)));
-    w.act = reinterpret_cast<float *>(take(sizeof(float) * (P + T) * I));
+    w.sorted = reinterpret_cast<int *>(take(sizeof(int) * R));
+    w.xb = reinterpret_cast<uint16_t *>(take(2 * size_t(T) * H));
+    w.act = reinterpret_cast<uint16_t *>(take(2 * R * I));
     w.y_part = reinterpret_cast<float *>(take(sizeof(float) * P * H));
     w.y_shared = reinterpret_cast<float *>(take(sizeof(float) * size_t(T) * H));
+    w.sx = reinterpret_cast<float *>(take(sizeof(float) * size_t(T) * (H / 128)));
+    w.sa = reinterpret_cast<float *>(take(sizeof(float) * R * (I / 128)));
     return w;
 }
 
@@ -289,25 +464,33 @@ hipError_t launch_prefill_ffn(const float *x, int T, int H, int I, int E, int k,
                               int dtype, const void *shared_w, float *y, bool accumulate, const PrefillWorkspace &ws,
                               int *err_flags, hipStream_t s) {
     if (T == 0) return hipSuccess;
+    if (!prefill_dtype_supported(dtype)) return hipErrorInvalidValue;
     const auto *pl = static_cast<const uint8_t *>(pool);
     const auto *sw = static_cast<const uint8_t *>(shared_w);
     const int has_shared = sw != nullptr;
-    hipError_t e = launch(prefill_align_kernel, dim3(1), dim3(kAlignThreads), 0, s, ids, T, k, E, slot_of, has_shared,
-                          ws, H, err_flags);
+    const size_t n8 = size_t(T) * H / 8;
+    const size_t cvt_blocks = std::min<size_t>(1024, (n8 + kPlanThreads - 1) / kPlanThreads);
+    hipError_t e = launch(prefill_plan_kernel, dim3(unsigned(1 + cvt_blocks)), dim3(kPlanThreads), 0, s, ids, T, k,
+                          E, slot_of, has_shared, x, H, dtype == INT4 ? 1 : 0, ws, err_flags);
     if (e != hipSuccess) return e;
     const int mt = max_tiles(T, k, E);
+    const int nb1 = (2 * I + kTileN - 1) / kTileN, nb2 = (H + kTileN - 1) / kTileN;
     const size_t doff = down_offset(H, I, dtype);
-    const dim3 g1(2 * I / kTileN, mt), g2(H / kTileN, mt);
-#define PF_CASE(DT)                                                                                          \
-    if (dtype == DT) {                                                                                       \
-        e = launch(prefill_gemm_kernel<DT, false>, g1, dim3(kBlock), 0, s, x, T, H, I, k, pl, expert_bytes, sw, \
-                   doff, ws);                                                                                \
-        if (e == hipSuccess)                                                                                 \
-            e = launch(prefill_gemm_kernel<DT, true>, g2, dim3(kBlock), 0, s, x, T, H, I, k, pl, expert_bytes, sw, \
-                       doff, ws);                                                                            \
+    // grids rounded up to whole XCD rounds: the block -> work map needs 8 * ceil(work / 8) blocks
+    const unsigned g1 = unsigned((mt * nb1 + kXcds - 1) / kXcds * kXcds), g2 = unsigned((mt * nb2 + kXcds - 1) / kXcds * kXcds);
+    if (dtype == INT4) {
+        e = launch(prefill_gemm_kernel<INT4, false>, dim3(g1), dim3(kBlock), 0, s, T, H, I, k, pl,
+                   expert_bytes, sw, doff, nb1, ws);
+        if (e == hipSuccess)
+            e = launch(prefill_gemm_kernel<INT4, true>, dim3(g2), dim3(kBlock), 0, s, T, H, I, k, pl,
+                       expert_bytes, sw, doff, nb2, ws);
+    } else {
+        e = launch(prefill_gemm_kernel<BF16, false>, dim3(g1), dim3(kBlock), 0, s, T, H, I, k, pl,
+                   expert_bytes, sw, doff, nb1, ws);
+        if (e == hipSuccess)
+            e = launch(prefill_gemm_kernel<BF16, true>, dim3(g2), dim3(kBlock), 0, s, T, H, I, k, pl,
+                       expert_bytes, sw, doff, nb2, ws);
     }
-    PF_CASE(F32) PF_CASE(BF16) PF_CASE(INT4)
-#undef PF_CASE
     if (e != hipSuccess) return e;
     return launch_combine(ws.y_part, weights, has_shared ? ws.y_shared : nullptr, T, k, H, y, accumulate, s);
 }

@@ -72,6 +72,19 @@ def test_route_parity_configs(cfg, T, norm):
         check_route(x, wr, wl.router_dtype, wl.k, norm=norm)
 
 
+@pytest.mark.parametrize("norm", [False, True])
+def test_route_prefill_chunk_and_ragged_tiles(norm):
+    """Many-token routing (the matrix-core router): config 5's 2048-token chunk over 256 experts, and a
+    ragged 70 x 130 case whose last token and expert tiles are partial."""
+    wl = synth.workload(5, L=1)
+    check_route(synth.prefill_states(wl), synth.router_weights(wl, 0), wl.router_dtype, wl.k, norm=norm)
+    rng = np.random.default_rng(130)
+    x = (rng.standard_normal((70, 384)) * 3.0).astype(np.float32)
+    wr = synth.bf16_bits(rng.standard_normal((130, 384)).astype(np.float32) * 0.05)
+    bias = rng.standard_normal((70, 130)).astype(np.float32)
+    check_route(x, wr, synth.BF16, 5, bias, norm=norm)
+
+
 def test_route_with_mask_bias_selects_the_drawn_sets():
     wl = synth.workload(3, T=16)
     wr = synth.router_weights(wl, 0)
@@ -406,3 +419,14 @@ def test_prefill_invalid_ids_contribute_nothing():
     ref = oracle.moe_ffn(x, ok_ids, np.full((3, 1), 0.5), ex, wl.H, wl.I, wl.dtype)
     ref[1] += 0.5 * oracle.expert_forward(x[1], ex[2], wl.H, wl.I, wl.dtype)
     assert normwise(y.cpu().numpy(), ref) <= PREFILL_TOL[wl.dtype]
+
+
+def test_prefill_rejects_fp32_weights():
+    wl = synth.Workload("prefill-f32", H=256, E=4, k=2, I=128, dtype=synth.F32, cfg_id=97)
+    ex, _ = _experts(wl)
+    x = np.zeros((2, 256), np.float32)
+    ids = np.array([[0, 1], [2, 3]], np.int32)
+    w = np.full((2, 2), 0.5, np.float32)
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_prefill_grouped(dev(x), dev(ids), dev(w), dev(ex.reshape(-1)), wl.expert_bytes, wl.dtype, wl.I, wl.E)
+    assert ei.value.code == -1
