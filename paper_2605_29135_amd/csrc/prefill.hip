@@ -20,6 +20,7 @@
 #include "device_common.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace moe {
 namespace {
@@ -261,155 +262,166 @@ __global__ __launch_bounds__(kBlock, 2) void prefill_gemm_kernel(int T, int H, i
         }
     }
 
-    floatx4 acc[4][4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    // The main loop and the epilogue are instantiated for 1..4 live 16-row blocks: 16-row blocks that
+    // are all padding take no MFMA, A read or fold (a group of 70 rows has a second tile of 6 rows).
+    auto body = [&](auto mb_tag) __attribute__((always_inline)) {
+        constexpr int MB = decltype(mb_tag)::value;
+        floatx4 acc[MB][4];
+    #pragma unroll
+        for (int i = 0; i < MB; ++i)
+    #pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
-    u32x4 ra[R::A16];       // next round's A segment of this thread
-    uint4 rb[4][R::B16];    // next round's weights of this lane, one entry per 16-column block
-    uint32_t rsb[4] = {0u, 0u, 0u, 0u};  // their raw bf16 scale bits (widened at use: no wait after the load)
-    float rS = 0.f;         // next round's group sum of row tid (int4, tid < 64)
-    // 32-bit byte offsets of this lane's weight rows (and scale rows) within the expert matrix
-    uint32_t boff[4], soff[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-        const uint32_t n = uint32_t(min(wn0 + 16 * j + lr, N - 1));
-        boff[j] = DT == INT4 ? n * uint32_t(K / 2) + uint32_t(R::SEG * lg / 2) : (n * uint32_t(K) + uint32_t(R::SEG * lg)) * 2u;
-        soff[j] = n * uint32_t(KG);
-    }
-    const int rounds = K / R::BK;
-    // Software pipeline: iteration r issues round r+1's loads, multiplies round r out of LDS and
-    // registers, then stores round r+1's A into the other LDS buffer.
-    for (int r = -1; r < rounds; ++r) {
-        uint4 cb[4][R::B16];
-        float cs[4];
-#pragma unroll
+        u32x4 ra[R::A16];       // next round's A segment of this thread
+        uint4 rb[4][R::B16];    // next round's weights of this lane, one entry per 16-column block
+        uint32_t rsb[4] = {0u, 0u, 0u, 0u};  // their raw bf16 scale bits (widened at use: no wait after the load)
+        float rS = 0.f;         // next round's group sum of row tid (int4, tid < 64)
+        // 32-bit byte offsets of this lane's weight rows (and scale rows) within the expert matrix
+        uint32_t boff[4], soff[4];
+    #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            cs[j] = bf16_bits_to_float(rsb[j]);
-#pragma unroll
-            for (int i = 0; i < R::B16; ++i) cb[j][i] = rb[j][i];
+            const uint32_t n = uint32_t(min(wn0 + 16 * j + lr, N - 1));
+            boff[j] = DT == INT4 ? n * uint32_t(K / 2) + uint32_t(R::SEG * lg / 2) : (n * uint32_t(K) + uint32_t(R::SEG * lg)) * 2u;
+            soff[j] = n * uint32_t(KG);
         }
-        if (r + 1 < rounds) {
-            const int k0 = (r + 1) * R::BK;
-#pragma unroll
-            for (int i = 0; i < R::A16; ++i) ra[i] = *reinterpret_cast<const u32x4 *>(asrc + k0 + sc + 8 * i);
-            if constexpr (kOffset) {
-                if (tid < kTileM) rS = ssrc[r + 1];
-            }
-#pragma unroll
+        const int rounds = K / R::BK;
+        // Software pipeline: iteration r issues round r+1's loads, multiplies round r out of LDS and
+        // registers, then stores round r+1's A into the other LDS buffer.
+        for (int r = -1; r < rounds; ++r) {
+            uint4 cb[4][R::B16];
+            float cs[4];
+    #pragma unroll
             for (int j = 0; j < 4; ++j) {
-                if constexpr (DT == INT4) {
-                    rb[j][0] = *reinterpret_cast<const uint4 *>(bmat + boff[j] + uint32_t(k0 / 2));
-                    rsb[j] = bscale[soff[j] + uint32_t(k0 / 128)];
-                } else {
-#pragma unroll
-                    for (int i = 0; i < R::B16; ++i)
-                        rb[j][i] = *reinterpret_cast<const uint4 *>(bmat + boff[j] + uint32_t(k0 * 2 + 16 * i));
-                }
+                cs[j] = bf16_bits_to_float(rsb[j]);
+    #pragma unroll
+                for (int i = 0; i < R::B16; ++i) cb[j][i] = rb[j][i];
             }
-        }
-        if (r >= 0) {
-            const int buf = r & 1;
-            floatx4 tmp[4][4];
-#pragma unroll
-            for (int s = 0; s < R::STEPS; ++s) {
-                bf16x8 a[4];
-#pragma unroll
-                for (int i = 0; i < 4; ++i)
-                    a[i] = *reinterpret_cast<const bf16x8 *>(&As[buf][(16 * i + lr) * R::LDS + R::SEG * lg + 8 * s]);
-#pragma unroll
+            if (r + 1 < rounds) {
+                const int k0 = (r + 1) * R::BK;
+    #pragma unroll
+                for (int i = 0; i < R::A16; ++i) ra[i] = *reinterpret_cast<const u32x4 *>(asrc + k0 + sc + 8 * i);
+                if constexpr (kOffset) {
+                    if (tid < kTileM) rS = ssrc[r + 1];
+                }
+    #pragma unroll
                 for (int j = 0; j < 4; ++j) {
-                    if constexpr (kOffset) {
-                        const uint32_t d = s == 0 ? cb[j][0].x : s == 1 ? cb[j][0].y : s == 2 ? cb[j][0].z : cb[j][0].w;
-                        const bf16x8 b = int4_offset8(d);
-#pragma unroll
-                        for (int i = 0; i < 4; ++i)
-                            tmp[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
-                                a[i], b, s == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : tmp[i][j], 0, 0, 0);
+                    if constexpr (DT == INT4) {
+                        rb[j][0] = *reinterpret_cast<const uint4 *>(bmat + boff[j] + uint32_t(k0 / 2));
+                        rsb[j] = bscale[soff[j] + uint32_t(k0 / 128)];
                     } else {
-                        const bf16x8 b = __builtin_bit_cast(bf16x8, cb[j][s]);
-#pragma unroll
-                        for (int i = 0; i < 4; ++i)
-                            acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b, acc[i][j], 0, 0, 0);
+    #pragma unroll
+                        for (int i = 0; i < R::B16; ++i)
+                            rb[j][i] = *reinterpret_cast<const uint4 *>(bmat + boff[j] + uint32_t(k0 * 2 + 16 * i));
                     }
                 }
             }
-            if constexpr (kOffset) {
-                // rows of this lane: m = 16i + 4lg + q
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    const float4 sv = *reinterpret_cast<const float4 *>(&Ss[buf][16 * i + 4 * lg]);
-                    const float svq[4] = {sv.x, sv.y, sv.z, sv.w};
-#pragma unroll
+            if (r >= 0) {
+                const int buf = r & 1;
+                floatx4 tmp[MB][4];
+    #pragma unroll
+                for (int s = 0; s < R::STEPS; ++s) {
+                    bf16x8 a[MB];
+    #pragma unroll
+                    for (int i = 0; i < MB; ++i)
+                        a[i] = *reinterpret_cast<const bf16x8 *>(&As[buf][(16 * i + lr) * R::LDS + R::SEG * lg + 8 * s]);
+    #pragma unroll
                     for (int j = 0; j < 4; ++j) {
-                        const float off = -136.f * cs[j];
-#pragma unroll
-                        for (int q = 0; q < 4; ++q) acc[i][j][q] = fmaf(cs[j], tmp[i][j][q], fmaf(off, svq[q], acc[i][j][q]));
+                        if constexpr (kOffset) {
+                            const uint32_t d = s == 0 ? cb[j][0].x : s == 1 ? cb[j][0].y : s == 2 ? cb[j][0].z : cb[j][0].w;
+                            const bf16x8 b = int4_offset8(d);
+    #pragma unroll
+                            for (int i = 0; i < MB; ++i)
+                                tmp[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(
+                                    a[i], b, s == 0 ? floatx4{0.f, 0.f, 0.f, 0.f} : tmp[i][j], 0, 0, 0);
+                        } else {
+                            const bf16x8 b = __builtin_bit_cast(bf16x8, cb[j][s]);
+    #pragma unroll
+                            for (int i = 0; i < MB; ++i)
+                                acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a[i], b, acc[i][j], 0, 0, 0);
+                        }
+                    }
+                }
+                if constexpr (kOffset) {
+                    // rows of this lane: m = 16i + 4lg + q
+    #pragma unroll
+                    for (int i = 0; i < MB; ++i) {
+                        const float4 sv = *reinterpret_cast<const float4 *>(&Ss[buf][16 * i + 4 * lg]);
+                        const float svq[4] = {sv.x, sv.y, sv.z, sv.w};
+    #pragma unroll
+                        for (int j = 0; j < 4; ++j) {
+                            const float off = -136.f * cs[j];
+    #pragma unroll
+                            for (int q = 0; q < 4; ++q) acc[i][j][q] = fmaf(cs[j], tmp[i][j][q], fmaf(off, svq[q], acc[i][j][q]));
+                        }
                     }
                 }
             }
-        }
-        if (r + 1 < rounds) {
-            u32x4 *dst = reinterpret_cast<u32x4 *>(&As[(r + 1) & 1][sr * R::LDS + sc]);
-#pragma unroll
-            for (int i = 0; i < R::A16; ++i) dst[i] = ra[i];
-            if constexpr (kOffset) {
-                if (tid < kTileM) Ss[(r + 1) & 1][tid] = rS;
+            if (r + 1 < rounds) {
+                u32x4 *dst = reinterpret_cast<u32x4 *>(&As[(r + 1) & 1][sr * R::LDS + sc]);
+    #pragma unroll
+                for (int i = 0; i < R::A16; ++i) dst[i] = ra[i];
+                if constexpr (kOffset) {
+                    if (tid < kTileM) Ss[(r + 1) & 1][tid] = rS;
+                }
             }
+            __syncthreads();
         }
-        __syncthreads();
-    }
 
-    // epilogue: lane holds C[m = 16i + 4*lg + q][n = wn0 + 16j + lr]
-    float rowsum[4][4];  // int4 gate/up: this lane's bf16 activations summed per row
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            rowsum[i][q] = 0.f;
-            const int m = 16 * i + 4 * lg + q;
-            const int p = arow[m];
-#pragma unroll
-            for (int j = 0; j < 4; ++j) {
-                const int n = wn0 + 16 * j + lr;
-                const float v = acc[i][j][q];
-                if constexpr (DOWN) {
-                    if (active && p >= 0) {
-                        float *o = p < P ? ws.y_part + size_t(p) * H : ws.y_shared + size_t(p - P) * H;
-                        o[n] = v;
-                    }
-                } else {
-                    // W_gu rows 2i (gate) and 2i+1 (up) sit in neighbouring lanes
-                    const float partner = dpp<0xB1>(v);
-                    if ((lr & 1) == 0 && active && p >= 0) {
-                        const float a = v * __builtin_amdgcn_rcpf(1.f + __expf(-v)) * partner;
-                        const uint32_t ab = pack2(a, 0.f) & 0xffffu;
-                        const int c = n / 2;
-                        const int pos = kOffset ? (c & ~7) + perm8_pos(c & 7) : c;
-                        ws.act[size_t(base + m) * I + pos] = uint16_t(ab);
-                        rowsum[i][q] += __uint_as_float(ab << 16);
+        // epilogue: lane holds C[m = 16i + 4*lg + q][n = wn0 + 16j + lr]
+        float rowsum[MB][4];  // int4 gate/up: this lane's bf16 activations summed per row
+    #pragma unroll
+        for (int i = 0; i < MB; ++i)
+    #pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                rowsum[i][q] = 0.f;
+                const int m = 16 * i + 4 * lg + q;
+                const int p = arow[m];
+    #pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int n = wn0 + 16 * j + lr;
+                    const float v = acc[i][j][q];
+                    if constexpr (DOWN) {
+                        if (active && p >= 0) {
+                            float *o = p < P ? ws.y_part + size_t(p) * H : ws.y_shared + size_t(p - P) * H;
+                            o[n] = v;
+                        }
+                    } else {
+                        // W_gu rows 2i (gate) and 2i+1 (up) sit in neighbouring lanes
+                        const float partner = dpp<0xB1>(v);
+                        if ((lr & 1) == 0 && active && p >= 0) {
+                            const float a = v * __builtin_amdgcn_rcpf(1.f + __expf(-v)) * partner;
+                            const uint32_t ab = pack2(a, 0.f) & 0xffffu;
+                            const int c = n / 2;
+                            const int pos = kOffset ? (c & ~7) + perm8_pos(c & 7) : c;
+                            ws.act[size_t(base + m) * I + pos] = uint16_t(ab);
+                            rowsum[i][q] += __uint_as_float(ab << 16);
+                        }
                     }
                 }
             }
+        if constexpr (kOffset && !DOWN) {
+            // group sums of the activations for the down GEMM: this block's 256 gate/up columns are
+            // the 128 activation columns of down group nb
+    #pragma unroll
+            for (int i = 0; i < MB; ++i)
+    #pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    float v = rowsum[i][q];
+                    v += __shfl_xor(v, 1);
+                    v += __shfl_xor(v, 2);
+                    v += __shfl_xor(v, 4);
+                    v += __shfl_xor(v, 8);
+                    if (lr == 0) Sred[wave][16 * i + 4 * lg + q] = v;
+                }
+            __syncthreads();
+            if (tid < rows) ws.sa[size_t(base + tid) * (I / 128) + nb] = Sred[0][tid] + Sred[1][tid] + Sred[2][tid] + Sred[3][tid];
         }
-    if constexpr (kOffset && !DOWN) {
-        // group sums of the activations for the down GEMM: this block's 256 gate/up columns are
-        // the 128 activation columns of down group nb
-#pragma unroll
-        for (int i = 0; i < 4; ++i)
-#pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                float v = rowsum[i][q];
-                v += __shfl_xor(v, 1);
-                v += __shfl_xor(v, 2);
-                v += __shfl_xor(v, 4);
-                v += __shfl_xor(v, 8);
-                if (lr == 0) Sred[wave][16 * i + 4 * lg + q] = v;
-            }
-        __syncthreads();
-        if (tid < rows) ws.sa[size_t(base + tid) * (I / 128) + nb] = Sred[0][tid] + Sred[1][tid] + Sred[2][tid] + Sred[3][tid];
+    };
+    switch ((rows + 15) / 16) {
+        case 1: body(std::integral_constant<int, 1>{}); break;
+        case 2: body(std::integral_constant<int, 2>{}); break;
+        case 3: body(std::integral_constant<int, 3>{}); break;
+        default: body(std::integral_constant<int, 4>{}); break;
     }
 }
 
