@@ -284,6 +284,7 @@ typedef struct {
     const void *const *shared_w;    /* host array [L] of device shared-expert blobs, or NULL */
     moe_cache *cache;               /* residency of the routed experts */
     int max_tokens;                 /* largest T passed to moe_stack_decode_step (<= 16) */
+    int max_prefill_tokens;         /* largest T passed to moe_stack_prefill (0: no prefill) */
 } moe_stack_desc;
 
 MOE_API int moe_stack_create(const moe_stack_desc *desc, moe_stack **out);
@@ -298,6 +299,18 @@ MOE_API int moe_stack_destroy(moe_stack *s);
  * receive each layer's routing when non-NULL. */
 MOE_API int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *logit_bias,
                           int32_t *ids_out, float *weights_out, void *stream);
+
+/* Prompt evaluation (prefill; its rate is reported beside decode in the table
+ * of sec. 8.1) over every layer, in place on x (device fp32 [T x H]):
+ * x <- x + MoE_l(rmsnorm(x)) for l = 0..L-1, with each layer's routing on the
+ * matrix cores when the router is bf16 and T >= 16, and its expert FFN by
+ * moe_prefill_grouped (bf16 activations on the matrix cores; w_dtype MOE_BF16 or
+ * MOE_INT4G128).  Under a budget each layer copies its T*k ids to the host and
+ * runs one lookup for the chunk's distinct experts, which must fit in the cache
+ * (MOE_ERR_BUDGET otherwise).  1 <= T <= max_prefill_tokens; ids_out / weights_out
+ * as for moe_stack_decode_step; `step` is the residency step of the chunk. */
+MOE_API int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out, float *weights_out,
+                              void *stream);
 
 /* Mean device time (ms) of one launch of kernel `which` (0 = router logits and
  * top-k, 1 = expert gate/up + SwiGLU, 2 = expert down + combine).  Each

@@ -54,7 +54,8 @@ EVENT_DTYPE = np.dtype([("t", "<i4"), ("layer", "<i4"), ("expert", "<i4"),
 class StackDesc(C.Structure):
     _fields_ = [("n_layers", C.c_int), ("H", C.c_int), ("I", C.c_int), ("E", C.c_int), ("k", C.c_int),
                 ("w_dtype", C.c_int), ("router_dtype", C.c_int), ("router_w", C.POINTER(C.c_void_p)),
-                ("shared_w", C.POINTER(C.c_void_p)), ("cache", C.c_void_p), ("max_tokens", C.c_int)]
+                ("shared_w", C.POINTER(C.c_void_p)), ("cache", C.c_void_p), ("max_tokens", C.c_int),
+                ("max_prefill_tokens", C.c_int)]
 
 
 _lib = None
@@ -88,6 +89,7 @@ def lib() -> C.CDLL:
             "moe_stack_destroy": [P],
             "moe_stack_decode_step": [P, I, P, I, P, P, P, P],
             "moe_stack_kernel_time": [P, I, I, P, C.POINTER(C.c_double)],
+            "moe_stack_prefill": [P, I, P, I, P, P, P],
             "moe_hbm_read_probe": [P, SZ, P, P],
         }
         for name, args in sig.items():
@@ -305,10 +307,10 @@ class ExpertCache:
 
 
 class MoeStack:
-    """Owner of one moe_stack (decode step over L MoE layers on a cache)."""
+    """Owner of one moe_stack (decode steps and prefill chunks over L MoE layers on a cache)."""
 
     def __init__(self, cache: ExpertCache, H: int, I: int, E: int, k: int, w_dtype: int, router_dtype: int,
-                 router_w: list, shared_w: list | None = None, max_tokens: int = 1):
+                 router_w: list, shared_w: list | None = None, max_tokens: int = 1, max_prefill_tokens: int = 0):
         self._router = (C.c_void_p * len(router_w))(*[_dev(w, "router_w") for w in router_w])
         self._shared = None
         if shared_w is not None:
@@ -317,7 +319,7 @@ class MoeStack:
         d = StackDesc(len(router_w), H, I, E, k, w_dtype, router_dtype,
                       C.cast(self._router, C.POINTER(C.c_void_p)),
                       C.cast(self._shared, C.POINTER(C.c_void_p)) if self._shared is not None else None,
-                      cache.handle, max_tokens)
+                      cache.handle, max_tokens, max_prefill_tokens)
         h = C.c_void_p()
         _check(lib().moe_stack_create(C.byref(d), C.byref(h)), "moe_stack_create")
         self._h = h
@@ -339,6 +341,16 @@ class MoeStack:
                                            _dev(ids_out, "ids_out", torch.int32),
                                            _dev(weights_out, "weights_out", torch.float32), _stream(stream)),
                "moe_stack_decode_step")
+        return x
+
+    def prefill(self, step: int, x, ids_out=None, weights_out=None, stream=None):
+        """Prompt chunk: x <- x + MoE_l(rmsnorm(x)) over every layer, in place on the device tensor x [T x H]."""
+        import torch
+        T = x.shape[0]
+        _check(lib().moe_stack_prefill(self._h, step, _dev(x, "x", torch.float32), T,
+                                       _dev(ids_out, "ids_out", torch.int32),
+                                       _dev(weights_out, "weights_out", torch.float32), _stream(stream)),
+               "moe_stack_prefill")
         return x
 
     def kernel_time(self, which: int, n: int = 200, stream=None) -> float:

@@ -1,7 +1,9 @@
-// stack.cpp -- decode step over a stack of MoE layers: x <- x + MoE_l(rmsnorm(x)),
-// l = 0..L-1 (attention is the identity; the pre-norm is fused into the router).  Under a budget each layer brings its ids to
-// the host, runs the slot lookup, then enqueues the expert FFN and releases
-// the slots; with every expert resident the whole step stays on the device.
+// stack.cpp -- decode step and prefill chunk over a stack of MoE layers:
+// x <- x + MoE_l(rmsnorm(x)), l = 0..L-1 (attention is the identity; for a
+// decode step the pre-norm is fused into the router).  Under a budget each
+// layer brings its ids to the host, runs the slot lookup, then enqueues the
+// expert FFN and releases the slots; with every expert resident the whole
+// step stays on the device.
 #include <string.h>
 
 #include <vector>
@@ -39,6 +41,9 @@ struct moe_stack {
     int32_t *slots_host = nullptr; // [Tmax x k] slot of each id after the lookup
     void *ws = nullptr;
     size_t ws_bytes = 0;
+    void *pws = nullptr;        // prefill workspace (max_prefill_tokens > 0)
+    size_t pws_bytes = 0;
+    int tcap = 0;               // rows of the per-token buffers: max(max_tokens, max_prefill_tokens)
     hipEvent_t ids_ready = nullptr;
     float *scratch_x = nullptr;  // device [Tmax x H] scratch input/output of kernel re-launches
     float *scratch_y = nullptr;  // device [Tmax x H]
@@ -57,6 +62,7 @@ int moe_stack_destroy(moe_stack *s) {
     if (s->ids_host) (void)hipHostFree(s->ids_host);
     delete[] s->slots_host;
     if (s->ws) (void)hipFree(s->ws);
+    if (s->pws) (void)hipFree(s->pws);
     if (s->ids_ready) (void)hipEventDestroy(s->ids_ready);
     if (s->scratch_x) (void)hipFree(s->scratch_x);
     if (s->scratch_y) (void)hipFree(s->scratch_y);
@@ -71,6 +77,10 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: bad L/E/k (%d/%d/%d)", d->n_layers, d->E, d->k);
     if (d->max_tokens < 1 || d->max_tokens > MOE_MAX_DECODE_TOKENS)
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: max_tokens must be in [1, %d]", MOE_MAX_DECODE_TOKENS);
+    if (d->max_prefill_tokens < 0 || d->max_prefill_tokens > (1 << 20))
+        return moe::fail(MOE_ERR_INVALID_ARG, "stack: max_prefill_tokens must be in [0, 2^20]");
+    if (d->max_prefill_tokens > 0 && !moe::prefill_dtype_supported(d->w_dtype))
+        return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefill needs MOE_BF16 or MOE_INT4G128 experts");
     if (!moe::ffn_shape_supported(d->H, d->I, d->w_dtype) || !moe::router_shape_supported(d->H, d->router_dtype))
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: unsupported H/I/dtype");
     if (!d->router_w || !d->cache) return moe::fail(MOE_ERR_INVALID_ARG, "stack: router weights and cache required");
@@ -93,7 +103,8 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
         delete s;
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: cache slots are smaller than one expert blob");
     }
-    const int T = d->max_tokens;
+    const int T = d->max_tokens > d->max_prefill_tokens ? d->max_tokens : d->max_prefill_tokens;
+    s->tcap = T;
     hipError_t e;
     auto bail = [&](hipError_t err, const char *what) {
         int code = moe::fail_hip(err, what);
@@ -107,12 +118,17 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
     if ((e = hipHostMalloc(&s->ids_host, sizeof(int32_t) * T * d->k, 0)) != hipSuccess) return bail(e, "stack buffers");
     s->slots_host = new int32_t[size_t(T) * d->k];
     s->last.assign(d->n_layers, LastLayer{});
-    s->ws_bytes = moe::ffn_workspace_bytes(T, d->k, d->I);
+    s->ws_bytes = moe::ffn_workspace_bytes(d->max_tokens, d->k, d->I);
     if ((e = hipMalloc(&s->ws, s->ws_bytes)) != hipSuccess) return bail(e, "stack workspace");
+    if (d->max_prefill_tokens > 0) {
+        s->pws_bytes = moe::prefill_workspace_bytes(d->max_prefill_tokens, d->k, d->E, d->H, d->I);
+        if ((e = hipMalloc(&s->pws, s->pws_bytes)) != hipSuccess) return bail(e, "stack prefill workspace");
+    }
     if ((e = hipEventCreateWithFlags(&s->ids_ready, hipEventDisableTiming)) != hipSuccess)
         return bail(e, "stack event");
-    if ((e = hipMalloc(&s->scratch_x, sizeof(float) * T * d->H)) != hipSuccess) return bail(e, "stack buffers");
-    if ((e = hipMalloc(&s->scratch_y, sizeof(float) * T * d->H)) != hipSuccess) return bail(e, "stack buffers");
+    const size_t Td = size_t(d->max_tokens);
+    if ((e = hipMalloc(&s->scratch_x, sizeof(float) * Td * d->H)) != hipSuccess) return bail(e, "stack buffers");
+    if ((e = hipMalloc(&s->scratch_y, sizeof(float) * Td * d->H)) != hipSuccess) return bail(e, "stack buffers");
     *out = s;
     moe::clear_error();
     return MOE_OK;
@@ -162,6 +178,49 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
                                    plan.n ? &plan : nullptr);
         s->last[l] = LastLayer{true, T, l, ids, w, slot_of, pool, plan};
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: expert FFN");
+        if (s->budgeted) {
+            int st = expert_cache_release(d.cache, strm);
+            if (st != MOE_OK) return st;
+        }
+    }
+    moe::clear_error();
+    return MOE_OK;
+}
+
+int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out, float *weights_out,
+                      void *stream) {
+    if (!s || !x) return moe::fail(MOE_ERR_INVALID_ARG, "stack prefill: NULL argument");
+    if (s->d.max_prefill_tokens < 1) return moe::fail(MOE_ERR_INVALID_ARG, "stack prefill: created without prefill");
+    if (T < 1 || T > s->d.max_prefill_tokens)
+        return moe::fail(MOE_ERR_INVALID_ARG, "stack prefill: T=%d outside [1, %d]", T, s->d.max_prefill_tokens);
+    auto strm = static_cast<hipStream_t>(stream);
+    int *eflags = moe::device_error_flags();
+    if (!eflags) return moe::fail(MOE_ERR_HIP, "device error flags unavailable");
+    const auto &d = s->d;
+    const moe::PrefillWorkspace ws = moe::prefill_workspace(s->pws, T, d.k, d.E, d.H, d.I);
+    for (int l = 0; l < d.n_layers; ++l) {
+        int32_t *ids = ids_out ? ids_out + size_t(l) * T * d.k : s->ids;
+        float *w = weights_out ? weights_out + size_t(l) * T * d.k : s->weights;
+        hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, nullptr, s->logits,
+                                                 true, s->h, strm);
+        if (e == hipSuccess) e = moe::launch_topk_softmax(s->logits, T, d.E, d.k, ids, w, eflags, strm);
+        if (e != hipSuccess) return moe::fail_hip(e, "stack prefill: routing");
+        const int32_t *slot_of = s->slot_table + size_t(l) * d.E;
+        const uint8_t *pool = static_cast<const uint8_t *>(s->pool);
+        if (s->budgeted) {
+            e = hipMemcpyAsync(s->ids_host, ids, sizeof(int32_t) * T * d.k, hipMemcpyDeviceToHost, strm);
+            if (e == hipSuccess) e = hipEventRecord(s->ids_ready, strm);
+            if (e == hipSuccess) e = hipEventSynchronize(s->ids_ready);
+            if (e != hipSuccess) return moe::fail_hip(e, "stack prefill: ids to host");
+            int st = expert_cache_lookup(d.cache, step, l, s->ids_host, T * d.k, s->slots_host, nullptr, strm);
+            if (st != MOE_OK) return st;
+        } else {
+            pool += size_t(l) * d.E * s->expert_bytes;  // preloaded: expert e of layer l sits at slot l * E + e
+            slot_of = nullptr;
+        }
+        e = moe::launch_prefill_ffn(s->h, T, d.H, d.I, d.E, d.k, ids, w, slot_of, pool, s->expert_bytes, d.w_dtype,
+                                    s->shared_w.empty() ? nullptr : s->shared_w[l], x, true, ws, eflags, strm);
+        if (e != hipSuccess) return moe::fail_hip(e, "stack prefill: expert FFN");
         if (s->budgeted) {
             int st = expert_cache_release(d.cache, strm);
             if (st != MOE_OK) return st;

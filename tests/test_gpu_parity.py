@@ -430,3 +430,100 @@ def test_prefill_rejects_fp32_weights():
     with pytest.raises(moe.MoeError) as ei:
         moe.moe_prefill_grouped(dev(x), dev(ids), dev(w), dev(ex.reshape(-1)), wl.expert_bytes, wl.dtype, wl.I, wl.E)
     assert ei.value.code == -1
+
+
+# ---------------------------------------------------------- stack prefill ---
+def _oracle_chain(wl, x0, g_ids, g_w, host_layers):
+    """x <- x + MoE_l(rmsnorm(x)) per layer in fp64, routed by the given ids and weights."""
+    xr = x0.astype(np.float64)
+    for l in range(wl.L):
+        if l not in host_layers:
+            host_layers[l] = synth.layer_experts(wl, l)
+        sh = synth.expert_blob(wl, l, None) if wl.shared else None
+        hr = oracle.rmsnorm(xr.astype(np.float32)).astype(np.float32)
+        xr = xr + oracle.moe_ffn(hr, g_ids[l], g_w[l].astype(np.float64), host_layers[l], wl.H, wl.I, wl.dtype, sh)
+    return xr
+
+
+@pytest.mark.parametrize("dtype,shared", [(synth.BF16, False), (synth.INT4G128, True)])
+def test_stack_prefill_then_decode_budgeted(dtype, shared):
+    """A prompt chunk through a budgeted stack whose layers evict each other (one layer's experts fit, three
+    do not), then decode steps on the same cache: the residency log equals the oracle LRU's, and outputs match
+    the oracle chain routed by the GPU's ids."""
+    H = 2048 if dtype == synth.INT4G128 else 512
+    wl = synth.Workload("prefill stack", H=H, E=32, k=4, I=256, L=3, dtype=dtype, shared=shared,
+                        routing="zipf_overlap", cfg_id=110 + dtype)
+    capacity, T, steps = 40, 96, 3
+    buf = _pinned_store(wl)
+    eb = wl.expert_bytes
+    reserved = wl.L * eb if shared else 0
+    cache = moe.ExpertCache(wl.L, wl.E, eb, capacity * eb + reserved, buf.ptr, wl.E * eb, eb, reserved_bytes=reserved)
+    routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
+    shw = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)] if shared else None
+    stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shw, max_tokens=1,
+                         max_prefill_tokens=T)
+    o = oracle.LRU(capacity, wl.L, wl.E)
+    host_layers = {}
+    x0 = np.random.default_rng(dtype).standard_normal((T, wl.H)).astype(np.float32)
+    x = dev(x0)
+    ids = torch.empty((wl.L, T, wl.k), dtype=torch.int32, device=DEV)
+    w = torch.empty((wl.L, T, wl.k), dtype=torch.float32, device=DEV)
+    stack.prefill(0, x, ids, w)
+    moe.moe_sync_check()
+    g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
+    for l in range(wl.L):
+        assert ((g_ids[l] >= 0) & (g_ids[l] < wl.E)).all()
+        assert np.allclose(g_w[l].sum(axis=1), 1.0, atol=1e-5)
+        assert o.lookup(0, l, g_ids[l].reshape(-1)) == oracle.OK
+    xr = _oracle_chain(wl, x0, g_ids, g_w, host_layers)
+    assert normwise(x.cpu().numpy() - x0, xr - x0) <= PREFILL_TOL[dtype]
+    sets = synth.routing_sets(wl, steps=steps)
+    for t in range(steps):
+        xd0 = synth.hidden_states(wl, t)
+        bias = np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)])
+        xd = dev(xd0)
+        di = torch.empty((wl.L, 1, wl.k), dtype=torch.int32, device=DEV)
+        dw = torch.empty((wl.L, 1, wl.k), dtype=torch.float32, device=DEV)
+        stack.decode_step(1 + t, xd, dev(bias), di, dw)
+        moe.moe_sync_check()
+        for l in range(wl.L):
+            assert o.lookup(1 + t, l, di.cpu().numpy()[l].reshape(-1)) == oracle.OK
+        xr = _oracle_chain(wl, xd0, di.cpu().numpy(), dw.cpu().numpy(), host_layers)
+        assert normwise(xd.cpu().numpy() - xd0, xr - xd0) <= TOL[dtype]
+    ev, oev = cache.trace(), o.events()
+    assert len(ev) == len(oev)
+    assert (ev.view(np.int32).reshape(-1, 6) == oev.view(np.int32).reshape(-1, 6)).all()
+    s = cache.stats()
+    assert s["evictions"] > 0 and s["occupancy"] <= capacity
+    stack.close()
+    cache.close()
+    buf.close()
+
+
+def test_stack_prefill_config5_two_layers_sampled():
+    """Config 5's full 2048-token chunk through two of its layers (6 GiB budget: 3923 slots), checked on
+    sampled tokens against the oracle chain."""
+    wl = synth.workload(5, L=2)
+    buf = _pinned_store(wl)
+    eb = wl.expert_bytes
+    reserved = wl.L * eb
+    cache = moe.ExpertCache(wl.L, wl.E, eb, wl.budget_bytes, buf.ptr, wl.E * eb, eb, reserved_bytes=reserved)
+    routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
+    shw = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)]
+    stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shw, max_tokens=1,
+                         max_prefill_tokens=wl.prefill)
+    x0 = synth.prefill_states(wl)
+    x = dev(x0)
+    ids = torch.empty((wl.L, wl.prefill, wl.k), dtype=torch.int32, device=DEV)
+    w = torch.empty((wl.L, wl.prefill, wl.k), dtype=torch.float32, device=DEV)
+    stack.prefill(0, x, ids, w)
+    moe.moe_sync_check()
+    sample = np.random.default_rng(5).choice(wl.prefill, 12, replace=False)
+    g_ids, g_w = ids.cpu().numpy()[:, sample], w.cpu().numpy()[:, sample]
+    xr = _oracle_chain(wl, x0[sample], g_ids, g_w, {})
+    assert normwise(x.cpu().numpy()[sample] - x0[sample], xr - x0[sample]) <= PREFILL_TOL[wl.dtype]
+    s = cache.stats()
+    assert s["misses"] == len(np.unique(ids.cpu().numpy()[0])) + len(np.unique(ids.cpu().numpy()[1]))
+    stack.close()
+    cache.close()
+    buf.close()
