@@ -196,7 +196,8 @@ typedef struct {
     size_t expert_bytes;       /* bytes of one expert blob; multiple of 256 */
     size_t budget_bytes;       /* HBM budget for expert weights */
     size_t reserved_bytes;     /* part of the budget held by always-resident weights (shared experts) */
-    const void *host_base;     /* pinned host store; expert (l, e) at host_base + l*host_layer_stride + e*host_expert_stride */
+    const void *host_base;     /* pinned host store, one hipHostMalloc allocation; expert (l, e) at
+                                  host_base + l*host_layer_stride + e*host_expert_stride (blob size a multiple of 16) */
     size_t host_layer_stride;  /* 0 lets layers alias one host copy (keys stay distinct) */
     size_t host_expert_stride;
     int policy;                /* MOE_POLICY_LRU */
@@ -222,6 +223,10 @@ typedef struct {
 
 /* Create a cache: allocates capacity * expert_bytes of HBM for the slots, a
  * copy stream and its events, and the device slot table int32 [L x E].
+ * Fills (selective loads, sec. 4) are done by kernels that read the blobs from
+ * the host store over PCIe, all of a lookup's fills and slot-table changes in
+ * one launch (per 32 fills): a demand lookup enqueues them on its compute
+ * stream, a prefetch on the cache's copy stream.
  * MOE_ERR_BUDGET if capacity < 1 (or < L*E with MOE_CACHE_PRELOAD);
  * MOE_ERR_NOT_PINNED if host_base is not hipHostMalloc memory.  PRELOAD fills
  * every slot synchronously before returning.  With MOE_CACHE_HOST_SIM no HIP

@@ -5,6 +5,8 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "../../include/moe_budget.h"
+
 struct moe_cache;
 
 namespace moe {
@@ -27,8 +29,14 @@ FfnWorkspace ffn_workspace(void *base, int T, int k, int I);
 // Kernel launchers (all asynchronous on `s`).  Shapes are validated by the caller.
 hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int T, int H, int E,
                                 const float *bias, float *logits, bool norm, float *h_out, hipStream_t s);
+// Host-visible mailbox for one token's ids (coherent pinned memory): the top-k
+// kernel writes ids[0..k), then, after a system-scope fence, seq.
+struct IdsMailbox {
+    uint32_t seq;
+    int32_t ids[MOE_MAX_TOPK];
+};
 hipError_t launch_topk_softmax(const float *logits, int T, int E, int k, int32_t *ids, float *weights,
-                               int *err_flags, hipStream_t s);
+                               int *err_flags, hipStream_t s, IdsMailbox *pub = nullptr, uint32_t seq = 0);
 
 // Which expert kernels launch_expert_ffn enqueues (grouping goes with gate/up).
 enum : int { kFfnGateUp = 1, kFfnDown = 2, kFfnBoth = 3 };
@@ -50,6 +58,20 @@ hipError_t launch_combine(const float *y_partial, const float *weights, const fl
                           int k, int H, float *y, bool accumulate, hipStream_t s);
 hipError_t launch_slot_update(int32_t *table, const int32_t *index, const int32_t *value, int n,
                               hipStream_t s);
+// A batch of expert fills (host blob -> HBM slot, `bytes` each, a multiple of
+// 16) and the slot-table changes that go with them, done by one kernel.
+constexpr int kMaxFillBatch = 32;
+struct FillBatch {
+    int n = 0;            // fills
+    int n_tab = 0;        // table entries
+    long long bytes = 0;  // bytes per fill
+    const uint8_t *src[kMaxFillBatch];  // pinned host memory, device-accessible
+    uint8_t *dst[kMaxFillBatch];
+    int32_t *table = nullptr;
+    int32_t tab_idx[2 * kMaxFillBatch];
+    int32_t tab_val[2 * kMaxFillBatch];
+};
+hipError_t launch_fill_slots(const FillBatch &b, hipStream_t s);
 hipError_t launch_hbm_read(const void *buf, size_t bytes, float *sink, hipStream_t s);
 
 // Prefill (any T): pairs grouped by expert, grouped bf16 MFMA GEMMs, rank-order combine.

@@ -125,14 +125,24 @@ __device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wou
 }
 
 // One wave per token.
+// With `pub` (one token), the wave also publishes its ids to host memory: the
+// ids, then a system-scope fence, then the sequence number `seq` in pub->seq,
+// so a host that sees the new sequence number reads complete ids.
 __global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__restrict__ logits, int T,
                                                               int E, int k, int32_t *__restrict__ ids,
-                                                              float *__restrict__ wout, int *err) {
+                                                              float *__restrict__ wout, int *err,
+                                                              IdsMailbox *pub, uint32_t seq) {
     __shared__ TopkScratch sc[kBlock / kWave];
     const int wave = threadIdx.x / kWave;
     const int t = blockIdx.x * (kBlock / kWave) + wave;
     if (t >= T) return;
     topk_wave<false>(logits + size_t(t) * E, E, k, ids + size_t(t) * k, wout + size_t(t) * k, err, &sc[wave]);
+    if (pub && t == 0) {
+        const int lane = threadIdx.x & (kWave - 1);
+        if (lane < k) pub->ids[lane] = ids[lane];  // this lane wrote ids[lane] itself
+        __threadfence_system();
+        if (lane == 0) __hip_atomic_store(&pub->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
 }
 
 // --------------------------------------------------------------- router ---
@@ -734,6 +744,37 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const float *__restrict
 }
 
 // ------------------------------------------------------------ slot table ---
+// Expert fills as one kernel: each block streams a share of one expert blob
+// from pinned host memory (read over PCIe) into its HBM slot; block (0, 0) also
+// writes the slot-table changes of the batch.  Later kernels on the stream see
+// both.  Reads of host memory need many bytes in flight: each thread keeps
+// kFillUnroll 16-byte loads outstanding.
+constexpr int kFillUnroll = 4;
+__global__ __launch_bounds__(kBlock) void fill_slots_kernel(FillBatch b) {
+    const int f = blockIdx.y;
+    if (f == 0 && blockIdx.x == 0)
+        for (int i = threadIdx.x; i < b.n_tab; i += kBlock) b.table[b.tab_idx[i]] = b.tab_val[i];
+    const size_t n16 = size_t(b.bytes) / 16;
+    const size_t per = (n16 + gridDim.x - 1) / gridDim.x;
+    const size_t beg = size_t(blockIdx.x) * per;
+    const size_t end = beg + per < n16 ? beg + per : n16;
+    const uint4 *src = reinterpret_cast<const uint4 *>(b.src[f]);
+    uint4 *dst = reinterpret_cast<uint4 *>(b.dst[f]);
+    for (size_t i = beg + threadIdx.x; i < end; i += size_t(kBlock) * kFillUnroll) {
+        uint4 v[kFillUnroll];
+#pragma unroll
+        for (int u = 0; u < kFillUnroll; ++u) {
+            const size_t j = i + size_t(u) * kBlock;
+            v[u] = j < end ? src[j] : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < kFillUnroll; ++u) {
+            const size_t j = i + size_t(u) * kBlock;
+            if (j < end) dst[j] = v[u];
+        }
+    }
+}
+
 constexpr int kSlotBatch = 32;
 struct SlotUpdates {
     int n;
@@ -842,9 +883,10 @@ hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int 
 }
 
 hipError_t launch_topk_softmax(const float *logits, int T, int E, int k, int32_t *ids, float *weights,
-                               int *err_flags, hipStream_t s) {
+                               int *err_flags, hipStream_t s, IdsMailbox *pub, uint32_t seq) {
     if (T == 0) return hipSuccess;
-    topk_softmax_kernel<<<(T + 3) / 4, kBlock, 0, s>>>(logits, T, E, k, ids, weights, err_flags);
+    if (pub && T != 1) return hipErrorInvalidValue;
+    topk_softmax_kernel<<<(T + 3) / 4, kBlock, 0, s>>>(logits, T, E, k, ids, weights, err_flags, pub, seq);
     return hipGetLastError();
 }
 
@@ -955,6 +997,16 @@ hipError_t launch_hbm_read(const void *buf, size_t bytes, float *sink, hipStream
     const size_t per_block = size_t(kReadLoads) * kBlock;  // 16-byte words per block
     const size_t blocks = (n16 + per_block - 1) / per_block;
     hbm_read_kernel<<<unsigned(blocks), kBlock, 0, s>>>(static_cast<const uint8_t *>(buf), n16, sink);
+    return hipGetLastError();
+}
+
+hipError_t launch_fill_slots(const FillBatch &b, hipStream_t s) {
+    if (b.n < 1 || b.n > kMaxFillBatch || b.n_tab < 0 || b.n_tab > 2 * kMaxFillBatch || b.bytes <= 0 || b.bytes % 16)
+        return hipErrorInvalidValue;
+    // about 64 blocks keep a 9 MiB blob's PCIe reads at full rate; smaller blobs take fewer
+    long long bpf = b.bytes / (128 << 10);
+    bpf = bpf < 4 ? 4 : (bpf > 64 ? 64 : bpf);
+    fill_slots_kernel<<<dim3(unsigned(bpf), unsigned(b.n)), kBlock, 0, s>>>(b);
     return hipGetLastError();
 }
 

@@ -43,19 +43,6 @@ __device__ __forceinline__ uint32_t pack2(float lo, float hi) {
     return __builtin_bit_cast(uint32_t, __builtin_convertvector(floatx2{lo, hi}, bf16x2));
 }
 
-// Eight signed nibbles of one dword (element e in bits 4e..4e+3) times a scale -> four packed bf16 pairs.
-__device__ __forceinline__ bf16x8 dequant8(uint32_t v, float s) {
-    uint32_t w[4];
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-        // the builtin returns the type of its source (unsigned): convert to int before widening
-        const float lo = float(int(__builtin_amdgcn_sbfe(v, 8 * e, 4))) * s;
-        const float hi = float(int(__builtin_amdgcn_sbfe(v, 8 * e + 4, 4))) * s;
-        w[e] = pack2(lo, hi);
-    }
-    return __builtin_bit_cast(bf16x8, make_uint4(w[0], w[1], w[2], w[3]));
-}
-
 // int4 -> bf16 with the offset form used by the grouped GEMM: for the eight
 // nibbles of one dword (element e in bits 4e..4e+3, two's complement q), the
 // bf16 pattern 0x4300 | (r ^ 8) is exactly 128 + (q + 8) = 136 + q.  Two bit

@@ -9,9 +9,14 @@
 // evicts the least recently used slot whose expert the same step does not need.
 //
 // Device ordering (per cache):
-//   copy stream : [wait last reader of each victim] [H2D fills] [slot-table update] -> fill event
-//   compute     : waits on the fill event, then the caller enqueues the FFN, then release()
-//                 records the slots' last-reader event.
+//   demand lookup : on the compute stream, after any earlier prefetch's fills:
+//                   [H2D fills] [slot-table update], then the caller's FFN, then
+//                   release() records the slots' last-reader event.  The fills
+//                   need no wait for a victim read on the same stream (stream
+//                   order already puts it first); a victim read on another
+//                   stream is waited for unless its event has completed.
+//   prefetch      : the same on the copy stream (waiting for the victims' last
+//                   readers), ending in an event the next demand lookup waits on.
 // Events come from a ring; an entry is synchronised before it is re-recorded,
 // so a slot whose reader entry was recycled has provably finished being read.
 #include <stdarg.h>
@@ -84,14 +89,17 @@ struct moe_cache {
     uint64_t epoch = 0;
 
     uint8_t *pool = nullptr;            // device (or host under sim) slots
+    const uint8_t *host_dev = nullptr;  // device-side address of the pinned host store (fill kernels read it)
     int32_t *dev_slot_of = nullptr;     // device (or host under sim) table [L*E]
     hipStream_t copy = nullptr;
     EventRing ring;
     std::vector<EvRef> reader;          // last recorded reader of each slot
+    std::vector<hipStream_t> reader_stream;  // the stream that reader ran on
     std::vector<int> unreleased;        // slots handed out by the last lookup
     hipStream_t last_compute = nullptr;
     bool have_last_compute = false;
     EvRef prefetch_done;                // copy-stream point after the latest prefetch's fills
+    std::vector<std::pair<const uint8_t *, uint8_t *>> pending;  // fills placed by the current lookup
 
     std::vector<moe_cache_event> log;
     moe_cache_stats st{};
@@ -135,7 +143,10 @@ int release_pending(moe_cache *c, hipStream_t s) {
         EvRef r;
         hipError_t e = c->ring.record(s, &r);
         if (e != hipSuccess) return moe::fail_hip(e, "recording slot release");
-        for (int slot : c->unreleased) c->reader[slot] = r;
+        for (int slot : c->unreleased) {
+            c->reader[slot] = r;
+            c->reader_stream[slot] = s;
+        }
     }
     c->unreleased.clear();
     return MOE_OK;
@@ -149,7 +160,7 @@ const uint8_t *host_blob(const moe_cache *c, int layer, int expert) {
 // Insert (layer, e) at a free or victim slot and queue its fill.  Returns the
 // slot, or -1 with the error recorded.
 int place_and_fill(moe_cache *c, int layer, int e, int32_t *victim, std::vector<int32_t> *chg_idx,
-                   std::vector<int32_t> *chg_val, int *status) {
+                   std::vector<int32_t> *chg_val, int *status, hipStream_t fill) {
     int s;
     *victim = -1;
     if (!c->free_slots.empty()) {
@@ -175,19 +186,15 @@ int place_and_fill(moe_cache *c, int layer, int e, int32_t *victim, std::vector<
     if (c->sim) {
         memcpy(dst, src, c->d.expert_bytes);
     } else {
-        if (c->ring.live(c->reader[s])) {
-            hipError_t r = hipStreamWaitEvent(c->copy, c->ring.event(c->reader[s]), 0);
-            if (r != hipSuccess) *status = moe::fail_hip(r, "ordering fill after last reader");
+        if (c->ring.live(c->reader[s]) && c->reader_stream[s] != fill) {
+            const hipEvent_t ev = c->ring.event(c->reader[s]);
+            if (hipEventQuery(ev) != hipSuccess) {
+                hipError_t r = hipStreamWaitEvent(fill, ev, 0);
+                if (r != hipSuccess) *status = moe::fail_hip(r, "ordering fill after last reader");
+            }
         }
-        hipError_t r = hipMemcpyAsync(dst, src, c->d.expert_bytes, hipMemcpyHostToDevice, c->copy);
-        if (r != hipSuccess) {
-            // the slot stays unmapped so that a retry misses again
-            c->free_slots.push(s);
-            c->key_of_slot[s] = -1;
-            *status = moe::fail(MOE_ERR_COPY, "fill of expert (%d, %d) failed: %s", layer, e,
-                                hipGetErrorString(r));
-            return -1;
-        }
+        // copied by the lookup's fill kernels, which read the store through its device-side address
+        c->pending.emplace_back(c->host_dev + (src - static_cast<const uint8_t *>(c->d.host_base)), dst);
     }
     c->key_of_slot[s] = key;
     c->slot_of_key[key] = s;
@@ -198,9 +205,11 @@ int place_and_fill(moe_cache *c, int layer, int e, int32_t *victim, std::vector<
     return s;
 }
 
-// Applies slot-table changes (last value per entry wins) after the fills on the
-// copy stream and returns the event marking the end of that work.
-int publish(moe_cache *c, std::vector<int32_t> &idx, std::vector<int32_t> &val, EvRef *done) {
+// Enqueues the lookup's fills and slot-table changes (last value per entry
+// wins) on `strm`: kernels that stream the blobs from host memory into their
+// slots and write the table entries; with `done`, records the event marking
+// the end of that work.  Under HOST_SIM the fills were done in place.
+int publish(moe_cache *c, std::vector<int32_t> &idx, std::vector<int32_t> &val, hipStream_t strm, EvRef *done) {
     std::vector<int32_t> ui, uv;
     for (size_t i = 0; i < idx.size(); ++i) {
         bool later = false;
@@ -215,10 +224,44 @@ int publish(moe_cache *c, std::vector<int32_t> &idx, std::vector<int32_t> &val, 
         for (size_t i = 0; i < ui.size(); ++i) c->dev_slot_of[ui[i]] = uv[i];
         return MOE_OK;
     }
-    hipError_t e = moe::launch_slot_update(c->dev_slot_of, ui.data(), uv.data(), int(ui.size()), c->copy);
-    if (e != hipSuccess) return moe::fail_hip(e, "slot-table update");
-    e = c->ring.record(c->copy, done);
-    if (e != hipSuccess) return moe::fail_hip(e, "recording fill event");
+    const size_t nf = c->pending.size();
+    const size_t nb = (nf + moe::kMaxFillBatch - 1) / moe::kMaxFillBatch;
+    size_t t = 0;
+    hipError_t e = hipSuccess;
+    for (size_t b = 0; b < nb && e == hipSuccess; ++b) {
+        moe::FillBatch fb;
+        fb.bytes = (long long)c->d.expert_bytes;
+        fb.table = c->dev_slot_of;
+        for (size_t i = b * moe::kMaxFillBatch; i < nf && fb.n < moe::kMaxFillBatch; ++i, ++fb.n) {
+            fb.src[fb.n] = c->pending[i].first;
+            fb.dst[fb.n] = c->pending[i].second;
+        }
+        // table entries: an even share per batch, the rest with the last batch
+        const size_t share = b + 1 == nb ? ui.size() - t : std::min(ui.size() - t, size_t(2 * moe::kMaxFillBatch));
+        for (size_t j = 0; j < share && fb.n_tab < 2 * moe::kMaxFillBatch; ++j, ++t, ++fb.n_tab) {
+            fb.tab_idx[fb.n_tab] = ui[t];
+            fb.tab_val[fb.n_tab] = uv[t];
+        }
+        e = moe::launch_fill_slots(fb, strm);
+    }
+    if (e == hipSuccess && t < ui.size())  // more changes than the batches carry (not expected)
+        e = moe::launch_slot_update(c->dev_slot_of, ui.data() + t, uv.data() + t, int(ui.size() - t), strm);
+    c->pending.clear();
+    if (e != hipSuccess) {
+        // the lookup's placements stay unmapped, so that a retry misses again
+        for (size_t i = 0; i < idx.size(); ++i) {
+            if (val[i] < 0 || c->key_of_slot[val[i]] != idx[i]) continue;
+            c->slot_of_key[idx[i]] = -1;
+            c->key_of_slot[val[i]] = -1;
+            unlink(c, val[i]);
+            c->free_slots.push(val[i]);
+        }
+        return moe::fail(MOE_ERR_COPY, "expert fill launch failed: %s", hipGetErrorString(e));
+    }
+    if (done) {
+        e = c->ring.record(strm, done);
+        if (e != hipSuccess) return moe::fail_hip(e, "recording fill event");
+    }
     return MOE_OK;
 }
 
@@ -231,6 +274,14 @@ int lookup_impl(moe_cache *c, int step, int layer, const int32_t *ids, int n, bo
     if (c->have_last_compute) {
         st = release_pending(c, c->last_compute);
         if (st != MOE_OK) return st;
+    }
+    const hipStream_t fill = prefetch ? c->copy : compute;
+    if (!prefetch && !c->sim && c->ring.live(c->prefetch_done)) {
+        // earlier prefetches' fills and table updates land before this lookup's fills and compute:
+        // a hit may be one of them, and a victim may be a prefetched slot still being filled
+        hipError_t e = hipStreamWaitEvent(compute, c->ring.event(c->prefetch_done), 0);
+        if (e != hipSuccess) return moe::fail_hip(e, "ordering compute after prefetch");
+        c->prefetch_done = EvRef{};
     }
     ++c->epoch;
     for (int e : R) c->step_mark[layer * c->E + e] = c->epoch;
@@ -252,7 +303,7 @@ int lookup_impl(moe_cache *c, int step, int layer, const int32_t *ids, int n, bo
             continue;
         }
         int32_t victim;
-        s = place_and_fill(c, layer, e, &victim, &chg_idx, &chg_val, &st);
+        s = place_and_fill(c, layer, e, &victim, &chg_idx, &chg_val, &st, fill);
         if (s < 0) break;
         if (prefetch) {
             ++c->st.prefetches;
@@ -264,24 +315,11 @@ int lookup_impl(moe_cache *c, int step, int layer, const int32_t *ids, int n, bo
     }
     if (!chg_idx.empty()) {
         EvRef done;
-        int pst = publish(c, chg_idx, chg_val, &done);
+        int pst = publish(c, chg_idx, chg_val, fill, prefetch ? &done : nullptr);
         if (pst != MOE_OK && st == MOE_OK) st = pst;
-        if (!c->sim && pst == MOE_OK) {
-            if (prefetch) {
-                c->prefetch_done = done;
-            } else {
-                hipError_t e = hipStreamWaitEvent(compute, c->ring.event(done), 0);
-                if (e != hipSuccess && st == MOE_OK) st = moe::fail_hip(e, "ordering compute after fills");
-            }
-        }
+        if (!c->sim && pst == MOE_OK && prefetch) c->prefetch_done = done;
     }
     if (!prefetch) {
-        // earlier prefetches' fills (and table updates) must land before this step's compute
-        if (!c->sim && c->ring.live(c->prefetch_done)) {
-            hipError_t e = hipStreamWaitEvent(compute, c->ring.event(c->prefetch_done), 0);
-            if (e != hipSuccess && st == MOE_OK) st = moe::fail_hip(e, "ordering compute after prefetch");
-            c->prefetch_done = EvRef{};
-        }
         for (int e : R) {
             const int s = c->slot_of_key[layer * c->E + e];
             if (s >= 0) c->unreleased.push_back(s);
@@ -335,6 +373,7 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
     c->next.assign(c->C, -1);
     c->step_mark.assign(keys, 0);
     c->reader.assign(c->C, EvRef{});
+    c->reader_stream.assign(c->C, nullptr);
     c->st.capacity = c->C;
 
     auto cleanup = [&](int code) {
@@ -355,6 +394,13 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
             delete c;
             return moe::fail(MOE_ERR_NOT_PINNED, "host store is not page-locked memory");
         }
+        void *hd = nullptr;
+        if ((e = hipHostGetDevicePointer(&hd, const_cast<void *>(d->host_base), 0)) != hipSuccess || !hd) {
+            (void)hipGetLastError();
+            delete c;
+            return moe::fail(MOE_ERR_NOT_PINNED, "host store has no device mapping (allocate it with hipHostMalloc)");
+        }
+        c->host_dev = static_cast<const uint8_t *>(hd);
         if ((e = hipMalloc(&c->pool, pool_bytes)) != hipSuccess)
             return cleanup(moe::fail_hip(e, "allocating the slot pool"));
         if ((e = hipMalloc(&c->dev_slot_of, sizeof(int32_t) * keys)) != hipSuccess)

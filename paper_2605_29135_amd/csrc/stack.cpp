@@ -6,6 +6,8 @@
 // step stays on the device.
 #include <string.h>
 
+#include <atomic>
+#include <chrono>
 #include <vector>
 
 #include "internal.h"
@@ -45,10 +47,38 @@ struct moe_stack {
     size_t pws_bytes = 0;
     int tcap = 0;               // rows of the per-token buffers: max(max_tokens, max_prefill_tokens)
     hipEvent_t ids_ready = nullptr;
+    moe::IdsMailbox *mbox = nullptr;      // coherent pinned: one token's ids published by the top-k kernel
+    moe::IdsMailbox *mbox_dev = nullptr;  // its device address
+    uint32_t mbox_seq = 0;
     float *scratch_x = nullptr;  // device [Tmax x H] scratch input/output of kernel re-launches
     float *scratch_y = nullptr;  // device [Tmax x H]
     std::vector<LastLayer> last;  // per layer, arguments of the last decode step
 };
+
+namespace {
+
+// Wait until the top-k kernel has published sequence number `seq`, then copy
+// the ids.  A bounded spin: should the sequence number not appear, the stream
+// is synchronised so that a failed kernel reports its error.
+int wait_published_ids(moe_stack *s, uint32_t seq, hipStream_t strm) {
+    volatile uint32_t *flag = &s->mbox->seq;
+    const auto t0 = std::chrono::steady_clock::now();
+    for (uint64_t spin = 0; *flag != seq; ++spin) {
+        if ((spin & 4095) == 4095 && std::chrono::steady_clock::now() - t0 > std::chrono::seconds(10)) {
+            hipError_t e = hipStreamSynchronize(strm);
+            if (e != hipSuccess) return moe::fail_hip(e, "stack step: routing");
+            if (*flag != seq) return moe::fail(MOE_ERR_HIP, "stack step: the routing kernel did not publish its ids");
+            break;
+        }
+        __builtin_ia32_pause();
+    }
+    std::atomic_thread_fence(std::memory_order_acquire);
+    const volatile int32_t *src = s->mbox->ids;
+    for (int j = 0; j < s->d.k; ++j) s->ids_host[j] = src[j];
+    return MOE_OK;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -64,6 +94,7 @@ int moe_stack_destroy(moe_stack *s) {
     if (s->ws) (void)hipFree(s->ws);
     if (s->pws) (void)hipFree(s->pws);
     if (s->ids_ready) (void)hipEventDestroy(s->ids_ready);
+    if (s->mbox) (void)hipHostFree(s->mbox);
     if (s->scratch_x) (void)hipFree(s->scratch_x);
     if (s->scratch_y) (void)hipFree(s->scratch_y);
     delete s;
@@ -126,6 +157,12 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
     }
     if ((e = hipEventCreateWithFlags(&s->ids_ready, hipEventDisableTiming)) != hipSuccess)
         return bail(e, "stack event");
+    if ((e = hipHostMalloc(reinterpret_cast<void **>(&s->mbox), sizeof(moe::IdsMailbox),
+                           hipHostMallocCoherent | hipHostMallocMapped)) != hipSuccess)
+        return bail(e, "stack ids mailbox");
+    memset(s->mbox, 0, sizeof(moe::IdsMailbox));
+    if ((e = hipHostGetDevicePointer(reinterpret_cast<void **>(&s->mbox_dev), s->mbox, 0)) != hipSuccess)
+        return bail(e, "stack ids mailbox");
     const size_t Td = size_t(d->max_tokens);
     if ((e = hipMalloc(&s->scratch_x, sizeof(float) * Td * d->H)) != hipSuccess) return bail(e, "stack buffers");
     if ((e = hipMalloc(&s->scratch_y, sizeof(float) * Td * d->H)) != hipSuccess) return bail(e, "stack buffers");
@@ -148,15 +185,25 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
         int32_t *ids = ids_out ? ids_out + size_t(l) * T * d.k : s->ids;
         float *w = weights_out ? weights_out + size_t(l) * T * d.k : s->weights;
         const float *bias = logit_bias ? logit_bias + size_t(l) * T * d.E : nullptr;
+        // one token under a budget: the top-k kernel publishes its ids straight to host memory
+        const bool mailbox = s->budgeted && T == 1;
+        const uint32_t seq = mailbox ? ++s->mbox_seq : 0;
         hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, bias, s->logits,
                                                  true, s->h, strm);
-        if (e == hipSuccess) e = moe::launch_topk_softmax(s->logits, T, d.E, d.k, ids, w, eflags, strm);
+        if (e == hipSuccess)
+            e = moe::launch_topk_softmax(s->logits, T, d.E, d.k, ids, w, eflags, strm, mailbox ? s->mbox_dev : nullptr,
+                                         seq);
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: routing");
         if (s->budgeted) {
-            e = hipMemcpyAsync(s->ids_host, ids, sizeof(int32_t) * T * d.k, hipMemcpyDeviceToHost, strm);
-            if (e == hipSuccess) e = hipEventRecord(s->ids_ready, strm);
-            if (e == hipSuccess) e = hipEventSynchronize(s->ids_ready);
-            if (e != hipSuccess) return moe::fail_hip(e, "stack step: ids to host");
+            if (mailbox) {
+                int st = wait_published_ids(s, seq, strm);
+                if (st != MOE_OK) return st;
+            } else {
+                e = hipMemcpyAsync(s->ids_host, ids, sizeof(int32_t) * T * d.k, hipMemcpyDeviceToHost, strm);
+                if (e == hipSuccess) e = hipEventRecord(s->ids_ready, strm);
+                if (e == hipSuccess) e = hipEventSynchronize(s->ids_ready);
+                if (e != hipSuccess) return moe::fail_hip(e, "stack step: ids to host");
+            }
             int st = expert_cache_lookup(d.cache, step, l, s->ids_host, T * d.k, s->slots_host, nullptr, strm);
             if (st != MOE_OK) return st;
         }

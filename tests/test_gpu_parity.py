@@ -527,3 +527,54 @@ def test_stack_prefill_config5_two_layers_sampled():
     stack.close()
     cache.close()
     buf.close()
+
+
+def test_cache_prefetch_and_demand_fills_on_device():
+    """Device residency ordering, with no host synchronisation between steps: prefetches fill on the copy
+    stream, demand lookups fill on the compute stream, each FFN reads the pool through the device slot table.
+    With 6 slots, demand lookups evict prefetched slots (possibly still filling) and hit prefetched experts.
+    Every FFN output matches the oracle on the experts it asked for; the residency log matches the oracle's."""
+    wl = synth.Workload("cache order", H=256, E=16, k=4, I=128, L=2, dtype=synth.BF16, cfg_id=120)
+    C, steps = 6, 40
+    buf = _pinned_store(wl)
+    eb = wl.expert_bytes
+    cache = moe.ExpertCache(wl.L, wl.E, eb, C * eb, buf.ptr, wl.E * eb, eb)
+    table, pool = cache.slot_table()
+    o = oracle.LRU(C, wl.L, wl.E)
+    rng = np.random.default_rng(0)
+    host = {l: synth.layer_experts(wl, l) for l in range(wl.L)}
+    ids_np = np.stack([rng.choice(wl.E, wl.k, replace=False) for _ in range(steps)]).astype(np.int32)[:, None, :]
+    w_np = rng.random((steps, 1, wl.k)).astype(np.float32)
+    w_np /= w_np.sum(axis=2, keepdims=True)
+    x_np = rng.standard_normal((steps, 1, wl.H)).astype(np.float32)
+    ids_d, w_d, x_d = dev(ids_np), dev(w_np), dev(x_np)
+    y_d = torch.zeros((steps, 1, wl.H), dtype=torch.float32, device=DEV)
+    ws = torch.empty(moe.moe_ffn_workspace_bytes(1, wl.k, wl.I), dtype=torch.uint8, device=DEV)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    for t in range(steps):
+        l = t % 2
+        if t % 3 == 0:
+            pf = rng.choice(wl.E, 3, replace=False).astype(np.int32)
+            cache.prefetch(t, 1 - l, pf)
+            assert o.lookup(t, 1 - l, pf, prefetch=True) == oracle.OK
+        cache.lookup(t, l, ids_np[t].reshape(-1), stream)
+        assert o.lookup(t, l, ids_np[t].reshape(-1)) == oracle.OK
+        rc = moe.lib().moe_expert_ffn_grouped(
+            x_d[t].data_ptr(), 1, wl.H, wl.I, wl.E, wl.k, ids_d[t].data_ptr(), w_d[t].data_ptr(),
+            table + 4 * l * wl.E, pool, eb, wl.dtype, None, y_d[t].data_ptr(), ws.data_ptr(),
+            ws.numel(), 0, stream.cuda_stream)
+        assert rc == 0, moe.lib().moe_last_error()
+        cache.release(stream)
+    moe.moe_sync_check()
+    y = y_d.cpu().numpy()
+    for t in range(steps):
+        ref = oracle.moe_ffn(x_np[t], ids_np[t], w_np[t].astype(np.float64), host[t % 2], wl.H, wl.I, wl.dtype)
+        assert normwise(y[t], ref) <= TOL[wl.dtype], t
+    ev, oev = cache.trace(), o.events()
+    assert len(ev) == len(oev)
+    assert (ev.view(np.int32).reshape(-1, 6) == oev.view(np.int32).reshape(-1, 6)).all()
+    s = cache.stats()
+    assert s["prefetches"] > 0 and s["evictions"] > 0
+    cache.close()
+    buf.close()
