@@ -119,15 +119,20 @@ def hbm_ceiling(torch, moe, launch_bytes: int, n_launch: int = 40, stream_bytes:
 
 
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cfg4_gateup_hbm_traffic.txt")
-GATEUP_SOURCES = [os.path.join(ROOT, "paper_2605_29135_amd", "csrc", f) for f in ("kernels.hip", "device_common.h")]
+CSRC = os.path.join(ROOT, "paper_2605_29135_amd", "csrc")
 
 
 def gateup_source_hash() -> str:
+    """sha256 of the gate/up kernel's own source text and of the device helpers it uses."""
     import hashlib
-    h = hashlib.sha256()
-    for f in GATEUP_SOURCES:
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+    with open(os.path.join(CSRC, "kernels.hip")) as fh:
+        src = fh.read()
+    i0 = src.index("void gateup_kernel(")
+    i0 = src.rindex("template", 0, i0)
+    i1 = src.index("\n}\n", i0) + 3
+    h = hashlib.sha256(src[i0:i1].encode())
+    with open(os.path.join(CSRC, "device_common.h"), "rb") as fh:
+        h.update(fh.read())
     return h.hexdigest()
 
 
