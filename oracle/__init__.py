@@ -64,6 +64,8 @@ def lib() -> C.CDLL:
         _lib.oracle_lru_stats.argtypes = [P, P]
         _lib.oracle_lru_slot_of.argtypes = [P, I32, I32]
         _lib.oracle_lru_occupancy.argtypes = [P]
+        _lib.oracle_opt_misses.argtypes = [P, P, I32, I32, I32]
+        _lib.oracle_opt_misses.restype = C.c_longlong
         del D
     return _lib
 
@@ -197,3 +199,14 @@ class LRU:
 
     def occupancy(self) -> int:
         return int(lib().oracle_lru_occupancy(self._h))
+
+
+def opt_misses(steps, n_keys: int, capacity: int) -> int:
+    """Fewest fills any replacement policy needs for `steps` (a list of arrays of distinct keys, each step's
+    keys resident together) with `capacity` slots: Belady's farthest-next-use rule at step granularity.
+    Returns -1 if a step needs more than `capacity` keys."""
+    keys = np.concatenate([np.asarray(st, np.int32).reshape(-1) for st in steps]) if steps else np.zeros(0, np.int32)
+    offsets = np.zeros(len(steps) + 1, np.int32)
+    offsets[1:] = np.cumsum([len(np.asarray(st).reshape(-1)) for st in steps])
+    keys = np.ascontiguousarray(keys, np.int32)
+    return int(lib().oracle_opt_misses(keys.ctypes.data, offsets.ctypes.data, len(steps), n_keys, capacity))

@@ -20,6 +20,9 @@
  *     selective load brings sub-modules in and evict makes room; sec. 4 names
  *     least-recently-used eviction as the conventional policy; sec. 5:
  *     memory-constrained execution): an LRU slot table of fixed capacity.
+ *   - offline bound on residency: the fewest fills any replacement policy
+ *     could need for a demand trace (Belady's farthest-next-use rule at step
+ *     granularity), the yardstick against which LRU's fills are reported.
  *
  * Readings where the paper is silent (all of it; it withholds its method):
  *   no router bias or noise; softmax over the selected k only (equal to a full
@@ -463,4 +466,93 @@ int oracle_lru_occupancy(const oracle_lru *c)
     for (int s = 0; s < c->C; s++)
         n += c->key_of_slot[s] >= 0;
     return n;
+}
+
+/* ------------------------------------------------------------------------
+ * Offline bound: the fewest fills any replacement policy needs for a demand
+ * trace (Belady's farthest-next-use rule, applied at step granularity).
+ *
+ * Step i needs the distinct keys keys[offsets[i] .. offsets[i+1]) resident
+ * together.  A missing key is filled; when all C slots are taken, the victim
+ * is the resident key outside step i whose next step of use is the farthest
+ * (a key never used again counts as infinitely far; ties: the smaller key).
+ * Returns the number of fills (compulsory ones included), or -1 if a step
+ * needs more than C keys or an argument is invalid.
+ */
+long long oracle_opt_misses(const int32_t *keys, const int32_t *offsets, int n_steps, int n_keys, int C)
+{
+    if (n_steps < 0 || n_keys < 1 || C < 1 || (n_steps > 0 && (!keys || !offsets)))
+        return -1;
+    const int32_t never = INT32_MAX;
+    size_t n = n_steps > 0 ? (size_t)offsets[n_steps] : 0;
+    int32_t *nxt = malloc((n + 1) * sizeof *nxt);      /* next step of use of each occurrence's key */
+    int32_t *last = malloc((size_t)n_keys * sizeof *last);
+    int32_t *res_key = malloc((size_t)C * sizeof *res_key);
+    int32_t *res_next = malloc((size_t)C * sizeof *res_next);
+    int32_t *where = malloc((size_t)n_keys * sizeof *where);   /* index in res_*, or -1 */
+    uint8_t *in_step = calloc((size_t)n_keys, 1);
+    long long misses = -1;
+    if (!nxt || !last || !res_key || !res_next || !where || !in_step)
+        goto out;
+    for (int k = 0; k < n_keys; k++) {
+        last[k] = never;
+        where[k] = -1;
+    }
+    for (int i = n_steps - 1; i >= 0; i--) {
+        for (int32_t p = offsets[i]; p < offsets[i + 1]; p++) {
+            if (keys[p] < 0 || keys[p] >= n_keys)
+                goto out;
+            nxt[p] = last[keys[p]];
+        }
+        for (int32_t p = offsets[i]; p < offsets[i + 1]; p++)
+            last[keys[p]] = i;
+    }
+    int nres = 0;
+    long long fills = 0;
+    for (int i = 0; i < n_steps; i++) {
+        if (offsets[i + 1] - offsets[i] > C)
+            goto out;
+        for (int32_t p = offsets[i]; p < offsets[i + 1]; p++)
+            in_step[keys[p]] = 1;
+        for (int32_t p = offsets[i]; p < offsets[i + 1]; p++) {
+            const int32_t k = keys[p];
+            if (where[k] >= 0) {
+                res_next[where[k]] = nxt[p];
+                continue;
+            }
+            fills++;
+            if (nres == C) {
+                int v = -1;
+                for (int r = 0; r < nres; r++) {
+                    if (in_step[res_key[r]])
+                        continue;
+                    if (v < 0 || res_next[r] > res_next[v] ||
+                        (res_next[r] == res_next[v] && res_key[r] < res_key[v]))
+                        v = r;
+                }
+                if (v < 0)
+                    goto out;
+                where[res_key[v]] = -1;
+                nres--;
+                res_key[v] = res_key[nres];
+                res_next[v] = res_next[nres];
+                if (v < nres)
+                    where[res_key[v]] = v;
+            }
+            res_key[nres] = k;
+            res_next[nres] = nxt[p];
+            where[k] = nres++;
+        }
+        for (int32_t p = offsets[i]; p < offsets[i + 1]; p++)
+            in_step[keys[p]] = 0;
+    }
+    misses = fills;
+out:
+    free(nxt);
+    free(last);
+    free(res_key);
+    free(res_next);
+    free(where);
+    free(in_step);
+    return misses;
 }

@@ -452,3 +452,86 @@ def test_lru_errors():
     assert c.occupancy() == 2 and len(c.events()) == 2
     with pytest.raises(ValueError):
         oracle.LRU(0, 1, 1)
+
+
+# ------------------------------------------------------------ OPT bound ---
+def _golden_kv(name):
+    kv = {}
+    for line in open(os.path.join(GOLDEN, name)):
+        if line.strip() and not line.startswith("#"):
+            key, *vals = line.split()
+            kv[key] = [int(v) for v in vals]
+    return kv
+
+
+def _brute_min_fills(steps, C):
+    """Exhaustive search over every eviction choice: the fewest fills that keep each step's keys resident
+    together with C slots (no prefetching: keys enter only when a step needs them)."""
+    from functools import lru_cache
+
+    @lru_cache(maxsize=None)
+    def go(i, pos, resident):
+        if i == len(steps):
+            return 0
+        st = steps[i]
+        if pos == len(st):
+            return go(i + 1, 0, resident)
+        k = st[pos]
+        if k in resident:
+            return go(i, pos + 1, resident)
+        if len(resident) < C:
+            return 1 + go(i, pos + 1, resident | {k})
+        best = None
+        for v in resident:
+            if v in st:  # the step's own keys stay resident
+                continue
+            r = 1 + go(i, pos + 1, (resident - {v}) | {k})
+            best = r if best is None else min(best, r)
+        return best if best is not None else 10 ** 9
+
+    return go(0, 0, frozenset())
+
+
+def test_opt_textbook_example():
+    g = _golden_kv("opt_textbook.txt")
+    steps = [[k] for k in g["reference"]]
+    assert oracle.opt_misses(steps, g["experts"][0], g["capacity"][0]) == g["faults"][0] == len(g["fault_steps"])
+
+
+@pytest.mark.parametrize("seed", range(150))
+def test_opt_equals_exhaustive_search(seed):
+    rng = np.random.default_rng(seed)
+    n_keys = int(rng.integers(3, 8))
+    C = int(rng.integers(1, 5))
+    steps = []
+    for _ in range(int(rng.integers(1, 13))):
+        m = int(rng.integers(1, min(C, n_keys) + 1))
+        steps.append(sorted(rng.choice(n_keys, m, replace=False).tolist()))
+    assert oracle.opt_misses(steps, n_keys, C) == _brute_min_fills(tuple(tuple(s) for s in steps), C)
+
+
+def test_opt_bounds_lru_and_simple_cases():
+    rng = np.random.default_rng(11)
+    E, L, k = 32, 2, 4
+    p = 1.0 / np.arange(1, E + 1) ** 1.1
+    p /= p.sum()
+    steps, keys = [], []
+    for t in range(300):
+        layer = t % L
+        ids = np.sort(rng.choice(E, k, replace=False, p=p)).astype(np.int32)
+        steps.append((layer, ids))
+        keys.append(layer * E + ids)
+    distinct = len(np.unique(np.concatenate(keys)))
+    prev = None
+    for C in (k, 6, 10, 16, 24, distinct):
+        o = oracle.LRU(C, L, E)
+        for t, (layer, ids) in enumerate(steps):
+            assert o.lookup(t, layer, ids) == oracle.OK
+        lru = o.stats()["misses"]
+        opt = oracle.opt_misses(keys, L * E, C)
+        assert distinct <= opt <= lru
+        if prev is not None:
+            assert opt <= prev  # more slots never need more fills
+        prev = opt
+    assert oracle.opt_misses(keys, L * E, distinct) == distinct  # everything fits: compulsory fills only
+    assert oracle.opt_misses([[0, 1, 2]], 3, 2) == -1  # a step larger than the cache
