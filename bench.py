@@ -42,6 +42,9 @@ def parse():
     ap.add_argument("--host-alias", action="store_true",
                     help="let every layer read layer 0's host copy (keys stay distinct; same PCIe traffic)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="budget of the oracle CPU baseline")
+    ap.add_argument("--prefetch", type=int, default=0,
+                    help="speculative prefetch per layer (most often demanded non-resident experts of the next "
+                         "layer); 0 = off, the LRU residency the workload specifies")
     ap.add_argument("--replays", type=int, default=5,
                     help="replays of the last step's launches (one per layer) for the per-launch device time")
     return ap.parse_args()
@@ -167,6 +170,40 @@ def expert_kernel_bytes(wl, n_exp, T):
     return n_exp * gu_w + T * H * 4 + rows * I * 4, n_exp * dn_w + rows * I * 4 + T * H * 8
 
 
+def residency_bound(moe, cache, E, capacity, step_bytes_per_token=None):
+    """LRU fills of the run's whole demand trace (every lookup from the cold cache on) next to the fewest
+    fills any replacement policy could make on the same trace (moe_opt_fills)."""
+    ev = cache.trace()
+    # prefetched experts that a later demand lookup found resident
+    n_pf, used, pending = int((ev["kind"] == moe.EVENT_PREFETCH).sum()), 0, set()
+    if n_pf:
+        for t_, layer, ex, kind, _, victim in ev.tolist():
+            if victim >= 0:
+                pending.discard(victim)
+            kk = layer * E + ex
+            if kind == moe.EVENT_PREFETCH:
+                pending.add(kk)
+            elif kind == moe.EVENT_HIT and kk in pending:
+                used += 1
+                pending.discard(kk)
+    ev = ev[ev["kind"] != moe.EVENT_PREFETCH]
+    if ev.size == 0:
+        return None
+    keys = (ev["layer"].astype(np.int64) * E + ev["expert"]).astype(np.int32)
+    step_key = ev["t"].astype(np.int64) * 1_000_000 + ev["layer"]
+    starts = np.flatnonzero(np.r_[True, step_key[1:] != step_key[:-1]])
+    offsets = np.r_[starts, ev.size].astype(np.int32)
+    n_keys = int(ev["layer"].max() + 1) * E
+    opt = moe.moe_opt_fills_flat(keys, offsets, n_keys, capacity)
+    lru = int((ev["kind"] == moe.EVENT_MISS).sum())
+    out = {"scope": "every lookup of the run from a cold cache (warm-up included)", "lookups": int(ev.size),
+           "lru_fills": lru, "opt_fills": int(opt), "opt_over_lru": opt / lru if lru else None}
+    if n_pf:
+        out["prefetch_fills"] = n_pf
+        out["prefetches_used"] = used  # demanded again before being evicted
+    return out
+
+
 def cpu_baseline(wl, store, steps, bias_np, x_np, budget_s, shared=None):
     """The oracle on the host cores: whole tokens through every layer, no budget."""
     import oracle
@@ -239,7 +276,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     def make():
         cache = moe.ExpertCache(L, E, eb, wl.budget_bytes, buf.ptr, E * eb, eb, reserved_bytes=L * eb)
         stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=1,
-                             max_prefill_tokens=Tp)
+                             max_prefill_tokens=Tp, prefetch=args.prefetch)
         return cache, stack
 
     # warm-up on a throw-away cache (kernels loaded, allocator warm), so the timed run starts cold
@@ -275,6 +312,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     st3 = cache.stats()
     ktimes = {name: stack.kernel_time(w, args.replays) for w, name in enumerate(["route", "gateup", "down"])}
     moe.moe_sync_check()
+    bound = residency_bound(moe, cache, E, st3["capacity"])
     stack.close()
     cache.close()
 
@@ -321,7 +359,8 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
                 "router-chosen prefill routing, Zipf-overlap decode routing masks)",
         "config": {"workload": wl.name, "layers": L, "experts": E, "top_k": k, "shared_expert": True,
                    "hidden": H, "intermediate": I, "prefill_tokens": Tp, "decode_tokens_per_step": 1,
-                   "budget_bytes": wl.budget_bytes, "slots": st3["capacity"], "host_store_bytes": L * E * eb},
+                   "budget_bytes": wl.budget_bytes, "slots": st3["capacity"], "host_store_bytes": L * E * eb,
+                   "prefetch_per_layer": args.prefetch},
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU (int4 decode)", "achieved": gu_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gu_gbps / HBM_PEAK_GBPS,
                      "bytes_per_launch": gu_bytes, "mean_launch_us": gu_ms * 1e3,
@@ -341,7 +380,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
                                  "peak": 2500.0, "unit": "TFLOP/s",
                                  "frac": pf_flop / (pf_ms * 1e-3) / 1e12 / 2500.0}},
         "residency": {**d_dec, "miss_rate": d_dec["misses"] / d_dec["lookups"] if d_dec["lookups"] else 0.0,
-                      "misses_per_token": d_dec["misses"] / steps},
+                      "misses_per_token": d_dec["misses"] / steps, "bound": bound},
         "pcie": {"h2d_bytes_per_token": h2d_tok, "achieved_GBps": d_dec["h2d_bytes"] / t_decode / 1e9,
                  "ceiling_GBps": ceil, "frac": d_dec["h2d_bytes"] / t_decode / 1e9 / ceil,
                  "tokens_per_s_bound": ceil * 1e9 / h2d_tok if h2d_tok else None},
@@ -412,7 +451,8 @@ def main():
     budget = wl.budget_bytes if budgeted else L * E * eb + reserved
     cache = moe.ExpertCache(L, E, eb, budget, buf.ptr, 0 if alias else E * eb, eb, reserved_bytes=reserved,
                             preload=not budgeted)
-    stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T)
+    stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T,
+                         prefetch=args.prefetch if budgeted else 0)
     t_setup = time.perf_counter() - t_setup
 
     stream = torch.cuda.current_stream()
@@ -466,6 +506,8 @@ def main():
     hbm = hbm_ceiling(torch, moe, gu_bytes)
     traffic, traffic_src = measured_traffic()
 
+    bound = residency_bound(moe, cache, E, st1["capacity"]) if budgeted else None
+
     # ---- oracle on the host cores (bounded sample of the timed tokens), with a parity check
     sample = list(range(args.warmup, n_steps))
     cpu_tps, outs, cpu_dt = cpu_baseline(wl, lambda l: store[0 if alias else l], sample, bias_np
@@ -494,7 +536,8 @@ def main():
         "data": "synthetic (seeded N(0,0.02) weights, N(0,1) hidden states, Zipf-overlap routing masks)",
         "config": {"workload": wl_name, "layers": L, "experts": E, "top_k": k, "hidden": H, "intermediate": I,
                    "tokens_per_step": T, "budget_bytes": budget, "slots": st1["capacity"],
-                   "host_store_bytes": L_store * E * eb, "host_layers_aliased": bool(alias)},
+                   "host_store_bytes": L_store * E * eb, "host_layers_aliased": bool(alias),
+                   "prefetch_per_layer": args.prefetch if budgeted else 0},
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU", "achieved": gu_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": gu_gbps / HBM_PEAK_GBPS if gu_gbps else None,
@@ -509,7 +552,7 @@ def main():
                     "down_GBps": dn_gbps, "down_bytes_per_launch": dn_bytes,
                     "ffn_GBps": (gu_bytes + dn_bytes) / ((gu_ms + dn_ms) * 1e-3) / 1e9 if gu_ms else None},
         "residency": {**d, "miss_rate": d["misses"] / d["lookups"] if d["lookups"] else 0.0,
-                      "misses_per_token": d["misses"] / (args.steps * T)},
+                      "misses_per_token": d["misses"] / (args.steps * T), "bound": bound},
         "pcie": pcie,
         "cpu_baseline": {"value": round(cpu_tps, 4), "unit": "tokens/s", "cores": oracle.threads_used(),
                          "kind": "oracle",

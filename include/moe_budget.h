@@ -290,6 +290,9 @@ typedef struct {
     moe_cache *cache;               /* residency of the routed experts */
     int max_tokens;                 /* largest T passed to moe_stack_decode_step (<= 16) */
     int max_prefill_tokens;         /* largest T passed to moe_stack_prefill (0: no prefill) */
+    int prefetch;                   /* one-token decode under a budget: after each layer, prefetch up to this
+                                       many experts of the next layer -- its most often demanded ones that
+                                       are not resident (ties: lower id); 0 = off */
 } moe_stack_desc;
 
 MOE_API int moe_stack_create(const moe_stack_desc *desc, moe_stack **out);
@@ -326,6 +329,18 @@ MOE_API int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *
  * slots are still current).  Outputs go to scratch buffers: the residual
  * stream and the residency state are untouched.  Synchronous. */
 MOE_API int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *mean_ms);
+
+/* Offline residency bound (host call; no device work).  For a demand trace in
+ * which step i needs the distinct keys keys[offsets[i] .. offsets[i+1])
+ * resident together (key = layer * E + expert, < n_keys; offsets[0] = 0), the
+ * fewest fills any replacement policy with `capacity` slots needs, compulsory
+ * fills included: Belady's farthest-next-use rule at step granularity.  It
+ * bounds from below what the LRU residency (sec. 4's conventional policy) or
+ * any other policy can do on the same trace.  MOE_ERR_BUDGET if a step has more
+ * than `capacity` keys; MOE_ERR_RANGE for a key outside [0, n_keys);
+ * MOE_ERR_INVALID_ARG for bad offsets or a key repeated within a step. */
+MOE_API int moe_opt_fills(const int32_t *keys, const int32_t *offsets, int n_steps, int n_keys, int capacity,
+                          uint64_t *fills_out);
 
 /* Measurement aid, not part of the method: streams `bytes` of device memory
  * once, with the 16-byte nontemporal loads the expert kernels use for weight

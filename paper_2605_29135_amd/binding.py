@@ -55,7 +55,7 @@ class StackDesc(C.Structure):
     _fields_ = [("n_layers", C.c_int), ("H", C.c_int), ("I", C.c_int), ("E", C.c_int), ("k", C.c_int),
                 ("w_dtype", C.c_int), ("router_dtype", C.c_int), ("router_w", C.POINTER(C.c_void_p)),
                 ("shared_w", C.POINTER(C.c_void_p)), ("cache", C.c_void_p), ("max_tokens", C.c_int),
-                ("max_prefill_tokens", C.c_int)]
+                ("max_prefill_tokens", C.c_int), ("prefetch", C.c_int)]
 
 
 _lib = None
@@ -91,6 +91,7 @@ def lib() -> C.CDLL:
             "moe_stack_kernel_time": [P, I, I, P, C.POINTER(C.c_double)],
             "moe_stack_prefill": [P, I, P, I, P, P, P],
             "moe_hbm_read_probe": [P, SZ, P, P],
+            "moe_opt_fills": [P, P, I, I, I, U64P],
         }
         for name, args in sig.items():
             fn = getattr(L, name)
@@ -215,6 +216,29 @@ def moe_prefill_grouped(x, ids, weights, pool, expert_bytes: int, w_dtype: int, 
     return y_out
 
 
+def moe_opt_fills(steps, n_keys: int, capacity: int) -> int:
+    """Fewest fills any replacement policy needs for `steps` (arrays of distinct keys, each step's keys
+    resident together) with `capacity` slots (host-side analysis in the library)."""
+    arrs = [np.ascontiguousarray(np.asarray(s_, np.int32).reshape(-1)) for s_ in steps]
+    keys = np.ascontiguousarray(np.concatenate(arrs) if arrs else np.zeros(0, np.int32), dtype=np.int32)
+    offsets = np.zeros(len(arrs) + 1, np.int32)
+    offsets[1:] = np.cumsum([a.size for a in arrs])
+    out = C.c_uint64()
+    _check(lib().moe_opt_fills(keys.ctypes.data, offsets.ctypes.data, len(arrs), n_keys, capacity, C.byref(out)),
+           "moe_opt_fills")
+    return out.value
+
+
+def moe_opt_fills_flat(keys, offsets, n_keys: int, capacity: int) -> int:
+    """moe_opt_fills on a flat trace: keys int32 [n], offsets int32 [steps + 1]."""
+    keys = np.ascontiguousarray(keys, dtype=np.int32)
+    offsets = np.ascontiguousarray(offsets, dtype=np.int32)
+    out = C.c_uint64()
+    _check(lib().moe_opt_fills(keys.ctypes.data, offsets.ctypes.data, offsets.size - 1, n_keys, capacity,
+                               C.byref(out)), "moe_opt_fills")
+    return out.value
+
+
 def moe_hbm_read_probe(buf, sink, stream=None):
     """Stream the device tensor `buf` once with the expert kernels' 16-byte loads (measurement aid)."""
     import torch
@@ -310,7 +334,8 @@ class MoeStack:
     """Owner of one moe_stack (decode steps and prefill chunks over L MoE layers on a cache)."""
 
     def __init__(self, cache: ExpertCache, H: int, I: int, E: int, k: int, w_dtype: int, router_dtype: int,
-                 router_w: list, shared_w: list | None = None, max_tokens: int = 1, max_prefill_tokens: int = 0):
+                 router_w: list, shared_w: list | None = None, max_tokens: int = 1, max_prefill_tokens: int = 0,
+                 prefetch: int = 0):
         self._router = (C.c_void_p * len(router_w))(*[_dev(w, "router_w") for w in router_w])
         self._shared = None
         if shared_w is not None:
@@ -319,7 +344,7 @@ class MoeStack:
         d = StackDesc(len(router_w), H, I, E, k, w_dtype, router_dtype,
                       C.cast(self._router, C.POINTER(C.c_void_p)),
                       C.cast(self._shared, C.POINTER(C.c_void_p)) if self._shared is not None else None,
-                      cache.handle, max_tokens, max_prefill_tokens)
+                      cache.handle, max_tokens, max_prefill_tokens, prefetch)
         h = C.c_void_p()
         _check(lib().moe_stack_create(C.byref(d), C.byref(h)), "moe_stack_create")
         self._h = h

@@ -108,6 +108,7 @@ void clear_error();
 // Slot stride of a cache's pool; whether it was preloaded (slot = layer * E + expert, never evicted).
 size_t cache_expert_bytes(const struct ::moe_cache *c);
 bool cache_preloaded(const struct ::moe_cache *c);
+bool cache_resident(const struct ::moe_cache *c, int layer, int expert);  // host mirror
 
 // Sticky error-flag word of the current device (set up on first use).
 int *device_error_flags();

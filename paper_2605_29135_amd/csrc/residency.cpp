@@ -339,6 +339,9 @@ int lookup_impl(moe_cache *c, int step, int layer, const int32_t *ids, int n, bo
 
 size_t moe::cache_expert_bytes(const moe_cache *c) { return c->d.expert_bytes; }
 bool moe::cache_preloaded(const moe_cache *c) { return c->d.flags & MOE_CACHE_PRELOAD; }
+bool moe::cache_resident(const moe_cache *c, int layer, int expert) {
+    return c->slot_of_key[size_t(layer) * c->E + expert] >= 0;
+}
 
 extern "C" {
 

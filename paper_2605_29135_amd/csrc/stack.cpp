@@ -6,6 +6,7 @@
 // step stays on the device.
 #include <string.h>
 
+#include <algorithm>
 #include <atomic>
 #include <chrono>
 #include <vector>
@@ -50,6 +51,7 @@ struct moe_stack {
     moe::IdsMailbox *mbox = nullptr;      // coherent pinned: one token's ids published by the top-k kernel
     moe::IdsMailbox *mbox_dev = nullptr;  // its device address
     uint32_t mbox_seq = 0;
+    std::vector<uint32_t> demand;          // [L x E] demand lookups per expert (prefetch ranking)
     float *scratch_x = nullptr;  // device [Tmax x H] scratch input/output of kernel re-launches
     float *scratch_y = nullptr;  // device [Tmax x H]
     std::vector<LastLayer> last;  // per layer, arguments of the last decode step
@@ -76,6 +78,26 @@ int wait_published_ids(moe_stack *s, uint32_t seq, hipStream_t strm) {
     const volatile int32_t *src = s->mbox->ids;
     for (int j = 0; j < s->d.k; ++j) s->ids_host[j] = src[j];
     return MOE_OK;
+}
+
+// Speculative prefetch after layer l of a one-token step: the next layer's (the
+// next step's first layer after the last) most often demanded experts that are
+// not resident, up to d.prefetch of them, ties to the lower id.
+int prefetch_next(moe_stack *s, int step, int l) {
+    const auto &d = s->d;
+    const int ln = (l + 1) % d.n_layers, sn = l + 1 == d.n_layers ? step + 1 : step;
+    std::vector<std::pair<uint32_t, int32_t>> cand;
+    cand.reserve(size_t(d.E));
+    for (int e = 0; e < d.E; ++e)
+        if (!moe::cache_resident(d.cache, ln, e)) cand.emplace_back(s->demand[size_t(ln) * d.E + e], e);
+    const size_t n = std::min(cand.size(), size_t(d.prefetch));
+    if (n == 0) return MOE_OK;
+    std::partial_sort(cand.begin(), cand.begin() + n, cand.end(), [](const auto &a, const auto &b) {
+        return a.first != b.first ? a.first > b.first : a.second < b.second;
+    });
+    int32_t ids[MOE_MAX_EXPERTS];
+    for (size_t i = 0; i < n; ++i) ids[i] = cand[i].second;
+    return expert_cache_prefetch(d.cache, sn, ln, ids, int(n));
 }
 
 }  // namespace
@@ -110,6 +132,8 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: max_tokens must be in [1, %d]", MOE_MAX_DECODE_TOKENS);
     if (d->max_prefill_tokens < 0 || d->max_prefill_tokens > (1 << 20))
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: max_prefill_tokens must be in [0, 2^20]");
+    if (d->prefetch < 0 || d->prefetch > d->E)
+        return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefetch must be in [0, E]");
     if (d->max_prefill_tokens > 0 && !moe::prefill_dtype_supported(d->w_dtype))
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefill needs MOE_BF16 or MOE_INT4G128 experts");
     if (!moe::ffn_shape_supported(d->H, d->I, d->w_dtype) || !moe::router_shape_supported(d->H, d->router_dtype))
@@ -149,6 +173,7 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
     if ((e = hipHostMalloc(&s->ids_host, sizeof(int32_t) * T * d->k, 0)) != hipSuccess) return bail(e, "stack buffers");
     s->slots_host = new int32_t[size_t(T) * d->k];
     s->last.assign(d->n_layers, LastLayer{});
+    s->demand.assign(size_t(d->n_layers) * d->E, 0u);
     s->ws_bytes = moe::ffn_workspace_bytes(d->max_tokens, d->k, d->I);
     if ((e = hipMalloc(&s->ws, s->ws_bytes)) != hipSuccess) return bail(e, "stack workspace");
     if (d->max_prefill_tokens > 0) {
@@ -206,6 +231,7 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
             }
             int st = expert_cache_lookup(d.cache, step, l, s->ids_host, T * d.k, s->slots_host, nullptr, strm);
             if (st != MOE_OK) return st;
+            for (int j = 0; j < T * d.k; ++j) ++s->demand[size_t(l) * d.E + s->ids_host[j]];
         }
         // Where this layer's experts live: after a lookup the host knows every
         // slot (T == 1 passes them to the kernels directly); preloaded slots are
@@ -227,6 +253,7 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: expert FFN");
         if (s->budgeted) {
             int st = expert_cache_release(d.cache, strm);
+            if (st == MOE_OK && d.prefetch > 0 && T == 1) st = prefetch_next(s, step, l);  // after the release
             if (st != MOE_OK) return st;
         }
     }

@@ -170,3 +170,41 @@ def test_sim_cache_preload_and_errors():
     with pytest.raises(moe.MoeError) as ei:
         st.cache(L * E - 1, preload=True)
     assert ei.value.code == -4
+
+
+def _zipf_steps(rng, L, E, k, steps, s=1.1):
+    p = 1.0 / np.arange(1, E + 1) ** s
+    p /= p.sum()
+    perms = [rng.permutation(E) for _ in range(L)]
+    out = []
+    for t in range(steps):
+        for layer in range(L):
+            ids = np.sort(perms[layer][rng.choice(E, k, replace=False, p=p)]).astype(np.int32)
+            out.append(layer * E + ids)
+    return out
+
+
+@pytest.mark.parametrize("seed,L,E,k,steps,C", [(0, 2, 16, 2, 60, 5), (1, 4, 32, 4, 200, 24),
+                                                 (2, 40, 128, 8, 64, 682), (3, 3, 8, 8, 30, 8)])
+def test_opt_fills_matches_oracle(seed, L, E, k, steps, C):
+    """The library's offline bound (host code) equals the oracle's on Zipf traces, up to config 4's shape."""
+    trace = _zipf_steps(np.random.default_rng(seed), L, E, k, steps)
+    got = moe.moe_opt_fills(trace, L * E, C)
+    assert got == oracle.opt_misses(trace, L * E, C)
+    o = oracle.LRU(C, L, E)
+    for i, keys in enumerate(trace):
+        assert o.lookup(i, int(keys[0]) // E, keys % E) == oracle.OK
+    assert got <= o.stats()["misses"]
+
+
+def test_opt_fills_rejects_bad_traces():
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_opt_fills([[0, 1, 2]], 3, 2)
+    assert ei.value.code == -4
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_opt_fills([[0, 5]], 3, 2)
+    assert ei.value.code == -2
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_opt_fills([[1, 1]], 3, 2)
+    assert ei.value.code == -1
+    assert moe.moe_opt_fills([], 3, 2) == 0

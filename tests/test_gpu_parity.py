@@ -578,3 +578,58 @@ def test_cache_prefetch_and_demand_fills_on_device():
     assert s["prefetches"] > 0 and s["evictions"] > 0
     cache.close()
     buf.close()
+
+
+def test_stack_decode_with_prefetch():
+    """One-token decode with speculative prefetch (2 experts per layer): the residency log equals the oracle
+    LRU replaying the same demand lookups and prefetches, every prefetch picked the next layer's most often
+    demanded non-resident experts (ties: lower id), and outputs match the oracle chain."""
+    wl = synth.Workload("prefetch stack", H=512, E=32, k=4, I=256, L=3, dtype=synth.BF16, routing="zipf_overlap",
+                        cfg_id=130)
+    capacity, steps, P = 20, 30, 2
+    buf = _pinned_store(wl)
+    eb = wl.expert_bytes
+    cache = moe.ExpertCache(wl.L, wl.E, eb, capacity * eb, buf.ptr, wl.E * eb, eb)
+    routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
+    stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, None, prefetch=P)
+    sets = synth.routing_sets(wl, steps=steps)
+    host_layers = {}
+    for t in range(steps):
+        x0 = synth.hidden_states(wl, t)
+        bias = np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)])
+        x = dev(x0)
+        ids = torch.empty((wl.L, 1, wl.k), dtype=torch.int32, device=DEV)
+        w = torch.empty((wl.L, 1, wl.k), dtype=torch.float32, device=DEV)
+        stack.decode_step(t, x, dev(bias), ids, w)
+        moe.moe_sync_check()
+        if t % 7 == 0:
+            xr = _oracle_chain(wl, x0, ids.cpu().numpy(), w.cpu().numpy(), host_layers)
+            assert normwise(x.cpu().numpy() - x0, xr - x0) <= TOL[wl.dtype]
+    ev = cache.trace()
+    # replay: consecutive events of one call share (t, layer) and demand-or-prefetch kind
+    kind_pf = ev["kind"] == moe.EVENT_PREFETCH
+    key = ev["t"].astype(np.int64) * 4096 + ev["layer"] * 2 + kind_pf
+    starts = np.flatnonzero(np.r_[True, key[1:] != key[:-1]])
+    ends = np.r_[starts[1:], ev.size]
+    o = oracle.LRU(capacity, wl.L, wl.E)
+    counts = np.zeros((wl.L, wl.E), np.int64)
+    n_pf = 0
+    for a, b in zip(starts, ends):
+        t, layer, ex = int(ev["t"][a]), int(ev["layer"][a]), ev["expert"][a:b]
+        if kind_pf[a]:
+            resident = np.array([o.slot_of(layer, e) >= 0 for e in range(wl.E)])
+            cand = [e for e in range(wl.E) if not resident[e]]
+            cand.sort(key=lambda e: (-counts[layer, e], e))
+            assert sorted(ex.tolist()) == sorted(cand[:P])
+            assert o.lookup(t, layer, ex, prefetch=True) == oracle.OK
+            n_pf += b - a
+        else:
+            assert o.lookup(t, layer, ex) == oracle.OK
+            counts[layer, ex] += 1
+    oev = o.events()
+    assert len(ev) == len(oev)
+    assert (ev.view(np.int32).reshape(-1, 6) == oev.view(np.int32).reshape(-1, 6)).all()
+    assert n_pf > 0 and cache.stats()["prefetches"] == n_pf
+    stack.close()
+    cache.close()
+    buf.close()
