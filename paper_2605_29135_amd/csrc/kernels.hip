@@ -405,6 +405,10 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     const uint8_t *__restrict__ shared_w, const float *__restrict__ weights, int *groups,
     float *__restrict__ act, int *err, FfnPlan plan) {
     constexpr int EPC = Fmt<DT>::EPC;
+    // One int4 token: a wave streams 2 KiB of weights (two rows at H = 2048) but would read 8 KiB of
+    // x, so the block stages x in LDS once.  With bf16 or f32 weights the wave's x read is no larger
+    // than its weight stream and staging only adds a barrier.
+    constexpr bool STAGE_X = ONE_TOKEN && DT == INT4;
     const int lane = threadIdx.x & (kWave - 1);
     const int g = blockIdx.y;
     const uint8_t *blob;
@@ -438,13 +442,13 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
         blob = s == -2 ? shared_w : pool + size_t(s) * expert_bytes;
     }
     const int i = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
-    if (i >= I) return;
+    if (!STAGE_X && i >= I) return;  // when x is staged, every wave joins the block's staging below
     const int P = T * k;
-    // The first pair's activations are loaded before the weight stream: loads
-    // retire in issue order, so waiting for x never waits for the weights.
     float xv[NCH][EPC];
     float wp0;  // combine weight of the first pair (1 for the shared expert)
-    {
+    if constexpr (!STAGE_X) {
+        // The first pair's activations are loaded before the weight stream: loads
+        // retire in issue order, so waiting for x never waits for the weights.
         const int p0 = ONE_TOKEN ? single : pairs[pstart];
         wp0 = p0 < P ? weights[p0] : 1.f;
         const float *xt = x + size_t(p0 < P ? p0 / k : p0 - P) * H;
@@ -460,7 +464,8 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
         }
     }
     const size_t rb = row_bytes_of(DT, H);
-    const uint8_t *gate = blob + size_t(2 * i) * rb;
+    const int iw = i < I ? i : I - 1;  // staging x: a wave past I loads a valid row and stores nothing
+    const uint8_t *gate = blob + size_t(2 * iw) * rb;
     const uint8_t *up = gate + rb;
     uint4 wg[NCH], wu[NCH];
     float sg[NCH], su[NCH];
@@ -473,8 +478,35 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
         if constexpr (DT == INT4) {
             const uint16_t *sc = reinterpret_cast<const uint16_t *>(blob + size_t(I) * H);
             const int groups_per_row = H / 128;
-            sg[c] = in ? bf16_bits_to_float(sc[size_t(2 * i) * groups_per_row + col0 / 128]) : 0.f;
-            su[c] = in ? bf16_bits_to_float(sc[size_t(2 * i + 1) * groups_per_row + col0 / 128]) : 0.f;
+            sg[c] = in ? bf16_bits_to_float(sc[size_t(2 * iw) * groups_per_row + col0 / 128]) : 0.f;
+            su[c] = in ? bf16_bits_to_float(sc[size_t(2 * iw + 1) * groups_per_row + col0 / 128]) : 0.f;
+        }
+    }
+    if constexpr (STAGE_X) {
+        // The token row is the same for every wave of the block: it is staged in LDS once, behind the
+        // weight loads, transposed to [chunk][quarter][lane] so that each read of a quarter is 64
+        // consecutive 16-byte words.
+        extern __shared__ float4 xsh[];
+        constexpr int Q = EPC / 4;
+        wp0 = single < P ? weights[single] : 1.f;
+        const float4 *xt4 = reinterpret_cast<const float4 *>(x + size_t(single < P ? single / k : single - P) * H);
+        for (int f = threadIdx.x; f < H / 4; f += kBlock) {
+            const int l = (f / Q) % kWave, cc = f / Q / kWave, q = f % Q;
+            xsh[(cc * Q + q) * kWave + l] = xt4[f];
+        }
+        __syncthreads();
+        if (i >= I) return;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int col0 = (c * kWave + lane) * EPC;
+#pragma unroll
+            for (int q = 0; q < Q; ++q) {
+                const float4 v = col0 < H ? xsh[(c * Q + q) * kWave + lane] : make_float4(0.f, 0.f, 0.f, 0.f);
+                xv[c][4 * q] = v.x;
+                xv[c][4 * q + 1] = v.y;
+                xv[c][4 * q + 2] = v.z;
+                xv[c][4 * q + 3] = v.w;
+            }
         }
     }
     for (int q = 0; q < pcount; ++q) {
@@ -791,8 +823,10 @@ __global__ void slot_update_kernel(int32_t *table, SlotUpdates u) {
 template <int NCH>
 constexpr int nch_index() { return NCH == 1 ? 0 : NCH == 2 ? 1 : NCH == 4 ? 2 : 3; }
 
+int elems_per_chunk(int dtype) { return dtype == F32 ? 4 : dtype == BF16 ? 8 : 32; }
+
 int chunks_per_row(int H, int dtype) {
-    const int epc = dtype == F32 ? 4 : dtype == BF16 ? 8 : 32;
+    const int epc = elems_per_chunk(dtype);
     const int need = (H + kWave * epc - 1) / (kWave * epc);
     for (int n : {1, 2, 4, 8})
         if (need <= n) return n;
@@ -910,10 +944,12 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
     const int groups = one ? k + has_shared : (T * k < E ? T * k : E) + has_shared;
     const dim3 ggrid((I + 3) / 4, groups);
     const int nch = chunks_per_row(H, dtype);
+    // One-token int4 x staging covers every lane's chunk slots, [nch][EPC/4][64] float4, not just H floats.
+    const size_t x_lds = dtype == INT4 ? sizeof(float) * size_t(nch) * kWave * elems_per_chunk(dtype) : 0;
     bool launched = !(parts & kFfnGateUp);
 #define GU_CASE(DT, N)                                                                              \
     if (!launched && dtype == DT && nch == N) {                                                     \
-        e = one ? launch(gateup_kernel<DT, N, true>, ggrid, kBlock, 0, s, x, T, H, I, E, k, ids, \
+        e = one ? launch(gateup_kernel<DT, N, true>, ggrid, kBlock, x_lds, s, x, T, H, I, E, k, ids, \
                          slot_of, pl, expert_bytes, sw, weights, ws.groups, ws.act, err_flags, pl1) \
                 : launch(gateup_kernel<DT, N, false>, ggrid, kBlock, 0, s, x, T, H, I, E, k, ids, \
                          slot_of, pl, expert_bytes, sw, weights, ws.groups, ws.act, err_flags, FfnPlan{}); \

@@ -193,6 +193,22 @@ def test_ffn_grouping_duplicates_slots_and_accumulate(dtype):
         check_ffn(wl, x, ids, w, ex, None, accumulate=True)
 
 
+@pytest.mark.parametrize("dtype,H", [(synth.F32, 384), (synth.BF16, 256), (synth.BF16, 640), (synth.INT4G128, 256),
+                                     (synth.INT4G128, 2176), (synth.INT4G128, 4224)])
+def test_ffn_one_token_partial_chunks(dtype, H):
+    """One-token decode at widths where the last 64-lane chunk of a row is only partly filled."""
+    wl = synth.Workload("one-token widths", H=H, E=12, k=3, I=256, dtype=dtype, router_dtype=synth.F32, shared=True,
+                        cfg_id=200 + H + dtype)
+    ex, sh = _experts(wl)
+    rng = np.random.default_rng(H + dtype)
+    for _ in range(2):
+        x = rng.standard_normal((1, wl.H)).astype(np.float32)
+        ids = rng.choice(wl.E, size=(1, wl.k), replace=False).astype(np.int32)
+        w = rng.random((1, wl.k)).astype(np.float32)
+        check_ffn(wl, x, ids, w, ex, sh, slot_perm=rng.permutation(wl.E))
+        check_ffn(wl, x, ids, w, ex, None, accumulate=True)
+
+
 def test_ffn_invalid_ids_raise_and_contribute_nothing():
     wl = synth.Workload("bad-ids", H=256, E=8, k=2, I=128, dtype=synth.BF16, cfg_id=95)
     ex, _ = _experts(wl)
