@@ -310,7 +310,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     t_decode = time.perf_counter() - t0
     moe.moe_sync_check()
     st3 = cache.stats()
-    ktimes = {name: stack.kernel_time(w, args.replays) for w, name in enumerate(["route", "gateup", "down"])}
+    ktimes = {name: stack.kernel_time(w, args.replays) for w, name in enumerate(["route", "gateup", "down", "ffn"])}
     moe.moe_sync_check()
     bound = residency_bound(moe, cache, E, st3["capacity"])
     stack.close()
@@ -370,7 +370,8 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
                      "frac_of_practical": gu_gbps / hbm["launch_GBps"]},
         "hbm_ceiling": hbm,
         "kernels": {"route_us": ktimes["route"] * 1e3, "gateup_us": gu_ms * 1e3, "down_us": dn_ms * 1e3,
-                    "down_bytes_per_launch": dn_bytes, "down_GBps": dn_bytes / (dn_ms * 1e-3) / 1e9},
+                    "down_bytes_per_launch": dn_bytes, "down_GBps": dn_bytes / (dn_ms * 1e-3) / 1e9,
+                    "ffn_us": ktimes["ffn"] * 1e3, "ffn_GBps": (gu_bytes + dn_bytes) / (ktimes["ffn"] * 1e-3) / 1e9},
         "prefill": {"tokens": Tp, "tokens_per_s": Tp / t_prefill, "ms": t_prefill * 1e3,
                     "h2d_bytes": d_pf["h2d_bytes"], "misses": d_pf["misses"],
                     "h2d_GBps": d_pf["h2d_bytes"] / t_prefill / 1e9,
@@ -473,7 +474,7 @@ def main():
     moe.moe_sync_check(stream)
     st1 = cache.stats()
     # per-launch device time: each kernel of the last layer re-launched back to back between two events
-    ktimes = {name: stack.kernel_time(w, args.replays) for w, name in enumerate(["route", "gateup", "down"])}
+    ktimes = {name: stack.kernel_time(w, args.replays) for w, name in enumerate(["route", "gateup", "down", "ffn"])}
     moe.moe_sync_check(stream)
 
     tok_s = args.steps * T / elapsed
@@ -550,7 +551,8 @@ def main():
         "hbm_ceiling": hbm,
         "kernels": {"route_us": rt_ms * 1e3, "gateup_us": gu_ms * 1e3, "down_us": dn_ms * 1e3,
                     "down_GBps": dn_gbps, "down_bytes_per_launch": dn_bytes,
-                    "ffn_GBps": (gu_bytes + dn_bytes) / ((gu_ms + dn_ms) * 1e-3) / 1e9 if gu_ms else None},
+                    "ffn_us": ktimes["ffn"] * 1e3,
+                    "ffn_GBps": (gu_bytes + dn_bytes) / (ktimes["ffn"] * 1e-3) / 1e9 if ktimes["ffn"] else None},
         "residency": {**d, "miss_rate": d["misses"] / d["lookups"] if d["lookups"] else 0.0,
                       "misses_per_token": d["misses"] / (args.steps * T), "bound": bound},
         "pcie": pcie,

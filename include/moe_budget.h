@@ -321,7 +321,8 @@ MOE_API int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *
                               void *stream);
 
 /* Mean device time (ms) of one launch of kernel `which` (0 = router logits and
- * top-k, 1 = expert gate/up + SwiGLU, 2 = expert down + combine).  Each
+ * top-k, 1 = expert gate/up + SwiGLU, 2 = expert down + combine, 3 = the whole
+ * expert FFN as the decode step issues it, both launches).  Each
  * layer's launch of the last decode step is re-issued with the same
  * arguments, in step order, captured into one HIP graph on a private stream
  * (ordered after `stream`); the graph is replayed n times between two HIP

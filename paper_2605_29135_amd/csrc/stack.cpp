@@ -305,7 +305,7 @@ int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out,
 }
 
 int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *mean_ms) {
-    if (!s || !mean_ms || which < 0 || which > 2 || n < 1)
+    if (!s || !mean_ms || which < 0 || which > 3 || n < 1)
         return moe::fail(MOE_ERR_INVALID_ARG, "kernel_time: bad argument");
     for (const LastLayer &ll : s->last)
         if (!ll.valid) return moe::fail(MOE_ERR_INVALID_ARG, "kernel_time: no decode step has run yet");
@@ -340,7 +340,7 @@ int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *
         return moe::launch_expert_ffn(s->scratch_x, T, d.H, d.I, d.E, d.k, ll.ids, ll.weights, ll.slot_of, ll.pool,
                                       s->expert_bytes, d.w_dtype, s->shared_w.empty() ? nullptr : s->shared_w[l],
                                       s->scratch_y, false, ws, eflags, cs, ll.plan.n ? &ll.plan : nullptr,
-                                      which == 1 ? moe::kFfnGateUp : moe::kFfnDown);
+                                      which == 1 ? moe::kFfnGateUp : which == 2 ? moe::kFfnDown : moe::kFfnBoth);
     };
     // Multi-token steps under a budget read the device slot table, where an
     // earlier layer's experts may have been evicted since: replay only the
