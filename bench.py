@@ -121,7 +121,8 @@ def hbm_ceiling(torch, moe, launch_bytes: int, n_launch: int = 40, stream_bytes:
                       f"{launch_bytes} B over distinct memory replayed from a graph"}
 
 
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "cfg4_gateup_hbm_traffic.txt")
+TRAFFIC_FILES = {4: os.path.join(ROOT, "profiles", "cfg4_gateup_hbm_traffic.txt"),
+                 5: os.path.join(ROOT, "profiles", "cfg5_gateup_hbm_traffic.txt")}
 CSRC = os.path.join(ROOT, "paper_2605_29135_amd", "csrc")
 
 
@@ -139,20 +140,21 @@ def gateup_source_hash() -> str:
     return h.hexdigest()
 
 
-def measured_traffic():
+def measured_traffic(cfg=4):
     """HBM bytes per gate/up launch from the committed counter summary (FETCH_SIZE + WRITE_SIZE, each
     calibrated by a known-size kernel), or None when the kernel source changed since they were taken."""
-    if not os.path.exists(TRAFFIC_FILE):
+    path = TRAFFIC_FILES[cfg]
+    if not os.path.exists(path):
         return None, "no counter summary"
     kv = {}
-    with open(TRAFFIC_FILE) as fh:
+    with open(path) as fh:
         for line in fh:
             if ":" in line and not line.startswith("#"):
                 key, val = line.split(":", 1)
                 kv[key.strip()] = val.strip()
     if kv.get("kernel_source_sha256") != gateup_source_hash():
         return None, "kernel source changed since the counters were taken"
-    return float(kv["hbm_bytes_per_launch"]), TRAFFIC_FILE[len(ROOT) + 1:]
+    return float(kv["hbm_bytes_per_launch"]), path[len(ROOT) + 1:]
 
 
 def expert_kernel_bytes(wl, n_exp, T):
@@ -321,6 +323,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     gu_ms, dn_ms = ktimes["gateup"], ktimes["down"]
     gu_gbps = gu_bytes / (gu_ms * 1e-3) / 1e9
     hbm = hbm_ceiling(torch, moe, gu_bytes)
+    traffic, traffic_src = measured_traffic(5)
 
     # the prompt chunk's expert FFN on the matrix cores, one layer with its experts resident
     layer_blob = torch.from_numpy(np.ascontiguousarray(store[L - 1]).reshape(-1)).to(dev)
@@ -366,7 +369,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
                      "bytes_per_launch": gu_bytes, "mean_launch_us": gu_ms * 1e3,
                      "timing": f"the last step's {L} launches (one per layer, same arguments) in one HIP graph, "
                                f"replayed {args.replays}x between HIP events",
-                     "traffic": None, "practical_ceiling_GBps": hbm["launch_GBps"],
+                     "traffic": traffic, "traffic_source": traffic_src, "practical_ceiling_GBps": hbm["launch_GBps"],
                      "frac_of_practical": gu_gbps / hbm["launch_GBps"]},
         "hbm_ceiling": hbm,
         "kernels": {"route_us": ktimes["route"] * 1e3, "gateup_us": gu_ms * 1e3, "down_us": dn_ms * 1e3,
@@ -505,7 +508,7 @@ def main():
                 "ceiling_method": "hipMemcpyAsync from hipHostMalloc memory, 64 MiB and expert-size chunks"}
 
     hbm = hbm_ceiling(torch, moe, gu_bytes)
-    traffic, traffic_src = measured_traffic()
+    traffic, traffic_src = measured_traffic(4)
 
     bound = residency_bound(moe, cache, E, st1["capacity"]) if budgeted else None
 

@@ -699,9 +699,12 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
         ent_ok[j] = ok;
     }
     __syncthreads();
-    // 3. weight loads of this wave's output row
+    // 3. weight loads of this wave's output row.  Workgroup b runs on XCD b mod 8: consecutive row tiles
+    // go to the same XCD, so the blocks that share a cache line of int4 row scales share one L2.
     const int lane = threadIdx.x & (kWave - 1);
-    const int h = min(blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave), H - 1);
+    const int nb = gridDim.x;
+    const int tile = (nb & 7) ? int(blockIdx.x) : int(blockIdx.x & 7) * (nb >> 3) + int(blockIdx.x >> 3);
+    const int h = min(tile * (kBlock / kWave) + (threadIdx.x / kWave), H - 1);
     const size_t rb = row_bytes_of(DT, I);
     const unsigned cpr = unsigned(rb / 16);  // chunks per expert row
     const unsigned total = unsigned(NE) * cpr;
@@ -754,7 +757,7 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
         }
     }
     const float v = wave_sum(acc);
-    const int hrow = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
+    const int hrow = tile * (kBlock / kWave) + (threadIdx.x / kWave);
     if (lane == 0 && hrow < H) {
         float *o = y + size_t(t) * H + hrow;
         *o = accumulate ? *o + v : v;
