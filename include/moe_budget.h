@@ -72,6 +72,7 @@ extern "C" {
 
 /* ---- residency ---- */
 #define MOE_POLICY_LRU 0
+#define MOE_POLICY_ROTARY 1 /* rotary slot group: a ring of slots swept by a hand (sec. 4, Fig. 2) */
 #define MOE_CACHE_PRELOAD 1  /* start with every expert resident at slot layer*E + expert */
 #define MOE_CACHE_HOST_SIM 2 /* no device: slots live in host memory and fills are memcpy */
 
@@ -183,9 +184,22 @@ MOE_API int moe_combine(const float *y_partial, const float *weights, const floa
                 int H, float *y_out, int flags, void *stream);
 
 /* ======================================================================= */
-/* Expert residency: LRU slot table in HBM, misses filled from pinned host   */
+/* Expert residency: slot table in HBM, misses filled from pinned host      */
 /* memory (paper Fig. 1: host tier, slot group, lookup table sub-module id  */
-/* -> slot, selective load, evict; sec. 4: LRU as the conventional policy)  */
+/* -> slot, selective load, evict; sec. 4: LRU as the conventional policy,  */
+/* and the rotary slot group whose residency advances around a ring).       */
+/*                                                                         */
+/* Replacement at step granularity: a lookup takes the step's ascending     */
+/* unique experts; a miss takes the lowest free slot, else a victim whose   */
+/* expert the same step does not need.                                      */
+/*   MOE_POLICY_LRU: the least recently used slot (one stamp per lookup).   */
+/*   MOE_POLICY_ROTARY: the slots form a ring with a hand; a demand hit     */
+/*     raises its slot's charge by one (at most charge_max), a new entry    */
+/*     starts uncharged; a miss rotates the hand forward, passing over the  */
+/*     step's own slots, taking one charge from each charged slot it passes */
+/*     and stopping at the first uncharged one, which is the victim; the    */
+/*     hand then moves past it.  The paper does not disclose how its        */
+/*     rotation is steered: the charges are this library's reading.         */
 /* ======================================================================= */
 
 typedef struct moe_cache moe_cache;
@@ -200,8 +214,9 @@ typedef struct {
                                   host_base + l*host_layer_stride + e*host_expert_stride (blob size a multiple of 16) */
     size_t host_layer_stride;  /* 0 lets layers alias one host copy (keys stay distinct) */
     size_t host_expert_stride;
-    int policy;                /* MOE_POLICY_LRU */
+    int policy;                /* MOE_POLICY_LRU or MOE_POLICY_ROTARY */
     int flags;                 /* MOE_CACHE_PRELOAD | MOE_CACHE_HOST_SIM */
+    int charge_max;            /* MOE_POLICY_ROTARY: most charge a slot holds, 0..65535 (0 = cyclic FIFO) */
 } moe_cache_desc;
 
 typedef struct {

@@ -55,6 +55,8 @@ def lib() -> C.CDLL:
         _lib.oracle_expert_weight.restype = C.c_double
         _lib.oracle_lru_new.argtypes = [I32, I32, I32, I32]
         _lib.oracle_lru_new.restype = P
+        _lib.oracle_rotary_new.argtypes = [I32, I32, I32, I32, I32]
+        _lib.oracle_rotary_new.restype = P
         _lib.oracle_lru_free.argtypes = [P]
         _lib.oracle_lru_lookup.argtypes = [P, I32, I32, P, I32, I32]
         _lib.oracle_lru_n_events.argtypes = [P]
@@ -173,6 +175,7 @@ class LRU:
             raise ValueError("oracle_lru_new: invalid arguments")
         self.C, self.L, self.E = capacity, L, E
 
+
     def __del__(self):
         h, self._h = getattr(self, "_h", None), None
         if h:
@@ -200,6 +203,17 @@ class LRU:
     def occupancy(self) -> int:
         return int(lib().oracle_lru_occupancy(self._h))
 
+
+class Rotary(LRU):
+    """Rotary slot group (paper sec. 4, Figs. 1-2): slots on a ring swept by a hand; hits charge their slot
+    (up to charge_max), a miss rotates the hand forward past the step's own slots and charged slots (each
+    giving up one charge) to the first uncharged slot.  charge_max = 0 is cyclic (FIFO) replacement."""
+
+    def __init__(self, capacity: int, L: int, E: int, charge_max: int, preload: bool = False):
+        self._h = lib().oracle_rotary_new(capacity, L, E, charge_max, int(preload))
+        if not self._h:
+            raise ValueError("oracle_rotary_new: invalid arguments")
+        self.C, self.L, self.E = capacity, L, E
 
 def opt_misses(steps, n_keys: int, capacity: int) -> int:
     """Fewest fills any replacement policy needs for `steps` (a list of arrays of distinct keys, each step's

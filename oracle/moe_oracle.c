@@ -19,7 +19,12 @@
  *     the accelerator holds slots, a lookup table maps sub-module id to slot,
  *     selective load brings sub-modules in and evict makes room; sec. 4 names
  *     least-recently-used eviction as the conventional policy; sec. 5:
- *     memory-constrained execution): an LRU slot table of fixed capacity.
+ *     memory-constrained execution): an LRU slot table of fixed capacity,
+ *     and the rotary slot group of sec. 4 and Fig. 2 (the slots form a ring
+ *     that is rotated forward, cyclic replacement instead of recency order;
+ *     how the rotation is steered is not disclosed, so the steering here is
+ *     our reading: a per-slot charge raised by hits, spent by the passing
+ *     hand).
  *   - offline bound on residency: the fewest fills any replacement policy
  *     could need for a demand trace (Belady's farthest-next-use rule at step
  *     granularity), the yardstick against which LRU's fills are reported.
@@ -287,24 +292,34 @@ typedef struct {
     int32_t t, layer, expert, kind, slot, victim_key;
 } oracle_event;
 
+#define OR_POLICY_LRU 0
+#define OR_POLICY_ROTARY 1
+
 typedef struct {
     int C, L, E;
+    int policy;           /* OR_POLICY_LRU or OR_POLICY_ROTARY */
+    int charge_max;       /* rotary: the most charge a slot can hold */
     int32_t *key_of_slot; /* layer * E + expert, or -1 for a free slot */
-    uint64_t *stamp;      /* recency stamp of each slot */
+    uint64_t *stamp;      /* LRU: recency stamp of each slot */
+    int *charge;          /* rotary: charge of each slot */
+    int hand;             /* rotary: the ring position the next rotation starts from */
     uint64_t ctr;
     oracle_event *ev;
     size_t n_ev, cap_ev;
     uint64_t hits, misses, prefetches, evictions;
 } oracle_lru;
 
-oracle_lru *oracle_lru_new(int capacity, int L, int E, int preload)
+static oracle_lru *residency_new(int capacity, int L, int E, int preload, int policy, int charge_max)
 {
-    if (capacity < 1 || L < 1 || E < 1 || (preload && capacity < L * E))
+    if (capacity < 1 || L < 1 || E < 1 || (preload && capacity < L * E) || charge_max < 0)
         return NULL;
     oracle_lru *c = calloc(1, sizeof *c);
     c->C = capacity;
     c->L = L;
     c->E = E;
+    c->policy = policy;
+    c->charge_max = charge_max;
+    c->charge = calloc((size_t)capacity, sizeof(int));
     c->key_of_slot = malloc(sizeof(int32_t) * (size_t)capacity);
     c->stamp = calloc((size_t)capacity, sizeof(uint64_t));
     for (int s = 0; s < capacity; s++)
@@ -317,12 +332,31 @@ oracle_lru *oracle_lru_new(int capacity, int L, int E, int preload)
     return c;
 }
 
+oracle_lru *oracle_lru_new(int capacity, int L, int E, int preload)
+{
+    return residency_new(capacity, L, E, preload, OR_POLICY_LRU, 0);
+}
+
+/* Rotary slot group (sec. 4, Figs. 1-2): the C slots form a ring with a hand.
+ * Our steering of the rotation: a demand hit raises its slot's charge by one
+ * (at most charge_max); a new entry starts uncharged.  A miss with no free slot
+ * rotates the hand forward one slot at a time: a slot whose expert the current
+ * step needs is passed over unchanged, a charged slot gives up one charge and
+ * is passed over, and the first uncharged slot is the victim; the new entry
+ * takes it and the hand moves on past it.  With charge_max = 0 this is cyclic
+ * (first-in first-out) replacement. */
+oracle_lru *oracle_rotary_new(int capacity, int L, int E, int charge_max, int preload)
+{
+    return residency_new(capacity, L, E, preload, OR_POLICY_ROTARY, charge_max);
+}
+
 void oracle_lru_free(oracle_lru *c)
 {
     if (!c)
         return;
     free(c->key_of_slot);
     free(c->stamp);
+    free(c->charge);
     free(c->ev);
     free(c);
 }
@@ -366,8 +400,18 @@ static int ascending_unique(const int32_t *ids, int n, int32_t *out)
     return m;
 }
 
-/* Where a non-resident key goes: the lowest free slot, else the slot with the
- * smallest stamp whose key is not in R (the step's set stays resident). */
+static int in_step(const oracle_lru *c, int layer, const int32_t *R, int m, int32_t key)
+{
+    for (int j = 0; j < m; j++)
+        if (key == layer * c->E + R[j])
+            return 1;
+    return 0;
+}
+
+/* Where a non-resident key goes: the lowest free slot; else, LRU: the slot with
+ * the smallest stamp whose key is not in R (the step's set stays resident);
+ * rotary: the slot at which the forward rotation stops (see oracle_rotary_new).
+ * Some slot outside R exists whenever R holds a key that is not resident. */
 static int place(oracle_lru *c, int layer, const int32_t *R, int m, int32_t *victim)
 {
     for (int s = 0; s < c->C; s++)
@@ -375,14 +419,23 @@ static int place(oracle_lru *c, int layer, const int32_t *R, int m, int32_t *vic
             *victim = -1;
             return s;
         }
+    if (c->policy == OR_POLICY_ROTARY) {
+        for (;;) {
+            int s = c->hand;
+            c->hand = (c->hand + 1) % c->C;
+            if (in_step(c, layer, R, m, c->key_of_slot[s]))
+                continue;
+            if (c->charge[s] > 0) {
+                c->charge[s]--;
+                continue;
+            }
+            *victim = c->key_of_slot[s];
+            return s;
+        }
+    }
     int best = -1;
     for (int s = 0; s < c->C; s++) {
-        int32_t key = c->key_of_slot[s];
-        int in_step = 0;
-        for (int j = 0; j < m; j++)
-            if (key == layer * c->E + R[j])
-                in_step = 1;
-        if (in_step)
+        if (in_step(c, layer, R, m, c->key_of_slot[s]))
             continue;
         if (best < 0 || c->stamp[s] < c->stamp[best])
             best = s;
@@ -413,6 +466,8 @@ int oracle_lru_lookup(oracle_lru *c, int t, int layer, const int32_t *ids, int n
             if (prefetch)
                 continue; /* resident: a prefetch leaves it untouched */
             c->stamp[s] = ++c->ctr;
+            if (c->charge[s] < c->charge_max)
+                c->charge[s]++;
             c->hits++;
             log_event(c, t, layer, R[j], 0, s, -1);
             continue;
@@ -423,6 +478,7 @@ int oracle_lru_lookup(oracle_lru *c, int t, int layer, const int32_t *ids, int n
             c->evictions++;
         c->key_of_slot[s] = key;
         c->stamp[s] = ++c->ctr;
+        c->charge[s] = 0;
         if (prefetch)
             c->prefetches++;
         else

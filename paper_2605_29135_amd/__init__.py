@@ -5,7 +5,7 @@ residency runtime, C ABI in ``include/moe_budget.h``); :mod:`.binding` only
 marshals torch device tensors into it.
 """
 from .binding import (  # noqa: F401
-    EVENT_HIT, EVENT_MISS, EVENT_PREFETCH, MOE_ACCUMULATE, MOE_BF16, MOE_ROUTE_RMSNORM, MOE_F32, MOE_INT4G128, ExpertCache,
+    EVENT_HIT, EVENT_MISS, EVENT_PREFETCH, MOE_ACCUMULATE, MOE_BF16, MOE_ROUTE_RMSNORM, MOE_F32, MOE_INT4G128, MOE_POLICY_LRU, MOE_POLICY_ROTARY, ExpertCache,
     MoeError, MoeStack, PinnedBuffer, header_symbols, lib, moe_combine, moe_expert_ffn_grouped, moe_hbm_read_probe, moe_opt_fills, moe_opt_fills_flat,
     moe_ffn_workspace_bytes, moe_init, moe_prefill_grouped, moe_prefill_workspace_bytes, moe_route_topk,
     moe_sync_check)

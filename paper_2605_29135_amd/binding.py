@@ -23,6 +23,7 @@ MOE_F32, MOE_BF16, MOE_INT4G128 = 0, 1, 2
 MOE_ACCUMULATE = 1
 MOE_ROUTE_RMSNORM = 1
 MOE_POLICY_LRU = 0
+MOE_POLICY_ROTARY = 1
 MOE_CACHE_PRELOAD, MOE_CACHE_HOST_SIM = 1, 2
 EVENT_HIT, EVENT_MISS, EVENT_PREFETCH = 0, 1, 2
 MAX_DECODE_TOKENS = 16
@@ -38,7 +39,7 @@ class CacheDesc(C.Structure):
     _fields_ = [("n_layers", C.c_int), ("n_experts", C.c_int), ("expert_bytes", C.c_size_t),
                 ("budget_bytes", C.c_size_t), ("reserved_bytes", C.c_size_t), ("host_base", C.c_void_p),
                 ("host_layer_stride", C.c_size_t), ("host_expert_stride", C.c_size_t),
-                ("policy", C.c_int), ("flags", C.c_int)]
+                ("policy", C.c_int), ("flags", C.c_int), ("charge_max", C.c_int)]
 
 
 class CacheStats(C.Structure):
@@ -260,14 +261,15 @@ def moe_combine(y_partial, weights, y_shared=None, y_out=None, accumulate: bool 
 
 
 class ExpertCache:
-    """Owner of one expert_cache (LRU slot table in HBM over a pinned host store)."""
+    """Owner of one expert_cache (slot table in HBM over a pinned host store; LRU or rotary replacement)."""
 
     def __init__(self, n_layers: int, n_experts: int, expert_bytes: int, budget_bytes: int, host_base: int,
                  host_layer_stride: int, host_expert_stride: int, reserved_bytes: int = 0,
-                 preload: bool = False, host_sim: bool = False):
+                 preload: bool = False, host_sim: bool = False, policy: int = MOE_POLICY_LRU,
+                 charge_max: int = 0):
         d = CacheDesc(n_layers, n_experts, expert_bytes, budget_bytes, reserved_bytes, host_base,
-                      host_layer_stride, host_expert_stride, MOE_POLICY_LRU,
-                      (MOE_CACHE_PRELOAD if preload else 0) | (MOE_CACHE_HOST_SIM if host_sim else 0))
+                      host_layer_stride, host_expert_stride, policy,
+                      (MOE_CACHE_PRELOAD if preload else 0) | (MOE_CACHE_HOST_SIM if host_sim else 0), charge_max)
         h = C.c_void_p()
         _check(lib().expert_cache_create(C.byref(d), C.byref(h)), "expert_cache_create")
         self._h = h

@@ -1,12 +1,18 @@
-// residency.cpp -- expert slot table in HBM with least-recently-used replacement.
+// residency.cpp -- expert slot table in HBM, LRU or rotary replacement.
 //
 // The paper's residency picture (sec. 4, Fig. 1): every sub-module (expert)
 // lives in the host tier; the accelerator holds a fixed group of slots; a
 // lookup table maps sub-module id to slot; missing sub-modules are brought in
 // by a selective load after an eviction makes room; the whole runs inside a
-// memory budget (sec. 5).  Replacement here is LRU at step granularity: a
-// step's ascending unique experts take one recency stamp each, and a miss
-// evicts the least recently used slot whose expert the same step does not need.
+// memory budget (sec. 5).  Replacement is at step granularity: a step's
+// ascending unique experts are looked up in turn, and a miss never evicts an
+// expert the same step needs.  LRU: one recency stamp per lookup, the least
+// recent slot is the victim.  Rotary (sec. 4, Fig. 2: the slot group advances
+// around a cycle): the slots form a ring with a hand; demand hits charge their
+// slot (saturating at charge_max); a miss turns the hand forward past the
+// step's own slots and past charged slots (each losing one charge) to the first
+// uncharged slot.  The charges are this library's reading of how the paper's
+// rotation is steered, which it does not disclose.
 //
 // Device ordering (per cache):
 //   demand lookup : on the compute stream, after any earlier prefetch's fills:
@@ -82,8 +88,12 @@ struct moe_cache {
 
     std::vector<int32_t> key_of_slot;  // layer*E + expert, -1 = free
     std::vector<int32_t> slot_of_key;  // host mirror of the device table [L*E]
-    std::vector<int32_t> prev, next;   // recency list over slots, head = least recent
+    std::vector<int32_t> prev, next;   // LRU: recency list over slots, head = least recent
     int head = -1, tail = -1;
+    bool rotary = false;
+    int charge_max = 0;
+    std::vector<uint16_t> charge;      // rotary: charge of each slot
+    int hand = 0;                      // rotary: ring position the next rotation starts from
     std::priority_queue<int, std::vector<int>, std::greater<int>> free_slots;
     std::vector<uint64_t> step_mark;   // == epoch while the key is in the current step's set
     uint64_t epoch = 0;
@@ -167,17 +177,33 @@ int place_and_fill(moe_cache *c, int layer, int e, int32_t *victim, std::vector<
         s = c->free_slots.top();
         c->free_slots.pop();
     } else {
-        s = c->head;
-        while (s >= 0 && c->step_mark[c->key_of_slot[s]] == c->epoch) s = c->next[s];
-        if (s < 0) {  // unreachable while |R| <= C
-            *status = moe::fail(MOE_ERR_BUDGET, "no evictable slot");
-            return -1;
+        if (c->rotary) {
+            // Some slot holds an expert outside the step (the key being placed is not resident and the
+            // step has at most C experts), and every full turn takes a charge from each such slot, so the
+            // hand stops within (charge_max + 1) turns.
+            for (;;) {
+                s = c->hand;
+                c->hand = c->hand + 1 == c->C ? 0 : c->hand + 1;
+                if (c->step_mark[c->key_of_slot[s]] == c->epoch) continue;
+                if (c->charge[s] > 0) {
+                    --c->charge[s];
+                    continue;
+                }
+                break;
+            }
+        } else {
+            s = c->head;
+            while (s >= 0 && c->step_mark[c->key_of_slot[s]] == c->epoch) s = c->next[s];
+            if (s < 0) {  // unreachable while |R| <= C
+                *status = moe::fail(MOE_ERR_BUDGET, "no evictable slot");
+                return -1;
+            }
+            unlink(c, s);
         }
         *victim = c->key_of_slot[s];
         c->slot_of_key[*victim] = -1;
         chg_idx->push_back(*victim);
         chg_val->push_back(-1);
-        unlink(c, s);
         ++c->st.evictions;
     }
     const int32_t key = layer * c->E + e;
@@ -200,7 +226,8 @@ int place_and_fill(moe_cache *c, int layer, int e, int32_t *victim, std::vector<
     c->slot_of_key[key] = s;
     chg_idx->push_back(key);
     chg_val->push_back(s);
-    push_recent(c, s);
+    if (c->rotary) c->charge[s] = 0;
+    else push_recent(c, s);
     c->st.h2d_bytes += c->d.expert_bytes;
     return s;
 }
@@ -294,8 +321,12 @@ int lookup_impl(moe_cache *c, int step, int layer, const int32_t *ids, int n, bo
         int s = c->slot_of_key[key];
         if (s >= 0) {
             if (prefetch) continue;  // a prefetch leaves resident experts untouched
-            unlink(c, s);
-            push_recent(c, s);
+            if (c->rotary) {
+                if (c->charge[s] < c->charge_max) ++c->charge[s];
+            } else {
+                unlink(c, s);
+                push_recent(c, s);
+            }
             ++c->st.hits;
             ++c->st.lookups;
             hit_of[r] = 1;
@@ -352,7 +383,10 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
         return moe::fail(MOE_ERR_INVALID_ARG, "n_layers, n_experts and expert_bytes must be positive");
     if (d->expert_bytes % 256)
         return moe::fail(MOE_ERR_INVALID_ARG, "expert_bytes (%zu) must be a multiple of 256", d->expert_bytes);
-    if (d->policy != MOE_POLICY_LRU) return moe::fail(MOE_ERR_INVALID_ARG, "unknown policy %d", d->policy);
+    if (d->policy != MOE_POLICY_LRU && d->policy != MOE_POLICY_ROTARY)
+        return moe::fail(MOE_ERR_INVALID_ARG, "unknown policy %d", d->policy);
+    if (d->policy == MOE_POLICY_ROTARY && (d->charge_max < 0 || d->charge_max > 65535))
+        return moe::fail(MOE_ERR_INVALID_ARG, "charge_max (%d) must be in [0, 65535]", d->charge_max);
     if (!d->host_base) return moe::fail(MOE_ERR_INVALID_ARG, "host_base is NULL");
     if (d->reserved_bytes > d->budget_bytes)
         return moe::fail(MOE_ERR_BUDGET, "reserved bytes exceed the budget");
@@ -378,6 +412,9 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
     c->reader.assign(c->C, EvRef{});
     c->reader_stream.assign(c->C, nullptr);
     c->st.capacity = c->C;
+    c->rotary = d->policy == MOE_POLICY_ROTARY;
+    c->charge_max = c->rotary ? d->charge_max : 0;
+    c->charge.assign(c->C, 0);
 
     auto cleanup = [&](int code) {
         expert_cache_destroy(c);
@@ -428,7 +465,7 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
                 }
                 c->key_of_slot[s] = s;
                 c->slot_of_key[s] = s;
-                push_recent(c, s);
+                if (!c->rotary) push_recent(c, s);
             }
         if (c->sim) {
             for (size_t i = 0; i < keys; ++i) c->dev_slot_of[i] = int32_t(i);

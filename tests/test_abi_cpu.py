@@ -47,9 +47,10 @@ class SimStore:
                     np.full(eb // 4, l * E + e, np.int32).tobytes(), np.uint8)
         self.layer_stride = E * eb if layer_stride is None else layer_stride
 
-    def cache(self, C_slots, preload=False):
+    def cache(self, C_slots, preload=False, policy=moe.MOE_POLICY_LRU, charge_max=0):
         return moe.ExpertCache(self.L, self.E, self.eb, C_slots * self.eb, self.buf.ctypes.data,
-                               self.layer_stride, self.eb, preload=preload, host_sim=True)
+                               self.layer_stride, self.eb, preload=preload, host_sim=True, policy=policy,
+                               charge_max=charge_max)
 
 
 def _pool_key(cache, slot, eb):
@@ -113,6 +114,44 @@ def test_sim_cache_prefetch_matches_oracle():
         assert o.lookup(t, l, ids, prefetch=pre) == oracle.OK
     assert _as_tuples(c.trace()) == _as_tuples(o.events())
     assert c.stats()["prefetches"] == o.stats()["prefetches"] > 0
+
+
+@pytest.mark.parametrize("seed,L,E,n,C_slots,Q", [(0, 2, 12, 3, 5, 0), (1, 3, 16, 8, 8, 1), (2, 1, 40, 8, 20, 3),
+                                                   (3, 4, 128, 8, 60, 32), (4, 2, 20, 4, 9, 2)])
+def test_sim_cache_rotary_matches_oracle(seed, L, E, n, C_slots, Q):
+    """The rotary slot group against the oracle's: demand lookups and prefetches, event for event."""
+    rng = np.random.default_rng(50 + seed)
+    st = SimStore(L, E)
+    c = st.cache(C_slots, policy=moe.MOE_POLICY_ROTARY, charge_max=Q)
+    o = oracle.Rotary(C_slots, L, E, charge_max=Q)
+    for t in range(400):
+        l = int(rng.integers(0, L))
+        ids = rng.integers(0, E, size=int(rng.integers(1, n + 1)))
+        pre = bool(rng.random() < 0.2)
+        if pre:
+            c.prefetch(t, l, ids)
+        else:
+            slots, _ = c.lookup(t, l, ids)
+            for i, e in enumerate(ids):
+                assert (_pool_key(c, slots[i], st.eb) == l * E + e).all()
+            c.release()
+        assert o.lookup(t, l, ids, prefetch=pre) == oracle.OK
+    assert _as_tuples(c.trace()) == _as_tuples(o.events())
+    s, so = c.stats(), o.stats()
+    assert (s["hits"], s["misses"], s["prefetches"], s["evictions"]) == \
+        (so["hits"], so["misses"], so["prefetches"], so["evictions"])
+    assert s["occupancy"] == o.occupancy() <= C_slots
+    table = _table(c, L, E)
+    assert all(table[l * E + e] == o.slot_of(l, e) for l in range(L) for e in range(E))
+
+
+def test_sim_cache_rotary_rejects_bad_charge():
+    st = SimStore(1, 4)
+    for q in (-1, 65536):
+        with pytest.raises(moe.MoeError):
+            st.cache(2, policy=moe.MOE_POLICY_ROTARY, charge_max=q)
+    with pytest.raises(moe.MoeError):
+        st.cache(2, policy=7)
 
 
 def test_sim_cache_golden_step_sets():

@@ -454,6 +454,144 @@ def test_lru_errors():
         oracle.LRU(0, 1, 1)
 
 
+# ------------------------------------------------------- rotary slot group ---
+def test_golden_rotary_fifo_belady_anomaly():
+    g = {}
+    for line in _golden_lines("rotary_fifo_belady.txt"):
+        g[line[0]] = [int(v) for v in line[1:]]
+    ref = g["reference"]
+    for C in (3, 4):
+        c = oracle.Rotary(C, 1, 8, charge_max=0)
+        lru = oracle.LRU(C, 1, 8)
+        for t, e in enumerate(ref):
+            assert c.lookup(t, 0, [e]) == oracle.OK
+            lru.lookup(t, 0, [e])
+        ev = c.events()
+        miss = ev[ev["kind"] == oracle.MISS]
+        assert c.stats()["misses"] == g[f"fifo{C}_faults"][0]
+        assert miss["t"].tolist() == g[f"fifo{C}_fault_steps"]
+        assert [v for v in miss["victim_key"].tolist() if v >= 0] == g[f"fifo{C}_victims"]
+        if C == 3:
+            assert miss["slot"].tolist() == g["fifo3_slots"]
+        assert lru.stats()["misses"] == g[f"lru{C}_faults"][0]
+
+
+def _second_chance_queue_model(trace, C, Q):
+    """Generalised second chance written as a queue: entries wait in a queue in the order the hand meets
+    them; the front entry goes to the back if the step needs it, or if it still holds a charge (spending
+    one); otherwise it leaves and the newcomer joins at the back.  Hits add a charge up to Q.  trace items:
+    (layer, ids, prefetch).  Returns (t, layer, expert, kind, slot, victim_key) tuples, victim keys as
+    layer * 1000 + expert."""
+    from collections import deque
+    q = deque()                 # [key, slot] in hand order
+    charge, slot_of, free = {}, {}, list(range(C))
+    events = []
+    for t, (layer, ids, pf) in enumerate(trace):
+        R = sorted(set(int(e) for e in ids))
+        need = {(layer, e) for e in R}
+        for e in R:
+            key = (layer, e)
+            if key in slot_of:
+                if not pf:
+                    charge[key] = min(charge[key] + 1, Q)
+                    events.append((t, layer, e, 0, slot_of[key], -1))
+                continue
+            if free:
+                s, victim = free.pop(0), -1
+                q.append([key, s])
+            else:
+                while True:
+                    k0, s0 = q[0]
+                    q.rotate(-1)
+                    if k0 in need:
+                        continue
+                    if charge[k0] > 0:
+                        charge[k0] -= 1
+                        continue
+                    break
+                # the victim is now at the back: it becomes the newcomer's entry
+                q[-1] = [key, s0]
+                s, victim = s0, k0[0] * 1000 + k0[1]
+                del slot_of[k0], charge[k0]
+            slot_of[key], charge[key] = s, 0
+            events.append((t, layer, e, 2 if pf else 1, s, victim))
+    return events
+
+
+@pytest.mark.parametrize("seed", range(4))
+def test_rotary_matches_second_chance_queue(seed):
+    rng = np.random.default_rng(700 + seed)
+    L, E = 3, 1000
+    trace = [(int(rng.integers(0, L)), rng.integers(0, 12, size=int(rng.integers(1, 4))), bool(rng.random() < 0.15))
+             for _ in range(400)]
+    for C in (3, 4, 7, 12):
+        for Q in (0, 1, 2, 5):
+            c = oracle.Rotary(C, L, E, charge_max=Q)
+            for t, (layer, ids, pf) in enumerate(trace):
+                assert c.lookup(t, layer, ids, prefetch=pf) == oracle.OK
+            assert _events_tuples(c.events()) == _second_chance_queue_model(trace, C, Q)
+
+
+def test_rotary_without_charge_evicts_in_entry_order():
+    rng = np.random.default_rng(41)
+    C = 6
+    c = oracle.Rotary(C, 1, 40, charge_max=0)
+    order = []
+    for t in range(300):
+        e = int(rng.integers(0, 40))
+        c.lookup(t, 0, [e])
+        ev = c.events()[-1]
+        if ev["kind"] == oracle.MISS:
+            if ev["victim_key"] >= 0:
+                assert ev["victim_key"] == order.pop(0)   # the oldest entry leaves, hits notwithstanding
+            order.append(e)
+    assert len(order) == C
+
+
+def test_rotary_charge_keeps_a_hot_expert():
+    # expert 0 is used every step beside a cyclic sweep over C others: cyclic replacement evicts it once per
+    # turn of the hand, a charged ring never does (each pass spends one charge, each step restores one)
+    C = 5
+    for Q, evicted in ((0, True), (1, False), (3, False)):
+        c = oracle.Rotary(C, 1, 40, charge_max=Q)
+        for t in range(200):
+            c.lookup(2 * t, 0, [0])
+            c.lookup(2 * t + 1, 0, [1 + t % C])
+        ev = c.events()
+        assert bool((ev["victim_key"] == 0).any()) == evicted
+
+
+def test_rotary_counts_occupancy_and_compulsory_misses():
+    rng = np.random.default_rng(43)
+    L, E, n = 3, 32, 8
+    trace = _random_trace(rng, 400, L, E, n)
+    lookups = sum(len(set(ids.tolist())) for _, ids in trace)
+    for C in (n, 13, 40):
+        c = oracle.Rotary(C, L, E, charge_max=3)
+        for t, (l, ids) in enumerate(trace):
+            c.lookup(t, l, ids)
+            assert c.occupancy() <= C
+            assert all(c.slot_of(l, int(e)) >= 0 for e in ids)  # the step's experts are resident together
+        st = c.stats()
+        assert st["hits"] + st["misses"] == lookups
+    distinct = {(l, int(e)) for l, ids in trace for e in ids}
+    c = oracle.Rotary(len(distinct), L, E, charge_max=3)
+    for t, (l, ids) in enumerate(trace):
+        c.lookup(t, l, ids)
+    assert c.stats()["misses"] == len(distinct) and c.stats()["evictions"] == 0
+
+
+def test_rotary_errors_and_preload():
+    c = oracle.Rotary(2, 2, 4, charge_max=1)
+    assert c.lookup(0, 0, [4]) == oracle.ERR_RANGE
+    assert c.lookup(0, 2, [0]) == oracle.ERR_ARG
+    assert c.lookup(0, 0, [0, 1, 2]) == oracle.ERR_BUDGET
+    with pytest.raises(ValueError):
+        oracle.Rotary(2, 1, 4, charge_max=-1)
+    p = oracle.Rotary(6, 2, 3, charge_max=2, preload=True)
+    assert [p.slot_of(l, e) for l in range(2) for e in range(3)] == list(range(6))
+
+
 # ------------------------------------------------------------ OPT bound ---
 def _golden_kv(name):
     kv = {}
