@@ -27,6 +27,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "MoE decode tokens/sec at batch 1 under 6 GB expert budget; expert-FFN HBM GB/s vs peak"
 HBM_PEAK_GBPS = 8000.0
+POLICIES = {"lru": 0, "rotary": 1}  # MOE_POLICY_LRU, MOE_POLICY_ROTARY
 
 
 def parse():
@@ -45,6 +46,9 @@ def parse():
     ap.add_argument("--prefetch", type=int, default=0,
                     help="speculative prefetch per layer (most often demanded non-resident experts of the next "
                          "layer); 0 = off, the LRU residency the workload specifies")
+    ap.add_argument("--policy", choices=["lru", "rotary"], default="lru",
+                    help="replacement policy of the expert slots (the workloads specify LRU)")
+    ap.add_argument("--charge-max", type=int, default=32, help="rotary policy: most charge a slot holds")
     ap.add_argument("--replays", type=int, default=5,
                     help="replays of the last step's launches (one per layer) for the per-launch device time")
     return ap.parse_args()
@@ -172,9 +176,28 @@ def expert_kernel_bytes(wl, n_exp, T):
     return n_exp * gu_w + T * H * 4 + rows * I * 4, n_exp * dn_w + rows * I * 4 + T * H * 8
 
 
-def residency_bound(moe, cache, E, capacity, step_bytes_per_token=None):
-    """LRU fills of the run's whole demand trace (every lookup from the cold cache on) next to the fewest
-    fills any replacement policy could make on the same trace (moe_opt_fills)."""
+def replay_fills(moe, ev, L, E, capacity, policy, charge_max=0):
+    """Fills a host-simulated cache of the library makes when the demand trace `ev` (hit and miss events,
+    in order) is looked up again step by step under another replacement policy (placeholder 256-byte blobs:
+    the decisions do not depend on the bytes)."""
+    eb = 256
+    host = np.zeros(L * E * eb, np.uint8)
+    c = moe.ExpertCache(L, E, eb, capacity * eb, host.ctypes.data, E * eb, eb, host_sim=True, policy=policy,
+                        charge_max=charge_max)
+    step_key = ev["t"].astype(np.int64) * 1_000_000 + ev["layer"]
+    starts = np.r_[np.flatnonzero(np.r_[True, step_key[1:] != step_key[:-1]]), ev.size]
+    for a, b in zip(starts[:-1], starts[1:]):
+        c.lookup(int(ev["t"][a]), int(ev["layer"][a]), ev["expert"][a:b])
+        c.release()
+    fills = c.stats()["misses"]
+    c.close()
+    return int(fills)
+
+
+def residency_bound(moe, cache, E, capacity, step_bytes_per_token=None, policy="lru"):
+    """The run's fills over its whole demand trace (every lookup from the cold cache on), the same trace
+    replayed under each replacement policy of the library (host simulation), and the fewest fills any
+    policy could make on it (moe_opt_fills)."""
     ev = cache.trace()
     # prefetched experts that a later demand lookup found resident
     n_pf, used, pending = int((ev["kind"] == moe.EVENT_PREFETCH).sum()), 0, set()
@@ -196,10 +219,16 @@ def residency_bound(moe, cache, E, capacity, step_bytes_per_token=None):
     starts = np.flatnonzero(np.r_[True, step_key[1:] != step_key[:-1]])
     offsets = np.r_[starts, ev.size].astype(np.int32)
     n_keys = int(ev["layer"].max() + 1) * E
+    L = int(ev["layer"].max() + 1)
     opt = moe.moe_opt_fills_flat(keys, offsets, n_keys, capacity)
-    lru = int((ev["kind"] == moe.EVENT_MISS).sum())
+    run_fills = int((ev["kind"] == moe.EVENT_MISS).sum())
+    lru = run_fills if policy == "lru" else replay_fills(moe, ev, L, E, capacity, moe.MOE_POLICY_LRU)
+    rotary = {str(q): replay_fills(moe, ev, L, E, capacity, moe.MOE_POLICY_ROTARY, q) for q in (0, 4, 32)}
     out = {"scope": "every lookup of the run from a cold cache (warm-up included)", "lookups": int(ev.size),
-           "lru_fills": lru, "opt_fills": int(opt), "opt_over_lru": opt / lru if lru else None}
+           "run_policy": policy, "run_fills": run_fills,
+           "lru_fills": lru, "rotary_fills_by_charge_max": rotary, "opt_fills": int(opt),
+           "opt_over_lru": opt / lru if lru else None,
+           "rotary32_over_lru": rotary["32"] / lru if lru else None}
     if n_pf:
         out["prefetch_fills"] = n_pf
         out["prefetches_used"] = used  # demanded again before being evicted
@@ -276,7 +305,8 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     t_setup = time.perf_counter() - t_setup
 
     def make():
-        cache = moe.ExpertCache(L, E, eb, wl.budget_bytes, buf.ptr, E * eb, eb, reserved_bytes=L * eb)
+        cache = moe.ExpertCache(L, E, eb, wl.budget_bytes, buf.ptr, E * eb, eb, reserved_bytes=L * eb,
+                                policy=POLICIES[args.policy], charge_max=args.charge_max)
         stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=1,
                              max_prefill_tokens=Tp, prefetch=args.prefetch)
         return cache, stack
@@ -314,7 +344,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     st3 = cache.stats()
     ktimes = {name: stack.kernel_time(w, args.replays) for w, name in enumerate(["route", "gateup", "down", "ffn"])}
     moe.moe_sync_check()
-    bound = residency_bound(moe, cache, E, st3["capacity"])
+    bound = residency_bound(moe, cache, E, st3["capacity"], policy=args.policy)
     stack.close()
     cache.close()
 
@@ -363,7 +393,8 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
         "config": {"workload": wl.name, "layers": L, "experts": E, "top_k": k, "shared_expert": True,
                    "hidden": H, "intermediate": I, "prefill_tokens": Tp, "decode_tokens_per_step": 1,
                    "budget_bytes": wl.budget_bytes, "slots": st3["capacity"], "host_store_bytes": L * E * eb,
-                   "prefetch_per_layer": args.prefetch},
+                   "prefetch_per_layer": args.prefetch, "policy": args.policy,
+                   **({"charge_max": args.charge_max} if args.policy == "rotary" else {})},
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU (int4 decode)", "achieved": gu_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gu_gbps / HBM_PEAK_GBPS,
                      "bytes_per_launch": gu_bytes, "mean_launch_us": gu_ms * 1e3,
@@ -454,7 +485,7 @@ def main():
     reserved = L * eb if wl.shared else 0
     budget = wl.budget_bytes if budgeted else L * E * eb + reserved
     cache = moe.ExpertCache(L, E, eb, budget, buf.ptr, 0 if alias else E * eb, eb, reserved_bytes=reserved,
-                            preload=not budgeted)
+                            preload=not budgeted, policy=POLICIES[args.policy], charge_max=args.charge_max)
     stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T,
                          prefetch=args.prefetch if budgeted else 0)
     t_setup = time.perf_counter() - t_setup
@@ -510,7 +541,7 @@ def main():
     hbm = hbm_ceiling(torch, moe, gu_bytes)
     traffic, traffic_src = measured_traffic(4)
 
-    bound = residency_bound(moe, cache, E, st1["capacity"]) if budgeted else None
+    bound = residency_bound(moe, cache, E, st1["capacity"], policy=args.policy) if budgeted else None
 
     # ---- oracle on the host cores (bounded sample of the timed tokens), with a parity check
     sample = list(range(args.warmup, n_steps))
@@ -541,7 +572,8 @@ def main():
         "config": {"workload": wl_name, "layers": L, "experts": E, "top_k": k, "hidden": H, "intermediate": I,
                    "tokens_per_step": T, "budget_bytes": budget, "slots": st1["capacity"],
                    "host_store_bytes": L_store * E * eb, "host_layers_aliased": bool(alias),
-                   "prefetch_per_layer": args.prefetch if budgeted else 0},
+                   "prefetch_per_layer": args.prefetch if budgeted else 0, "policy": args.policy,
+                   **({"charge_max": args.charge_max} if args.policy == "rotary" else {})},
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU", "achieved": gu_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": gu_gbps / HBM_PEAK_GBPS if gu_gbps else None,

@@ -255,17 +255,20 @@ def _pinned_store(wl, layers_alias=False):
     return buf
 
 
-def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=None, T=1):
-    """Decode `steps` steps through the stack; check events exactly and outputs within tolerance."""
+def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=None, T=1, charge_max=None):
+    """Decode `steps` steps through the stack; check events exactly and outputs within tolerance.  With
+    charge_max the slots use the rotary policy (else LRU)."""
     buf = _pinned_store(wl, layers_alias)
     eb = wl.expert_bytes
+    policy = moe.MOE_POLICY_LRU if charge_max is None else moe.MOE_POLICY_ROTARY
     cache = moe.ExpertCache(wl.L, wl.E, eb, capacity * eb + (wl.L * eb if wl.shared else 0), buf.ptr,
-                            0 if layers_alias else wl.E * eb, eb, reserved_bytes=wl.L * eb if wl.shared else 0)
+                            0 if layers_alias else wl.E * eb, eb, reserved_bytes=wl.L * eb if wl.shared else 0,
+                            policy=policy, charge_max=charge_max or 0)
     routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
     shared = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)] if wl.shared else None
     stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T)
     sets = synth.routing_sets(wl, steps=steps, T=T)
-    o = oracle.LRU(capacity, wl.L, wl.E)
+    o = oracle.LRU(capacity, wl.L, wl.E) if charge_max is None else oracle.Rotary(capacity, wl.L, wl.E, charge_max)
     check_steps = set(range(steps) if check_steps is None else check_steps)
     host_layers = {}
     for t in range(steps):
@@ -293,7 +296,7 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
                 xr = xr + oracle.moe_ffn(hr, g_ids[l], g_w[l], host_layers[lsrc], wl.H, wl.I, wl.dtype, sh)
             assert normwise(x.cpu().numpy() - x0, xr - x0) <= TOL[wl.dtype]
     n_ev = len(cache.trace())
-    for which in range(3):  # re-launch timing leaves the residency state alone
+    for which in range(4):  # re-launch timing leaves the residency state alone
         assert stack.kernel_time(which, 5) > 0
     moe.moe_sync_check()
     assert len(cache.trace()) == n_ev
@@ -313,6 +316,15 @@ def test_budgeted_stack_small_evicting():
     wl = synth.Workload("small stack", H=512, E=32, k=4, I=256, L=4, dtype=synth.BF16, routing="zipf_overlap",
                         cfg_id=97)
     s = run_stack_and_check(wl, steps=40, capacity=24)
+    assert s["evictions"] > 0
+
+
+@pytest.mark.parametrize("charge_max", [0, 3])
+def test_budgeted_stack_rotary_slots(charge_max):
+    """The stack over a rotary slot group: residency decisions event for event against the oracle's ring."""
+    wl = synth.Workload("small stack", H=512, E=32, k=4, I=256, L=4, dtype=synth.BF16, routing="zipf_overlap",
+                        cfg_id=97)
+    s = run_stack_and_check(wl, steps=40, capacity=24, charge_max=charge_max)
     assert s["evictions"] > 0
 
 
