@@ -308,6 +308,17 @@ typedef struct {
     int prefetch;                   /* one-token decode under a budget: after each layer, prefetch up to this
                                        many experts of the next layer -- its most often demanded ones that
                                        are not resident (ties: lower id); 0 = off */
+    int recall;                     /* one-token decode under a budget: reverse rotation (sec. 4, Fig. 2: a
+                                       recurring context returns the slot group to a prior set).  The stack
+                                       keeps up to this many snapshots of past tokens -- the token's layer-0
+                                       expert set as its context signature (the routing result of the
+                                       hidden state, Fig. 1) and its expert set at every layer.  When a
+                                       token's layer-0 set shares >= recall_overlap experts with a snapshot
+                                       (the most shared; ties: the most recent), the stack prefetches that
+                                       snapshot's layer l+1 set after each layer l's release.  At the end of
+                                       a token its snapshot replaces one with the same signature, else the
+                                       oldest.  0 = off; at most 4096 */
+    int recall_overlap;             /* 1..k shared layer-0 experts a recall needs (0 means k) */
 } moe_stack_desc;
 
 MOE_API int moe_stack_create(const moe_stack_desc *desc, moe_stack **out);

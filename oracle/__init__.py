@@ -215,6 +215,58 @@ class Rotary(LRU):
             raise ValueError("oracle_rotary_new: invalid arguments")
         self.C, self.L, self.E = capacity, L, E
 
+class Recall:
+    """Reverse rotation of the slot group (paper sec. 4, Fig. 2: when an earlier context recurs the
+    residency returns to the slot set it had).  Our reading: a token's context signature is its layer-0
+    expert set (the routing result of its hidden state, Fig. 1); up to `capacity` past tokens are remembered
+    with their expert set at every layer.  A token whose signature shares at least `overlap` experts (0 means
+    all k) with a remembered one recalls the one sharing the most (ties: the most recently stored), and the
+    slot group is asked to bring back that token's set of each later layer.  After the token, it is
+    remembered in place of a remembered token with the same signature, else of the oldest."""
+
+    def __init__(self, capacity: int, k: int, overlap: int = 0):
+        self.capacity, self.k = capacity, k
+        self.need = overlap if overlap else k
+        self.snaps = []   # [signature (frozenset), per-layer sets, order stored, token]
+        self.n = 0
+
+    def step(self, t: int, sets):
+        """Token t's expert sets per layer (lists of k ids).  Returns (recalled token or -1, [(layer, ids)]
+        for layers 1..L-1), then remembers token t."""
+        s0 = frozenset(int(e) for e in sets[0])
+        best, best_n = None, -1
+        for snap in self.snaps:
+            n = len(s0 & snap[0])
+            if n >= self.need and (n > best_n or (n == best_n and snap[2] > best[2])):
+                best, best_n = snap, n
+        calls = [] if best is None else [(l, list(best[1][l])) for l in range(1, len(sets))]
+        self.n += 1
+        new = [s0, [[int(e) for e in st] for st in sets], self.n, t]
+        for i, snap in enumerate(self.snaps):
+            if snap[0] == s0:
+                self.snaps[i] = new
+                break
+        else:
+            if len(self.snaps) < self.capacity:
+                self.snaps.append(new)
+            else:
+                i = min(range(len(self.snaps)), key=lambda j: self.snaps[j][2])
+                self.snaps[i] = new
+        return (-1 if best is None else best[3]), calls
+
+
+def replay_decode(cache, token_sets, recall: Recall | None = None):
+    """Drive an oracle slot table (LRU or Rotary) the way one-token decode does: per token, per layer, the
+    demand lookup of that layer's set, then (with recall) the prefetch of the recalled next-layer set."""
+    for t, sets in enumerate(token_sets):
+        calls = dict(recall.step(t, sets)[1]) if recall is not None else {}
+        for l, ids in enumerate(sets):
+            cache.lookup(t, l, ids)
+            if l + 1 in calls:
+                cache.lookup(t, l + 1, calls[l + 1], prefetch=True)
+    return cache
+
+
 def opt_misses(steps, n_keys: int, capacity: int) -> int:
     """Fewest fills any replacement policy needs for `steps` (a list of arrays of distinct keys, each step's
     keys resident together) with `capacity` slots: Belady's farthest-next-use rule at step granularity.

@@ -56,7 +56,8 @@ class StackDesc(C.Structure):
     _fields_ = [("n_layers", C.c_int), ("H", C.c_int), ("I", C.c_int), ("E", C.c_int), ("k", C.c_int),
                 ("w_dtype", C.c_int), ("router_dtype", C.c_int), ("router_w", C.POINTER(C.c_void_p)),
                 ("shared_w", C.POINTER(C.c_void_p)), ("cache", C.c_void_p), ("max_tokens", C.c_int),
-                ("max_prefill_tokens", C.c_int), ("prefetch", C.c_int)]
+                ("max_prefill_tokens", C.c_int), ("prefetch", C.c_int), ("recall", C.c_int),
+                ("recall_overlap", C.c_int)]
 
 
 _lib = None
@@ -337,7 +338,7 @@ class MoeStack:
 
     def __init__(self, cache: ExpertCache, H: int, I: int, E: int, k: int, w_dtype: int, router_dtype: int,
                  router_w: list, shared_w: list | None = None, max_tokens: int = 1, max_prefill_tokens: int = 0,
-                 prefetch: int = 0):
+                 prefetch: int = 0, recall: int = 0, recall_overlap: int = 0):
         self._router = (C.c_void_p * len(router_w))(*[_dev(w, "router_w") for w in router_w])
         self._shared = None
         if shared_w is not None:
@@ -346,7 +347,7 @@ class MoeStack:
         d = StackDesc(len(router_w), H, I, E, k, w_dtype, router_dtype,
                       C.cast(self._router, C.POINTER(C.c_void_p)),
                       C.cast(self._shared, C.POINTER(C.c_void_p)) if self._shared is not None else None,
-                      cache.handle, max_tokens, max_prefill_tokens, prefetch)
+                      cache.handle, max_tokens, max_prefill_tokens, prefetch, recall, recall_overlap)
         h = C.c_void_p()
         _check(lib().moe_stack_create(C.byref(d), C.byref(h)), "moe_stack_create")
         self._h = h

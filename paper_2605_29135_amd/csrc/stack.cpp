@@ -17,6 +17,14 @@
 namespace {
 
 // Arguments of the last layer's launches, for re-launching them in isolation.
+// A past token remembered for reverse rotation: its layer-0 expert set (sorted,
+// the context signature) and its expert set at every layer.
+struct Snapshot {
+    std::vector<int32_t> sig;   // [k] ascending
+    std::vector<int32_t> sets;  // [L x k] in rank order
+    uint64_t stamp = 0;         // token counter when stored
+};
+
 struct LastLayer {
     bool valid = false;
     int T = 0, layer = 0;
@@ -52,6 +60,10 @@ struct moe_stack {
     moe::IdsMailbox *mbox_dev = nullptr;  // its device address
     uint32_t mbox_seq = 0;
     std::vector<uint32_t> demand;          // [L x E] demand lookups per expert (prefetch ranking)
+    std::vector<Snapshot> snaps;           // reverse rotation: remembered tokens (<= d.recall)
+    std::vector<int32_t> cur_sets;         // [L x k] the current token's expert sets
+    int recalled = -1;                     // snapshot recalled for the current token, or -1
+    uint64_t tokens = 0;                   // one-token decode steps so far (snapshot stamps)
     float *scratch_x = nullptr;  // device [Tmax x H] scratch input/output of kernel re-launches
     float *scratch_y = nullptr;  // device [Tmax x H]
     std::vector<LastLayer> last;  // per layer, arguments of the last decode step
@@ -83,6 +95,49 @@ int wait_published_ids(moe_stack *s, uint32_t seq, hipStream_t strm) {
 // Speculative prefetch after layer l of a one-token step: the next layer's (the
 // next step's first layer after the last) most often demanded experts that are
 // not resident, up to d.prefetch of them, ties to the lower id.
+// The snapshot whose signature shares the most experts with `s0` (the token's
+// layer-0 ids), at least the configured overlap; ties go to the most recent.
+int find_recall(const moe_stack *s, const int32_t *s0) {
+    const auto &d = s->d;
+    const int need = d.recall_overlap > 0 ? d.recall_overlap : d.k;
+    int best = -1, best_n = 0;
+    for (size_t i = 0; i < s->snaps.size(); ++i) {
+        const Snapshot &sn = s->snaps[i];
+        int n = 0;
+        for (int j = 0; j < d.k; ++j)
+            n += std::binary_search(sn.sig.begin(), sn.sig.end(), s0[j]) ? 1 : 0;
+        if (n < need) continue;
+        if (best < 0 || n > best_n || (n == best_n && sn.stamp > s->snaps[best].stamp)) {
+            best = int(i);
+            best_n = n;
+        }
+    }
+    return best;
+}
+
+// End of a one-token step: remember it, over a snapshot with the same signature, else the oldest.
+void store_snapshot(moe_stack *s) {
+    const auto &d = s->d;
+    Snapshot sn;
+    sn.sig.assign(s->cur_sets.begin(), s->cur_sets.begin() + d.k);
+    std::sort(sn.sig.begin(), sn.sig.end());
+    sn.sets = s->cur_sets;
+    sn.stamp = ++s->tokens;
+    for (Snapshot &o : s->snaps)
+        if (o.sig == sn.sig) {
+            o = std::move(sn);
+            return;
+        }
+    if (int(s->snaps.size()) < d.recall) {
+        s->snaps.push_back(std::move(sn));
+        return;
+    }
+    size_t oldest = 0;
+    for (size_t i = 1; i < s->snaps.size(); ++i)
+        if (s->snaps[i].stamp < s->snaps[oldest].stamp) oldest = i;
+    s->snaps[oldest] = std::move(sn);
+}
+
 int prefetch_next(moe_stack *s, int step, int l) {
     const auto &d = s->d;
     const int ln = (l + 1) % d.n_layers, sn = l + 1 == d.n_layers ? step + 1 : step;
@@ -134,6 +189,8 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: max_prefill_tokens must be in [0, 2^20]");
     if (d->prefetch < 0 || d->prefetch > d->E)
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefetch must be in [0, E]");
+    if (d->recall < 0 || d->recall > 4096 || d->recall_overlap < 0 || d->recall_overlap > d->k)
+        return moe::fail(MOE_ERR_INVALID_ARG, "stack: recall must be in [0, 4096], recall_overlap in [0, k]");
     if (d->max_prefill_tokens > 0 && !moe::prefill_dtype_supported(d->w_dtype))
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefill needs MOE_BF16 or MOE_INT4G128 experts");
     if (!moe::ffn_shape_supported(d->H, d->I, d->w_dtype) || !moe::router_shape_supported(d->H, d->router_dtype))
@@ -174,6 +231,7 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
     s->slots_host = new int32_t[size_t(T) * d->k];
     s->last.assign(d->n_layers, LastLayer{});
     s->demand.assign(size_t(d->n_layers) * d->E, 0u);
+    s->cur_sets.assign(size_t(d->n_layers) * d->k, 0);
     s->ws_bytes = moe::ffn_workspace_bytes(d->max_tokens, d->k, d->I);
     if ((e = hipMalloc(&s->ws, s->ws_bytes)) != hipSuccess) return bail(e, "stack workspace");
     if (d->max_prefill_tokens > 0) {
@@ -206,6 +264,7 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
     if (!eflags) return moe::fail(MOE_ERR_HIP, "device error flags unavailable");
     const auto &d = s->d;
     const moe::FfnWorkspace ws = moe::ffn_workspace(s->ws, T, d.k, d.I);
+    s->recalled = -1;
     for (int l = 0; l < d.n_layers; ++l) {
         int32_t *ids = ids_out ? ids_out + size_t(l) * T * d.k : s->ids;
         float *w = weights_out ? weights_out + size_t(l) * T * d.k : s->weights;
@@ -232,6 +291,10 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
             int st = expert_cache_lookup(d.cache, step, l, s->ids_host, T * d.k, s->slots_host, nullptr, strm);
             if (st != MOE_OK) return st;
             for (int j = 0; j < T * d.k; ++j) ++s->demand[size_t(l) * d.E + s->ids_host[j]];
+            if (d.recall > 0 && T == 1) {
+                std::copy(s->ids_host, s->ids_host + d.k, s->cur_sets.begin() + size_t(l) * d.k);
+                if (l == 0) s->recalled = find_recall(s, s->ids_host);
+            }
         }
         // Where this layer's experts live: after a lookup the host knows every
         // slot (T == 1 passes them to the kernels directly); preloaded slots are
@@ -254,8 +317,17 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
         if (s->budgeted) {
             int st = expert_cache_release(d.cache, strm);
             if (st == MOE_OK && d.prefetch > 0 && T == 1) st = prefetch_next(s, step, l);  // after the release
+            if (st == MOE_OK && s->recalled >= 0 && T == 1 && l + 1 < d.n_layers) {
+                // reverse rotation: bring back the recalled token's next-layer set ahead of demand
+                const Snapshot &sn = s->snaps[size_t(s->recalled)];
+                st = expert_cache_prefetch(d.cache, step, l + 1, sn.sets.data() + size_t(l + 1) * d.k, d.k);
+            }
             if (st != MOE_OK) return st;
         }
+    }
+    if (s->budgeted && d.recall > 0 && T == 1) {
+        store_snapshot(s);
+        s->recalled = -1;
     }
     moe::clear_error();
     return MOE_OK;

@@ -59,9 +59,12 @@ class Workload:
     T: int = 1             # tokens per decode step
     steps: int = 1
     budget_bytes: int | None = None   # expert-slot HBM budget; None = all resident
-    routing: str = "router"           # "router" | "zipf" | "zipf_overlap"
+    routing: str = "router"           # "router" | "zipf" | "zipf_overlap" | "topics"
     zipf_s: float = 1.1
     overlap: float = 0.7
+    topics: int = 4                   # "topics": latent contexts the tokens move between
+    topic_stay: float = 0.9           # "topics": chance a token keeps the previous token's context
+    topic_keep: float = 0.85          # "topics": chance each expert of the context's profile set is drawn
     prefill: int = 0       # prefill chunk length (tokens); 0 = none
     sigma_w: float = 0.02
     seed: int = 0
@@ -368,12 +371,26 @@ def _gumbel_topk(scores: np.ndarray, m: int) -> np.ndarray:
     return np.sort(idx)
 
 
+def topic_sequence(wl: Workload, steps: int, T: int) -> np.ndarray:
+    """Context of each (step, token) for "topics" routing ``[steps x T]``: a Markov chain that keeps the
+    previous token's context with probability topic_stay, else moves to one of the others uniformly."""
+    rng = _rng(wl.seed, wl.cfg_id, _KEY_ROUTE, 1 << 20)
+    z = np.zeros((steps, T), dtype=np.int64)
+    for tok in range(T):
+        for t in range(1, steps):
+            z[t, tok] = z[t - 1, tok]
+            if rng.random() >= wl.topic_stay:
+                z[t, tok] = (z[t - 1, tok] + 1 + rng.integers(0, wl.topics - 1)) % wl.topics
+    return z
+
+
 def routing_sets(wl: Workload, steps: int | None = None, T: int | None = None) -> np.ndarray:
     """Drawn expert sets ``[steps x L x T x k]`` int32 (ascending ids per set)."""
     steps = wl.steps if steps is None else steps
     T = wl.T if T is None else T
     E, k = wl.E, wl.k
     out = np.empty((steps, wl.L, T, k), dtype=np.int32)
+    z = topic_sequence(wl, steps, T) if wl.routing == "topics" else None
     for l in range(wl.L):
         rng = _rng(wl.seed, wl.cfg_id, _KEY_ROUTE, l)
         logp = zipf_log_probs(wl, l, rng)
@@ -396,6 +413,19 @@ def routing_sets(wl: Workload, steps: int | None = None, T: int | None = None) -
                             if keep.size < k else keep
                     out[t, l, tok] = s
                     prev = s
+        elif wl.routing == "topics":
+            # each context has its own Zipf ranking of the layer's experts and a profile set drawn from it;
+            # a token keeps each profile expert with probability topic_keep and refills from its context
+            logps = [zipf_log_probs(wl, l, _rng(wl.seed, wl.cfg_id, _KEY_ROUTE, l, c + 1)) for c in range(wl.topics)]
+            profile = [_gumbel_topk(lp + rng.gumbel(size=E), k) for lp in logps]
+            for tok in range(T):
+                for t in range(steps):
+                    c = int(z[t, tok])
+                    keep = profile[c][rng.random(k) < wl.topic_keep]
+                    g = logps[c] + rng.gumbel(size=E)
+                    g[profile[c]] = -np.inf
+                    out[t, l, tok] = np.sort(np.concatenate([keep, _gumbel_topk(g, k - keep.size)])) \
+                        if keep.size < k else keep
         else:
             raise ValueError(f"workload routing {wl.routing!r} draws no sets")
     return out

@@ -255,9 +255,10 @@ def _pinned_store(wl, layers_alias=False):
     return buf
 
 
-def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=None, T=1, charge_max=None):
+def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=None, T=1, charge_max=None,
+                        recall=0, recall_overlap=0):
     """Decode `steps` steps through the stack; check events exactly and outputs within tolerance.  With
-    charge_max the slots use the rotary policy (else LRU)."""
+    charge_max the slots use the rotary policy (else LRU); with recall the stack recalls prior slot sets."""
     buf = _pinned_store(wl, layers_alias)
     eb = wl.expert_bytes
     policy = moe.MOE_POLICY_LRU if charge_max is None else moe.MOE_POLICY_ROTARY
@@ -266,7 +267,9 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
                             policy=policy, charge_max=charge_max or 0)
     routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
     shared = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)] if wl.shared else None
-    stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T)
+    stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T,
+                         recall=recall, recall_overlap=recall_overlap)
+    rec = oracle.Recall(recall, wl.k, recall_overlap) if recall else None
     sets = synth.routing_sets(wl, steps=steps, T=T)
     o = oracle.LRU(capacity, wl.L, wl.E) if charge_max is None else oracle.Rotary(capacity, wl.L, wl.E, charge_max)
     check_steps = set(range(steps) if check_steps is None else check_steps)
@@ -280,9 +283,12 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
         stack.decode_step(t, x, dev(bias), ids, w)
         moe.moe_sync_check()
         g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
+        calls = dict(rec.step(t, [g_ids[l].reshape(-1) for l in range(wl.L)])[1]) if rec else {}
         for l in range(wl.L):
             assert (np.sort(g_ids[l], axis=1) == sets[t, l]).all()
             assert o.lookup(t, l, g_ids[l].reshape(-1)) == oracle.OK
+            if l + 1 in calls:
+                assert o.lookup(t, l + 1, calls[l + 1], prefetch=True) == oracle.OK
         if t in check_steps:
             # oracle chain in fp64 from the same input, routed by the GPU's ids and weights:
             # x <- x + MoE(rmsnorm(x)) per layer
@@ -326,6 +332,16 @@ def test_budgeted_stack_rotary_slots(charge_max):
                         cfg_id=97)
     s = run_stack_and_check(wl, steps=40, capacity=24, charge_max=charge_max)
     assert s["evictions"] > 0
+
+
+@pytest.mark.parametrize("charge_max,overlap", [(None, 3), (2, 0)])
+def test_budgeted_stack_recall_on_recurring_contexts(charge_max, overlap):
+    """Reverse rotation: a token whose layer-0 set matches a remembered token's prefetches that token's
+    later-layer sets; the log (lookups and prefetches) event for event against the oracle's replay."""
+    wl = synth.Workload("topic stack", H=512, E=32, k=4, I=256, L=4, dtype=synth.BF16, routing="topics", topics=3,
+                        cfg_id=96)
+    s = run_stack_and_check(wl, steps=40, capacity=20, charge_max=charge_max, recall=4, recall_overlap=overlap)
+    assert s["prefetches"] > 0 and s["evictions"] > 0
 
 
 def test_budgeted_stack_tokens_and_shared_int4():

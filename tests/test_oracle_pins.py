@@ -592,6 +592,43 @@ def test_rotary_errors_and_preload():
     assert [p.slot_of(l, e) for l in range(2) for e in range(3)] == list(range(6))
 
 
+def test_golden_recall_contexts():
+    lines = _golden_lines("recall_contexts.txt")
+    tokens = [[[int(v) for v in ln[2 + 2 * l:4 + 2 * l]] for l in range(3)] for ln in lines if ln[0] == "token"]
+    for ln in (ln for ln in lines if ln[0] == "recalled"):
+        M, ov, want = int(ln[1]), int(ln[2]), [int(v) for v in ln[3:]]
+        rec = oracle.Recall(M, 2, ov)
+        got = []
+        for t, sets in enumerate(tokens):
+            who, calls = rec.step(t, sets)
+            got.append(who)
+            assert [l for l, _ in calls] == ([1, 2] if who >= 0 else [])
+            if who >= 0:
+                assert [c[1] for c in calls] == tokens[who][1:]
+            if (M, ov, t) == (1, 1, 4):
+                v = next(ln2 for ln2 in lines if ln2[0] == "calls_t4_1_1")[1:]
+                assert calls == [(int(v[0]), [int(v[1]), int(v[2])]), (int(v[3]), [int(v[4]), int(v[5])])]
+        assert got == want, (M, ov, got)
+
+
+def test_recall_prefetch_of_a_recurring_context_turns_misses_into_prefetch_hits():
+    # two alternating contexts that do not fit together: without recall every layer's set misses on each
+    # return; with recall (exact signatures) each later layer's set is prefetched and found resident
+    L, k, C = 4, 2, 8   # one context needs L * k = 8 slots
+    A = [[10 * l + 1, 10 * l + 2] for l in range(L)]
+    B = [[10 * l + 5, 10 * l + 6] for l in range(L)]
+    seq = [A, B] * 6
+    plain = oracle.replay_decode(oracle.LRU(C, L, 64), seq)
+    rec = oracle.replay_decode(oracle.LRU(C, L, 64), seq, oracle.Recall(4, k))
+    sp, sr = plain.stats(), rec.stats()
+    assert sp["misses"] == len(seq) * L * k                      # every lookup misses
+    assert sr["misses"] == 2 * L * k + (len(seq) - 2) * k         # only layer 0 misses once both are remembered
+    assert sr["prefetches"] == (len(seq) - 2) * (L - 1) * k
+    for cache in (oracle.Rotary(C, L, 64, 3), oracle.LRU(C, L, 64)):
+        oracle.replay_decode(cache, seq, oracle.Recall(4, k))
+        assert cache.occupancy() <= C
+
+
 # ------------------------------------------------------------ OPT bound ---
 def _golden_kv(name):
     kv = {}
