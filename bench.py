@@ -49,6 +49,16 @@ def parse():
     ap.add_argument("--policy", choices=["lru", "rotary"], default="lru",
                     help="replacement policy of the expert slots (the workloads specify LRU)")
     ap.add_argument("--charge-max", type=int, default=32, help="rotary policy: most charge a slot holds")
+    ap.add_argument("--recall", type=int, default=0,
+                    help="reverse rotation: remembered tokens whose slot sets a recurring layer-0 routing recalls "
+                         "(0 = off)")
+    ap.add_argument("--recall-overlap", type=int, default=0,
+                    help="layer-0 experts a recalled token must share (0 = all k)")
+    ap.add_argument("--routing", choices=["zipf_overlap", "topics"], default="zipf_overlap",
+                    help="config 4 routing: the specified Zipf(1.1) 70%% overlap, or recurring contexts "
+                         "(--topics contexts, a token keeps its context with --topic-stay)")
+    ap.add_argument("--topics", type=int, default=8)
+    ap.add_argument("--topic-stay", type=float, default=0.9)
     ap.add_argument("--replays", type=int, default=5,
                     help="replays of the last step's launches (one per layer) for the per-launch device time")
     return ap.parse_args()
@@ -222,10 +232,11 @@ def residency_bound(moe, cache, E, capacity, step_bytes_per_token=None, policy="
     L = int(ev["layer"].max() + 1)
     opt = moe.moe_opt_fills_flat(keys, offsets, n_keys, capacity)
     run_fills = int((ev["kind"] == moe.EVENT_MISS).sum())
-    lru = run_fills if policy == "lru" else replay_fills(moe, ev, L, E, capacity, moe.MOE_POLICY_LRU)
+    # the run's own misses are plain LRU's only when nothing was prefetched; otherwise replay the demand trace
+    lru = run_fills if (policy == "lru" and n_pf == 0) else replay_fills(moe, ev, L, E, capacity, moe.MOE_POLICY_LRU)
     rotary = {str(q): replay_fills(moe, ev, L, E, capacity, moe.MOE_POLICY_ROTARY, q) for q in (0, 4, 32)}
     out = {"scope": "every lookup of the run from a cold cache (warm-up included)", "lookups": int(ev.size),
-           "run_policy": policy, "run_fills": run_fills,
+           "run_policy": policy, "run_demand_fills": run_fills,
            "lru_fills": lru, "rotary_fills_by_charge_max": rotary, "opt_fills": int(opt),
            "opt_over_lru": opt / lru if lru else None,
            "rotary32_over_lru": rotary["32"] / lru if lru else None}
@@ -451,7 +462,11 @@ def main():
         args.steps = 2048
     dev = torch.device("cuda:0")
     T = args.tokens
-    if args.config == 4:
+    if args.config == 4 and args.routing == "topics":
+        wl = synth.workload(4, routing="topics", topics=args.topics, topic_stay=args.topic_stay,
+                            name=f"cfg4 shapes with recurring contexts: 40-layer bf16 H2048 E128 k8 I768, 6 GiB, "
+                                 f"{args.topics} contexts, stay {args.topic_stay}, keep 0.85")
+    elif args.config == 4:
         wl = synth.workload(4)
     else:
         wl = synth.workload(args.config, T=T)
@@ -487,7 +502,8 @@ def main():
     cache = moe.ExpertCache(L, E, eb, budget, buf.ptr, 0 if alias else E * eb, eb, reserved_bytes=reserved,
                             preload=not budgeted, policy=POLICIES[args.policy], charge_max=args.charge_max)
     stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T,
-                         prefetch=args.prefetch if budgeted else 0)
+                         prefetch=args.prefetch if budgeted else 0, recall=args.recall if budgeted else 0,
+                         recall_overlap=args.recall_overlap)
     t_setup = time.perf_counter() - t_setup
 
     stream = torch.cuda.current_stream()
@@ -573,7 +589,8 @@ def main():
                    "tokens_per_step": T, "budget_bytes": budget, "slots": st1["capacity"],
                    "host_store_bytes": L_store * E * eb, "host_layers_aliased": bool(alias),
                    "prefetch_per_layer": args.prefetch if budgeted else 0, "policy": args.policy,
-                   **({"charge_max": args.charge_max} if args.policy == "rotary" else {})},
+                   **({"charge_max": args.charge_max} if args.policy == "rotary" else {}),
+                   **({"recall": args.recall, "recall_overlap": args.recall_overlap or k} if args.recall else {})},
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU", "achieved": gu_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": gu_gbps / HBM_PEAK_GBPS if gu_gbps else None,
