@@ -49,6 +49,10 @@ def parse():
     ap.add_argument("--policy", choices=["lru", "rotary"], default="lru",
                     help="replacement policy of the expert slots (the workloads specify LRU)")
     ap.add_argument("--charge-max", type=int, default=32, help="rotary policy: most charge a slot holds")
+    ap.add_argument("--residency", choices=["host", "device"], default="device",
+                    help="where the slot table's decisions are made: lookup kernels (the default: no host round "
+                         "trip), or the host after each layer's ids reach it (needed by --prefetch / --recall); "
+                         "the decisions are the same")
     ap.add_argument("--recall", type=int, default=0,
                     help="reverse rotation: remembered tokens whose slot sets a recurring layer-0 routing recalls "
                          "(0 = off)")
@@ -317,7 +321,8 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
 
     def make():
         cache = moe.ExpertCache(L, E, eb, wl.budget_bytes, buf.ptr, E * eb, eb, reserved_bytes=L * eb,
-                                policy=POLICIES[args.policy], charge_max=args.charge_max)
+                                policy=POLICIES[args.policy], charge_max=args.charge_max,
+                                device=args.residency == "device")
         stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=1,
                              max_prefill_tokens=Tp, prefetch=args.prefetch)
         return cache, stack
@@ -404,7 +409,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
         "config": {"workload": wl.name, "layers": L, "experts": E, "top_k": k, "shared_expert": True,
                    "hidden": H, "intermediate": I, "prefill_tokens": Tp, "decode_tokens_per_step": 1,
                    "budget_bytes": wl.budget_bytes, "slots": st3["capacity"], "host_store_bytes": L * E * eb,
-                   "prefetch_per_layer": args.prefetch, "policy": args.policy,
+                   "prefetch_per_layer": args.prefetch, "policy": args.policy, "residency": args.residency,
                    **({"charge_max": args.charge_max} if args.policy == "rotary" else {})},
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU (int4 decode)", "achieved": gu_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gu_gbps / HBM_PEAK_GBPS,
@@ -444,6 +449,8 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
 
 def main():
     args = parse()
+    if (args.prefetch or args.recall) and args.residency == "device":
+        args.residency = "host"  # prefetch and recall decide on the host
     if args.gpus != 1:
         print(f"bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
               f"(asked for --gpus {args.gpus})", file=sys.stderr)
@@ -500,7 +507,8 @@ def main():
     reserved = L * eb if wl.shared else 0
     budget = wl.budget_bytes if budgeted else L * E * eb + reserved
     cache = moe.ExpertCache(L, E, eb, budget, buf.ptr, 0 if alias else E * eb, eb, reserved_bytes=reserved,
-                            preload=not budgeted, policy=POLICIES[args.policy], charge_max=args.charge_max)
+                            preload=not budgeted, policy=POLICIES[args.policy], charge_max=args.charge_max,
+                            device=budgeted and args.residency == "device")
     stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T,
                          prefetch=args.prefetch if budgeted else 0, recall=args.recall if budgeted else 0,
                          recall_overlap=args.recall_overlap)
@@ -589,6 +597,7 @@ def main():
                    "tokens_per_step": T, "budget_bytes": budget, "slots": st1["capacity"],
                    "host_store_bytes": L_store * E * eb, "host_layers_aliased": bool(alias),
                    "prefetch_per_layer": args.prefetch if budgeted else 0, "policy": args.policy,
+                   "residency": args.residency if budgeted else "preloaded",
                    **({"charge_max": args.charge_max} if args.policy == "rotary" else {}),
                    **({"recall": args.recall, "recall_overlap": args.recall_overlap or k} if args.recall else {})},
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU", "achieved": gu_gbps,

@@ -75,6 +75,7 @@ extern "C" {
 #define MOE_POLICY_ROTARY 1 /* rotary slot group: a ring of slots swept by a hand (sec. 4, Fig. 2) */
 #define MOE_CACHE_PRELOAD 1  /* start with every expert resident at slot layer*E + expert */
 #define MOE_CACHE_HOST_SIM 2 /* no device: slots live in host memory and fills are memcpy */
+#define MOE_CACHE_DEVICE 4   /* decisions on the device: lookups are kernels (expert_cache_lookup_device) */
 
 #define MOE_EVENT_HIT 0
 #define MOE_EVENT_MISS 1
@@ -247,6 +248,27 @@ typedef struct {
  * every slot synchronously before returning.  With MOE_CACHE_HOST_SIM no HIP
  * call is made: slots are host memory and `dev_slot_of` is a host array. */
 MOE_API int expert_cache_create(const moe_cache_desc *desc, moe_cache **out);
+
+/* MOE_CACHE_DEVICE: the slot table's decision state (slot keys, LRU stamps or
+ * rotary charges, counters, a log of up to 2^21 decisions and a fill list;
+ * about 50 MB of HBM besides the slots) lives on the device, and a lookup is a
+ * kernel that takes the same decisions as expert_cache_lookup, followed by a
+ * kernel that streams the misses from the host store: a decode step needs no
+ * host round trip.  Needs capacity <= 4096 and n_experts <= 256; cannot be
+ * combined with MOE_CACHE_HOST_SIM.  In this mode expert_cache_lookup and
+ * expert_cache_prefetch return MOE_ERR_INVALID_ARG, expert_cache_release does
+ * nothing, and expert_cache_stats / expert_cache_trace synchronise the device. */
+
+/* Device lookup (MOE_CACHE_DEVICE only): enqueues on `stream` the lookup of the
+ * experts ids_dev[0..n) (device int32, e.g. as written by moe_route_topk) of
+ * `layer`, tagged `step`, and the fills of its misses; kernels that run later on
+ * `stream` see the updated slot table.  slots_out_dev (device int32 [n], or
+ * NULL) receives the slot of each id after the lookup.  Ids outside [0, E) raise MOE_ERR_RANGE
+ * and a step with more distinct experts than slots MOE_ERR_BUDGET in the device
+ * flags (moe_sync_check); such a lookup changes nothing.  Lookups must be
+ * ordered: issue them on one stream. */
+MOE_API int expert_cache_lookup_device(moe_cache *c, int step, int layer, const int32_t *ids_dev, int n,
+                                       int32_t *slots_out_dev, void *stream);
 
 /* Wait for the cache's copies and free everything it owns. */
 MOE_API int expert_cache_destroy(moe_cache *c);

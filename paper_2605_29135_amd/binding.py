@@ -24,7 +24,7 @@ MOE_ACCUMULATE = 1
 MOE_ROUTE_RMSNORM = 1
 MOE_POLICY_LRU = 0
 MOE_POLICY_ROTARY = 1
-MOE_CACHE_PRELOAD, MOE_CACHE_HOST_SIM = 1, 2
+MOE_CACHE_PRELOAD, MOE_CACHE_HOST_SIM, MOE_CACHE_DEVICE = 1, 2, 4
 EVENT_HIT, EVENT_MISS, EVENT_PREFETCH = 0, 1, 2
 MAX_DECODE_TOKENS = 16
 
@@ -82,6 +82,7 @@ def lib() -> C.CDLL:
             "expert_cache_create": [C.POINTER(CacheDesc), C.POINTER(P)],
             "expert_cache_destroy": [P],
             "expert_cache_lookup": [P, I, I, P, I, P, P, P],
+            "expert_cache_lookup_device": [P, I, I, P, I, P, P],
             "expert_cache_prefetch": [P, I, I, P, I],
             "expert_cache_release": [P, P],
             "expert_cache_slot_table": [P, C.POINTER(P), C.POINTER(P)],
@@ -267,10 +268,11 @@ class ExpertCache:
     def __init__(self, n_layers: int, n_experts: int, expert_bytes: int, budget_bytes: int, host_base: int,
                  host_layer_stride: int, host_expert_stride: int, reserved_bytes: int = 0,
                  preload: bool = False, host_sim: bool = False, policy: int = MOE_POLICY_LRU,
-                 charge_max: int = 0):
+                 charge_max: int = 0, device: bool = False):
         d = CacheDesc(n_layers, n_experts, expert_bytes, budget_bytes, reserved_bytes, host_base,
                       host_layer_stride, host_expert_stride, policy,
-                      (MOE_CACHE_PRELOAD if preload else 0) | (MOE_CACHE_HOST_SIM if host_sim else 0), charge_max)
+                      (MOE_CACHE_PRELOAD if preload else 0) | (MOE_CACHE_HOST_SIM if host_sim else 0) |
+                      (MOE_CACHE_DEVICE if device else 0), charge_max)
         h = C.c_void_p()
         _check(lib().expert_cache_create(C.byref(d), C.byref(h)), "expert_cache_create")
         self._h = h
@@ -296,6 +298,14 @@ class ExpertCache:
         _check(lib().expert_cache_lookup(self._h, step, layer, a.ctypes.data, a.size, slots.ctypes.data,
                                          hit.ctypes.data, s), "expert_cache_lookup")
         return slots, hit
+
+    def lookup_device(self, step: int, layer: int, ids, slots_out=None, stream=None):
+        """Device lookup (MOE_CACHE_DEVICE): enqueues the lookup of device int32 ids and its fills; slots_out
+        (device int32, optional) receives each id's slot."""
+        import torch
+        _check(lib().expert_cache_lookup_device(self._h, step, layer, _dev(ids, "ids", torch.int32), ids.numel(),
+                                                _dev(slots_out, "slots_out", torch.int32), _stream(stream)),
+               "expert_cache_lookup_device")
 
     def prefetch(self, step: int, layer: int, ids):
         a = np.ascontiguousarray(np.asarray(ids).reshape(-1), dtype=np.int32)

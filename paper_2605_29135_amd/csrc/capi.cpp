@@ -93,6 +93,7 @@ int moe_sync_check(void *stream) {
         if (v & moe::kErrRange) return fail(MOE_ERR_RANGE, "an expert id was outside [0, E)");
         if (v & moe::kErrNonfinite) return fail(MOE_ERR_NONFINITE, "a router logit was NaN or infinite");
         if (v & moe::kErrNotResident) return fail(MOE_ERR_NOT_RESIDENT, "an expert had no slot");
+        if (v & moe::kErrBudget) return fail(MOE_ERR_BUDGET, "a device lookup needed more experts than slots");
     }
     moe::clear_error();
     return MOE_OK;

@@ -12,7 +12,7 @@ struct moe_cache;
 namespace moe {
 
 // Sticky device error bits (OR-ed by kernels into the per-device flag word).
-enum : int { kErrRange = 1, kErrNonfinite = 2, kErrNotResident = 4 };
+enum : int { kErrRange = 1, kErrNonfinite = 2, kErrNotResident = 4, kErrBudget = 8 };
 
 // Bytes of one expert blob and the byte offset of W_d inside it.
 size_t expert_blob_bytes(int H, int I, int dtype);
@@ -72,6 +72,38 @@ struct FillBatch {
     int32_t tab_val[2 * kMaxFillBatch];
 };
 hipError_t launch_fill_slots(const FillBatch &b, hipStream_t s);
+
+// Device-resident residency (MOE_CACHE_DEVICE): the whole decision state of the
+// slot table lives in HBM and one kernel per lookup updates it, so a decode step
+// needs no host round trip.  Decisions are those of the host runtime (LRU or
+// rotary), event for event.
+constexpr int kDevMaxSlots = 4096;
+enum : int { kScalCtr, kScalHand, kScalNextFree, kScalHits, kScalMisses, kScalEvictions, kScalEvents, kDevScalars };
+struct DevResidency {
+    int32_t *key_of_slot = nullptr;      // [C] layer*E + expert, -1 = free
+    uint64_t *stamp = nullptr;           // [C] LRU: recency stamp
+    uint16_t *charge = nullptr;          // [C] rotary: charge
+    int32_t *slot_of_key = nullptr;      // [L*E] the device slot table
+    unsigned long long *scal = nullptr;  // [kDevScalars]
+    moe_cache_event *events = nullptr;   // [cap_events] decision log
+    long long cap_events = 0;
+    long long *fill_src = nullptr;       // [E] byte offset in the host store of each fill's blob
+    int32_t *fill_slot = nullptr;        // [E] its slot
+    int32_t *n_fill = nullptr;           // [1] fills of the last lookup
+};
+struct DevLookup {
+    int C, L, E, layer, step, rotary, charge_max;
+    long long layer_stride, expert_stride;
+};
+// slots_out (device, optional): slots_out[i] = slot of ids[i] after the lookup.
+hipError_t launch_dev_lookup(const DevResidency &r, const DevLookup &p, const int32_t *ids, int n, int32_t *slots_out,
+                             int *err, hipStream_t s);
+// One token: top-k of its logits fused with the device lookup of the selected experts (one block).
+hipError_t launch_topk_lookup(const float *logits, int E, int k, int32_t *ids, float *weights, int *err_flags,
+                              const DevResidency &r, const DevLookup &p, int32_t *slots_out, hipStream_t s);
+// Streams the last lookup's fills (at most max_fills) from the host store into their slots.
+hipError_t launch_dev_fill(const DevResidency &r, const uint8_t *host_dev, uint8_t *pool, long long expert_bytes,
+                           int max_fills, hipStream_t s);
 hipError_t launch_hbm_read(const void *buf, size_t bytes, float *sink, hipStream_t s);
 
 // Prefill (any T): pairs grouped by expert, grouped bf16 MFMA GEMMs, rank-order combine.
@@ -109,6 +141,11 @@ void clear_error();
 size_t cache_expert_bytes(const struct ::moe_cache *c);
 bool cache_preloaded(const struct ::moe_cache *c);
 bool cache_resident(const struct ::moe_cache *c, int layer, int expert);  // host mirror
+bool cache_device(const struct ::moe_cache *c);  // lookups run on the device (MOE_CACHE_DEVICE)
+// MOE_CACHE_DEVICE, one token: enqueue top-k of `logits` fused with the lookup of the chosen experts, then
+// the fills of its misses.  Returns an MOE_ERR_* code.
+int cache_topk_lookup(struct ::moe_cache *c, int step, int layer, const float *logits, int k, int32_t *ids,
+                      float *weights, int32_t *slots_out, int *err_flags, hipStream_t s);
 
 // Sticky error-flag word of the current device (set up on first use).
 int *device_error_flags();

@@ -9,6 +9,7 @@
 
 #include "internal.h"
 #include "device_common.h"
+#include "residency_dev.h"
 #include "../../include/moe_budget.h"
 
 namespace moe {
@@ -72,6 +73,7 @@ __device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wou
         if (lane < k) {
             ids[lane] = -1;
             wout[lane] = 0.f;
+            sc->rid[lane] = -1;
         }
         if (lane == 0) atomicOr(err, kErrNonfinite);
         return;
@@ -143,6 +145,26 @@ __global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__res
         __threadfence_system();
         if (lane == 0) __hip_atomic_store(&pub->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
     }
+}
+
+// One token's top-k fused with the device lookup of its experts (MOE_CACHE_DEVICE
+// decode): wave 0 ranks the experts and writes ids and weights, then the whole
+// block takes the slot table's decisions for them -- one launch and no global
+// round trip between the routing result and the residency decisions.
+template <bool ROTARY>
+__global__ __launch_bounds__(kBlock) void topk_lookup_kernel(const float *__restrict__ logits, int E, int k,
+                                                             int32_t *__restrict__ ids, float *__restrict__ wout,
+                                                             int *err, DevResidency r, DevLookup p,
+                                                             int32_t *__restrict__ slots_out) {
+    static_assert(kBlock == devres::kDevThreads, "the lookup body runs on the whole block");
+    __shared__ TopkScratch sc;
+    __shared__ int32_t ids_l[MOE_MAX_TOPK];
+    if (threadIdx.x < kWave) {
+        topk_wave<false>(logits, E, k, ids, wout, err, &sc);
+        if (int(threadIdx.x) < k) ids_l[threadIdx.x] = sc.rid[threadIdx.x];  // the ranked ids (-1 if non-finite)
+    }
+    __syncthreads();
+    devres::dev_lookup_body<ROTARY>(r, p, ids_l, k, slots_out, err);
 }
 
 // --------------------------------------------------------------- router ---
@@ -917,6 +939,16 @@ hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int 
     ROUTER_CASE(BF16, 1) ROUTER_CASE(BF16, 2) ROUTER_CASE(BF16, 4) ROUTER_CASE(BF16, 8)
 #undef ROUTER_CASE
     return hipErrorInvalidValue;
+}
+
+hipError_t launch_topk_lookup(const float *logits, int E, int k, int32_t *ids, float *weights, int *err_flags,
+                              const DevResidency &r, const DevLookup &p, int32_t *slots_out, hipStream_t s) {
+    if (p.C < 1 || p.C > kDevMaxSlots || p.E != E || E > MOE_MAX_EXPERTS || k < 1 || k > MOE_MAX_TOPK ||
+        p.layer < 0 || p.layer >= p.L)
+        return hipErrorInvalidValue;
+    if (p.rotary) topk_lookup_kernel<true><<<1, kBlock, 0, s>>>(logits, E, k, ids, weights, err_flags, r, p, slots_out);
+    else topk_lookup_kernel<false><<<1, kBlock, 0, s>>>(logits, E, k, ids, weights, err_flags, r, p, slots_out);
+    return hipGetLastError();
 }
 
 hipError_t launch_topk_softmax(const float *logits, int T, int E, int k, int32_t *ids, float *weights,

@@ -113,6 +113,9 @@ struct moe_cache {
 
     std::vector<moe_cache_event> log;
     moe_cache_stats st{};
+
+    bool dev_mode = false;   // MOE_CACHE_DEVICE: decisions and log on the device
+    moe::DevResidency dr;
 };
 
 namespace {
@@ -373,6 +376,64 @@ bool moe::cache_preloaded(const moe_cache *c) { return c->d.flags & MOE_CACHE_PR
 bool moe::cache_resident(const moe_cache *c, int layer, int expert) {
     return c->slot_of_key[size_t(layer) * c->E + expert] >= 0;
 }
+bool moe::cache_device(const moe_cache *c) { return c->dev_mode; }
+
+int moe::cache_topk_lookup(moe_cache *c, int step, int layer, const float *logits, int k, int32_t *ids,
+                           float *weights, int32_t *slots_out, int *err_flags, hipStream_t s) {
+    if (!c || !c->dev_mode || layer < 0 || layer >= c->L)
+        return moe::fail(MOE_ERR_INVALID_ARG, "fused top-k lookup needs a MOE_CACHE_DEVICE cache and a valid layer");
+    moe::DevLookup p{c->C, c->L, c->E, layer, step, c->d.policy == MOE_POLICY_ROTARY ? 1 : 0, c->charge_max,
+                     (long long)c->d.host_layer_stride, (long long)c->d.host_expert_stride};
+    hipError_t e = moe::launch_topk_lookup(logits, c->E, k, ids, weights, err_flags, c->dr, p, slots_out, s);
+    if (e == hipSuccess)
+        e = moe::launch_dev_fill(c->dr, c->host_dev, c->pool, (long long)c->d.expert_bytes, std::min(k, c->E), s);
+    return e == hipSuccess ? MOE_OK : moe::fail_hip(e, "fused top-k lookup");
+}
+
+namespace {
+constexpr long long kDevEvents = 1 << 21;
+
+// Device state of a MOE_CACHE_DEVICE cache, initialised like the host state.
+int dev_state_create(moe_cache *c, bool preload) {
+    moe::DevResidency &r = c->dr;
+    const size_t C = size_t(c->C);
+    hipError_t e = hipMalloc(&r.key_of_slot, sizeof(int32_t) * C);
+    if (e == hipSuccess) e = hipMalloc(&r.stamp, sizeof(uint64_t) * C);
+    if (e == hipSuccess) e = hipMalloc(&r.charge, sizeof(uint16_t) * C);
+    if (e == hipSuccess) e = hipMalloc(&r.scal, sizeof(unsigned long long) * moe::kDevScalars);
+    if (e == hipSuccess) e = hipMalloc(&r.events, sizeof(moe_cache_event) * size_t(kDevEvents));
+    if (e == hipSuccess) e = hipMalloc(&r.fill_src, sizeof(long long) * size_t(c->E));
+    if (e == hipSuccess) e = hipMalloc(&r.fill_slot, sizeof(int32_t) * size_t(c->E));
+    if (e == hipSuccess) e = hipMalloc(&r.n_fill, sizeof(int32_t));
+    if (e != hipSuccess) return moe::fail_hip(e, "allocating the device residency state");
+    r.cap_events = kDevEvents;
+    r.slot_of_key = c->dev_slot_of;
+    std::vector<uint64_t> stamp(C, 0);
+    std::vector<unsigned long long> scal(moe::kDevScalars, 0);
+    if (preload) {
+        for (size_t s = 0; s < C; ++s) stamp[s] = s + 1;  // preloaded in slot order, as the oracle's stamps
+        scal[moe::kScalCtr] = C;
+        scal[moe::kScalNextFree] = C;
+    }
+    std::vector<uint16_t> charge(C, 0);
+    e = hipMemcpy(r.key_of_slot, c->key_of_slot.data(), sizeof(int32_t) * C, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(r.stamp, stamp.data(), sizeof(uint64_t) * C, hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemcpy(r.charge, charge.data(), sizeof(uint16_t) * C, hipMemcpyHostToDevice);
+    if (e == hipSuccess)
+        e = hipMemcpy(r.scal, scal.data(), sizeof(unsigned long long) * scal.size(), hipMemcpyHostToDevice);
+    if (e == hipSuccess) e = hipMemset(r.n_fill, 0, sizeof(int32_t));
+    return e == hipSuccess ? MOE_OK : moe::fail_hip(e, "initialising the device residency state");
+}
+
+void dev_state_destroy(moe_cache *c) {
+    moe::DevResidency &r = c->dr;
+    for (void *p : {static_cast<void *>(r.key_of_slot), static_cast<void *>(r.stamp), static_cast<void *>(r.charge),
+                    static_cast<void *>(r.scal), static_cast<void *>(r.events), static_cast<void *>(r.fill_src),
+                    static_cast<void *>(r.fill_slot), static_cast<void *>(r.n_fill)})
+        if (p) (void)hipFree(p);
+    r = moe::DevResidency{};
+}
+}  // namespace
 
 extern "C" {
 
@@ -398,8 +459,16 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
         return moe::fail(MOE_ERR_BUDGET, "preload needs %zu slots, the budget holds %zu", keys, cap);
     if (keys > size_t(INT32_MAX)) return moe::fail(MOE_ERR_INVALID_ARG, "too many experts");
 
+    const bool dev_mode = d->flags & MOE_CACHE_DEVICE;
+    if (dev_mode && (d->flags & MOE_CACHE_HOST_SIM))
+        return moe::fail(MOE_ERR_INVALID_ARG, "MOE_CACHE_DEVICE cannot be combined with MOE_CACHE_HOST_SIM");
+    if (dev_mode && (std::min(cap, preload ? keys : cap) > size_t(moe::kDevMaxSlots) || d->n_experts > MOE_MAX_EXPERTS))
+        return moe::fail(MOE_ERR_INVALID_ARG, "MOE_CACHE_DEVICE needs at most %d slots and %d experts per layer",
+                         moe::kDevMaxSlots, MOE_MAX_EXPERTS);
+
     auto *c = new moe_cache();
     c->d = *d;
+    c->dev_mode = dev_mode;
     c->L = d->n_layers;
     c->E = d->n_experts;
     c->C = int(std::min(cap, preload ? keys : cap));
@@ -478,6 +547,10 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
     } else {
         for (int s = 0; s < c->C; ++s) c->free_slots.push(s);
     }
+    if (c->dev_mode) {
+        const int st = dev_state_create(c, preload);
+        if (st != MOE_OK) return cleanup(st);
+    }
     *out = c;
     return MOE_OK;
 }
@@ -491,6 +564,7 @@ int expert_cache_destroy(moe_cache *c) {
         if (c->copy) (void)hipStreamSynchronize(c->copy);
         if (c->have_last_compute) (void)hipStreamSynchronize(c->last_compute);
         c->ring.destroy();
+        dev_state_destroy(c);
         if (c->copy) (void)hipStreamDestroy(c->copy);
         if (c->pool) (void)hipFree(c->pool);
         if (c->dev_slot_of) (void)hipFree(c->dev_slot_of);
@@ -499,18 +573,41 @@ int expert_cache_destroy(moe_cache *c) {
     return MOE_OK;
 }
 
+int expert_cache_lookup_device(moe_cache *c, int step, int layer, const int32_t *ids_dev, int n,
+                               int32_t *slots_out_dev, void *stream) {
+    if (!c) return moe::fail(MOE_ERR_INVALID_ARG, "cache is NULL");
+    if (!c->dev_mode) return moe::fail(MOE_ERR_INVALID_ARG, "device lookups need a MOE_CACHE_DEVICE cache");
+    if (layer < 0 || layer >= c->L) return moe::fail(MOE_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, c->L);
+    if (n < 0 || (n > 0 && !ids_dev)) return moe::fail(MOE_ERR_INVALID_ARG, "bad ids");
+    if (n == 0) return MOE_OK;
+    int *err = moe::device_error_flags();
+    if (!err) return moe::fail(MOE_ERR_HIP, "device error flags unavailable");
+    moe::DevLookup p{c->C, c->L, c->E, layer, step, c->d.policy == MOE_POLICY_ROTARY ? 1 : 0, c->charge_max,
+                     (long long)c->d.host_layer_stride, (long long)c->d.host_expert_stride};
+    auto s = static_cast<hipStream_t>(stream);
+    hipError_t e = moe::launch_dev_lookup(c->dr, p, ids_dev, n, slots_out_dev, err, s);
+    if (e == hipSuccess)
+        e = moe::launch_dev_fill(c->dr, c->host_dev, c->pool, (long long)c->d.expert_bytes, std::min(n, c->E), s);
+    if (e != hipSuccess) return moe::fail_hip(e, "device lookup");
+    moe::clear_error();
+    return MOE_OK;
+}
+
 int expert_cache_lookup(moe_cache *c, int step, int layer, const int32_t *ids_host, int n,
                         int32_t *slots_out, uint8_t *hit_out, void *compute_stream) {
+    if (c && c->dev_mode) return moe::fail(MOE_ERR_INVALID_ARG, "a MOE_CACHE_DEVICE cache looks up on the device");
     return lookup_impl(c, step, layer, ids_host, n, false, slots_out, hit_out,
                        static_cast<hipStream_t>(compute_stream));
 }
 
 int expert_cache_prefetch(moe_cache *c, int step, int layer, const int32_t *ids_host, int n) {
+    if (c && c->dev_mode) return moe::fail(MOE_ERR_INVALID_ARG, "a MOE_CACHE_DEVICE cache does not prefetch");
     return lookup_impl(c, step, layer, ids_host, n, true, nullptr, nullptr, nullptr);
 }
 
 int expert_cache_release(moe_cache *c, void *compute_stream) {
     if (!c) return moe::fail(MOE_ERR_INVALID_ARG, "cache is NULL");
+    if (c->dev_mode) return MOE_OK;  // one stream orders every fill after the earlier readers
     return release_pending(c, static_cast<hipStream_t>(compute_stream));
 }
 
@@ -523,6 +620,21 @@ int expert_cache_slot_table(moe_cache *c, const int32_t **dev_slot_of, const voi
 
 int expert_cache_stats(moe_cache *c, moe_cache_stats *out) {
     if (!c || !out) return moe::fail(MOE_ERR_INVALID_ARG, "NULL argument");
+    if (c->dev_mode) {
+        unsigned long long v[moe::kDevScalars];
+        hipError_t e = hipDeviceSynchronize();
+        if (e == hipSuccess) e = hipMemcpy(v, c->dr.scal, sizeof v, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return moe::fail_hip(e, "reading device residency counters");
+        *out = moe_cache_stats{};
+        out->hits = v[moe::kScalHits];
+        out->misses = v[moe::kScalMisses];
+        out->lookups = out->hits + out->misses;
+        out->evictions = v[moe::kScalEvictions];
+        out->h2d_bytes = out->misses * c->d.expert_bytes;
+        out->capacity = c->C;
+        out->occupancy = int32_t(std::min<unsigned long long>(v[moe::kScalNextFree], (unsigned long long)c->C));
+        return MOE_OK;
+    }
     *out = c->st;
     int occ = 0;
     for (int32_t k : c->key_of_slot) occ += k >= 0;
@@ -532,6 +644,23 @@ int expert_cache_stats(moe_cache *c, moe_cache_stats *out) {
 
 int expert_cache_trace(moe_cache *c, size_t first, moe_cache_event *buf, size_t cap, size_t *n_out) {
     if (!c || !n_out || (cap && !buf)) return moe::fail(MOE_ERR_INVALID_ARG, "NULL argument");
+    if (c->dev_mode) {
+        unsigned long long n_ev = 0;
+        hipError_t e = hipDeviceSynchronize();
+        if (e == hipSuccess)
+            e = hipMemcpy(&n_ev, c->dr.scal + moe::kScalEvents, sizeof n_ev, hipMemcpyDeviceToHost);
+        if (e != hipSuccess) return moe::fail_hip(e, "reading the device decision log");
+        if (n_ev > (unsigned long long)c->dr.cap_events)
+            return moe::fail(MOE_ERR_INVALID_ARG, "the device decision log overflowed (%llu > %lld decisions)", n_ev,
+                             c->dr.cap_events);
+        size_t n = 0;
+        if (first < n_ev) n = std::min<size_t>(cap, size_t(n_ev) - first);
+        if (n && (e = hipMemcpy(buf, c->dr.events + first, n * sizeof(moe_cache_event), hipMemcpyDeviceToHost)) !=
+                     hipSuccess)
+            return moe::fail_hip(e, "reading the device decision log");
+        *n_out = n;
+        return MOE_OK;
+    }
     size_t n = 0;
     if (first < c->log.size()) n = std::min(cap, c->log.size() - first);
     if (n) memcpy(buf, c->log.data() + first, n * sizeof(moe_cache_event));

@@ -1,0 +1,222 @@
+// residency_dev.h -- the device lookup of the slot table as a block-wide device
+// function (kDevThreads threads), shared by the lookup kernel and by the fused
+// one-token top-k + lookup kernel.  See residency_dev.hip for what it decides.
+#pragma once
+#include "internal.h"
+
+namespace moe {
+namespace devres {
+
+constexpr int kDevThreads = 256;
+constexpr int kDevPerThread = kDevMaxSlots / kDevThreads;  // slots each thread stages
+constexpr int kWaveDev = 64;
+
+template <bool ROTARY>
+__device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const DevLookup &p, const int32_t *ids, int n,
+                                                int32_t *__restrict__ slots_out, int *err) {
+    __shared__ int32_t key_of[kDevMaxSlots];
+    __shared__ uint64_t stamp[ROTARY ? 1 : kDevMaxSlots];
+    __shared__ uint16_t charge[ROTARY ? kDevMaxSlots : 1];
+    __shared__ uint32_t present[MOE_MAX_EXPERTS / 32];
+    __shared__ int32_t R[MOE_MAX_EXPERTS];
+    __shared__ int32_t slot_of_e[MOE_MAX_EXPERTS];  // slot of each expert of the step, by expert id
+    __shared__ int32_t pre[MOE_MAX_EXPERTS];        // slot of each expert of the layer before the step
+    __shared__ unsigned long long scal_sh[kDevScalars];
+    __shared__ int m_sh, bad_sh, need_sh;
+    __shared__ unsigned long long red_v[kDevThreads / kWaveDev];
+    __shared__ int red_s[kDevThreads / kWaveDev];
+    const int tid = threadIdx.x;
+    const int C = p.C, E = p.E, layer = p.layer;
+    {
+        // every global read of the lookup is in flight at once, before any is used (clamped indices, no
+        // branches): the slot state, the layer's row of the slot table, the step's ids and the counters
+        const int32_t row = r.slot_of_key[layer * E + min(tid, E - 1)];
+        const int32_t id0 = ids[min(tid, max(n - 1, 0))];
+        const unsigned long long sc0 = r.scal[min(tid, kDevScalars - 1)];
+        int32_t kv[kDevPerThread];
+        uint64_t sv[kDevPerThread];
+#pragma unroll
+        for (int u = 0; u < kDevPerThread; ++u) {
+            const int sc = min(tid + u * kDevThreads, C - 1);
+            kv[u] = r.key_of_slot[sc];
+            if constexpr (ROTARY) sv[u] = r.charge[sc];
+            else sv[u] = r.stamp[sc];
+        }
+#pragma unroll
+        for (int u = 0; u < kDevPerThread; ++u) {
+            const int s = tid + u * kDevThreads;
+            if (s < C) {
+                key_of[s] = kv[u];
+                if constexpr (ROTARY) charge[s] = uint16_t(sv[u]);
+                else stamp[s] = sv[u];
+            }
+        }
+        if (tid < E) pre[tid] = row;
+        if (tid < kDevScalars) scal_sh[tid] = sc0;
+        if (tid < MOE_MAX_EXPERTS / 32) present[tid] = 0u;
+        if (tid == 0) bad_sh = 0;
+        __syncthreads();
+        for (int i = tid; i < n; i += kDevThreads) {
+            const int e = i == tid ? id0 : ids[i];  // steps of more than one block of ids read the rest here
+            if (e < 0 || e >= E) atomicOr(&bad_sh, 1);
+            else atomicOr(&present[e >> 5], 1u << (e & 31));
+        }
+    }
+    __syncthreads();
+    if (tid == 0) {
+        int m = 0;
+        for (int w = 0; w < (E + 31) / 32; ++w)
+            for (uint32_t b = present[w]; b; b &= b - 1u) R[m++] = w * 32 + __builtin_ctz(b);
+        m_sh = m;
+        if (bad_sh) {
+            atomicOr(err, kErrRange);  // no state change, as the host lookup
+        } else if (m > C) {
+            atomicOr(err, kErrBudget);
+            bad_sh = 1;
+        }
+        if (bad_sh) r.n_fill[0] = 0;  // nothing for the fill kernel to do
+    }
+    __syncthreads();
+    if (bad_sh) return;
+    const int m = m_sh;
+    auto pinned = [&](int k2) {  // is slot key k2 an expert of this step?
+        const int e2 = k2 - layer * E;
+        return e2 >= 0 && e2 < E && ((present[e2 >> 5] >> (e2 & 31)) & 1u);
+    };
+    // lane 0 of the block keeps the counters in registers
+    unsigned long long ctr = 0, hand = 0, next_free = 0, hits = 0, misses = 0, evictions = 0, n_ev = 0;
+    int n_fill = 0;
+    if (tid == 0) {
+        ctr = scal_sh[kScalCtr];
+        hand = scal_sh[kScalHand];
+        next_free = scal_sh[kScalNextFree];
+        hits = scal_sh[kScalHits];
+        misses = scal_sh[kScalMisses];
+        evictions = scal_sh[kScalEvictions];
+        n_ev = scal_sh[kScalEvents];
+    }
+    auto log = [&](int e, int kind, int s, int victim) {
+        if (n_ev < (unsigned long long)r.cap_events) r.events[n_ev] = moe_cache_event{p.step, layer, e, kind, s, victim};
+        ++n_ev;
+    };
+    auto place = [&](int e, int s) {  // lane 0: the new entry (layer, e) takes slot s
+        const int key = layer * E + e;
+        const int victim = key_of[s];
+        if (victim >= 0) {
+            r.slot_of_key[victim] = -1;
+            ++evictions;
+        }
+        key_of[s] = key;
+        r.slot_of_key[key] = s;
+        if constexpr (ROTARY) charge[s] = 0;
+        else stamp[s] = ++ctr;
+        ++misses;
+        log(e, MOE_EVENT_MISS, s, victim);
+        slot_of_e[e] = s;
+        r.fill_src[n_fill] = (long long)layer * p.layer_stride + (long long)e * p.expert_stride;
+        r.fill_slot[n_fill] = s;
+        ++n_fill;
+    };
+    // Lane 0 walks the step's experts in order, with no block barrier, until an LRU miss finds no free
+    // slot; then the whole block looks for the least recently used slot outside the step, lane 0 places
+    // the expert there, and the walk goes on.  A resident expert of the step keeps its slot for the whole
+    // step (victims are never the step's own), so the row read at the start stays valid.
+    int j = 0;  // lane 0's position in R
+    for (;;) {
+        if (tid == 0) {
+            need_sh = 0;
+            for (; j < m; ++j) {
+                const int e = R[j];
+                const int s = pre[e];
+                if (s >= 0) {
+                    if constexpr (ROTARY) {
+                        if (charge[s] < p.charge_max) ++charge[s];
+                    } else {
+                        stamp[s] = ++ctr;
+                    }
+                    ++hits;
+                    slot_of_e[e] = s;
+                    log(e, MOE_EVENT_HIT, s, -1);
+                } else if (next_free < (unsigned long long)C) {
+                    place(e, int(next_free++));
+                } else if constexpr (ROTARY) {
+                    // some slot holds an expert outside the step, and each full turn takes a charge from
+                    // every such slot, so the hand stops within charge_max + 1 turns
+                    int s2;
+                    for (;;) {
+                        s2 = int(hand);
+                        hand = hand + 1 == (unsigned long long)C ? 0 : hand + 1;
+                        if (pinned(key_of[s2])) continue;
+                        if (charge[s2] > 0) {
+                            --charge[s2];
+                            continue;
+                        }
+                        break;
+                    }
+                    place(e, s2);
+                } else {
+                    need_sh = 1;  // R[j] waits for the block-wide search
+                    break;
+                }
+            }
+        }
+        __syncthreads();
+        if (!need_sh) break;  // every thread read the same value after the barrier
+        if constexpr (!ROTARY) {
+            // least recently used slot outside the step (stamps are unique)
+            unsigned long long best = ~0ull;
+            int bs = -1;
+            for (int s = tid; s < C; s += kDevThreads)
+                if (!pinned(key_of[s]) && stamp[s] < best) {
+                    best = stamp[s];
+                    bs = s;
+                }
+#pragma unroll
+            for (int off = kWaveDev / 2; off > 0; off >>= 1) {
+                const unsigned long long ob = __shfl_xor(best, off);
+                const int os = __shfl_xor(bs, off);
+                if (ob < best) {
+                    best = ob;
+                    bs = os;
+                }
+            }
+            if ((tid & (kWaveDev - 1)) == 0) {
+                red_v[tid / kWaveDev] = best;
+                red_s[tid / kWaveDev] = bs;
+            }
+            __syncthreads();
+            if (tid == 0) {
+                for (int w = 1; w < kDevThreads / kWaveDev; ++w)
+                    if (red_v[w] < best) {
+                        best = red_v[w];
+                        bs = red_s[w];
+                    }
+                place(R[j], bs);
+                ++j;
+            }
+            // the search read need_sh and the state before lane 0 changes them in the next round
+            __syncthreads();
+        }
+    }
+    if (tid == 0) {
+        r.scal[kScalCtr] = ctr;
+        r.scal[kScalHand] = hand;
+        r.scal[kScalNextFree] = next_free;
+        r.scal[kScalHits] = hits;
+        r.scal[kScalMisses] = misses;
+        r.scal[kScalEvictions] = evictions;
+        r.scal[kScalEvents] = n_ev;
+        r.n_fill[0] = n_fill;
+    }
+    __syncthreads();
+    if (slots_out)
+        for (int i = tid; i < n; i += kDevThreads) slots_out[i] = slot_of_e[ids[i]];
+    for (int s = tid; s < C; s += kDevThreads) {
+        r.key_of_slot[s] = key_of[s];
+        if constexpr (ROTARY) r.charge[s] = charge[s];
+        else r.stamp[s] = stamp[s];
+    }
+}
+
+}  // namespace devres
+}  // namespace moe

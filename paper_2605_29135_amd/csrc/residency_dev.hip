@@ -1,0 +1,83 @@
+// residency_dev.hip -- the slot table's replacement decisions made on the device.
+//
+// The residency of sec. 4 and Fig. 1 (host tier, slot group, lookup table from
+// sub-module id to slot, selective load, evict) with every decision taken by a
+// kernel, so that a decode step enqueues route -> lookup -> fills -> expert FFN
+// for every layer without waiting for the host.  One lookup kernel per step
+// (one block): it stages the slot keys and their stamps (LRU) or charges
+// (rotary) in LDS, forms the step's ascending unique experts from a presence
+// bitmap, and takes the same decisions, in the same order, as the host runtime:
+// a hit refreshes its slot; a miss takes the lowest free slot, else the least
+// recently used slot (LRU: a block-wide arg-min over the stamps of slots whose
+// expert the step does not need) or the slot where the forward rotation stops
+// (rotary: one lane turns the hand over the LDS copy).  Each decision is logged,
+// the slot table is updated in place, and the misses form a fill list that the
+// fill kernel then streams from pinned host memory.
+#include "residency_dev.h"
+
+namespace moe {
+namespace {
+
+using namespace devres;
+constexpr int kFillUnrollDev = 4;
+
+template <bool ROTARY>
+__global__ __launch_bounds__(kDevThreads) void dev_lookup_kernel(DevResidency r, DevLookup p,
+                                                                 const int32_t *__restrict__ ids, int n,
+                                                                 int32_t *__restrict__ slots_out, int *err) {
+    dev_lookup_body<ROTARY>(r, p, ids, n, slots_out, err);
+}
+
+// Block (x, f) streams its share of fill f; blocks past the lookup's fill count exit.
+__global__ __launch_bounds__(kDevThreads) void dev_fill_kernel(const long long *__restrict__ src_off,
+                                                               const int32_t *__restrict__ slot,
+                                                               const int32_t *__restrict__ n_fill,
+                                                               const uint8_t *__restrict__ host_dev,
+                                                               uint8_t *__restrict__ pool, long long bytes) {
+    const int f = blockIdx.y;
+    if (f >= n_fill[0]) return;
+    const size_t n16 = size_t(bytes) / 16;
+    const size_t per = (n16 + gridDim.x - 1) / gridDim.x;
+    const size_t beg = size_t(blockIdx.x) * per;
+    const size_t end = beg + per < n16 ? beg + per : n16;
+    const uint4 *src = reinterpret_cast<const uint4 *>(host_dev + src_off[f]);
+    uint4 *dst = reinterpret_cast<uint4 *>(pool + size_t(slot[f]) * size_t(bytes));
+    for (size_t i = beg + threadIdx.x; i < end; i += size_t(kDevThreads) * kFillUnrollDev) {
+        uint4 v[kFillUnrollDev];
+#pragma unroll
+        for (int u = 0; u < kFillUnrollDev; ++u) {
+            const size_t j = i + size_t(u) * kDevThreads;
+            v[u] = j < end ? src[j] : make_uint4(0u, 0u, 0u, 0u);
+        }
+#pragma unroll
+        for (int u = 0; u < kFillUnrollDev; ++u) {
+            const size_t j = i + size_t(u) * kDevThreads;
+            if (j < end) dst[j] = v[u];
+        }
+    }
+}
+
+}  // namespace
+
+hipError_t launch_dev_lookup(const DevResidency &r, const DevLookup &p, const int32_t *ids, int n, int32_t *slots_out,
+                             int *err, hipStream_t s) {
+    if (p.C < 1 || p.C > kDevMaxSlots || p.E < 1 || p.E > MOE_MAX_EXPERTS || p.layer < 0 || p.layer >= p.L || n < 0)
+        return hipErrorInvalidValue;
+    if (p.rotary) dev_lookup_kernel<true><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
+    else dev_lookup_kernel<false><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
+    return hipGetLastError();
+}
+
+hipError_t launch_dev_fill(const DevResidency &r, const uint8_t *host_dev, uint8_t *pool, long long expert_bytes,
+                           int max_fills, hipStream_t s) {
+    if (max_fills < 1) return hipSuccess;
+    if (expert_bytes <= 0 || expert_bytes % 16) return hipErrorInvalidValue;
+    long long bpf = expert_bytes / (128 << 10);  // about 64 blocks keep a 9 MiB blob's PCIe reads at full rate
+    bpf = bpf < 4 ? 4 : (bpf > 64 ? 64 : bpf);
+    dev_fill_kernel<<<dim3(unsigned(bpf), unsigned(max_fills)), kDevThreads, 0, s>>>(r.fill_src, r.fill_slot,
+                                                                                     r.n_fill, host_dev, pool,
+                                                                                     expert_bytes);
+    return hipGetLastError();
+}
+
+}  // namespace moe

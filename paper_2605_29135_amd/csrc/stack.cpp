@@ -50,6 +50,7 @@ struct moe_stack {
     float *weights = nullptr;   // device [Tmax x k]
     int32_t *ids_host = nullptr;  // pinned [Tmax x k]
     int32_t *slots_host = nullptr; // [Tmax x k] slot of each id after the lookup
+    int32_t *dev_slots = nullptr;  // device [L x max_tokens x k]: slot of each id after each layer's device lookup
     void *ws = nullptr;
     size_t ws_bytes = 0;
     void *pws = nullptr;        // prefill workspace (max_prefill_tokens > 0)
@@ -174,6 +175,7 @@ int moe_stack_destroy(moe_stack *s) {
     if (s->mbox) (void)hipHostFree(s->mbox);
     if (s->scratch_x) (void)hipFree(s->scratch_x);
     if (s->scratch_y) (void)hipFree(s->scratch_y);
+    if (s->dev_slots) (void)hipFree(s->dev_slots);
     delete s;
     return MOE_OK;
 }
@@ -191,6 +193,8 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefetch must be in [0, E]");
     if (d->recall < 0 || d->recall > 4096 || d->recall_overlap < 0 || d->recall_overlap > d->k)
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: recall must be in [0, 4096], recall_overlap in [0, k]");
+    if (d->cache && moe::cache_device(d->cache) && (d->prefetch > 0 || d->recall > 0))
+        return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefetch and recall need host lookups (not MOE_CACHE_DEVICE)");
     if (d->max_prefill_tokens > 0 && !moe::prefill_dtype_supported(d->w_dtype))
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefill needs MOE_BF16 or MOE_INT4G128 experts");
     if (!moe::ffn_shape_supported(d->H, d->I, d->w_dtype) || !moe::router_shape_supported(d->H, d->router_dtype))
@@ -229,6 +233,9 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
     if ((e = hipMalloc(&s->weights, sizeof(float) * T * d->k)) != hipSuccess) return bail(e, "stack buffers");
     if ((e = hipHostMalloc(&s->ids_host, sizeof(int32_t) * T * d->k, 0)) != hipSuccess) return bail(e, "stack buffers");
     s->slots_host = new int32_t[size_t(T) * d->k];
+    if (moe::cache_device(d->cache) &&
+        (e = hipMalloc(&s->dev_slots, sizeof(int32_t) * size_t(d->n_layers) * d->max_tokens * d->k)) != hipSuccess)
+        return bail(e, "stack buffers");
     s->last.assign(d->n_layers, LastLayer{});
     s->demand.assign(size_t(d->n_layers) * d->E, 0u);
     s->cur_sets.assign(size_t(d->n_layers) * d->k, 0);
@@ -269,16 +276,27 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
         int32_t *ids = ids_out ? ids_out + size_t(l) * T * d.k : s->ids;
         float *w = weights_out ? weights_out + size_t(l) * T * d.k : s->weights;
         const float *bias = logit_bias ? logit_bias + size_t(l) * T * d.E : nullptr;
-        // one token under a budget: the top-k kernel publishes its ids straight to host memory
-        const bool mailbox = s->budgeted && T == 1;
+        // lookups on the device need no ids on the host; otherwise one token under a budget has the
+        // top-k kernel publish its ids straight to host memory
+        const bool dev_lookup = s->budgeted && moe::cache_device(d.cache);
+        const bool mailbox = s->budgeted && T == 1 && !dev_lookup;
         const uint32_t seq = mailbox ? ++s->mbox_seq : 0;
         hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, bias, s->logits,
                                                  true, s->h, strm);
-        if (e == hipSuccess)
+        const bool fused = dev_lookup && T == 1;  // one token: top-k and the lookup in one kernel
+        if (e == hipSuccess && !fused)
             e = moe::launch_topk_softmax(s->logits, T, d.E, d.k, ids, w, eflags, strm, mailbox ? s->mbox_dev : nullptr,
                                          seq);
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: routing");
-        if (s->budgeted) {
+        if (fused) {
+            int st = moe::cache_topk_lookup(d.cache, step, l, s->logits, d.k, ids, w,
+                                            s->dev_slots + size_t(l) * d.max_tokens * d.k, eflags, strm);
+            if (st != MOE_OK) return st;
+        } else if (dev_lookup) {
+            int st = expert_cache_lookup_device(d.cache, step, l, ids, T * d.k,
+                                                s->dev_slots + size_t(l) * d.max_tokens * d.k, strm);
+            if (st != MOE_OK) return st;
+        } else if (s->budgeted) {
             if (mailbox) {
                 int st = wait_published_ids(s, seq, strm);
                 if (st != MOE_OK) return st;
@@ -302,7 +320,7 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
         moe::FfnPlan plan;
         const int32_t *slot_of = s->slot_table + size_t(l) * d.E;
         const uint8_t *pool = static_cast<const uint8_t *>(s->pool);
-        if (s->budgeted && T == 1) {
+        if (s->budgeted && T == 1 && !dev_lookup) {
             plan.n = d.k;
             for (int j = 0; j < d.k; ++j) plan.off[j] = (long long)s->slots_host[j] * (long long)s->expert_bytes;
         } else if (!s->budgeted) {
@@ -314,7 +332,7 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
                                    plan.n ? &plan : nullptr);
         s->last[l] = LastLayer{true, T, l, ids, w, slot_of, pool, plan};
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: expert FFN");
-        if (s->budgeted) {
+        if (s->budgeted && !dev_lookup) {
             int st = expert_cache_release(d.cache, strm);
             if (st == MOE_OK && d.prefetch > 0 && T == 1) st = prefetch_next(s, step, l);  // after the release
             if (st == MOE_OK && s->recalled >= 0 && T == 1 && l + 1 < d.n_layers) {
@@ -325,7 +343,7 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
             if (st != MOE_OK) return st;
         }
     }
-    if (s->budgeted && d.recall > 0 && T == 1) {
+    if (s->budgeted && d.recall > 0 && T == 1 && !moe::cache_device(d.cache)) {
         store_snapshot(s);
         s->recalled = -1;
     }
@@ -353,7 +371,11 @@ int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out,
         if (e != hipSuccess) return moe::fail_hip(e, "stack prefill: routing");
         const int32_t *slot_of = s->slot_table + size_t(l) * d.E;
         const uint8_t *pool = static_cast<const uint8_t *>(s->pool);
-        if (s->budgeted) {
+        const bool dev_lookup = s->budgeted && moe::cache_device(d.cache);
+        if (dev_lookup) {
+            int st = expert_cache_lookup_device(d.cache, step, l, ids, T * d.k, nullptr, strm);
+            if (st != MOE_OK) return st;
+        } else if (s->budgeted) {
             e = hipMemcpyAsync(s->ids_host, ids, sizeof(int32_t) * T * d.k, hipMemcpyDeviceToHost, strm);
             if (e == hipSuccess) e = hipEventRecord(s->ids_ready, strm);
             if (e == hipSuccess) e = hipEventSynchronize(s->ids_ready);
@@ -367,7 +389,7 @@ int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out,
         e = moe::launch_prefill_ffn(s->h, T, d.H, d.I, d.E, d.k, ids, w, slot_of, pool, s->expert_bytes, d.w_dtype,
                                     s->shared_w.empty() ? nullptr : s->shared_w[l], x, true, ws, eflags, strm);
         if (e != hipSuccess) return moe::fail_hip(e, "stack prefill: expert FFN");
-        if (s->budgeted) {
+        if (s->budgeted && !dev_lookup) {
             int st = expert_cache_release(d.cache, strm);
             if (st != MOE_OK) return st;
         }
@@ -387,6 +409,24 @@ int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *
     const auto &d = s->d;
     const int L = d.n_layers, T = s->last[0].T;
     const moe::FfnWorkspace ws = moe::ffn_workspace(s->ws, T, d.k, d.I);
+    // One token with device lookups: each layer's slots, as its lookup left them, become that layer's
+    // launch plan, so that every re-launch reads the slots the step read (later layers may have evicted
+    // some of them since, which only changes the bytes read, not where or how many).
+    std::vector<moe::FfnPlan> plans(static_cast<size_t>(L));
+    for (int l = 0; l < L; ++l) plans[size_t(l)] = s->last[size_t(l)].plan;
+    if (s->budgeted && moe::cache_device(d.cache) && T == 1) {
+        std::vector<int32_t> slots(size_t(L) * d.max_tokens * d.k);
+        hipError_t e0 = hipStreamSynchronize(strm);
+        if (e0 == hipSuccess)
+            e0 = hipMemcpy(slots.data(), s->dev_slots, sizeof(int32_t) * slots.size(), hipMemcpyDeviceToHost);
+        if (e0 != hipSuccess) return moe::fail_hip(e0, "kernel_time: reading the step's slots");
+        for (int l = 0; l < L; ++l) {
+            moe::FfnPlan &pl = plans[size_t(l)];
+            pl.n = d.k;
+            for (int j = 0; j < d.k; ++j)
+                pl.off[j] = (long long)slots[size_t(l) * d.max_tokens * d.k + j] * (long long)s->expert_bytes;
+        }
+    }
     // Every layer's launch of the last step, in step order, captured into one
     // graph on a private stream (so that host launch overhead does not starve
     // the device) and replayed n times.  The last layer's normalised input
@@ -411,7 +451,8 @@ int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *
         }
         return moe::launch_expert_ffn(s->scratch_x, T, d.H, d.I, d.E, d.k, ll.ids, ll.weights, ll.slot_of, ll.pool,
                                       s->expert_bytes, d.w_dtype, s->shared_w.empty() ? nullptr : s->shared_w[l],
-                                      s->scratch_y, false, ws, eflags, cs, ll.plan.n ? &ll.plan : nullptr,
+                                      s->scratch_y, false, ws, eflags, cs,
+                                      plans[size_t(l)].n ? &plans[size_t(l)] : nullptr,
                                       which == 1 ? moe::kFfnGateUp : which == 2 ? moe::kFfnDown : moe::kFfnBoth);
     };
     // Multi-token steps under a budget read the device slot table, where an

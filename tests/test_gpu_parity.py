@@ -256,7 +256,7 @@ def _pinned_store(wl, layers_alias=False):
 
 
 def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=None, T=1, charge_max=None,
-                        recall=0, recall_overlap=0):
+                        recall=0, recall_overlap=0, device=False):
     """Decode `steps` steps through the stack; check events exactly and outputs within tolerance.  With
     charge_max the slots use the rotary policy (else LRU); with recall the stack recalls prior slot sets."""
     buf = _pinned_store(wl, layers_alias)
@@ -264,7 +264,7 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
     policy = moe.MOE_POLICY_LRU if charge_max is None else moe.MOE_POLICY_ROTARY
     cache = moe.ExpertCache(wl.L, wl.E, eb, capacity * eb + (wl.L * eb if wl.shared else 0), buf.ptr,
                             0 if layers_alias else wl.E * eb, eb, reserved_bytes=wl.L * eb if wl.shared else 0,
-                            policy=policy, charge_max=charge_max or 0)
+                            policy=policy, charge_max=charge_max or 0, device=device)
     routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
     shared = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)] if wl.shared else None
     stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T,
@@ -318,10 +318,12 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
     return s
 
 
-def test_budgeted_stack_small_evicting():
+@pytest.mark.parametrize("device,charge_max", [(False, None), (True, None), (True, 3)])
+def test_budgeted_stack_small_evicting(device, charge_max):
+    """With device=True every lookup is a kernel (no host round trip); the decisions are the same."""
     wl = synth.Workload("small stack", H=512, E=32, k=4, I=256, L=4, dtype=synth.BF16, routing="zipf_overlap",
                         cfg_id=97)
-    s = run_stack_and_check(wl, steps=40, capacity=24)
+    s = run_stack_and_check(wl, steps=40, capacity=24, device=device, charge_max=charge_max)
     assert s["evictions"] > 0
 
 
@@ -351,11 +353,97 @@ def test_budgeted_stack_tokens_and_shared_int4():
     assert s["evictions"] > 0
 
 
-def test_budgeted_stack_full_size_config4_sampled():
+@pytest.mark.parametrize("device", [False, True])
+def test_budgeted_stack_full_size_config4_sampled(device):
     """The benchmark's configuration (40 layers, 6 GiB budget -> 682 slots), layers aliasing one host copy."""
     wl = synth.workload(4)
-    s = run_stack_and_check(wl, steps=6, capacity=wl.capacity(), layers_alias=True, check_steps=[0, 5])
+    s = run_stack_and_check(wl, steps=6, capacity=wl.capacity(), layers_alias=True, check_steps=[0, 5], device=device)
     assert s["capacity"] == 682 and s["misses"] > 0
+
+
+def _d2h(ptr, nbytes):
+    """Copy device memory the library owns (a raw pointer) to the host."""
+    import ctypes as C
+    hip = C.CDLL("libamdhip64.so")
+    hip.hipMemcpy.argtypes = [C.c_void_p, C.c_void_p, C.c_size_t, C.c_int]
+    hip.hipMemcpy.restype = C.c_int
+    out = np.empty(nbytes, np.uint8)
+    assert hip.hipMemcpy(out.ctypes.data, ptr, nbytes, 2) == 0  # device to host
+    return out
+
+
+@pytest.mark.parametrize("rotary,Q,C,L,E,nmax,steps", [(False, 0, 24, 3, 32, 8, 300), (True, 3, 24, 3, 32, 8, 300),
+                                                       (False, 0, 700, 40, 128, 40, 400),
+                                                       (True, 32, 700, 40, 128, 40, 400),
+                                                       (False, 0, 4096, 48, 256, 600, 120),
+                                                       (True, 0, 4096, 48, 256, 600, 120)])
+def test_device_lookups_match_oracle(rotary, Q, C, L, E, nmax, steps):
+    """Lookups made by the device kernel: decisions, counters, slot table and slot contents against the
+    oracle, for steps of up to nmax ids with repeats (prefill-sized at the largest capacity)."""
+    eb = 256
+    buf = moe.PinnedBuffer(L * E * eb)
+    buf.array.view(np.int32).reshape(L * E, eb // 4)[:] = np.arange(L * E, dtype=np.int32)[:, None]
+    cache = moe.ExpertCache(L, E, eb, C * eb, buf.ptr, E * eb, eb, device=True,
+                            policy=moe.MOE_POLICY_ROTARY if rotary else moe.MOE_POLICY_LRU, charge_max=Q)
+    o = oracle.Rotary(C, L, E, Q) if rotary else oracle.LRU(C, L, E)
+    rng = np.random.default_rng(C + 7 * Q + int(rotary))
+    ids = [rng.integers(0, E, size=int(rng.integers(1, nmax + 1))).astype(np.int32) for _ in range(steps)]
+    layers = rng.integers(0, L, size=steps)
+    ids_d = [dev(a) for a in ids]
+    slots_d = [torch.empty(a.size, dtype=torch.int32, device=DEV) for a in ids]
+    want_slots = []
+    torch.cuda.synchronize()
+    for t in range(steps):
+        cache.lookup_device(t, int(layers[t]), ids_d[t], slots_d[t])
+        assert o.lookup(t, int(layers[t]), ids[t]) == oracle.OK
+        want_slots.append([o.slot_of(int(layers[t]), int(e)) for e in ids[t]])
+    moe.moe_sync_check()
+    assert all(slots_d[t].cpu().tolist() == want_slots[t] for t in range(steps))
+    ev, oev = cache.trace(), o.events()
+    assert len(ev) == len(oev)
+    assert (ev.view(np.int32).reshape(-1, 6) == oev.view(np.int32).reshape(-1, 6)).all()
+    st, so = cache.stats(), o.stats()
+    assert (st["hits"], st["misses"], st["evictions"]) == (so["hits"], so["misses"], so["evictions"])
+    assert st["occupancy"] == o.occupancy() and st["h2d_bytes"] == st["misses"] * eb
+    table_p, pool_p = cache.slot_table()
+    table = _d2h(table_p, 4 * L * E).view(np.int32)
+    pool = _d2h(pool_p, C * eb).view(np.int32).reshape(C, eb // 4)
+    for l in range(L):
+        for e in range(E):
+            s = o.slot_of(l, e)
+            assert table[l * E + e] == s
+            if s >= 0:
+                assert (pool[s] == l * E + e).all()
+    cache.close()
+    buf.close()
+
+
+def test_device_lookup_errors_change_nothing():
+    L, E, C, eb = 2, 16, 4, 256
+    buf = moe.PinnedBuffer(L * E * eb)
+    cache = moe.ExpertCache(L, E, eb, C * eb, buf.ptr, E * eb, eb, device=True)
+    cache.lookup_device(0, 0, dev(np.array([1, 2, 2], np.int32)))
+    moe.moe_sync_check()
+    cache.lookup_device(1, 1, dev(np.array([3, 16], np.int32)))
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_sync_check()
+    assert ei.value.code == -2
+    cache.lookup_device(2, 1, dev(np.arange(5, dtype=np.int32)))
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_sync_check()
+    assert ei.value.code == -4
+    ev = cache.trace()
+    assert len(ev) == 2 and cache.stats()["misses"] == 2
+    with pytest.raises(moe.MoeError):
+        cache.lookup(3, 0, np.array([1], np.int32))
+    with pytest.raises(moe.MoeError):
+        cache.prefetch(3, 0, np.array([1], np.int32))
+    with pytest.raises(moe.MoeError):
+        cache.lookup_device(3, 2, dev(np.array([1], np.int32)))
+    cache.close()
+    with pytest.raises(moe.MoeError):
+        moe.ExpertCache(L, E, eb, 5000 * eb, buf.ptr, E * eb, eb, device=True)
+    buf.close()
 
 
 def test_full_size_config2_every_output():
