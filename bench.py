@@ -53,6 +53,9 @@ def parse():
                     help="where the slot table's decisions are made: lookup kernels (the default: no host round "
                          "trip), or the host after each layer's ids reach it (needed by --prefetch / --recall); "
                          "the decisions are the same")
+    ap.add_argument("--graph", action="store_true",
+                    help="with device residency, replay each token as one captured HIP graph "
+                         "(moe_stack_decode_graph) instead of enqueueing its launches")
     ap.add_argument("--recall", type=int, default=0,
                     help="reverse rotation: remembered tokens whose slot sets a recurring layer-0 routing recalls "
                          "(0 = off)")
@@ -66,6 +69,24 @@ def parse():
     ap.add_argument("--replays", type=int, default=5,
                     help="replays of the last step's launches (one per layer) for the per-launch device time")
     return ap.parse_args()
+
+
+def decoder(torch, stack, xs, bias, graph: bool):
+    """One decode token through the stack: the eager step, or (device residency, one token) the step's
+    captured graph replayed through fixed buffers -- the token's hidden state and routing mask copied in and
+    its output copied back, all inside the timed region."""
+    if not graph:
+        return lambda tag, t: stack.decode_step(tag, xs[t], None if bias is None else bias[t])
+    x_buf = torch.empty_like(xs[0])
+    b_buf = None if bias is None else torch.empty_like(bias[0])
+
+    def step(tag, t):
+        x_buf.copy_(xs[t])
+        if b_buf is not None:
+            b_buf.copy_(bias[t])
+        stack.decode_graph(tag, x_buf, b_buf)
+        xs[t].copy_(x_buf)
+    return step
 
 
 def pcie_ceiling_gbps(torch, moe, chunk: int, total: int) -> float:
@@ -328,10 +349,12 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
         return cache, stack
 
     # warm-up on a throw-away cache (kernels loaded, allocator warm), so the timed run starts cold
+    use_graph = args.residency == "device" and args.graph
     cache, stack = make()
     stack.prefill(0, torch.from_numpy(xp_np[:64]).to(dev))
+    dec = decoder(torch, stack, xs, bias, use_graph)
     for t in range(min(args.warmup, 8)):
-        stack.decode_step(1 + t, xs[t], bias[t])
+        dec(1 + t, t)
     moe.moe_sync_check()
     stack.close()
     cache.close()
@@ -347,7 +370,8 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     t_prefill = time.perf_counter() - t0
     moe.moe_sync_check()
     st1 = cache.stats()
-    run = lambda a, b: [stack.decode_step(1 + t, xs[t], bias[t]) for t in range(a, b)]
+    dec = decoder(torch, stack, xs, bias, use_graph)
+    run = lambda a, b: [dec(1 + t, t) for t in range(a, b)]
     run(0, args.warmup)
     moe.moe_sync_check()
     st2 = cache.stats()
@@ -410,6 +434,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
                    "hidden": H, "intermediate": I, "prefill_tokens": Tp, "decode_tokens_per_step": 1,
                    "budget_bytes": wl.budget_bytes, "slots": st3["capacity"], "host_store_bytes": L * E * eb,
                    "prefetch_per_layer": args.prefetch, "policy": args.policy, "residency": args.residency,
+                   "decode_graph": use_graph,
                    **({"charge_max": args.charge_max} if args.policy == "rotary" else {})},
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU (int4 decode)", "achieved": gu_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gu_gbps / HBM_PEAK_GBPS,
@@ -516,9 +541,12 @@ def main():
 
     stream = torch.cuda.current_stream()
 
+    use_graph = budgeted and args.residency == "device" and T == 1 and args.graph
+    dec = decoder(torch, stack, xs, bias, use_graph)
+
     def run(t0, t1):
         for t in range(t0, t1):
-            stack.decode_step(t, xs[t], None if bias is None else bias[t])
+            dec(t, t)
 
     # ---- warm-up, then the timed region
     run(0, args.warmup)
@@ -597,7 +625,7 @@ def main():
                    "tokens_per_step": T, "budget_bytes": budget, "slots": st1["capacity"],
                    "host_store_bytes": L_store * E * eb, "host_layers_aliased": bool(alias),
                    "prefetch_per_layer": args.prefetch if budgeted else 0, "policy": args.policy,
-                   "residency": args.residency if budgeted else "preloaded",
+                   "residency": args.residency if budgeted else "preloaded", "decode_graph": use_graph,
                    **({"charge_max": args.charge_max} if args.policy == "rotary" else {}),
                    **({"recall": args.recall, "recall_overlap": args.recall_overlap or k} if args.recall else {})},
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU", "achieved": gu_gbps,

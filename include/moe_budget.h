@@ -356,6 +356,17 @@ MOE_API int moe_stack_destroy(moe_stack *s);
 MOE_API int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *logit_bias,
                           int32_t *ids_out, float *weights_out, void *stream);
 
+/* moe_stack_decode_step for one token (T = 1), as a replayed HIP graph.  With a
+ * MOE_CACHE_DEVICE cache nothing in a step waits for the host, so the first call
+ * captures the step's launches (every layer's routing, fused top-k + lookup,
+ * fills and expert FFN) and later calls replay them after setting the step tag
+ * on the device; a call with other x / logit_bias / ids_out / weights_out
+ * pointers captures again (keep the buffers fixed and refill them).  Results
+ * and residency decisions are those of moe_stack_decode_step.  Without a device
+ * cache it is moe_stack_decode_step. */
+MOE_API int moe_stack_decode_graph(moe_stack *s, int step, float *x, const float *logit_bias, int32_t *ids_out,
+                                   float *weights_out, void *stream);
+
 /* Prompt evaluation (prefill; its rate is reported beside decode in the table
  * of sec. 8.1) over every layer, in place on x (device fp32 [T x H]):
  * x <- x + MoE_l(rmsnorm(x)) for l = 0..L-1, with each layer's routing on the

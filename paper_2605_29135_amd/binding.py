@@ -91,6 +91,7 @@ def lib() -> C.CDLL:
             "moe_stack_create": [C.POINTER(StackDesc), C.POINTER(P)],
             "moe_stack_destroy": [P],
             "moe_stack_decode_step": [P, I, P, I, P, P, P, P],
+            "moe_stack_decode_graph": [P, I, P, P, P, P, P],
             "moe_stack_kernel_time": [P, I, I, P, C.POINTER(C.c_double)],
             "moe_stack_prefill": [P, I, P, I, P, P, P],
             "moe_hbm_read_probe": [P, SZ, P, P],
@@ -379,6 +380,17 @@ class MoeStack:
                                            _dev(ids_out, "ids_out", torch.int32),
                                            _dev(weights_out, "weights_out", torch.float32), _stream(stream)),
                "moe_stack_decode_step")
+
+    def decode_graph(self, step: int, x, logit_bias=None, ids_out=None, weights_out=None, stream=None):
+        """One-token decode step as a replayed HIP graph (device residency); keep the tensors fixed."""
+        import torch
+        if x.shape[0] != 1:
+            raise ValueError("decode_graph takes one token")
+        _check(lib().moe_stack_decode_graph(self._h, step, _dev(x, "x", torch.float32),
+                                            _dev(logit_bias, "logit_bias", torch.float32),
+                                            _dev(ids_out, "ids_out", torch.int32),
+                                            _dev(weights_out, "weights_out", torch.float32), _stream(stream)),
+               "moe_stack_decode_graph")
         return x
 
     def prefill(self, step: int, x, ids_out=None, weights_out=None, stream=None):

@@ -94,7 +94,10 @@ struct DevResidency {
 struct DevLookup {
     int C, L, E, layer, step, rotary, charge_max;
     long long layer_stride, expert_stride;
+    const int *step_dev = nullptr;  // when set, the step tag of the decisions is read here instead of `step`
 };
+// Sets *p = v on the stream (a one-lane kernel: a graph replay reads the step tag from device memory).
+hipError_t launch_set_int(int *p, int v, hipStream_t s);
 // slots_out (device, optional): slots_out[i] = slot of ids[i] after the lookup.
 hipError_t launch_dev_lookup(const DevResidency &r, const DevLookup &p, const int32_t *ids, int n, int32_t *slots_out,
                              int *err, hipStream_t s);
@@ -145,7 +148,8 @@ bool cache_device(const struct ::moe_cache *c);  // lookups run on the device (M
 // MOE_CACHE_DEVICE, one token: enqueue top-k of `logits` fused with the lookup of the chosen experts, then
 // the fills of its misses.  Returns an MOE_ERR_* code.
 int cache_topk_lookup(struct ::moe_cache *c, int step, int layer, const float *logits, int k, int32_t *ids,
-                      float *weights, int32_t *slots_out, int *err_flags, hipStream_t s);
+                      float *weights, int32_t *slots_out, int *err_flags, hipStream_t s,
+                      const int *step_dev = nullptr);
 
 // Sticky error-flag word of the current device (set up on first use).
 int *device_error_flags();

@@ -379,11 +379,11 @@ bool moe::cache_resident(const moe_cache *c, int layer, int expert) {
 bool moe::cache_device(const moe_cache *c) { return c->dev_mode; }
 
 int moe::cache_topk_lookup(moe_cache *c, int step, int layer, const float *logits, int k, int32_t *ids,
-                           float *weights, int32_t *slots_out, int *err_flags, hipStream_t s) {
+                           float *weights, int32_t *slots_out, int *err_flags, hipStream_t s, const int *step_dev) {
     if (!c || !c->dev_mode || layer < 0 || layer >= c->L)
         return moe::fail(MOE_ERR_INVALID_ARG, "fused top-k lookup needs a MOE_CACHE_DEVICE cache and a valid layer");
     moe::DevLookup p{c->C, c->L, c->E, layer, step, c->d.policy == MOE_POLICY_ROTARY ? 1 : 0, c->charge_max,
-                     (long long)c->d.host_layer_stride, (long long)c->d.host_expert_stride};
+                     (long long)c->d.host_layer_stride, (long long)c->d.host_expert_stride, step_dev};
     hipError_t e = moe::launch_topk_lookup(logits, c->E, k, ids, weights, err_flags, c->dr, p, slots_out, s);
     if (e == hipSuccess)
         e = moe::launch_dev_fill(c->dr, c->host_dev, c->pool, (long long)c->d.expert_bytes, std::min(k, c->E), s);

@@ -22,6 +22,7 @@ __device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const Dev
     __shared__ int32_t slot_of_e[MOE_MAX_EXPERTS];  // slot of each expert of the step, by expert id
     __shared__ int32_t pre[MOE_MAX_EXPERTS];        // slot of each expert of the layer before the step
     __shared__ unsigned long long scal_sh[kDevScalars];
+    __shared__ int step_sh;
     __shared__ int m_sh, bad_sh, need_sh;
     __shared__ unsigned long long red_v[kDevThreads / kWaveDev];
     __shared__ int red_s[kDevThreads / kWaveDev];
@@ -31,6 +32,7 @@ __device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const Dev
         // every global read of the lookup is in flight at once, before any is used (clamped indices, no
         // branches): the slot state, the layer's row of the slot table, the step's ids and the counters
         const int32_t row = r.slot_of_key[layer * E + min(tid, E - 1)];
+        const int step_v = p.step_dev ? p.step_dev[0] : p.step;
         const int32_t id0 = ids[min(tid, max(n - 1, 0))];
         const unsigned long long sc0 = r.scal[min(tid, kDevScalars - 1)];
         int32_t kv[kDevPerThread];
@@ -54,7 +56,10 @@ __device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const Dev
         if (tid < E) pre[tid] = row;
         if (tid < kDevScalars) scal_sh[tid] = sc0;
         if (tid < MOE_MAX_EXPERTS / 32) present[tid] = 0u;
-        if (tid == 0) bad_sh = 0;
+        if (tid == 0) {
+            bad_sh = 0;
+            step_sh = step_v;
+        }
         __syncthreads();
         for (int i = tid; i < n; i += kDevThreads) {
             const int e = i == tid ? id0 : ids[i];  // steps of more than one block of ids read the rest here
@@ -96,7 +101,7 @@ __device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const Dev
         n_ev = scal_sh[kScalEvents];
     }
     auto log = [&](int e, int kind, int s, int victim) {
-        if (n_ev < (unsigned long long)r.cap_events) r.events[n_ev] = moe_cache_event{p.step, layer, e, kind, s, victim};
+        if (n_ev < (unsigned long long)r.cap_events) r.events[n_ev] = moe_cache_event{step_sh, layer, e, kind, s, victim};
         ++n_ev;
     };
     auto place = [&](int e, int s) {  // lane 0: the new entry (layer, e) takes slot s

@@ -57,7 +57,14 @@ __global__ __launch_bounds__(kDevThreads) void dev_fill_kernel(const long long *
     }
 }
 
+__global__ void set_int_kernel(int *p, int v) { *p = v; }
+
 }  // namespace
+
+hipError_t launch_set_int(int *p, int v, hipStream_t s) {
+    set_int_kernel<<<1, 1, 0, s>>>(p, v);
+    return hipGetLastError();
+}
 
 hipError_t launch_dev_lookup(const DevResidency &r, const DevLookup &p, const int32_t *ids, int n, int32_t *slots_out,
                              int *err, hipStream_t s) {

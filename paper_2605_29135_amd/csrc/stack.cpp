@@ -25,6 +25,14 @@ struct Snapshot {
     uint64_t stamp = 0;         // token counter when stored
 };
 
+// The buffers a captured decode graph was recorded with (a replay needs the same ones).
+struct GraphKey {
+    const float *x = nullptr, *bias = nullptr;
+    const int32_t *ids = nullptr;
+    const float *w = nullptr;
+    bool operator==(const GraphKey &o) const { return x == o.x && bias == o.bias && ids == o.ids && w == o.w; }
+};
+
 struct LastLayer {
     bool valid = false;
     int T = 0, layer = 0;
@@ -51,6 +59,9 @@ struct moe_stack {
     int32_t *ids_host = nullptr;  // pinned [Tmax x k]
     int32_t *slots_host = nullptr; // [Tmax x k] slot of each id after the lookup
     int32_t *dev_slots = nullptr;  // device [L x max_tokens x k]: slot of each id after each layer's device lookup
+    int *dev_step = nullptr;       // device: step tag of a replayed decode graph's decisions
+    hipGraphExec_t graph_exec = nullptr;  // one-token decode step captured for replay (device residency)
+    GraphKey graph_key;
     void *ws = nullptr;
     size_t ws_bytes = 0;
     void *pws = nullptr;        // prefill workspace (max_prefill_tokens > 0)
@@ -176,6 +187,8 @@ int moe_stack_destroy(moe_stack *s) {
     if (s->scratch_x) (void)hipFree(s->scratch_x);
     if (s->scratch_y) (void)hipFree(s->scratch_y);
     if (s->dev_slots) (void)hipFree(s->dev_slots);
+    if (s->dev_step) (void)hipFree(s->dev_step);
+    if (s->graph_exec) (void)hipGraphExecDestroy(s->graph_exec);
     delete s;
     return MOE_OK;
 }
@@ -234,7 +247,8 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
     if ((e = hipHostMalloc(&s->ids_host, sizeof(int32_t) * T * d->k, 0)) != hipSuccess) return bail(e, "stack buffers");
     s->slots_host = new int32_t[size_t(T) * d->k];
     if (moe::cache_device(d->cache) &&
-        (e = hipMalloc(&s->dev_slots, sizeof(int32_t) * size_t(d->n_layers) * d->max_tokens * d->k)) != hipSuccess)
+        ((e = hipMalloc(&s->dev_slots, sizeof(int32_t) * size_t(d->n_layers) * d->max_tokens * d->k)) != hipSuccess ||
+         (e = hipMalloc(&s->dev_step, sizeof(int))) != hipSuccess))
         return bail(e, "stack buffers");
     s->last.assign(d->n_layers, LastLayer{});
     s->demand.assign(size_t(d->n_layers) * d->E, 0u);
@@ -261,12 +275,14 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
     return MOE_OK;
 }
 
-int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *logit_bias,
-                          int32_t *ids_out, float *weights_out, void *stream) {
-    if (!s || !x) return moe::fail(MOE_ERR_INVALID_ARG, "stack step: NULL argument");
-    if (T < 1 || T > s->d.max_tokens)
-        return moe::fail(MOE_ERR_INVALID_ARG, "stack step: T=%d outside [1, %d]", T, s->d.max_tokens);
-    auto strm = static_cast<hipStream_t>(stream);
+}  // extern "C"
+
+namespace {
+// The work of one decode step, enqueued on `strm`.  With step_dev (device-resident
+// cache, one token: nothing waits for the host) the decisions take their step tag
+// from device memory, so that the enqueued work can be captured once and replayed.
+int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_bias, int32_t *ids_out,
+                   float *weights_out, hipStream_t strm, const int *step_dev) {
     int *eflags = moe::device_error_flags();
     if (!eflags) return moe::fail(MOE_ERR_HIP, "device error flags unavailable");
     const auto &d = s->d;
@@ -290,7 +306,7 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: routing");
         if (fused) {
             int st = moe::cache_topk_lookup(d.cache, step, l, s->logits, d.k, ids, w,
-                                            s->dev_slots + size_t(l) * d.max_tokens * d.k, eflags, strm);
+                                            s->dev_slots + size_t(l) * d.max_tokens * d.k, eflags, strm, step_dev);
             if (st != MOE_OK) return st;
         } else if (dev_lookup) {
             int st = expert_cache_lookup_device(d.cache, step, l, ids, T * d.k,
@@ -347,6 +363,62 @@ int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *
         store_snapshot(s);
         s->recalled = -1;
     }
+    moe::clear_error();
+    return MOE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *logit_bias,
+                          int32_t *ids_out, float *weights_out, void *stream) {
+    if (!s || !x) return moe::fail(MOE_ERR_INVALID_ARG, "stack step: NULL argument");
+    if (T < 1 || T > s->d.max_tokens)
+        return moe::fail(MOE_ERR_INVALID_ARG, "stack step: T=%d outside [1, %d]", T, s->d.max_tokens);
+    return enqueue_decode(s, step, x, T, logit_bias, ids_out, weights_out, static_cast<hipStream_t>(stream), nullptr);
+}
+
+int moe_stack_decode_graph(moe_stack *s, int step, float *x, const float *logit_bias, int32_t *ids_out,
+                           float *weights_out, void *stream) {
+    if (!s || !x) return moe::fail(MOE_ERR_INVALID_ARG, "stack step: NULL argument");
+    auto strm = static_cast<hipStream_t>(stream);
+    if (!s->budgeted || !moe::cache_device(s->d.cache))  // the step waits for the host: no graph
+        return enqueue_decode(s, step, x, 1, logit_bias, ids_out, weights_out, strm, nullptr);
+    const GraphKey key{x, logit_bias, ids_out, weights_out};
+    hipError_t e = hipSuccess;
+    if (!s->graph_exec || !(s->graph_key == key)) {
+        if (s->graph_exec) (void)hipGraphExecDestroy(s->graph_exec);
+        s->graph_exec = nullptr;
+        // capture on a private stream ordered after the caller's work; nothing is executed while capturing
+        hipStream_t cs = nullptr;
+        hipEvent_t ev = nullptr;
+        hipGraph_t g = nullptr;
+        e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
+        if (e == hipSuccess) e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+        if (e == hipSuccess) e = hipEventRecord(ev, strm);
+        if (e == hipSuccess) e = hipStreamWaitEvent(cs, ev, 0);
+        int st = MOE_OK;
+        if (e == hipSuccess) e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
+        if (e == hipSuccess) {
+            st = enqueue_decode(s, step, x, 1, logit_bias, ids_out, weights_out, cs, s->dev_step);
+            hipError_t e2 = hipStreamEndCapture(cs, &g);
+            if (e == hipSuccess) e = e2;
+        }
+        if (e == hipSuccess && st == MOE_OK) e = hipGraphInstantiate(&s->graph_exec, g, nullptr, nullptr, 0);
+        if (g) (void)hipGraphDestroy(g);
+        if (ev) (void)hipEventDestroy(ev);
+        if (cs) (void)hipStreamDestroy(cs);
+        if (st != MOE_OK) return st;
+        if (e != hipSuccess) {
+            s->graph_exec = nullptr;
+            return moe::fail_hip(e, "stack graph: capture");
+        }
+        s->graph_key = key;
+    }
+    e = moe::launch_set_int(s->dev_step, step, strm);
+    if (e == hipSuccess) e = hipGraphLaunch(s->graph_exec, strm);
+    if (e != hipSuccess) return moe::fail_hip(e, "stack graph: replay");
     moe::clear_error();
     return MOE_OK;
 }

@@ -256,7 +256,7 @@ def _pinned_store(wl, layers_alias=False):
 
 
 def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=None, T=1, charge_max=None,
-                        recall=0, recall_overlap=0, device=False):
+                        recall=0, recall_overlap=0, device=False, graph=False):
     """Decode `steps` steps through the stack; check events exactly and outputs within tolerance.  With
     charge_max the slots use the rotary policy (else LRU); with recall the stack recalls prior slot sets."""
     buf = _pinned_store(wl, layers_alias)
@@ -274,13 +274,24 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
     o = oracle.LRU(capacity, wl.L, wl.E) if charge_max is None else oracle.Rotary(capacity, wl.L, wl.E, charge_max)
     check_steps = set(range(steps) if check_steps is None else check_steps)
     host_layers = {}
+    if graph:  # a replayed graph reads and writes the same buffers every step
+        x_buf = torch.empty((T, wl.H), dtype=torch.float32, device=DEV)
+        b_buf = torch.empty((wl.L, T, wl.E), dtype=torch.float32, device=DEV)
+        ids_buf = torch.empty((wl.L, T, wl.k), dtype=torch.int32, device=DEV)
+        w_buf = torch.empty((wl.L, T, wl.k), dtype=torch.float32, device=DEV)
     for t in range(steps):
         x0 = synth.hidden_states(wl, t, T=T)
         bias = np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)])
-        x = dev(x0)
-        ids = torch.empty((wl.L, T, wl.k), dtype=torch.int32, device=DEV)
-        w = torch.empty((wl.L, T, wl.k), dtype=torch.float32, device=DEV)
-        stack.decode_step(t, x, dev(bias), ids, w)
+        if graph:
+            x, ids, w = x_buf, ids_buf, w_buf
+            x.copy_(dev(x0))
+            b_buf.copy_(dev(bias))
+            stack.decode_graph(t, x, b_buf, ids, w)
+        else:
+            x = dev(x0)
+            ids = torch.empty((wl.L, T, wl.k), dtype=torch.int32, device=DEV)
+            w = torch.empty((wl.L, T, wl.k), dtype=torch.float32, device=DEV)
+            stack.decode_step(t, x, dev(bias), ids, w)
         moe.moe_sync_check()
         g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
         calls = dict(rec.step(t, [g_ids[l].reshape(-1) for l in range(wl.L)])[1]) if rec else {}
@@ -318,13 +329,56 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
     return s
 
 
-@pytest.mark.parametrize("device,charge_max", [(False, None), (True, None), (True, 3)])
-def test_budgeted_stack_small_evicting(device, charge_max):
-    """With device=True every lookup is a kernel (no host round trip); the decisions are the same."""
+@pytest.mark.parametrize("device,charge_max,graph", [(False, None, False), (True, None, False), (True, 3, False),
+                                                    (True, None, True), (True, 2, True)])
+def test_budgeted_stack_small_evicting(device, charge_max, graph):
+    """With device=True every lookup is a kernel (no host round trip); with graph=True each step is a replay
+    of one captured graph.  The decisions are the same, and every replay is checked."""
     wl = synth.Workload("small stack", H=512, E=32, k=4, I=256, L=4, dtype=synth.BF16, routing="zipf_overlap",
                         cfg_id=97)
-    s = run_stack_and_check(wl, steps=40, capacity=24, device=device, charge_max=charge_max)
+    s = run_stack_and_check(wl, steps=40, capacity=24, device=device, charge_max=charge_max, graph=graph)
     assert s["evictions"] > 0
+
+
+def test_decode_graph_replays_equal_eager_steps():
+    """Twin stacks on twin device caches: graph replays against eager steps, bit for bit, with eager work and
+    synchronisations between the replays."""
+    wl = synth.Workload("graph stack", H=2048, E=64, k=8, I=256, L=3, dtype=synth.INT4G128, shared=True,
+                        routing="zipf_overlap", cfg_id=95)
+    eb, cap = wl.expert_bytes, 30
+    buf = _pinned_store(wl)
+    routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
+    shared = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)]
+    caches = [moe.ExpertCache(wl.L, wl.E, eb, (cap + wl.L) * eb, buf.ptr, wl.E * eb, eb, reserved_bytes=wl.L * eb,
+                              device=True) for _ in range(2)]
+    stacks = [moe.MoeStack(c, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shared) for c in caches]
+    sets = synth.routing_sets(wl, steps=12)
+    x_buf = torch.empty((1, wl.H), dtype=torch.float32, device=DEV)
+    b_buf = torch.empty((wl.L, 1, wl.E), dtype=torch.float32, device=DEV)
+    ids_buf = torch.empty((wl.L, 1, wl.k), dtype=torch.int32, device=DEV)
+    w_buf = torch.empty((wl.L, 1, wl.k), dtype=torch.float32, device=DEV)
+    for t in range(12):
+        x0 = dev(synth.hidden_states(wl, t))
+        bias = dev(np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)]))
+        xe = x0.clone()
+        ids_e = torch.empty_like(ids_buf)
+        w_e = torch.empty_like(w_buf)
+        stacks[0].decode_step(t, xe, bias, ids_e, w_e)
+        torch.cuda.synchronize()
+        x_buf.copy_(x0)
+        b_buf.copy_(bias)
+        stacks[1].decode_graph(t, x_buf, b_buf, ids_buf, w_buf)
+        moe.moe_sync_check()
+        assert torch.equal(x_buf, xe) and torch.equal(ids_buf, ids_e) and torch.equal(w_buf, w_e), t
+    ev0, ev1 = caches[0].trace(), caches[1].trace()
+    assert len(ev0) == len(ev1) > 0 and (ev0.view(np.int32) == ev1.view(np.int32)).all()
+    for which in range(4):
+        assert stacks[1].kernel_time(which, 3) > 0
+    moe.moe_sync_check()
+    for s_, c in zip(stacks, caches):
+        s_.close()
+        c.close()
+    buf.close()
 
 
 @pytest.mark.parametrize("charge_max", [0, 3])
