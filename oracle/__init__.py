@@ -1,8 +1,9 @@
 """CPU oracle for the MoE decode step under an expert budget -- TEST INFRASTRUCTURE.
 
 Only the tests, ``__graft_entry__.smoke()`` and the benchmark's CPU-baseline
-leg may import this package.  The arithmetic lives in ``moe_oracle.c`` (plain
-C, fp64); this module builds it with gcc and marshals numpy arrays into it.
+leg may import this package.  The arithmetic lives in ``moe_oracle.c`` and
+``attention_oracle.c`` (plain C, fp64); this module builds them with gcc and
+marshals numpy arrays into them.
 It shares no code with the HIP library.
 """
 from __future__ import annotations
@@ -15,6 +16,7 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "moe_oracle.c")
+_SRCS = [_SRC, os.path.join(_HERE, "attention_oracle.c")]
 _LIB = os.path.join(_HERE, "libmoe_oracle.so")
 
 F32, BF16, INT4G128 = 0, 1, 2
@@ -29,7 +31,7 @@ def build() -> str:
     """Compile ``libmoe_oracle.so`` (gcc -O2, OpenMP over output rows)."""
     tmp = _LIB + ".tmp"
     subprocess.run(["gcc", "-std=c11", "-O2", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Wextra",
-                    "-o", tmp, _SRC, "-lm"], check=True)
+                    "-o", tmp, *_SRCS, "-lm"], check=True)
     os.replace(tmp, _LIB)
     return _LIB
 
@@ -40,7 +42,7 @@ _lib = None
 def lib() -> C.CDLL:
     global _lib
     if _lib is None:
-        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        if not os.path.exists(_LIB) or os.path.getmtime(_LIB) < max(os.path.getmtime(f) for f in _SRCS):
             build()
         _lib = C.CDLL(_LIB)
         P, I32, SZ, D = C.c_void_p, C.c_int, C.c_size_t, C.POINTER(C.c_double)
@@ -56,6 +58,10 @@ def lib() -> C.CDLL:
         _lib.oracle_lru_new.argtypes = [I32, I32, I32, I32]
         _lib.oracle_lru_new.restype = P
         _lib.oracle_rotary_new.argtypes = [I32, I32, I32, I32, I32]
+        _lib.oracle_rope.argtypes = [P, I32, I32, C.c_double]
+        _lib.oracle_rope.restype = None
+        _lib.oracle_attention_decode.argtypes = [P, I32, I32, I32, I32, P, P, P, P, I32, I32, C.c_double,
+                                                 C.c_double, P]
         _lib.oracle_rotary_new.restype = P
         _lib.oracle_lru_free.argtypes = [P]
         _lib.oracle_lru_lookup.argtypes = [P, I32, I32, P, I32, I32]
@@ -266,6 +272,36 @@ def replay_decode(cache, token_sets, recall: Recall | None = None):
                 cache.lookup(t, l + 1, calls[l + 1], prefetch=True)
     return cache
 
+
+ROPE_THETA = 1.0e6
+
+
+def rope(v: np.ndarray, p: int, theta: float = ROPE_THETA) -> np.ndarray:
+    """Rotary position embedding (rotate-half form) of fp64 head vector(s) ``v [..., d]`` at position p."""
+    out = np.array(v, dtype=np.float64, copy=True)
+    flat = out.reshape(-1, out.shape[-1])
+    for row in flat:
+        lib().oracle_rope(_p(row), row.size, p, theta)
+    return flat.reshape(out.shape)
+
+
+def attention_decode(x, w_qkv, w_o, k_cache, v_cache, p: int, n_heads: int, n_kv: int,
+                     theta: float = ROPE_THETA, eps: float = RMS_EPS) -> np.ndarray:
+    """x + Attn(rmsnorm(x)) for one token at position p; k_cache / v_cache (bf16 bits, uint16
+    [n_kv x max_pos x head_dim]) hold positions < p and receive position p in place.  Returns fp64 [H]."""
+    x = _c(np.asarray(x).reshape(-1), np.float32)
+    H = x.size
+    n_kv_, max_pos, d = k_cache.shape
+    assert n_kv_ == n_kv and v_cache.shape == k_cache.shape
+    assert k_cache.flags.c_contiguous and v_cache.flags.c_contiguous and k_cache.dtype == np.uint16
+    wq = _c(w_qkv, np.uint16)
+    wo = _c(w_o, np.uint16)
+    y = np.empty(H, np.float64)
+    st = lib().oracle_attention_decode(_p(x), H, n_heads, n_kv, d, _p(wq), _p(wo), _p(k_cache), _p(v_cache),
+                                       max_pos, p, theta, eps, _p(y))
+    if st != OK:
+        raise ValueError(f"oracle_attention_decode status {st}")
+    return y
 
 def opt_misses(steps, n_keys: int, capacity: int) -> int:
     """Fewest fills any replacement policy needs for `steps` (a list of arrays of distinct keys, each step's

@@ -629,6 +629,101 @@ def test_recall_prefetch_of_a_recurring_context_turns_misses_into_prefetch_hits(
         assert cache.occupancy() <= C
 
 
+# ------------------------------------------------------ decoder attention ---
+def _bf16(a):
+    return synth.bf16_bits(np.asarray(a, np.float32))
+
+
+def _f(bits):
+    return synth.bf16_to_f32(np.asarray(bits, np.uint16)).astype(np.float64)
+
+
+def test_golden_rope_4d_and_properties():
+    g = {ln[0]: [float(v) for v in ln[1:]] for ln in _golden_lines("rope_4d.txt")}
+    out = oracle.rope(np.array(g["v"]), int(g["p"][0]), g["theta"][0])
+    assert np.allclose(out, g["rotated"], rtol=0, atol=1e-12)
+    rng = np.random.default_rng(3)
+    q, k = rng.standard_normal(128), rng.standard_normal(128)
+    assert np.array_equal(oracle.rope(q, 0), q)                                        # position 0: identity
+    assert abs(np.linalg.norm(oracle.rope(q, 777)) - np.linalg.norm(q)) < 1e-9        # a rotation
+    a = oracle.rope(q, 40) @ oracle.rope(k, 13)
+    b = oracle.rope(q, 1040) @ oracle.rope(k, 1013)                                   # only m - n matters
+    assert abs(a - b) < 1e-8
+
+
+def _attn_weights(H, n_heads, n_kv, d, wq=None, wk=None, wv=None, wo=None, seed=0):
+    rng = np.random.default_rng(seed)
+    rnd = lambda r, c: rng.standard_normal((r, c)) * 0.05
+    wq = rnd(n_heads * d, H) if wq is None else wq
+    wk = rnd(n_kv * d, H) if wk is None else wk
+    wv = rnd(n_kv * d, H) if wv is None else wv
+    wo = rnd(H, n_heads * d) if wo is None else wo
+    return _bf16(np.vstack([wq, wk, wv])), _bf16(wo)
+
+
+def test_attention_single_position_returns_the_value_heads():
+    H, n_heads, n_kv, d = 64, 4, 2, 16
+    wqkv, wo = _attn_weights(H, n_heads, n_kv, d)
+    x = np.random.default_rng(1).standard_normal(H).astype(np.float32)
+    kc = np.zeros((n_kv, 8, d), np.uint16)
+    vc = np.zeros_like(kc)
+    y = oracle.attention_decode(x, wqkv, wo, kc, vc, 0, n_heads, n_kv)
+    h = oracle.rmsnorm(x)[0]
+    v = _f(_bf16(_f(wqkv[(n_heads + n_kv) * d:]) @ h)).reshape(n_kv, d)   # bf16 as the cache holds it
+    att = np.concatenate([v[j // (n_heads // n_kv)] for j in range(n_heads)])
+    assert np.allclose(y, x + _f(wo) @ att, rtol=0, atol=1e-9)
+    assert np.array_equal(vc[:, 0], _bf16(v.astype(np.float32)))
+
+
+def test_attention_zero_query_attends_uniformly():
+    H, n_heads, n_kv, d, p = 32, 2, 1, 16, 5
+    wqkv, wo = _attn_weights(H, n_heads, n_kv, d, wq=np.zeros((n_heads * d, H)))
+    rng = np.random.default_rng(2)
+    kc = _bf16(rng.standard_normal((n_kv, 8, d)))
+    vc = _bf16(rng.standard_normal((n_kv, 8, d)))
+    x = rng.standard_normal(H).astype(np.float32)
+    y = oracle.attention_decode(x, wqkv, wo, kc, vc, p, n_heads, n_kv)
+    mean_v = _f(vc[0, :p + 1]).mean(axis=0)     # positions 0..p, the new value included
+    assert np.allclose(y, x + _f(wo) @ np.concatenate([mean_v, mean_v]), rtol=0, atol=1e-9)
+
+
+def test_attention_two_positions_closed_form():
+    """One head, d = 8, position 1: q = rope(rmsnorm(e0-ish)) makes the score of cached key alpha e0 equal to
+    alpha cos(1) (up to the norms' eps), the new key and value are zero: y = x + beta sigma(score) 1.  Fixes the
+    1/sqrt(d) scale, the rotation angle and pairing, the query norm, the softmax over both positions, W_o and
+    the residual."""
+    d = H = 8
+    alpha, beta, eps = 2.0, 0.5, 1e-6
+    wqkv, wo = _attn_weights(H, 1, 1, d, wq=np.eye(d), wk=np.zeros((d, H)), wv=np.zeros((d, H)), wo=np.eye(H))
+    kc = np.zeros((1, 4, d), np.uint16)
+    vc = np.zeros_like(kc)
+    kc[0, 0] = _bf16(alpha * np.eye(d)[0])
+    vc[0, 0] = _bf16(np.full(d, beta))
+    x = (3.0 * np.eye(d)[0]).astype(np.float32)
+    y = oracle.attention_decode(x, wqkv, wo, kc, vc, 1, 1, 1, theta=500.0, eps=eps)
+    h0 = 3.0 / np.sqrt(9.0 / d + eps)                 # rmsnorm(x)[0]
+    q0 = h0 / np.sqrt(h0 * h0 / d + eps)              # the query head's own norm
+    score = q0 * np.cos(1.0) * alpha / np.sqrt(d)     # dims (0, 4) turned by 1 rad at position 1
+    w0 = 1.0 / (1.0 + np.exp(-score))                 # softmax over (score, 0)
+    assert np.allclose(y, x + beta * w0 * np.ones(d), rtol=0, atol=1e-7)
+
+
+def test_attention_query_groups_share_their_key_value_head():
+    n_heads, n_kv, d, p = 4, 2, 4, 3
+    H = n_heads * d
+    z = np.zeros((n_heads * d, H))
+    wqkv, wo = _attn_weights(H, n_heads, n_kv, d, wq=z, wk=np.zeros((n_kv * d, H)), wv=np.zeros((n_kv * d, H)),
+                             wo=np.eye(H))
+    kc = np.zeros((n_kv, 4, d), np.uint16)
+    vc = np.zeros_like(kc)
+    vc[0, :p] = _bf16(np.ones(d))
+    vc[1, :p] = _bf16(np.full(d, 2.0))
+    x = np.random.default_rng(4).standard_normal(H).astype(np.float32)
+    y = oracle.attention_decode(x, wqkv, wo, kc, vc, p, n_heads, n_kv)
+    # uniform over 4 positions, the new value zero: heads 0, 1 read kv head 0, heads 2, 3 kv head 1
+    assert np.allclose(y - x, np.r_[np.full(2 * d, 0.75), np.full(2 * d, 1.5)], rtol=0, atol=1e-12)
+
+
 # ------------------------------------------------------------ OPT bound ---
 def _golden_kv(name):
     kv = {}
