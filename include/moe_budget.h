@@ -185,6 +185,39 @@ MOE_API int moe_combine(const float *y_partial, const float *weights, const floa
                 int H, float *y_out, int flags, void *stream);
 
 /* ======================================================================= */
+/* Decoder self-attention of one decode token (the block before each MoE)   */
+/* ======================================================================= */
+
+/* Device workspace bytes moe_attention_decode needs. */
+MOE_API size_t moe_attention_workspace_bytes(int n_heads, int n_kv, int head_dim, int max_pos);
+
+/* x <- x + W_o Attn(rmsnorm(x)) for one token at position p, in place on x
+ * (device fp32 [H]).  The paper runs its model with a 4096-token context and
+ * attention on the accelerator (sec. 6) but describes no attention arithmetic;
+ * this is a Qwen3-class reading: unit-gain RMS pre-norm (eps 1e-6);
+ * [q; k; v] = W_qkv h with n_heads query heads and n_kv key/value heads of
+ * head_dim each (query head j reads key/value head j / (n_heads / n_kv));
+ * every query and key head RMS-normalised (unit gain, eps 1e-6), then rotated
+ * by the rotary embedding of the rotate-half form (dims i and i + head_dim/2
+ * turned by p * theta^(-2i/head_dim)); the key and value stored at position p
+ * of the bf16 caches (round to nearest even); softmax(q . k / sqrt(head_dim))
+ * over positions 0..p; the heads' outputs concatenated through W_o.
+ *   w_qkv    device bf16 [(n_heads + 2 n_kv) head_dim x H]: query rows, key rows, value rows
+ *   w_o      device bf16 [H x n_heads head_dim]
+ *   k_cache  device bf16 [n_kv][head_dim / 8][max_pos][8] (8-dim pieces of each position's key, position-
+ *            contiguous, so that 64 positions of a piece are one 1 KiB read)
+ *   v_cache  device bf16 [n_kv][max_pos][head_dim]
+ *            positions < p are read, position p is written
+ *   workspace device, >= moe_attention_workspace_bytes(...), 16-byte aligned
+ * Needs H a multiple of 128, n_heads * head_dim a multiple of 128, head_dim a
+ * multiple of 8 up to 128, n_heads / n_kv <= 16, 0 <= p < max_pos, theta > 1;
+ * MOE_ERR_INVALID_ARG otherwise. */
+MOE_API int moe_attention_decode(float *x, int H, int n_heads, int n_kv, int head_dim, const void *w_qkv,
+                                 const void *w_o, void *k_cache, void *v_cache, int max_pos, int p, float theta,
+                                 void *workspace, size_t workspace_bytes, void *stream);
+
+
+/* ======================================================================= */
 /* Expert residency: slot table in HBM, misses filled from pinned host      */
 /* memory (paper Fig. 1: host tier, slot group, lookup table sub-module id  */
 /* -> slot, selective load, evict; sec. 4: LRU as the conventional policy,  */

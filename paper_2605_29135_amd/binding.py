@@ -77,6 +77,7 @@ def lib() -> C.CDLL:
             "moe_ffn_workspace_bytes": [I, I, I],
             "moe_expert_ffn_grouped": [P, I, I, I, I, I, P, P, P, P, SZ, I, P, P, P, SZ, I, P],
             "moe_combine": [P, P, P, I, I, I, P, I, P],
+            "moe_attention_decode": [P, I, I, I, I, P, P, P, P, I, I, C.c_float, P, SZ, P],
             "moe_prefill_workspace_bytes": [I, I, I, I, I],
             "moe_prefill_grouped": [P, I, I, I, I, I, P, P, P, P, SZ, I, P, P, P, SZ, I, P],
             "expert_cache_create": [C.POINTER(CacheDesc), C.POINTER(P)],
@@ -249,6 +250,40 @@ def moe_hbm_read_probe(buf, sink, stream=None):
     nbytes = buf.numel() * buf.element_size()
     _check(lib().moe_hbm_read_probe(_dev(buf, "buf"), nbytes, _dev(sink, "sink", torch.float32), _stream(stream)),
            "moe_hbm_read_probe")
+
+
+def moe_attention_workspace_bytes(n_heads: int, n_kv: int, head_dim: int, max_pos: int) -> int:
+    return int(lib().moe_attention_workspace_bytes(n_heads, n_kv, head_dim, max_pos))
+
+
+def key_cache_layout(k_plain: np.ndarray) -> np.ndarray:
+    """[n_kv, max_pos, d] keys -> the library's key-cache layout [n_kv, d/8, max_pos, 8]."""
+    n_kv, max_pos, d = k_plain.shape
+    return np.ascontiguousarray(k_plain.reshape(n_kv, max_pos, d // 8, 8).transpose(0, 2, 1, 3))
+
+
+def key_cache_plain(k_lib: np.ndarray) -> np.ndarray:
+    """Inverse of key_cache_layout: [n_kv, d/8, max_pos, 8] -> [n_kv, max_pos, d]."""
+    n_kv, dc, max_pos, _ = k_lib.shape
+    return np.ascontiguousarray(k_lib.transpose(0, 2, 1, 3)).reshape(n_kv, max_pos, dc * 8)
+
+
+def moe_attention_decode(x, w_qkv, w_o, k_cache, v_cache, p: int, n_heads: int, n_kv: int, theta: float = 1.0e6,
+                         workspace=None, stream=None):
+    """x <- x + W_o Attn(rmsnorm(x)) at position p, in place on the device fp32 tensor x [H].  k_cache
+    (bf16/int16 [n_kv, d/8, max_pos, 8]) and v_cache ([n_kv, max_pos, d]) receive position p."""
+    import torch
+    H = x.numel()
+    n_kv_, max_pos, d = v_cache.shape
+    nws = moe_attention_workspace_bytes(n_heads, n_kv, d, max_pos)
+    if workspace is None:
+        workspace = torch.empty(max(nws, 256), dtype=torch.uint8, device=x.device)
+    _check(lib().moe_attention_decode(_dev(x, "x", torch.float32), H, n_heads, n_kv, d, _dev(w_qkv, "w_qkv"),
+                                      _dev(w_o, "w_o"), _dev(k_cache, "k_cache"), _dev(v_cache, "v_cache"), max_pos,
+                                      p, theta, _dev(workspace, "workspace"),
+                                      workspace.numel() * workspace.element_size(), _stream(stream)),
+           "moe_attention_decode")
+    return x
 
 
 def moe_combine(y_partial, weights, y_shared=None, y_out=None, accumulate: bool = False, stream=None):

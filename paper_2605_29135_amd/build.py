@@ -9,7 +9,8 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libmoe_budget.so")
-SOURCES = ["kernels.hip", "prefill.hip", "residency.cpp", "residency_dev.hip", "capi.cpp", "stack.cpp", "analysis.cpp"]
+SOURCES = ["kernels.hip", "prefill.hip", "attention.hip", "residency.cpp", "residency_dev.hip", "capi.cpp", "stack.cpp",
+           "analysis.cpp"]
 
 # Packed fp32 ops stay off: the compiler would otherwise form v_pk_* fp32 ops
 # from scalar float code.  Hidden visibility exports only the MOE_API entry points.

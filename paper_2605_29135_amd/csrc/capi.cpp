@@ -210,6 +210,33 @@ int moe_combine(const float *y_partial, const float *weights, const float *y_sha
                          "combine launch");
 }
 
+size_t moe_attention_workspace_bytes(int n_heads, int n_kv, int head_dim, int max_pos) {
+    if (n_heads < 1 || n_kv < 1 || head_dim < 1 || max_pos < 1) return 0;
+    return moe::attention_workspace_bytes(n_heads, n_kv, head_dim, max_pos);
+}
+
+int moe_attention_decode(float *x, int H, int n_heads, int n_kv, int head_dim, const void *w_qkv, const void *w_o,
+                         void *k_cache, void *v_cache, int max_pos, int p, float theta, void *workspace,
+                         size_t workspace_bytes, void *stream) {
+    if (!x || !w_qkv || !w_o || !k_cache || !v_cache || !workspace)
+        return fail(MOE_ERR_INVALID_ARG, "attention: NULL pointer");
+    if (!moe::attention_shape_supported(H, n_heads, n_kv, head_dim, max_pos))
+        return fail(MOE_ERR_INVALID_ARG, "attention: unsupported shape (H %d, heads %d/%d, head_dim %d, max_pos %d)", H,
+                    n_heads, n_kv, head_dim, max_pos);
+    if (p < 0 || p >= max_pos) return fail(MOE_ERR_INVALID_ARG, "attention: position %d outside [0, %d)", p, max_pos);
+    if (!(theta > 1.f)) return fail(MOE_ERR_INVALID_ARG, "attention: rotary base must exceed 1");
+    if (!aligned16(x) || !aligned16(w_qkv) || !aligned16(w_o) || !aligned16(k_cache) || !aligned16(v_cache) ||
+        !aligned16(workspace))
+        return fail(MOE_ERR_INVALID_ARG, "attention: buffers must be 16-byte aligned");
+    if (workspace_bytes < moe::attention_workspace_bytes(n_heads, n_kv, head_dim, max_pos))
+        return fail(MOE_ERR_INVALID_ARG, "attention: workspace of %zu bytes, need %zu", workspace_bytes,
+                    moe::attention_workspace_bytes(n_heads, n_kv, head_dim, max_pos));
+    return finish_launch(moe::launch_attention_decode(x, H, n_heads, n_kv, head_dim, w_qkv, w_o,
+                                                      static_cast<uint16_t *>(k_cache), static_cast<uint16_t *>(v_cache),
+                                                      max_pos, p, theta, workspace, static_cast<hipStream_t>(stream)),
+                         "attention launch");
+}
+
 int moe_hbm_read_probe(const void *buf, size_t bytes, float *sink, void *stream) {
     if (!buf || !sink) return fail(MOE_ERR_INVALID_ARG, "hbm read probe: NULL pointer");
     if (bytes % 16 || reinterpret_cast<uintptr_t>(buf) % 16)

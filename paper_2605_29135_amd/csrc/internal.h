@@ -132,6 +132,13 @@ hipError_t launch_prefill_ffn(const float *x, int T, int H, int I, int E, int k,
                               int dtype, const void *shared_w, float *y, bool accumulate, const PrefillWorkspace &ws,
                               int *err_flags, hipStream_t s);
 
+// Decoder self-attention of one decode token (attention.hip).
+bool attention_shape_supported(int H, int n_heads, int n_kv, int head_dim, int max_pos);
+size_t attention_workspace_bytes(int n_heads, int n_kv, int head_dim, int max_pos);
+hipError_t launch_attention_decode(float *x, int H, int n_heads, int n_kv, int head_dim, const void *w_qkv,
+                                   const void *w_o, uint16_t *k_cache, uint16_t *v_cache, int max_pos, int p,
+                                   float theta, void *workspace, hipStream_t s);
+
 bool ffn_shape_supported(int H, int I, int dtype);
 bool router_shape_supported(int H, int dtype);
 

@@ -172,12 +172,13 @@ __global__ __launch_bounds__(kBlock) void topk_lookup_kernel(const float *__rest
 // h_t = x_t / sqrt(mean(x_t^2) + eps); one wave per (token, expert row).  Each
 // wave holds the whole token row (one 16-byte column chunk per lane and
 // pass), so it forms the norm itself; wave 0 of the token's first block
-// stores h_t for the expert FFN.
+// stores h_t for the expert FFN.  The same GEMV serves the attention block's
+// projections; `bias` may be `logits` itself (an in-place residual add: each
+// element is read and then written by the same lane).
 template <int DT, int NCH, bool NORM>
 __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__restrict__ x,
                                                                const uint8_t *__restrict__ w, int H,
-                                                               int E, const float *__restrict__ bias,
-                                                               float *__restrict__ logits,
+                                                               int E, const float *bias, float *logits,
                                                                float *__restrict__ h_out) {
     constexpr int EPC = Fmt<DT>::EPC;
     const int lane = threadIdx.x & (kWave - 1);

@@ -819,3 +819,75 @@ def test_stack_decode_with_prefetch():
     stack.close()
     cache.close()
     buf.close()
+
+
+# ------------------------------------------------------------- decoder attention ---
+# bf16 weights and caches, fp32 arithmetic: the attention block's output (x + W_o Attn) is compared as its
+# increment over x, normwise against the fp64 oracle.
+ATTN_TOL = 1e-2
+
+
+def _attn_case(H, n_heads, n_kv, d, max_pos, seed):
+    rng = np.random.default_rng(seed)
+    bf = lambda a: synth.bf16_bits(np.asarray(a, np.float32))
+    wqkv = bf(rng.standard_normal(((n_heads + 2 * n_kv) * d, H)) * 0.02)
+    wo = bf(rng.standard_normal((H, n_heads * d)) * 0.02)
+    kc = bf(rng.standard_normal((n_kv, max_pos, d)))    # unit-RMS keys, as normalised heads are
+    vc = bf(rng.standard_normal((n_kv, max_pos, d)))
+    x = rng.standard_normal(H).astype(np.float32)
+    return wqkv, wo, kc, vc, x
+
+
+def _i16(a):  # bf16 bits as a torch-friendly int16 device tensor
+    return dev(np.ascontiguousarray(a).view(np.int16))
+
+
+@pytest.mark.parametrize("H,nh,nkv,d,max_pos,p", [(256, 4, 2, 64, 300, 0), (256, 4, 2, 64, 300, 1),
+                                                  (256, 4, 2, 64, 300, 63), (256, 4, 2, 64, 300, 64),
+                                                  (256, 4, 2, 64, 300, 65), (256, 8, 1, 32, 300, 299),
+                                                  (512, 8, 2, 128, 256, 200), (2048, 32, 4, 128, 4096, 4095)])
+def test_attention_decode_parity(H, nh, nkv, d, max_pos, p):
+    wqkv, wo, kc, vc, x = _attn_case(H, nh, nkv, d, max_pos, seed=H + p)
+    kc_o, vc_o = kc.copy(), vc.copy()
+    y_ref = oracle.attention_decode(x, wqkv, wo, kc_o, vc_o, p, nh, nkv)
+    xd, kd, vd = dev(x), _i16(moe.key_cache_layout(kc)), _i16(vc)
+    moe.moe_attention_decode(xd, _i16(wqkv), _i16(wo), kd, vd, p, nh, nkv)
+    moe.moe_sync_check()
+    got = xd.cpu().numpy().astype(np.float64)
+    assert normwise(got - x, y_ref - x) <= ATTN_TOL
+    k_gpu = moe.key_cache_plain(kd.cpu().numpy().view(np.uint16))
+    v_gpu = vd.cpu().numpy().view(np.uint16)
+    others = np.arange(max_pos) != p
+    assert np.array_equal(k_gpu[:, others], kc[:, others]) and np.array_equal(v_gpu[:, others], vc[:, others])
+    f = lambda b: synth.bf16_to_f32(b).astype(np.float64)
+    assert np.abs(f(k_gpu[:, p]) - f(kc_o[:, p])).max() <= 1e-2 * max(1.0, np.abs(f(kc_o[:, p])).max())
+    assert np.abs(f(v_gpu[:, p]) - f(vc_o[:, p])).max() <= 1e-2 * max(1.0, np.abs(f(vc_o[:, p])).max())
+
+
+def test_attention_decode_sequence_appends_across_chunks():
+    """70 tokens from an empty cache (the 64-position chunk boundary crossed), GPU and oracle each keeping
+    their own caches; every step's output compared."""
+    H, nh, nkv, d, max_pos = 256, 4, 1, 64, 96
+    wqkv, wo, _, _, _ = _attn_case(H, nh, nkv, d, max_pos, seed=11)
+    kc_o = np.zeros((nkv, max_pos, d), np.uint16)
+    vc_o = np.zeros_like(kc_o)
+    kd, vd = _i16(moe.key_cache_layout(kc_o)), _i16(vc_o)
+    wq_d, wo_d = _i16(wqkv), _i16(wo)
+    rng = np.random.default_rng(12)
+    for p in range(70):
+        x = rng.standard_normal(H).astype(np.float32)
+        y_ref = oracle.attention_decode(x, wqkv, wo, kc_o, vc_o, p, nh, nkv)
+        xd = dev(x)
+        moe.moe_attention_decode(xd, wq_d, wo_d, kd, vd, p, nh, nkv)
+        moe.moe_sync_check()
+        assert normwise(xd.cpu().numpy().astype(np.float64) - x, y_ref - x) <= ATTN_TOL, p
+
+
+def test_attention_decode_rejects_bad_arguments():
+    H, nh, nkv, d, max_pos = 256, 4, 2, 64, 32
+    wqkv, wo, kc, vc, x = _attn_case(H, nh, nkv, d, max_pos, seed=5)
+    args = (_i16(wqkv), _i16(wo), _i16(moe.key_cache_layout(kc)), _i16(vc))
+    for p, nh_, nkv_ in ((max_pos, nh, nkv), (-1, nh, nkv), (0, 4, 3), (0, 40, 2)):
+        with pytest.raises(moe.MoeError) as ei:
+            moe.moe_attention_decode(dev(x), *args, p, nh_, nkv_)
+        assert ei.value.code == -1
