@@ -351,6 +351,18 @@ MOE_API int expert_cache_trace(moe_cache *c, size_t first, moe_cache_event *buf,
 
 typedef struct moe_stack moe_stack;
 
+/* A decoder self-attention block before each MoE block (moe_attention_decode),
+ * in place of the identity. */
+typedef struct {
+    int n_heads, n_kv, head_dim, max_pos;
+    float theta;                    /* rotary base */
+    int start_pos;                  /* position of the first decode step (caches hold 0..start_pos-1) */
+    const void *const *w_qkv;       /* host array [L] of device bf16 [(n_heads + 2 n_kv) head_dim x H] */
+    const void *const *w_o;         /* host array [L] of device bf16 [H x n_heads head_dim] */
+    void *const *k_cache;           /* host array [L] of device key caches, layout of moe_attention_decode */
+    void *const *v_cache;           /* host array [L] of device value caches */
+} moe_attention_desc;
+
 typedef struct {
     int n_layers, H, I, E, k;
     int w_dtype;                    /* expert storage type */
@@ -374,6 +386,10 @@ typedef struct {
                                        a token its snapshot replaces one with the same signature, else the
                                        oldest.  0 = off; at most 4096 */
     int recall_overlap;             /* 1..k shared layer-0 experts a recall needs (0 means k) */
+    const moe_attention_desc *attention; /* NULL: attention is the identity.  Otherwise each layer is
+                                       x <- x + Attn(rmsnorm(x)) then the MoE block; one-token steps only,
+                                       the position advancing by one per step from start_pos; copied at
+                                       creation (the arrays, not the device buffers they point to) */
 } moe_stack_desc;
 
 MOE_API int moe_stack_create(const moe_stack_desc *desc, moe_stack **out);
@@ -414,7 +430,9 @@ MOE_API int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *
 
 /* Mean device time (ms) of one launch of kernel `which` (0 = router logits and
  * top-k, 1 = expert gate/up + SwiGLU, 2 = expert down + combine, 3 = the whole
- * expert FFN as the decode step issues it, both launches).  Each
+ * expert FFN as the decode step issues it, both launches; 4 = the attention
+ * block, its five launches, at the last step's position -- this rewrites the
+ * caches' entries of that position).  Each
  * layer's launch of the last decode step is re-issued with the same
  * arguments, in step order, captured into one HIP graph on a private stream
  * (ordered after `stream`); the graph is replayed n times between two HIP

@@ -52,12 +52,18 @@ EVENT_DTYPE = np.dtype([("t", "<i4"), ("layer", "<i4"), ("expert", "<i4"),
                         ("kind", "<i4"), ("slot", "<i4"), ("victim_key", "<i4")])
 
 
+class AttentionDesc(C.Structure):
+    _fields_ = [("n_heads", C.c_int), ("n_kv", C.c_int), ("head_dim", C.c_int), ("max_pos", C.c_int),
+                ("theta", C.c_float), ("start_pos", C.c_int), ("w_qkv", C.POINTER(C.c_void_p)),
+                ("w_o", C.POINTER(C.c_void_p)), ("k_cache", C.POINTER(C.c_void_p)), ("v_cache", C.POINTER(C.c_void_p))]
+
+
 class StackDesc(C.Structure):
     _fields_ = [("n_layers", C.c_int), ("H", C.c_int), ("I", C.c_int), ("E", C.c_int), ("k", C.c_int),
                 ("w_dtype", C.c_int), ("router_dtype", C.c_int), ("router_w", C.POINTER(C.c_void_p)),
                 ("shared_w", C.POINTER(C.c_void_p)), ("cache", C.c_void_p), ("max_tokens", C.c_int),
                 ("max_prefill_tokens", C.c_int), ("prefetch", C.c_int), ("recall", C.c_int),
-                ("recall_overlap", C.c_int)]
+                ("recall_overlap", C.c_int), ("attention", C.POINTER(AttentionDesc))]
 
 
 _lib = None
@@ -384,16 +390,26 @@ class MoeStack:
 
     def __init__(self, cache: ExpertCache, H: int, I: int, E: int, k: int, w_dtype: int, router_dtype: int,
                  router_w: list, shared_w: list | None = None, max_tokens: int = 1, max_prefill_tokens: int = 0,
-                 prefetch: int = 0, recall: int = 0, recall_overlap: int = 0):
+                 prefetch: int = 0, recall: int = 0, recall_overlap: int = 0, attention: dict | None = None):
         self._router = (C.c_void_p * len(router_w))(*[_dev(w, "router_w") for w in router_w])
         self._shared = None
         if shared_w is not None:
             self._shared = (C.c_void_p * len(shared_w))(*[_dev(w, "shared_w") for w in shared_w])
         self._keep = (router_w, shared_w, cache)
+        att = None
+        if attention is not None:  # dict: n_heads, n_kv, head_dim, max_pos, theta, start_pos, w_qkv, w_o, k_cache, v_cache
+            arr = lambda ts, nm: (C.c_void_p * len(ts))(*[_dev(t, nm) for t in ts])
+            self._att_arrays = [arr(attention[nm], nm) for nm in ("w_qkv", "w_o", "k_cache", "v_cache")]
+            att = AttentionDesc(attention["n_heads"], attention["n_kv"], attention["head_dim"], attention["max_pos"],
+                                attention.get("theta", 1.0e6), attention.get("start_pos", 0),
+                                *[C.cast(a, C.POINTER(C.c_void_p)) for a in self._att_arrays])
+            self._att = att
+            self._keep = self._keep + (attention,)
         d = StackDesc(len(router_w), H, I, E, k, w_dtype, router_dtype,
                       C.cast(self._router, C.POINTER(C.c_void_p)),
                       C.cast(self._shared, C.POINTER(C.c_void_p)) if self._shared is not None else None,
-                      cache.handle, max_tokens, max_prefill_tokens, prefetch, recall, recall_overlap)
+                      cache.handle, max_tokens, max_prefill_tokens, prefetch, recall, recall_overlap,
+                      C.pointer(att) if att is not None else None)
         h = C.c_void_p()
         _check(lib().moe_stack_create(C.byref(d), C.byref(h)), "moe_stack_create")
         self._h = h

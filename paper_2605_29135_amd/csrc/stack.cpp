@@ -60,6 +60,13 @@ struct moe_stack {
     int32_t *slots_host = nullptr; // [Tmax x k] slot of each id after the lookup
     int32_t *dev_slots = nullptr;  // device [L x max_tokens x k]: slot of each id after each layer's device lookup
     int *dev_step = nullptr;       // device: step tag of a replayed decode graph's decisions
+    bool attn = false;             // a self-attention block before each MoE block
+    moe_attention_desc ad{};       // its shapes (the arrays below hold its per-layer buffers)
+    std::vector<const void *> a_wqkv, a_wo;
+    std::vector<void *> a_k, a_v;
+    void *attn_ws = nullptr;
+    int attn_pos = 0;              // position of the next decode step
+    int last_attn_pos = -1;        // position of the last one
     hipGraphExec_t graph_exec = nullptr;  // one-token decode step captured for replay (device residency)
     GraphKey graph_key;
     void *ws = nullptr;
@@ -188,6 +195,7 @@ int moe_stack_destroy(moe_stack *s) {
     if (s->scratch_y) (void)hipFree(s->scratch_y);
     if (s->dev_slots) (void)hipFree(s->dev_slots);
     if (s->dev_step) (void)hipFree(s->dev_step);
+    if (s->attn_ws) (void)hipFree(s->attn_ws);
     if (s->graph_exec) (void)hipGraphExecDestroy(s->graph_exec);
     delete s;
     return MOE_OK;
@@ -208,6 +216,16 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: recall must be in [0, 4096], recall_overlap in [0, k]");
     if (d->cache && moe::cache_device(d->cache) && (d->prefetch > 0 || d->recall > 0))
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefetch and recall need host lookups (not MOE_CACHE_DEVICE)");
+    if (const moe_attention_desc *a = d->attention) {
+        if (!moe::attention_shape_supported(d->H, a->n_heads, a->n_kv, a->head_dim, a->max_pos) || !(a->theta > 1.f) ||
+            a->start_pos < 0 || a->start_pos >= a->max_pos || !a->w_qkv || !a->w_o || !a->k_cache || !a->v_cache)
+            return moe::fail(MOE_ERR_INVALID_ARG, "stack: unsupported attention block");
+        for (int l = 0; l < d->n_layers; ++l)
+            if (!a->w_qkv[l] || !a->w_o[l] || !a->k_cache[l] || !a->v_cache[l])
+                return moe::fail(MOE_ERR_INVALID_ARG, "stack: attention buffers of layer %d missing", l);
+        if (d->max_prefill_tokens > 0 || d->max_tokens != 1)
+            return moe::fail(MOE_ERR_INVALID_ARG, "stack: an attention block decodes one token per step (no prefill)");
+    }
     if (d->max_prefill_tokens > 0 && !moe::prefill_dtype_supported(d->w_dtype))
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefill needs MOE_BF16 or MOE_INT4G128 experts");
     if (!moe::ffn_shape_supported(d->H, d->I, d->w_dtype) || !moe::router_shape_supported(d->H, d->router_dtype))
@@ -250,6 +268,23 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
         ((e = hipMalloc(&s->dev_slots, sizeof(int32_t) * size_t(d->n_layers) * d->max_tokens * d->k)) != hipSuccess ||
          (e = hipMalloc(&s->dev_step, sizeof(int))) != hipSuccess))
         return bail(e, "stack buffers");
+    if (const moe_attention_desc *a = d->attention) {
+        s->attn = true;
+        s->ad = *a;
+        for (int l = 0; l < d->n_layers; ++l) {
+            s->a_wqkv.push_back(a->w_qkv[l]);
+            s->a_wo.push_back(a->w_o[l]);
+            s->a_k.push_back(a->k_cache[l]);
+            s->a_v.push_back(a->v_cache[l]);
+        }
+        s->ad.w_qkv = s->ad.w_o = nullptr;
+        s->ad.k_cache = s->ad.v_cache = nullptr;
+        s->attn_pos = a->start_pos;
+        if ((e = hipMalloc(&s->attn_ws, moe::attention_workspace_bytes(a->n_heads, a->n_kv, a->head_dim, a->max_pos))) !=
+            hipSuccess)
+            return bail(e, "stack attention workspace");
+    }
+    s->d.attention = nullptr;  // the caller's descriptor need not outlive the call
     s->last.assign(d->n_layers, LastLayer{});
     s->demand.assign(size_t(d->n_layers) * d->E, 0u);
     s->cur_sets.assign(size_t(d->n_layers) * d->k, 0);
@@ -288,7 +323,17 @@ int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_b
     const auto &d = s->d;
     const moe::FfnWorkspace ws = moe::ffn_workspace(s->ws, T, d.k, d.I);
     s->recalled = -1;
+    if (s->attn && (T != 1 || s->attn_pos >= s->ad.max_pos))
+        return moe::fail(MOE_ERR_INVALID_ARG, T != 1 ? "stack step: an attention block decodes one token per step"
+                                                     : "stack step: the attention caches are full");
     for (int l = 0; l < d.n_layers; ++l) {
+        if (s->attn) {
+            hipError_t ea = moe::launch_attention_decode(x, d.H, s->ad.n_heads, s->ad.n_kv, s->ad.head_dim,
+                                                         s->a_wqkv[l], s->a_wo[l], static_cast<uint16_t *>(s->a_k[l]),
+                                                         static_cast<uint16_t *>(s->a_v[l]), s->ad.max_pos,
+                                                         s->attn_pos, s->ad.theta, s->attn_ws, strm);
+            if (ea != hipSuccess) return moe::fail_hip(ea, "stack step: attention");
+        }
         int32_t *ids = ids_out ? ids_out + size_t(l) * T * d.k : s->ids;
         float *w = weights_out ? weights_out + size_t(l) * T * d.k : s->weights;
         const float *bias = logit_bias ? logit_bias + size_t(l) * T * d.E : nullptr;
@@ -363,6 +408,7 @@ int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_b
         store_snapshot(s);
         s->recalled = -1;
     }
+    if (s->attn) s->last_attn_pos = s->attn_pos++;
     moe::clear_error();
     return MOE_OK;
 }
@@ -383,7 +429,7 @@ int moe_stack_decode_graph(moe_stack *s, int step, float *x, const float *logit_
                            float *weights_out, void *stream) {
     if (!s || !x) return moe::fail(MOE_ERR_INVALID_ARG, "stack step: NULL argument");
     auto strm = static_cast<hipStream_t>(stream);
-    if (!s->budgeted || !moe::cache_device(s->d.cache))  // the step waits for the host: no graph
+    if (!s->budgeted || !moe::cache_device(s->d.cache) || s->attn)  // host waits, or a moving position: no graph
         return enqueue_decode(s, step, x, 1, logit_bias, ids_out, weights_out, strm, nullptr);
     const GraphKey key{x, logit_bias, ids_out, weights_out};
     hipError_t e = hipSuccess;
@@ -471,8 +517,10 @@ int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out,
 }
 
 int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *mean_ms) {
-    if (!s || !mean_ms || which < 0 || which > 3 || n < 1)
+    if (!s || !mean_ms || which < 0 || which > 4 || n < 1)
         return moe::fail(MOE_ERR_INVALID_ARG, "kernel_time: bad argument");
+    if (which == 4 && (!s->attn || s->last_attn_pos < 0))
+        return moe::fail(MOE_ERR_INVALID_ARG, "kernel_time: no attention block, or no decode step yet");
     for (const LastLayer &ll : s->last)
         if (!ll.valid) return moe::fail(MOE_ERR_INVALID_ARG, "kernel_time: no decode step has run yet");
     auto strm = static_cast<hipStream_t>(stream);
@@ -515,6 +563,11 @@ int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *
     if (e == hipSuccess) e = hipStreamWaitEvent(cs, a, 0);
     auto enqueue = [&](const LastLayer &ll) -> hipError_t {
         const int l = ll.layer;
+        if (which == 4)
+            return moe::launch_attention_decode(s->scratch_x, d.H, s->ad.n_heads, s->ad.n_kv, s->ad.head_dim,
+                                                s->a_wqkv[l], s->a_wo[l], static_cast<uint16_t *>(s->a_k[l]),
+                                                static_cast<uint16_t *>(s->a_v[l]), s->ad.max_pos, s->last_attn_pos,
+                                                s->ad.theta, s->attn_ws, cs);
         if (which == 0) {
             hipError_t r = moe::launch_router_logits(s->scratch_x, s->router_w[l], d.router_dtype, T, d.H, d.E, nullptr,
                                                      s->logits, true, s->scratch_y, cs);

@@ -891,3 +891,58 @@ def test_attention_decode_rejects_bad_arguments():
         with pytest.raises(moe.MoeError) as ei:
             moe.moe_attention_decode(dev(x), *args, p, nh_, nkv_)
         assert ei.value.code == -1
+
+
+def test_stack_with_attention_blocks_matches_oracle_chain():
+    """Each layer x <- x + Attn(rmsnorm(x)), then the MoE block, over a budgeted device cache; the oracle
+    chain (its own caches, the GPU's routing) token by token."""
+    wl = synth.Workload("attn stack", H=256, E=16, k=2, I=128, L=3, dtype=synth.BF16, routing="zipf_overlap",
+                        cfg_id=94)
+    nh, nkv, d, max_pos, start = 4, 2, 64, 40, 20
+    eb, cap = wl.expert_bytes, 10
+    buf = _pinned_store(wl)
+    cache = moe.ExpertCache(wl.L, wl.E, eb, cap * eb, buf.ptr, wl.E * eb, eb, device=True)
+    routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
+    blocks = [_attn_case(wl.H, nh, nkv, d, max_pos, seed=300 + l) for l in range(wl.L)]
+    kc_o = [b[2].copy() for b in blocks]
+    vc_o = [b[3].copy() for b in blocks]
+    att = dict(n_heads=nh, n_kv=nkv, head_dim=d, max_pos=max_pos, theta=1.0e6, start_pos=start,
+               w_qkv=[_i16(b[0]) for b in blocks], w_o=[_i16(b[1]) for b in blocks],
+               k_cache=[_i16(moe.key_cache_layout(b[2])) for b in blocks], v_cache=[_i16(b[3]) for b in blocks])
+    stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, None, attention=att)
+    sets = synth.routing_sets(wl, steps=6)
+    experts = [synth.layer_experts(wl, l) for l in range(wl.L)]
+    for t in range(6):
+        x0 = synth.hidden_states(wl, t)
+        bias = np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)])
+        x = dev(x0)
+        ids = torch.empty((wl.L, 1, wl.k), dtype=torch.int32, device=DEV)
+        w = torch.empty((wl.L, 1, wl.k), dtype=torch.float32, device=DEV)
+        stack.decode_step(t, x, dev(bias), ids, w)
+        moe.moe_sync_check()
+        g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
+        xr = x0.astype(np.float64).reshape(-1)
+        for l in range(wl.L):
+            assert (np.sort(g_ids[l], axis=1) == sets[t, l]).all()
+            xr = oracle.attention_decode(xr.astype(np.float32), blocks[l][0], blocks[l][1], kc_o[l], vc_o[l],
+                                         start + t, nh, nkv)
+            hr = oracle.rmsnorm(xr.astype(np.float32)).astype(np.float32)
+            xr = xr + oracle.moe_ffn(hr, g_ids[l], g_w[l], experts[l], wl.H, wl.I, wl.dtype)[0]
+        assert normwise(x.cpu().numpy().reshape(-1) - x0.reshape(-1), xr - x0.reshape(-1)) <= ATTN_TOL, t
+    assert stack.kernel_time(4, 2) > 0
+    moe.moe_sync_check()
+    with pytest.raises(moe.MoeError):  # two tokens in one step
+        stack.decode_step(6, dev(np.zeros((2, wl.H), np.float32)))
+    stack.close()
+    with pytest.raises(moe.MoeError):  # prefill with an attention block
+        moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, None, attention=att,
+                     max_prefill_tokens=16)
+    full = dict(att, start_pos=max_pos - 1)
+    stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, None, attention=full)
+    stack.decode_step(100, dev(synth.hidden_states(wl, 7)))
+    moe.moe_sync_check()
+    with pytest.raises(moe.MoeError):  # the caches are full
+        stack.decode_step(101, dev(synth.hidden_states(wl, 8)))
+    stack.close()
+    cache.close()
+    buf.close()
