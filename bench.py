@@ -53,6 +53,11 @@ def parse():
                     help="where the slot table's decisions are made: lookup kernels (the default: no host round "
                          "trip), or the host after each layer's ids reach it (needed by --prefetch / --recall); "
                          "the decisions are the same")
+    ap.add_argument("--attention", action="store_true",
+                    help="config 4 shapes with a decoder self-attention block before each MoE block (32 query / 4 "
+                         "key-value heads of 128, bf16 KV cache of --context positions; the timed tokens are the "
+                         "cache's last positions)")
+    ap.add_argument("--context", type=int, default=4096, help="attention: positions of the KV cache")
     ap.add_argument("--graph", action="store_true",
                     help="with device residency, replay each token as one captured HIP graph "
                          "(moe_stack_decode_graph) instead of enqueueing its launches")
@@ -271,8 +276,20 @@ def residency_bound(moe, cache, E, capacity, step_bytes_per_token=None, policy="
     return out
 
 
-def cpu_baseline(wl, store, steps, bias_np, x_np, budget_s, shared=None):
-    """The oracle on the host cores: whole tokens through every layer, no budget."""
+def attention_kernel_line(att, H, ms, n_steps):
+    """The attention block's time per layer (its five launches at the last decode position) and the bytes it
+    must move: the QKV and output projection weights, and the keys and values of every position it reads."""
+    nh, nkv, hd = att["n_heads"], att["n_kv"], att["head_dim"]
+    n_pos = att["start_pos"] + n_steps
+    w_bytes = 2 * ((nh + 2 * nkv) * hd * H + H * nh * hd)
+    kv_bytes = 2 * 2 * n_pos * nkv * hd
+    return {"attention_us": ms * 1e3, "attention_bytes_per_layer": w_bytes + kv_bytes,
+            "attention_GBps": (w_bytes + kv_bytes) / (ms * 1e-3) / 1e9, "attention_positions": n_pos}
+
+
+def cpu_baseline(wl, store, steps, bias_np, x_np, budget_s, shared=None, attention=None):
+    """The oracle on the host cores: whole tokens through every layer, no budget.  attention(l, t, x) -> x,
+    when given, is each layer's attention block before its MoE block."""
     import oracle
     import synth
     routers = [synth.router_weights(wl, l) for l in range(wl.L)]
@@ -281,6 +298,8 @@ def cpu_baseline(wl, store, steps, bias_np, x_np, budget_s, shared=None):
     for i, t in enumerate(steps):
         x = x_np[t].astype(np.float64)
         for l in range(wl.L):
+            if attention is not None:
+                x = attention(l, t, x)
             h = oracle.rmsnorm(x.astype(np.float32)).astype(np.float32)
             z = oracle.router_logits(h, routers[l], wl.router_dtype) + bias_np[t, l]
             ids, w, _ = oracle.topk_softmax(z.astype(np.float32), wl.k)
@@ -534,9 +553,28 @@ def main():
     cache = moe.ExpertCache(L, E, eb, budget, buf.ptr, 0 if alias else E * eb, eb, reserved_bytes=reserved,
                             preload=not budgeted, policy=POLICIES[args.policy], charge_max=args.charge_max,
                             device=budgeted and args.residency == "device")
+    att = None
+    if args.attention:
+        # synthetic, seeded: N(0, 0.02) projection weights, an N(0, 1) cache prefix; the timed tokens take the
+        # cache's last positions
+        nh, nkv, hd, max_pos = 32, 4, 128, args.context
+        start = max_pos - n_steps
+        if start < 0:
+            raise SystemExit(f"--context {max_pos} is shorter than the {n_steps} decode steps")
+        gen = torch.Generator(device=dev)
+        att = dict(n_heads=nh, n_kv=nkv, head_dim=hd, max_pos=max_pos, theta=1.0e6, start_pos=start,
+                   w_qkv=[], w_o=[], k_cache=[], v_cache=[])
+        for l in range(L):
+            gen.manual_seed(7000 + l)
+            rnd = lambda *shape, sd=1.0: (torch.randn(*shape, generator=gen, device=dev) * sd).to(torch.bfloat16)
+            att["w_qkv"].append(rnd((nh + 2 * nkv) * hd, H, sd=0.02).view(torch.int16))
+            att["w_o"].append(rnd(H, nh * hd, sd=0.02).view(torch.int16))
+            att["k_cache"].append(rnd(nkv, hd // 8, max_pos, 8).view(torch.int16))
+            att["v_cache"].append(rnd(nkv, max_pos, hd).view(torch.int16))
+        torch.cuda.synchronize()
     stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T,
                          prefetch=args.prefetch if budgeted else 0, recall=args.recall if budgeted else 0,
-                         recall_overlap=args.recall_overlap)
+                         recall_overlap=args.recall_overlap, attention=att)
     t_setup = time.perf_counter() - t_setup
 
     stream = torch.cuda.current_stream()
@@ -559,8 +597,17 @@ def main():
     elapsed = time.perf_counter() - t0
     moe.moe_sync_check(stream)
     st1 = cache.stats()
+    # the oracle leg's copy of the attention state, taken before the attention timing rewrites the last position
+    att_host = None
+    if att is not None:
+        att_host = dict(wq=[t.cpu().numpy().view(np.uint16) for t in att["w_qkv"]],
+                        wo=[t.cpu().numpy().view(np.uint16) for t in att["w_o"]],
+                        kc=[moe.key_cache_plain(t.cpu().numpy().view(np.uint16)) for t in att["k_cache"]],
+                        vc=[t.cpu().numpy().view(np.uint16) for t in att["v_cache"]])
     # per-launch device time: each kernel of the last layer re-launched back to back between two events
     ktimes = {name: stack.kernel_time(w, args.replays) for w, name in enumerate(["route", "gateup", "down", "ffn"])}
+    if att is not None:
+        ktimes["attention"] = stack.kernel_time(4, args.replays)
     moe.moe_sync_check(stream)
 
     tok_s = args.steps * T / elapsed
@@ -597,9 +644,14 @@ def main():
 
     # ---- oracle on the host cores (bounded sample of the timed tokens), with a parity check
     sample = list(range(args.warmup, n_steps))
+    att_hook = None
+    if att_host is not None:
+        att_hook = lambda l, t, x: oracle.attention_decode(x.astype(np.float32), att_host["wq"][l], att_host["wo"][l],
+                                                           att_host["kc"][l], att_host["vc"][l], att["start_pos"] + t,
+                                                           att["n_heads"], att["n_kv"], theta=att["theta"])
     cpu_tps, outs, cpu_dt = cpu_baseline(wl, lambda l: store[0 if alias else l], sample, bias_np
                                          if bias_np is not None else np.zeros((n_steps, L, T, E), np.float32),
-                                         x_np, args.cpu_seconds)
+                                         x_np, args.cpu_seconds, attention=att_hook)
     gpu_x = xs[sample[0]:sample[0] + len(outs)].cpu().numpy().astype(np.float64)
     err = 0.0
     for i, o in enumerate(outs):
@@ -608,6 +660,10 @@ def main():
         err = max(err, float(np.abs(delta - delta_ref).max() / np.abs(delta_ref).max()))
 
     wl_name = wl.name if T == 1 else f"{wl.name} (T={T})"
+    if att is not None:
+        wl_name = (f"{wl_name}; with a decoder self-attention block per layer ({att['n_heads']}/{att['n_kv']} heads "
+                   f"of {att['head_dim']}, positions {att['start_pos']}..{att['start_pos'] + n_steps - 1} of a "
+                   f"{att['max_pos']}-position bf16 KV cache)")
     out = {
         "metric": METRIC,
         "value": round(tok_s, 3),
@@ -627,7 +683,10 @@ def main():
                    "prefetch_per_layer": args.prefetch if budgeted else 0, "policy": args.policy,
                    "residency": args.residency if budgeted else "preloaded", "decode_graph": use_graph,
                    **({"charge_max": args.charge_max} if args.policy == "rotary" else {}),
-                   **({"recall": args.recall, "recall_overlap": args.recall_overlap or k} if args.recall else {})},
+                   **({"recall": args.recall, "recall_overlap": args.recall_overlap or k} if args.recall else {}),
+                   **({"attention": {"n_heads": att["n_heads"], "n_kv": att["n_kv"], "head_dim": att["head_dim"],
+                                     "kv_positions": att["max_pos"], "first_position": att["start_pos"]}}
+                      if att is not None else {})},
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU", "achieved": gu_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": gu_gbps / HBM_PEAK_GBPS if gu_gbps else None,
@@ -641,7 +700,8 @@ def main():
         "kernels": {"route_us": rt_ms * 1e3, "gateup_us": gu_ms * 1e3, "down_us": dn_ms * 1e3,
                     "down_GBps": dn_gbps, "down_bytes_per_launch": dn_bytes,
                     "ffn_us": ktimes["ffn"] * 1e3,
-                    "ffn_GBps": (gu_bytes + dn_bytes) / (ktimes["ffn"] * 1e-3) / 1e9 if ktimes["ffn"] else None},
+                    "ffn_GBps": (gu_bytes + dn_bytes) / (ktimes["ffn"] * 1e-3) / 1e9 if ktimes["ffn"] else None,
+                    **(attention_kernel_line(att, H, ktimes["attention"], n_steps) if att is not None else {})},
         "residency": {**d, "miss_rate": d["misses"] / d["lookups"] if d["lookups"] else 0.0,
                       "misses_per_token": d["misses"] / (args.steps * T), "bound": bound},
         "pcie": pcie,

@@ -29,9 +29,9 @@ using dev::kBlock;
 using dev::kWave;
 using dev::wave_sum;
 using dev::BF16;
+using dev::dpp;
 
-constexpr int kAttnChunk = 64;     // positions per wave in the partial kernel
-constexpr int kAttnMaxGroup = 16;  // query heads per key/value head
+constexpr int kAttnChunk = 64;  // positions per block (one partial per query head) in the partial kernel
 
 __device__ __forceinline__ float wave_max(float v) {
 #pragma unroll
@@ -85,118 +85,254 @@ __global__ __launch_bounds__(kBlock) void attn_heads_kernel(float *__restrict__ 
     v_cache[(size_t(g) * max_pos + p) * d + lane + half] = f32_to_bf16_rne(vh[lane + half]);
 }
 
-// Block = 4 waves = 4 chunks of 64 positions of one key/value head g (blockIdx.y).  part layout:
-// [query head][chunk][d + 2] (unnormalised output, then max, then sum).  d is a multiple of 8, at most 128.
-__global__ __launch_bounds__(kBlock) void attn_partial_kernel(const float *__restrict__ q, int n_heads, int n_kv,
-                                                              int d, const uint16_t *__restrict__ k_cache,
-                                                              const uint16_t *__restrict__ v_cache, int max_pos,
-                                                              int n_pos, int n_chunks, float *__restrict__ part) {
-    __shared__ float qs[kAttnMaxGroup * 128];                       // the group's queries
-    __shared__ float prob[kBlock / kWave][kAttnMaxGroup][kAttnChunk];  // per wave: probabilities by head, position
+// Block = one chunk of 64 positions of key/value head g (blockIdx.y), 8 waves of 8 positions.  part layout:
+// [query head][chunk][d + 4] (unnormalised output, then max, then sum; rows padded to 16 bytes).  d is a
+// multiple of 8, at most 128.  Every load of a wave -- its positions' key pieces and their value rows, which
+// do not depend on the scores -- is issued before any is used: one memory round trip per wave.
+constexpr int kAttnWaves = 8;
+constexpr int kAttnBlock = kAttnWaves * kWave;      // threads of a partial block
+constexpr int kPosW = kAttnChunk / kAttnWaves;      // positions per wave
+constexpr int kSlices = kWave / kPosW;              // lanes per position in the scores (dimension slices)
+constexpr int kMaxDC = 16;                          // key pieces of 8 dims per position (d <= 128)
+constexpr int kPPS = kMaxDC / kSlices;              // key pieces per slice
+static_assert(kPosW == 8 && kSlices == 8, "lane layout of the partial kernel");
+
+// Max and sum over the 8 lanes of a half-row (DPP quad swaps and the half-row mirror).
+__device__ __forceinline__ float lanes8_max(float v) {
+    v = fmaxf(v, dpp<0xB1>(v));
+    v = fmaxf(v, dpp<0x4E>(v));
+    return fmaxf(v, dpp<0x141>(v));
+}
+__device__ __forceinline__ float lanes8_sum(float v) {
+    v += dpp<0xB1>(v);
+    v += dpp<0x4E>(v);
+    return v + dpp<0x141>(v);
+}
+
+// GROUP = query heads per key/value head; FULL = (d == 128).  Both compile time, so every loop over heads
+// and key pieces is static.
+//   scores: lane = slice * 8 + position; slice s dots key pieces s and s + 8 (8 dims each) with every query
+//           head of the group (queries read from LDS as float4 broadcasts), then the 8 slices are summed
+//           (row rotation by 8, then two cross-row swaps);
+//   softmax: per head, max and sum over the wave's 8 positions;
+//   output:  lane = dimension pair, the 8 value rows weighted by each head's probabilities (from LDS);
+//   merge:   the 8 waves' (max, sum, output) per head merged through LDS into the chunk's partial, at most
+//            8 heads per pass.
+template <int GROUP, bool FULL>
+__global__ __launch_bounds__(kAttnBlock) void attn_partial_kernel(const float *__restrict__ q, int d_arg,
+                                                                  const uint16_t *__restrict__ k_cache,
+                                                                  const uint16_t *__restrict__ v_cache,
+                                                                  int max_pos, int n_pos, int n_chunks,
+                                                                  float *__restrict__ part) {
+    constexpr int HB = GROUP < 8 ? GROUP : 8;  // heads per merge pass
+    __shared__ float4 qs4[GROUP * 128 / 4];                    // the group's queries, [head][d]
+    __shared__ float4 prob4[kAttnWaves][GROUP][kPosW / 4];     // per wave: probabilities [head][position]
+    __shared__ float wm[kAttnWaves][GROUP], ws[kAttnWaves][GROUP];
+    __shared__ float wo[kAttnWaves][HB][128];
+    float *qs = reinterpret_cast<float *>(qs4);
+    const int d = FULL ? 128 : d_arg, dc = d / 8;
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-    const int g = blockIdx.y, group = n_heads / n_kv;
-    for (int i = threadIdx.x; i < group * d; i += kBlock) qs[i] = q[size_t(g) * group * d + i];
+    const int g = blockIdx.y, chunk = blockIdx.x;
+    const int pl = lane % kPosW, slice = lane / kPosW;
+    const int pos0 = chunk * kAttnChunk + wave * kPosW;
+    const int n_here = max(0, min(kPosW, n_pos - pos0));  // live positions of this wave (wave 0 has >= 1)
+    const bool live = pl < n_here;
+    // 1. all loads, clamped to the last position: keys (lanes = slice, position), values (lanes = dimensions)
+    uint4 kw[kPPS];
+    const uint16_t *kb = k_cache + (size_t(g) * dc * max_pos + min(pos0 + pl, n_pos - 1)) * 8;
+#pragma unroll
+    for (int i = 0; i < kPPS; ++i) {
+        const int c = FULL ? slice + kSlices * i : min(slice + kSlices * i, dc - 1);
+        kw[i] = dev::load16(reinterpret_cast<const uint8_t *>(kb + size_t(c) * max_pos * 8));
+    }
+    const int dim = 2 * lane;
+    const bool dlive = FULL || dim < d;
+    uint32_t vv[kPosW];
+    const uint16_t *vb = v_cache + size_t(g) * max_pos * d + (dlive ? dim : 0);
+#pragma unroll
+    for (int j = 0; j < kPosW; ++j)
+        vv[j] = *reinterpret_cast<const uint32_t *>(vb + size_t(min(pos0 + j, n_pos - 1)) * d);
+    for (int i = threadIdx.x; i < GROUP * d; i += kAttnBlock) qs[i] = q[size_t(g) * GROUP * d + i];
     __syncthreads();
-    const int chunk = blockIdx.x * (kBlock / kWave) + wave;
-    if (chunk >= n_chunks) return;
-    const int pos = chunk * kAttnChunk + lane;
-    const bool live = pos < n_pos;
-    const int pc = live ? pos : n_pos - 1;  // clamped: loads stay in bounds, the score is discarded
-    // scores of this lane's position against every query head of the group
-    float sc[kAttnMaxGroup];
+    // 2. scores
+    float sc[GROUP];
 #pragma unroll
-    for (int h = 0; h < kAttnMaxGroup; ++h) sc[h] = 0.f;
-    const uint16_t *kb = k_cache + (size_t(g) * (d / 8) * max_pos + pc) * 8;
-    for (int c = 0; c < d / 8; ++c) {
-        const uint4 kw4 = dev::load16(reinterpret_cast<const uint8_t *>(kb + size_t(c) * max_pos * 8));
-        const uint32_t kw[4] = {kw4.x, kw4.y, kw4.z, kw4.w};
-        float kv[8];
+    for (int h = 0; h < GROUP; ++h) sc[h] = 0.f;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {  // dims 8c + 2i (low half) and 8c + 2i + 1 (high half)
-            kv[2 * i] = __uint_as_float(kw[i] << 16);
-            kv[2 * i + 1] = __uint_as_float(kw[i] & 0xffff0000u);
-        }
+    for (int i = 0; i < kPPS; ++i) {
+        const int c = slice + kSlices * i;
+        if (FULL || c < dc) {
+            const uint32_t kwv[4] = {kw[i].x, kw[i].y, kw[i].z, kw[i].w};
+            float kv[8];
 #pragma unroll
-        for (int h = 0; h < kAttnMaxGroup; ++h) {
-            if (h < group) {
-                const float *qh = qs + h * d + c * 8;
+            for (int u = 0; u < 4; ++u) {  // dims 8c + 2u (low half) and 8c + 2u + 1 (high half)
+                kv[2 * u] = __uint_as_float(kwv[u] << 16);
+                kv[2 * u + 1] = __uint_as_float(kwv[u] & 0xffff0000u);
+            }
 #pragma unroll
-                for (int i = 0; i < 8; ++i) sc[h] = fmaf(qh[i], kv[i], sc[h]);
+            for (int h = 0; h < GROUP; ++h) {
+                const float4 qa = qs4[(h * d + c * 8) / 4], qb = qs4[(h * d + c * 8) / 4 + 1];
+                float t = sc[h];
+                t = fmaf(qa.x, kv[0], t);
+                t = fmaf(qa.y, kv[1], t);
+                t = fmaf(qa.z, kv[2], t);
+                t = fmaf(qa.w, kv[3], t);
+                t = fmaf(qb.x, kv[4], t);
+                t = fmaf(qb.y, kv[5], t);
+                t = fmaf(qb.z, kv[6], t);
+                sc[h] = fmaf(qb.w, kv[7], t);
             }
         }
     }
+    // 3. softmax over the wave's positions; slice 0's lanes keep the probabilities in LDS
     const float scale = rsqrtf(float(d));
-    float mx[kAttnMaxGroup], sm[kAttnMaxGroup];
+    float mx[GROUP], sm[GROUP];
+    float *pw = reinterpret_cast<float *>(prob4[wave]);
 #pragma unroll
-    for (int h = 0; h < kAttnMaxGroup; ++h) {
-        if (h < group) {
-            const float s = live ? sc[h] * scale : -INFINITY;
-            mx[h] = wave_max(s);
-            const float e = live ? __expf(s - mx[h]) : 0.f;
-            sm[h] = wave_sum(e);
-            prob[wave][h][lane] = e;
-        }
+    for (int h = 0; h < GROUP; ++h) {
+        float t = sc[h];
+        t += dpp<0x128>(t);  // row rotation by 8: slices 2r and 2r + 1
+        t += __shfl_xor(t, 16);
+        t += __shfl_xor(t, 32);
+        const float s = live ? t * scale : -INFINITY;
+        mx[h] = lanes8_max(s);
+        const float e = live ? __expf(s - mx[h]) : 0.f;
+        sm[h] = lanes8_sum(e);
+        if (slice == 0) pw[h * kPosW + pl] = e;
     }
-    // the probabilities are this wave's own (waves past the last chunk have left): a wave-level LDS sync
+    // the probabilities are this wave's own: a wave-level LDS sync
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-    // output: lanes over dimensions (2 per lane), the chunk's value rows weighted by each head's probabilities
-    float o0[kAttnMaxGroup], o1[kAttnMaxGroup];
+    // 4. output: lanes over dimensions (2 per lane); probabilities are 0 past the live positions
+    float o0[GROUP], o1[GROUP];
 #pragma unroll
-    for (int h = 0; h < kAttnMaxGroup; ++h) o0[h] = o1[h] = 0.f;
-    const int dim = 2 * lane;
-    const bool dlive = dim < d;
-    const int n_here = min(kAttnChunk, n_pos - chunk * kAttnChunk);
-    const uint16_t *vb = v_cache + (size_t(g) * max_pos + size_t(chunk) * kAttnChunk) * d + (dlive ? dim : 0);
-    for (int j0 = 0; j0 < n_here; j0 += 8) {
-        uint32_t vv[8];
+    for (int h = 0; h < GROUP; ++h) o0[h] = o1[h] = 0.f;
 #pragma unroll
-        for (int u = 0; u < 8; ++u)  // 8 rows in flight; rows past n_here repeat the last live one (weight 0)
-            vv[u] = *reinterpret_cast<const uint32_t *>(vb + size_t(min(j0 + u, n_here - 1)) * d);
+    for (int j4 = 0; j4 < kPosW / 4; ++j4) {
+        float v0[4], v1[4];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            const float v0 = __uint_as_float(vv[u] << 16), v1 = __uint_as_float(vv[u] & 0xffff0000u);
-            const int j = j0 + u;
+        for (int u = 0; u < 4; ++u) {
+            v0[u] = __uint_as_float(vv[4 * j4 + u] << 16);
+            v1[u] = __uint_as_float(vv[4 * j4 + u] & 0xffff0000u);
+        }
 #pragma unroll
-            for (int h = 0; h < kAttnMaxGroup; ++h) {
-                if (h < group) {
-                    const float pr = j < n_here ? prob[wave][h][j] : 0.f;
-                    o0[h] = fmaf(pr, v0, o0[h]);
-                    o1[h] = fmaf(pr, v1, o1[h]);
-                }
-            }
+        for (int h = 0; h < GROUP; ++h) {
+            const float4 pr = prob4[wave][h][j4];
+            o0[h] = fmaf(pr.w, v0[3], fmaf(pr.z, v0[2], fmaf(pr.y, v0[1], fmaf(pr.x, v0[0], o0[h]))));
+            o1[h] = fmaf(pr.w, v1[3], fmaf(pr.z, v1[2], fmaf(pr.y, v1[1], fmaf(pr.x, v1[0], o1[h]))));
+        }
+    }
+    // 5. merge the 8 waves (a wave with no live position has max -inf, sum 0, output 0)
+    if (lane == 0) {
+#pragma unroll
+        for (int h = 0; h < GROUP; ++h) {
+            wm[wave][h] = mx[h];
+            ws[wave][h] = sm[h];
         }
     }
 #pragma unroll
-    for (int h = 0; h < kAttnMaxGroup; ++h) {
-        if (h < group) {
-            float *pp = part + (size_t(g * group + h) * n_chunks + chunk) * (d + 2);
-            if (dlive) {
-                pp[dim] = o0[h];
-                pp[dim + 1] = o1[h];
-            }
-            if (lane == 0) {
-                pp[d] = mx[h];
-                pp[d + 1] = sm[h];
+    for (int hb = 0; hb < GROUP / HB; ++hb) {
+        if (dlive) {
+#pragma unroll
+            for (int hh = 0; hh < HB; ++hh) {
+                wo[wave][hh][dim] = o0[hb * HB + hh];
+                wo[wave][hh][dim + 1] = o1[hb * HB + hh];
             }
         }
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < HB * d; idx += kAttnBlock) {
+            const int hh = idx / d, i = idx - hh * d, h = hb * HB + hh;
+            float M = wm[0][h];
+#pragma unroll
+            for (int w = 1; w < kAttnWaves; ++w) M = fmaxf(M, wm[w][h]);  // finite: wave 0 has a live position
+            float o = 0.f, S = 0.f;
+#pragma unroll
+            for (int w = 0; w < kAttnWaves; ++w) {
+                const float f = __expf(wm[w][h] - M);
+                o = fmaf(f, wo[w][hh][i], o);
+                S = fmaf(f, ws[w][h], S);
+            }
+            float *pp = part + (size_t(g * GROUP + h) * n_chunks + chunk) * (d + 4);
+            pp[i] = o;
+            if (i == 0) {
+                pp[d] = M;
+                pp[d + 1] = S;
+            }
+        }
+        if (hb + 1 < GROUP / HB) __syncthreads();  // before the next pass overwrites wo
     }
 }
 
-// One block per query head: att[h][i] = sum_c e^(m_c - M) o_c[i] / sum_c e^(m_c - M) s_c.
+// One block per query head: att[h][i] = sum_c e^(m_c - M) o_c[i] / sum_c e^(m_c - M) s_c.  Thread t first
+// issues the loads of its share of the outputs (4 dimensions as one float4, chunks t/32, t/32 + 8, ...),
+// then reads chunk t's max and sum (n_chunks <= kBlock) and the block reduces those to the weights.
+constexpr int kCombineBatch = 8;  // outputs loaded per thread per round trip
 __global__ __launch_bounds__(kBlock) void attn_combine_kernel(const float *__restrict__ part, int d, int n_chunks,
                                                               float *__restrict__ att) {
-    const int h = blockIdx.x;
-    const float *ph = part + size_t(h) * n_chunks * (d + 2);
-    float M = -INFINITY;
-    for (int c = 0; c < n_chunks; ++c) M = fmaxf(M, ph[size_t(c) * (d + 2) + d]);
-    float S = 0.f;
-    for (int c = 0; c < n_chunks; ++c) S += __expf(ph[size_t(c) * (d + 2) + d] - M) * ph[size_t(c) * (d + 2) + d + 1];
-    for (int i = threadIdx.x; i < d; i += kBlock) {
-        float acc = 0.f;
-        for (int c = 0; c < n_chunks; ++c) acc += __expf(ph[size_t(c) * (d + 2) + d] - M) * ph[size_t(c) * (d + 2) + i];
-        att[size_t(h) * d + i] = acc / S;
+    __shared__ float red[kBlock / kWave];
+    __shared__ float wgt[kBlock];
+    __shared__ float4 acc_sh[kBlock / 32][32];
+    const int h = blockIdx.x, tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+    const int stride = d + 4;
+    const float *ph = part + size_t(h) * n_chunks * stride;
+    const int i4 = tid % 32, cs = tid / 32;  // dimensions 4*i4..4*i4+3, chunks cs + 8k
+    const bool ilive = 4 * i4 < d;
+    float4 v[kCombineBatch];
+#pragma unroll
+    for (int k = 0; k < kCombineBatch; ++k) {
+        const int c = cs + (kBlock / 32) * k;
+        v[k] = (ilive && c < n_chunks) ? *reinterpret_cast<const float4 *>(ph + size_t(c) * stride + 4 * i4)
+                                       : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    const bool live = tid < n_chunks;
+    const float m = live ? ph[size_t(tid) * stride + d] : -INFINITY;
+    const float sv = live ? ph[size_t(tid) * stride + d + 1] : 0.f;
+    float M = wave_max(m);
+    if (lane == 0) red[wave] = M;
+    __syncthreads();
+    M = fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3]));
+    __syncthreads();
+    const float e = live ? __expf(m - M) : 0.f;
+    float S = wave_sum(e * sv);
+    if (lane == 0) red[wave] = S;
+    __syncthreads();
+    S = red[0] + red[1] + red[2] + red[3];
+    wgt[tid] = e / S;
+    __syncthreads();
+    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int base = 0;; base += kCombineBatch * (kBlock / 32)) {
+#pragma unroll
+        for (int k = 0; k < kCombineBatch; ++k) {
+            const int c = base + cs + (kBlock / 32) * k;
+            const float w = c < n_chunks ? wgt[c] : 0.f;
+            acc.x = fmaf(w, v[k].x, acc.x);
+            acc.y = fmaf(w, v[k].y, acc.y);
+            acc.z = fmaf(w, v[k].z, acc.z);
+            acc.w = fmaf(w, v[k].w, acc.w);
+        }
+        const int next = base + kCombineBatch * (kBlock / 32);
+        if (next >= n_chunks) break;
+#pragma unroll
+        for (int k = 0; k < kCombineBatch; ++k) {
+            const int c = next + cs + (kBlock / 32) * k;
+            v[k] = (ilive && c < n_chunks) ? *reinterpret_cast<const float4 *>(ph + size_t(c) * stride + 4 * i4)
+                                           : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    }
+    acc_sh[cs][i4] = acc;
+    __syncthreads();
+    if (tid < 32 && ilive) {
+        float4 r = acc_sh[0][tid];
+#pragma unroll
+        for (int k = 1; k < kBlock / 32; ++k) {
+            const float4 t = acc_sh[k][tid];
+            r.x += t.x;
+            r.y += t.y;
+            r.z += t.z;
+            r.w += t.w;
+        }
+        *reinterpret_cast<float4 *>(att + size_t(h) * d + 4 * tid) = r;
     }
 }
 
@@ -205,9 +341,11 @@ __global__ __launch_bounds__(kBlock) void attn_combine_kernel(const float *__res
 using dev::BF16;
 
 bool attention_shape_supported(int H, int n_heads, int n_kv, int d, int max_pos) {
+    const int grp = n_kv > 0 ? n_heads / n_kv : 0;
     return H > 0 && H % 128 == 0 && n_heads > 0 && n_kv > 0 && n_heads % n_kv == 0 &&
-           n_heads / n_kv <= kAttnMaxGroup && d >= 8 && d <= 128 && d % 8 == 0 && (n_heads * d) % 128 == 0 &&
-           max_pos > 0 && ffn_shape_supported(H, 128, BF16) && router_shape_supported(n_heads * d, BF16);
+           (grp == 1 || grp == 2 || grp == 4 || grp == 8 || grp == 16) && d >= 8 && d <= 128 && d % 8 == 0 && (n_heads * d) % 128 == 0 &&
+           max_pos > 0 && max_pos <= kBlock * kAttnChunk && ffn_shape_supported(H, 128, BF16) &&
+           router_shape_supported(n_heads * d, BF16);
 }
 
 static size_t align256a(size_t n) { return (n + 255) & ~size_t(255); }
@@ -215,7 +353,7 @@ static size_t align256a(size_t n) { return (n + 255) & ~size_t(255); }
 size_t attention_workspace_bytes(int n_heads, int n_kv, int d, int max_pos) {
     const size_t chunks = size_t((max_pos + kAttnChunk - 1) / kAttnChunk);
     return align256a(sizeof(float) * size_t(n_heads + 2 * n_kv) * d) + align256a(sizeof(float) * size_t(n_heads) * d) +
-           align256a(sizeof(float) * size_t(n_heads) * chunks * (d + 2));
+           align256a(sizeof(float) * size_t(n_heads) * chunks * (d + 4));
 }
 
 hipError_t launch_attention_decode(float *x, int H, int n_heads, int n_kv, int d, const void *w_qkv, const void *w_o,
@@ -235,8 +373,23 @@ hipError_t launch_attention_decode(float *x, int H, int n_heads, int n_kv, int d
     attn_heads_kernel<<<(n_heads + n_kv + 3) / 4, kBlock, 0, s>>>(qkv, n_heads, n_kv, d, k_cache, v_cache, max_pos, p,
                                                                    theta);
     if ((e = hipGetLastError()) != hipSuccess) return e;
-    attn_partial_kernel<<<dim3((n_chunks + 3) / 4, n_kv), kBlock, 0, s>>>(qkv, n_heads, n_kv, d, k_cache, v_cache,
-                                                                         max_pos, n_pos, n_chunks, part);
+    const dim3 pgrid(n_chunks, n_kv);
+    const bool full = d == 128;
+    switch (n_heads / n_kv) {
+#define ATTN_GROUP(G)                                                                                            \
+    case G:                                                                                                      \
+        if (full)                                                                                                \
+            attn_partial_kernel<G, true>                                                                         \
+                <<<pgrid, kAttnBlock, 0, s>>>(qkv, d, k_cache, v_cache, max_pos, n_pos, n_chunks, part);         \
+        else                                                                                                     \
+            attn_partial_kernel<G, false>                                                                        \
+                <<<pgrid, kAttnBlock, 0, s>>>(qkv, d, k_cache, v_cache, max_pos, n_pos, n_chunks, part);         \
+        break;
+        ATTN_GROUP(1) ATTN_GROUP(2) ATTN_GROUP(4) ATTN_GROUP(8) ATTN_GROUP(16)
+#undef ATTN_GROUP
+    default:
+        return hipErrorInvalidValue;
+    }
     if ((e = hipGetLastError()) != hipSuccess) return e;
     attn_combine_kernel<<<n_heads, kBlock, 0, s>>>(part, d, n_chunks, att);
     if ((e = hipGetLastError()) != hipSuccess) return e;
