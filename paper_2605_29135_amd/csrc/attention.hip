@@ -7,18 +7,17 @@
 // attention over positions 0..p, the output projection added to the residual.
 //
 //   1. QKV projection with the pre-norm: the router GEMV (one wave per row).
-//   2. attn_heads_kernel: one wave per query head and per key head: RMS norm over
-//      the head, rotation of the pairs (i, i + d/2) held by lane i, the query
-//      written back in place, key and value appended to the caches at p.
-//   3. attn_partial_kernel: one wave per (key/value head, 64 positions): lane j
-//      scores position j against every query head of the group (queries read as
-//      LDS broadcasts, keys as one 1 KiB contiguous load per 8 dimensions from
-//      the [d/8][position][8] key layout), per-head max and sum over the wave,
-//      then lanes switch to dimensions for the probability-weighted sum of the
-//      value rows (row-major value layout); partial (max, sum, output) per
-//      (query head, chunk).
-//   4. attn_combine_kernel: per query head, the chunks merged by log-sum-exp.
-//   5. Output projection: the same GEMV with the residual as its bias, in place.
+//   2. attn_partial_kernel: one block per (key/value head, 64 positions), 8 waves
+//      of 8 positions.  The block normalises and rotates its group's queries into
+//      LDS (the block of the last chunk also forms the key and value of p and
+//      appends them to the caches); lanes (dimension slice, position) score the
+//      positions against every query head of the group (queries read as LDS
+//      broadcasts, keys from the [d/8][position][8] layout), per-head max and sum
+//      over the wave's positions, then lanes switch to dimensions for the
+//      probability-weighted sum of the value rows (row-major value layout); the 8
+//      waves merge into one partial (max, sum, output) per (query head, chunk).
+//   3. attn_combine_kernel: per query head, the chunks merged by log-sum-exp.
+//   4. Output projection: the same GEMV with the residual as its bias, in place.
 #include "device_common.h"
 #include "internal.h"
 
@@ -47,45 +46,22 @@ __device__ __forceinline__ uint16_t f32_to_bf16_rne(float f) {
 
 __device__ __forceinline__ float bf16_to_f32(uint16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
-// Waves 0..n_heads-1: query heads (normalised and rotated in place in qkv);
-// waves n_heads..n_heads+n_kv-1: key heads, appended with their value heads.
-__global__ __launch_bounds__(kBlock) void attn_heads_kernel(float *__restrict__ qkv, int n_heads, int n_kv, int d,
-                                                            uint16_t *__restrict__ k_cache,
-                                                            uint16_t *__restrict__ v_cache, int max_pos, int p,
-                                                            float theta) {
-    const int lane = threadIdx.x & (kWave - 1);
-    const int w = blockIdx.x * (kBlock / kWave) + threadIdx.x / kWave;
-    if (w >= n_heads + n_kv) return;
-    const int half = d / 2;
-    float *head = qkv + size_t(w) * d;  // keys follow the queries in qkv
-    const bool on = lane < half;
-    float a = on ? head[lane] : 0.f, b = on ? head[lane + half] : 0.f;
-    const float inv = rsqrtf(wave_sum(a * a + b * b) / float(d) + 1e-6f);
-    a *= inv;
-    b *= inv;
-    // angle p * theta^(-2i/d), reduced in double so that positions up to thousands keep full precision
-    const double ang = double(p) * pow(double(theta), -2.0 * double(lane) / double(d));
+// Rotation of dimension pair (i, i + d/2) at position p: angle p * theta^(-2i/d).  The angle is formed and
+// reduced to [-pi, pi] in double, so thousands of positions keep full single precision in cos and sin.
+__device__ __forceinline__ void rope_cs(int p, int i, int d, float theta, float &c, float &s) {
+    const double inv_freq = exp2(-2.0 * double(i) / double(d) * log2(double(theta)));
+    const double ang = double(p) * inv_freq;
+    constexpr double kTwoPi = 6.283185307179586;
+    const double r = fma(-rint(ang * (1.0 / kTwoPi)), kTwoPi, ang);
     double sd, cd;
-    sincos(ang, &sd, &cd);
-    const float c = float(cd), s = float(sd);
-    const float ra = a * c - b * s, rb = b * c + a * s;
-    if (!on) return;
-    if (w < n_heads) {
-        head[lane] = ra;
-        head[lane + half] = rb;
-        return;
-    }
-    const int g = w - n_heads;
-    const float *vh = qkv + size_t(n_heads + n_kv + g) * d;
-    // key layout [g][d/8][max_pos][8]; value layout [g][max_pos][d]
-    auto kidx = [&](int i) { return ((size_t(g) * (d / 8) + i / 8) * max_pos + p) * 8 + (i % 8); };
-    k_cache[kidx(lane)] = f32_to_bf16_rne(ra);
-    k_cache[kidx(lane + half)] = f32_to_bf16_rne(rb);
-    v_cache[(size_t(g) * max_pos + p) * d + lane] = f32_to_bf16_rne(vh[lane]);
-    v_cache[(size_t(g) * max_pos + p) * d + lane + half] = f32_to_bf16_rne(vh[lane + half]);
+    sincos(r, &sd, &cd);
+    c = float(cd);
+    s = float(sd);
 }
 
-// Block = one chunk of 64 positions of key/value head g (blockIdx.y), 8 waves of 8 positions.  part layout:
+// Block = one chunk of 64 positions of key/value head g (blockIdx.y), 8 waves of 8 positions.  The block first
+// brings its group's queries to their final form (RMS norm over each head, rotation at p), and the block of the
+// last chunk also the key and value of position p, which it appends to the caches and uses from LDS.  part layout:
 // [query head][chunk][d + 4] (unnormalised output, then max, then sum; rows padded to 16 bytes).  d is a
 // multiple of 8, at most 128.  Every load of a wave -- its positions' key pieces and their value rows, which
 // do not depend on the scores -- is issued before any is used: one memory round trip per wave.
@@ -111,6 +87,8 @@ __device__ __forceinline__ float lanes8_sum(float v) {
 
 // GROUP = query heads per key/value head; FULL = (d == 128).  Both compile time, so every loop over heads
 // and key pieces is static.
+//   heads:   job j = wave, wave + 8, ...: query head j of the group, job GROUP (last chunk only) the key and
+//            value heads; lane i holds the pair (i, i + d/2);
 //   scores: lane = slice * 8 + position; slice s dots key pieces s and s + 8 (8 dims each) with every query
 //           head of the group (queries read from LDS as float4 broadcasts), then the 8 slices are summed
 //           (row rotation by 8, then two cross-row swaps);
@@ -119,20 +97,23 @@ __device__ __forceinline__ float lanes8_sum(float v) {
 //   merge:   the 8 waves' (max, sum, output) per head merged through LDS into the chunk's partial, at most
 //            8 heads per pass.
 template <int GROUP, bool FULL>
-__global__ __launch_bounds__(kAttnBlock) void attn_partial_kernel(const float *__restrict__ q, int d_arg,
-                                                                  const uint16_t *__restrict__ k_cache,
-                                                                  const uint16_t *__restrict__ v_cache,
-                                                                  int max_pos, int n_pos, int n_chunks,
+__global__ __launch_bounds__(kAttnBlock) void attn_partial_kernel(const float *__restrict__ qkv, int d_arg,
+                                                                  uint16_t *__restrict__ k_cache,
+                                                                  uint16_t *__restrict__ v_cache, int max_pos,
+                                                                  int n_pos, float theta, int n_chunks,
                                                                   float *__restrict__ part) {
     constexpr int HB = GROUP < 8 ? GROUP : 8;  // heads per merge pass
     __shared__ float4 qs4[GROUP * 128 / 4];                    // the group's queries, [head][d]
     __shared__ float4 prob4[kAttnWaves][GROUP][kPosW / 4];     // per wave: probabilities [head][position]
     __shared__ float wm[kAttnWaves][GROUP], ws[kAttnWaves][GROUP];
     __shared__ float wo[kAttnWaves][HB][128];
+    __shared__ uint4 knew4[128 / 8], vnew4[128 / 8];  // bf16 key and value of position p (last chunk)
     float *qs = reinterpret_cast<float *>(qs4);
+    uint16_t *knew = reinterpret_cast<uint16_t *>(knew4), *vnew = reinterpret_cast<uint16_t *>(vnew4);
     const int d = FULL ? 128 : d_arg, dc = d / 8;
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
-    const int g = blockIdx.y, chunk = blockIdx.x;
+    const int g = blockIdx.y, chunk = blockIdx.x, n_kv = gridDim.y, p = n_pos - 1;
+    const bool last = chunk == n_chunks - 1;  // holds position p
     const int pl = lane % kPosW, slice = lane / kPosW;
     const int pos0 = chunk * kAttnChunk + wave * kPosW;
     const int n_here = max(0, min(kPosW, n_pos - pos0));  // live positions of this wave (wave 0 has >= 1)
@@ -152,9 +133,60 @@ __global__ __launch_bounds__(kAttnBlock) void attn_partial_kernel(const float *_
 #pragma unroll
     for (int j = 0; j < kPosW; ++j)
         vv[j] = *reinterpret_cast<const uint32_t *>(vb + size_t(min(pos0 + j, n_pos - 1)) * d);
-    for (int i = threadIdx.x; i < GROUP * d; i += kAttnBlock) qs[i] = q[size_t(g) * GROUP * d + i];
+    // 2. heads: queries normalised and rotated into LDS; the new key and value (last chunk)
+    {
+        const int half = d / 2;
+        const bool on = lane < half;
+        float rc = 0.f, rs = 0.f;
+        rope_cs(p, lane, d, theta, rc, rs);
+        for (int j = wave; j < GROUP + (last ? 1 : 0); j += kAttnWaves) {
+            const int row = j < GROUP ? g * GROUP + j : GROUP * n_kv + g;  // query head, else key head
+            const float *src = qkv + size_t(row) * d;
+            float a = on ? src[lane] : 0.f, b = on ? src[lane + half] : 0.f;
+            const float inv = rsqrtf(wave_sum(a * a + b * b) / float(d) + 1e-6f);
+            a *= inv;
+            b *= inv;
+            const float ra = a * rc - b * rs, rb = b * rc + a * rs;
+            if (!on) continue;
+            if (j < GROUP) {
+                qs[j * d + lane] = ra;
+                qs[j * d + lane + half] = rb;
+                continue;
+            }
+            // key layout [g][d/8][max_pos][8]; value layout [g][max_pos][d]
+            const float *vsrc = qkv + size_t(GROUP * n_kv + n_kv + g) * d;
+            const uint16_t k0 = f32_to_bf16_rne(ra), k1 = f32_to_bf16_rne(rb);
+            const uint16_t v0 = f32_to_bf16_rne(vsrc[lane]), v1 = f32_to_bf16_rne(vsrc[lane + half]);
+            knew[lane] = k0;
+            knew[lane + half] = k1;
+            vnew[lane] = v0;
+            vnew[lane + half] = v1;
+            auto kidx = [&](int i) { return ((size_t(g) * dc + i / 8) * max_pos + p) * 8 + (i % 8); };
+            k_cache[kidx(lane)] = k0;
+            k_cache[kidx(lane + half)] = k1;
+            v_cache[(size_t(g) * max_pos + p) * d + lane] = v0;
+            v_cache[(size_t(g) * max_pos + p) * d + lane + half] = v1;
+        }
+    }
     __syncthreads();
-    // 2. scores
+    // Position p: the key and value just formed, not the cache's previous content.  Loads clamped to p (past
+    // the last position) take them too: their weight is 0, and 0 times a stale NaN would not be.
+    if (last) {
+        if (pos0 + pl >= p) {
+#pragma unroll
+            for (int i = 0; i < kPPS; ++i) {
+                const int c = slice + kSlices * i;
+                if (FULL || c < dc) kw[i] = knew4[c];
+            }
+        }
+        if (dlive) {
+            const uint32_t vp = *reinterpret_cast<const uint32_t *>(vnew + dim);
+#pragma unroll
+            for (int j = 0; j < kPosW; ++j)
+                if (pos0 + j >= p) vv[j] = vp;
+        }
+    }
+    // 3. scores
     float sc[GROUP];
 #pragma unroll
     for (int h = 0; h < GROUP; ++h) sc[h] = 0.f;
@@ -184,7 +216,7 @@ __global__ __launch_bounds__(kAttnBlock) void attn_partial_kernel(const float *_
             }
         }
     }
-    // 3. softmax over the wave's positions; slice 0's lanes keep the probabilities in LDS
+    // 4. softmax over the wave's positions; slice 0's lanes keep the probabilities in LDS
     const float scale = rsqrtf(float(d));
     float mx[GROUP], sm[GROUP];
     float *pw = reinterpret_cast<float *>(prob4[wave]);
@@ -204,7 +236,7 @@ __global__ __launch_bounds__(kAttnBlock) void attn_partial_kernel(const float *_
     __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");
     __builtin_amdgcn_wave_barrier();
     __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
-    // 4. output: lanes over dimensions (2 per lane); probabilities are 0 past the live positions
+    // 5. output: lanes over dimensions (2 per lane); probabilities are 0 past the live positions
     float o0[GROUP], o1[GROUP];
 #pragma unroll
     for (int h = 0; h < GROUP; ++h) o0[h] = o1[h] = 0.f;
@@ -223,7 +255,7 @@ __global__ __launch_bounds__(kAttnBlock) void attn_partial_kernel(const float *_
             o1[h] = fmaf(pr.w, v1[3], fmaf(pr.z, v1[2], fmaf(pr.y, v1[1], fmaf(pr.x, v1[0], o1[h]))));
         }
     }
-    // 5. merge the 8 waves (a wave with no live position has max -inf, sum 0, output 0)
+    // 6. merge the 8 waves (a wave with no live position has max -inf, sum 0, output 0)
     if (lane == 0) {
 #pragma unroll
         for (int h = 0; h < GROUP; ++h) {
@@ -370,9 +402,6 @@ hipError_t launch_attention_decode(float *x, int H, int n_heads, int n_kv, int d
     (void)max_chunks;
     hipError_t e = launch_router_logits(x, w_qkv, BF16, 1, H, rows, nullptr, qkv, true, nullptr, s);
     if (e != hipSuccess) return e;
-    attn_heads_kernel<<<(n_heads + n_kv + 3) / 4, kBlock, 0, s>>>(qkv, n_heads, n_kv, d, k_cache, v_cache, max_pos, p,
-                                                                   theta);
-    if ((e = hipGetLastError()) != hipSuccess) return e;
     const dim3 pgrid(n_chunks, n_kv);
     const bool full = d == 128;
     switch (n_heads / n_kv) {
@@ -380,10 +409,10 @@ hipError_t launch_attention_decode(float *x, int H, int n_heads, int n_kv, int d
     case G:                                                                                                      \
         if (full)                                                                                                \
             attn_partial_kernel<G, true>                                                                         \
-                <<<pgrid, kAttnBlock, 0, s>>>(qkv, d, k_cache, v_cache, max_pos, n_pos, n_chunks, part);         \
+                <<<pgrid, kAttnBlock, 0, s>>>(qkv, d, k_cache, v_cache, max_pos, n_pos, theta, n_chunks, part); \
         else                                                                                                     \
             attn_partial_kernel<G, false>                                                                        \
-                <<<pgrid, kAttnBlock, 0, s>>>(qkv, d, k_cache, v_cache, max_pos, n_pos, n_chunks, part);         \
+                <<<pgrid, kAttnBlock, 0, s>>>(qkv, d, k_cache, v_cache, max_pos, n_pos, theta, n_chunks, part); \
         break;
         ATTN_GROUP(1) ATTN_GROUP(2) ATTN_GROUP(4) ATTN_GROUP(8) ATTN_GROUP(16)
 #undef ATTN_GROUP
