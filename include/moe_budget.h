@@ -210,8 +210,9 @@ MOE_API size_t moe_attention_workspace_bytes(int n_heads, int n_kv, int head_dim
  *            positions < p are read, position p is written
  *   workspace device, >= moe_attention_workspace_bytes(...), 16-byte aligned
  * Needs H a multiple of 128, n_heads * head_dim a multiple of 128, head_dim a
- * multiple of 8 up to 128, n_heads / n_kv <= 16, 0 <= p < max_pos, theta > 1;
- * MOE_ERR_INVALID_ARG otherwise. */
+ * multiple of 8 up to 128, n_heads / n_kv one of 1, 2, 4, 8, 16, max_pos at most
+ * 16384, 0 <= p < max_pos, theta > 1; MOE_ERR_INVALID_ARG otherwise.  Cache
+ * content at positions above p is never used (it may be anything, NaN included). */
 MOE_API int moe_attention_decode(float *x, int H, int n_heads, int n_kv, int head_dim, const void *w_qkv,
                                  const void *w_o, void *k_cache, void *v_cache, int max_pos, int p, float theta,
                                  void *workspace, size_t workspace_bytes, void *stream);

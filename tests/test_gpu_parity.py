@@ -845,7 +845,9 @@ def _i16(a):  # bf16 bits as a torch-friendly int16 device tensor
 @pytest.mark.parametrize("H,nh,nkv,d,max_pos,p", [(256, 4, 2, 64, 300, 0), (256, 4, 2, 64, 300, 1),
                                                   (256, 4, 2, 64, 300, 63), (256, 4, 2, 64, 300, 64),
                                                   (256, 4, 2, 64, 300, 65), (256, 8, 1, 32, 300, 299),
-                                                  (512, 8, 2, 128, 256, 200), (2048, 32, 4, 128, 4096, 4095)])
+                                                  (512, 8, 2, 128, 256, 200), (2048, 32, 4, 128, 4096, 4095),
+                                                  (256, 16, 1, 128, 200, 130), (256, 2, 2, 128, 200, 7),
+                                                  (256, 4, 4, 32, 100, 99)])
 def test_attention_decode_parity(H, nh, nkv, d, max_pos, p):
     wqkv, wo, kc, vc, x = _attn_case(H, nh, nkv, d, max_pos, seed=H + p)
     kc_o, vc_o = kc.copy(), vc.copy()
@@ -862,6 +864,23 @@ def test_attention_decode_parity(H, nh, nkv, d, max_pos, p):
     f = lambda b: synth.bf16_to_f32(b).astype(np.float64)
     assert np.abs(f(k_gpu[:, p]) - f(kc_o[:, p])).max() <= 1e-2 * max(1.0, np.abs(f(kc_o[:, p])).max())
     assert np.abs(f(v_gpu[:, p]) - f(vc_o[:, p])).max() <= 1e-2 * max(1.0, np.abs(f(vc_o[:, p])).max())
+
+
+@pytest.mark.parametrize("p", [0, 64, 70, 127])
+def test_attention_decode_ignores_cache_content_past_p(p):
+    """NaN keys and values at positions p and above (position p is written before it is read; the partial
+    kernel's loads past the last position are clamped to p, with weight 0): output equals the oracle's."""
+    H, nh, nkv, d, max_pos = 256, 8, 2, 128, 160
+    wqkv, wo, kc, vc, x = _attn_case(H, nh, nkv, d, max_pos, seed=31 + p)
+    kc[:, p:], vc[:, p:] = 0x7FC0, 0x7FC0  # bf16 quiet NaN
+    kc_o, vc_o = kc.copy(), vc.copy()
+    y_ref = oracle.attention_decode(x, wqkv, wo, kc_o, vc_o, p, nh, nkv)
+    assert np.isfinite(y_ref).all()
+    xd = dev(x)
+    moe.moe_attention_decode(xd, _i16(wqkv), _i16(wo), _i16(moe.key_cache_layout(kc)), _i16(vc), p, nh, nkv)
+    moe.moe_sync_check()
+    got = xd.cpu().numpy().astype(np.float64)
+    assert np.isfinite(got).all() and normwise(got - x, y_ref - x) <= ATTN_TOL
 
 
 def test_attention_decode_sequence_appends_across_chunks():
@@ -887,7 +906,7 @@ def test_attention_decode_rejects_bad_arguments():
     H, nh, nkv, d, max_pos = 256, 4, 2, 64, 32
     wqkv, wo, kc, vc, x = _attn_case(H, nh, nkv, d, max_pos, seed=5)
     args = (_i16(wqkv), _i16(wo), _i16(moe.key_cache_layout(kc)), _i16(vc))
-    for p, nh_, nkv_ in ((max_pos, nh, nkv), (-1, nh, nkv), (0, 4, 3), (0, 40, 2)):
+    for p, nh_, nkv_ in ((max_pos, nh, nkv), (-1, nh, nkv), (0, 4, 3), (0, 40, 2), (0, 6, 2)):
         with pytest.raises(moe.MoeError) as ei:
             moe.moe_attention_decode(dev(x), *args, p, nh_, nkv_)
         assert ei.value.code == -1
