@@ -42,6 +42,27 @@ __device__ __forceinline__ float wave_sum(float v) {
            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
 }
 
+// Maximum (MAX) or minimum of a 64-bit value over the 64 lanes, returned in every lane: DPP quad swaps and
+// half-row / row mirrors reduce each row of 16; row broadcasts 15 and 31 carry the rows' results to lane 63.
+template <bool MAX>
+__device__ __forceinline__ uint64_t wave_reduce_u64(uint64_t v) {
+    auto pick = [](uint64_t a, uint64_t b) { return MAX ? (b > a ? b : a) : (b < a ? b : a); };
+    auto lo = [](uint64_t a) { return int(uint32_t(a)); };
+    auto hi = [](uint64_t a) { return int(uint32_t(a >> 32)); };
+    auto join = [](int l, int h) { return uint64_t(uint32_t(l)) | (uint64_t(uint32_t(h)) << 32); };
+#define MOE_DPP64(CTRL, ROWS) \
+    join(__builtin_amdgcn_update_dpp(lo(v), lo(v), CTRL, ROWS, 0xF, false), \
+         __builtin_amdgcn_update_dpp(hi(v), hi(v), CTRL, ROWS, 0xF, false))
+    v = pick(v, MOE_DPP64(0xB1, 0xF));   // quad_perm [1,0,3,2]
+    v = pick(v, MOE_DPP64(0x4E, 0xF));   // quad_perm [2,3,0,1]
+    v = pick(v, MOE_DPP64(0x141, 0xF));  // row_half_mirror
+    v = pick(v, MOE_DPP64(0x140, 0xF));  // row_mirror
+    v = pick(v, MOE_DPP64(0x142, 0xA));  // row_bcast:15 into rows 1 and 3
+    v = pick(v, MOE_DPP64(0x143, 0xC));  // row_bcast:31 into rows 2 and 3
+#undef MOE_DPP64
+    return join(__builtin_amdgcn_readlane(lo(v), 63), __builtin_amdgcn_readlane(hi(v), 63));
+}
+
 __device__ __forceinline__ float bf16_bits_to_float(uint32_t b16) { return __uint_as_float(b16 << 16); }
 
 __device__ __forceinline__ uint4 load16(const uint8_t *p) { return *reinterpret_cast<const uint4 *>(p); }

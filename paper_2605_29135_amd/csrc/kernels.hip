@@ -31,10 +31,11 @@ __device__ __forceinline__ uint32_t order_key(float z) {
     return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
 }
 
-struct TopkScratch {  // per wave, in LDS
-    uint32_t key[MOE_MAX_TOPK];
-    int32_t id[MOE_MAX_TOPK];
-    float z[MOE_MAX_TOPK];
+__device__ __forceinline__ float order_key_value(uint32_t key) {  // inverse of order_key (-0 comes back +0)
+    return __uint_as_float((key & 0x80000000u) ? (key ^ 0x80000000u) : ~key);
+}
+
+struct TopkScratch {  // per wave, in LDS: the selected ids and logits in rank order
     int32_t rid[MOE_MAX_TOPK];
     float rz[MOE_MAX_TOPK];
 };
@@ -46,28 +47,29 @@ __device__ __forceinline__ void wave_lds_sync() {
 }
 
 // Top-k of one token's E (<= 256) logits by one wave: ids ranked by (z desc, id
-// asc) and the softmax over the k selected.  A bisection over the 32 key bits
-// (ballot + popcount per bit) finds the k-th largest key; keys above it are
-// selected and ties at it are filled in ascending id; the k selected are then
-// ranked against each other.  COHERENT reads logits written by other
-// workgroups of the same launch.
+// asc) and the softmax over the k selected.  Each entry is a 64-bit rank key
+// (order key of z, then the complement of its id, so that a larger key is
+// ahead); every lane sorts its (up to 4) keys in registers, then k rounds each
+// take the wave maximum of the lanes' heads -- the next entry in rank order --
+// and the owning lane advances its list.  COHERENT reads logits written by
+// other workgroups of the same launch.
 template <bool COHERENT>
 __device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wout, int *err, TopkScratch *sc) {
     const int lane = threadIdx.x & (kWave - 1);
-    float v[4];
-    uint32_t key[4];
-    bool live[4];
+    uint64_t c[4];
     bool bad = false;
 #pragma unroll
     for (int m = 0; m < 4; ++m) {
         const int e = lane + kWave * m;
-        live[m] = e < E;
+        const bool live = e < E;
+        float v;
         if constexpr (COHERENT)
-            v[m] = live[m] ? __hip_atomic_load(z + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0.f;
+            v = live ? __hip_atomic_load(z + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0.f;
         else
-            v[m] = live[m] ? z[e] : 0.f;
-        if (live[m] && !isfinite(v[m])) bad = true;
-        key[m] = order_key(v[m]);
+            v = live ? z[e] : 0.f;
+        if (live && !isfinite(v)) bad = true;
+        // a live key is at least order_key(-FLT_MAX) << 32 > 0, so 0 never outranks a live entry
+        c[m] = live ? (uint64_t(order_key(v)) << 32) | uint64_t(~uint32_t(e)) : 0ull;
     }
     if (__any(bad)) {
         if (lane < k) {
@@ -76,53 +78,42 @@ __device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wou
             sc->rid[lane] = -1;
         }
         if (lane == 0) atomicOr(err, kErrNonfinite);
+        __builtin_amdgcn_wave_barrier();
         return;
     }
-    uint32_t kth = 0;
-    for (int b = 31; b >= 0; --b) {
-        const uint32_t cand = kth | (1u << b);
-        int cnt = 0;
-#pragma unroll
-        for (int m = 0; m < 4; ++m) cnt += __popcll(__ballot(live[m] && key[m] >= cand));
-        if (cnt >= k) kth = cand;
-    }
-    int above = 0;
-#pragma unroll
-    for (int m = 0; m < 4; ++m) above += __popcll(__ballot(live[m] && key[m] > kth));
-    const int need = k - above;  // ties at the threshold to take, lowest ids first
-    const uint64_t below = __lanemask_lt();
-    int eq_seen = 0, placed = 0;
-#pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        const bool eq = live[m] && key[m] == kth;
-        const uint64_t eqm = __ballot(eq);
-        const bool sel = (live[m] && key[m] > kth) || (eq && eq_seen + __popcll(eqm & below) < need);
-        const uint64_t selm = __ballot(sel);
-        if (sel) {
-            const int pos = placed + __popcll(selm & below);
-            sc->key[pos] = key[m];
-            sc->id[pos] = lane + kWave * m;
-            sc->z[pos] = v[m];
+    auto cswap = [&](int a, int b) {  // descending
+        const uint64_t x = c[a], y = c[b];
+        c[a] = x > y ? x : y;
+        c[b] = x > y ? y : x;
+    };
+    cswap(0, 1);
+    cswap(2, 3);
+    cswap(0, 2);
+    cswap(1, 3);
+    cswap(1, 2);
+    for (int r = 0; r < k; ++r) {
+        const uint64_t best = wave_reduce_u64<true>(c[0]);
+        const int id = int(~uint32_t(best));
+        if (lane == (id & (kWave - 1))) {
+            c[0] = c[1];
+            c[1] = c[2];
+            c[2] = c[3];
+            c[3] = 0ull;
         }
-        eq_seen += __popcll(eqm);
-        placed += __popcll(selm);
+        if (lane == 0) {
+            sc->rid[r] = id;
+            sc->rz[r] = order_key_value(uint32_t(best >> 32));
+        }
     }
     wave_lds_sync();
+    // softmax against the top logit, the denominator summed in rank order
+    const float z0 = sc->rz[0];
+    const float ez = lane < k ? expf(sc->rz[lane] - z0) : 0.f;
+    float sum = 0.f;
+    for (int j = 0; j < k; ++j) sum += __int_as_float(__builtin_amdgcn_readlane(__float_as_int(ez), j));
     if (lane < k) {
-        const uint32_t mk = sc->key[lane];
-        const int mi = sc->id[lane];
-        int r = 0;
-        for (int j = 0; j < k; ++j) r += (sc->key[j] > mk) || (sc->key[j] == mk && sc->id[j] < mi);
-        sc->rid[r] = mi;
-        sc->rz[r] = sc->z[lane];
-    }
-    wave_lds_sync();
-    if (lane < k) {
-        const float z0 = sc->rz[0];
-        float sum = 0.f;
-        for (int j = 0; j < k; ++j) sum += expf(sc->rz[j] - z0);  // rank order
         ids[lane] = sc->rid[lane];
-        wout[lane] = expf(sc->rz[lane] - z0) / sum;
+        wout[lane] = ez / sum;
     }
 }
 
@@ -148,9 +139,10 @@ __global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__res
 }
 
 // One token's top-k fused with the device lookup of its experts (MOE_CACHE_DEVICE
-// decode): wave 0 ranks the experts and writes ids and weights, then the whole
-// block takes the slot table's decisions for them -- one launch and no global
-// round trip between the routing result and the residency decisions.
+// decode): every thread first issues its reads of the slot state, then wave 0
+// ranks the experts and writes ids and weights while they are in flight, then
+// the whole block takes the slot table's decisions for them -- one launch and
+// one global round trip before the decisions.
 template <bool ROTARY>
 __global__ __launch_bounds__(kBlock) void topk_lookup_kernel(const float *__restrict__ logits, int E, int k,
                                                              int32_t *__restrict__ ids, float *__restrict__ wout,
@@ -159,12 +151,14 @@ __global__ __launch_bounds__(kBlock) void topk_lookup_kernel(const float *__rest
     static_assert(kBlock == devres::kDevThreads, "the lookup body runs on the whole block");
     __shared__ TopkScratch sc;
     __shared__ int32_t ids_l[MOE_MAX_TOPK];
+    devres::DevStaged st;
+    devres::dev_stage_issue<ROTARY>(r, p, st);
     if (threadIdx.x < kWave) {
         topk_wave<false>(logits, E, k, ids, wout, err, &sc);
         if (int(threadIdx.x) < k) ids_l[threadIdx.x] = sc.rid[threadIdx.x];  // the ranked ids (-1 if non-finite)
     }
     __syncthreads();
-    devres::dev_lookup_body<ROTARY>(r, p, ids_l, k, slots_out, err);
+    devres::dev_lookup_body<ROTARY>(r, p, st, ids_l, k, slots_out, err);
 }
 
 // --------------------------------------------------------------- router ---

@@ -25,7 +25,9 @@ template <bool ROTARY>
 __global__ __launch_bounds__(kDevThreads) void dev_lookup_kernel(DevResidency r, DevLookup p,
                                                                  const int32_t *__restrict__ ids, int n,
                                                                  int32_t *__restrict__ slots_out, int *err) {
-    dev_lookup_body<ROTARY>(r, p, ids, n, slots_out, err);
+    DevStaged st;
+    dev_stage_issue<ROTARY>(r, p, st);
+    dev_lookup_body<ROTARY>(r, p, st, ids, n, slots_out, err);
 }
 
 // Block (x, f) streams its share of fill f; blocks past the lookup's fill count exit.
