@@ -42,6 +42,22 @@ __device__ __forceinline__ float wave_sum(float v) {
            __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 48));
 }
 
+// Maximum (MAX) or minimum of a 32-bit unsigned value over the 64 lanes, returned in every lane (the same
+// DPP pattern as wave_reduce_u64 below).
+template <bool MAX>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t v) {
+    auto pick = [](uint32_t a, uint32_t b) { return MAX ? (b > a ? b : a) : (b < a ? b : a); };
+#define MOE_DPP32(CTRL, ROWS) uint32_t(__builtin_amdgcn_update_dpp(int(v), int(v), CTRL, ROWS, 0xF, false))
+    v = pick(v, MOE_DPP32(0xB1, 0xF));
+    v = pick(v, MOE_DPP32(0x4E, 0xF));
+    v = pick(v, MOE_DPP32(0x141, 0xF));
+    v = pick(v, MOE_DPP32(0x140, 0xF));
+    v = pick(v, MOE_DPP32(0x142, 0xA));
+    v = pick(v, MOE_DPP32(0x143, 0xC));
+#undef MOE_DPP32
+    return uint32_t(__builtin_amdgcn_readlane(int(v), 63));
+}
+
 // Maximum (MAX) or minimum of a 64-bit value over the 64 lanes, returned in every lane: DPP quad swaps and
 // half-row / row mirrors reduce each row of 16; row broadcasts 15 and 31 carry the rows' results to lane 63.
 template <bool MAX>

@@ -92,9 +92,19 @@ __device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wou
     cswap(1, 3);
     cswap(1, 2);
     for (int r = 0; r < k; ++r) {
-        const uint64_t best = wave_reduce_u64<true>(c[0]);
+        // the top key among the lanes' heads; the lowest id among heads sharing it (rare) by a second reduce
+        const uint32_t hk = uint32_t(c[0] >> 32);
+        const uint32_t top = wave_reduce_u32<true>(hk);
+        const uint64_t tied = __ballot(hk == top);
+        int wl = int(__builtin_ctzll(tied));
+        if (__popcll(tied) > 1) {
+            const uint32_t lo = hk == top ? uint32_t(c[0]) : 0u;  // complement of the id: larger is lower
+            const uint32_t lo_top = wave_reduce_u32<true>(lo);    // every lane takes part (not under the &&)
+            wl = int(__builtin_ctzll(__ballot(hk == top && lo == lo_top)));
+        }
+        const uint64_t best = (uint64_t(top) << 32) | uint64_t(uint32_t(__builtin_amdgcn_readlane(int(uint32_t(c[0])), wl)));
         const int id = int(~uint32_t(best));
-        if (lane == (id & (kWave - 1))) {
+        if (lane == wl) {
             c[0] = c[1];
             c[1] = c[2];
             c[2] = c[3];
@@ -143,7 +153,7 @@ __global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__res
 // ranks the experts and writes ids and weights while they are in flight, then
 // the whole block takes the slot table's decisions for them -- one launch and
 // one global round trip before the decisions.
-template <bool ROTARY>
+template <bool ROTARY, int PT>
 __global__ __launch_bounds__(kBlock) void topk_lookup_kernel(const float *__restrict__ logits, int E, int k,
                                                              int32_t *__restrict__ ids, float *__restrict__ wout,
                                                              int *err, DevResidency r, DevLookup p,
@@ -151,14 +161,14 @@ __global__ __launch_bounds__(kBlock) void topk_lookup_kernel(const float *__rest
     static_assert(kBlock == devres::kDevThreads, "the lookup body runs on the whole block");
     __shared__ TopkScratch sc;
     __shared__ int32_t ids_l[MOE_MAX_TOPK];
-    devres::DevStaged st;
-    devres::dev_stage_issue<ROTARY>(r, p, st);
+    devres::DevStaged<PT> st;
+    devres::dev_stage_issue<ROTARY, PT>(r, p, st);
     if (threadIdx.x < kWave) {
         topk_wave<false>(logits, E, k, ids, wout, err, &sc);
         if (int(threadIdx.x) < k) ids_l[threadIdx.x] = sc.rid[threadIdx.x];  // the ranked ids (-1 if non-finite)
     }
     __syncthreads();
-    devres::dev_lookup_body<ROTARY>(r, p, st, ids_l, k, slots_out, err);
+    devres::dev_lookup_body<ROTARY, PT>(r, p, st, ids_l, k, slots_out, err);
 }
 
 // --------------------------------------------------------------- router ---
@@ -941,8 +951,15 @@ hipError_t launch_topk_lookup(const float *logits, int E, int k, int32_t *ids, f
     if (p.C < 1 || p.C > kDevMaxSlots || p.E != E || E > MOE_MAX_EXPERTS || k < 1 || k > MOE_MAX_TOPK ||
         p.layer < 0 || p.layer >= p.L)
         return hipErrorInvalidValue;
-    if (p.rotary) topk_lookup_kernel<true><<<1, kBlock, 0, s>>>(logits, E, k, ids, weights, err_flags, r, p, slots_out);
-    else topk_lookup_kernel<false><<<1, kBlock, 0, s>>>(logits, E, k, ids, weights, err_flags, r, p, slots_out);
+    constexpr int PTL = devres::kDevPerThread;
+    const bool small = devres::dev_pt(p.C) == 4;
+#define TL_LAUNCH(RT, PTV) \
+    topk_lookup_kernel<RT, PTV><<<1, kBlock, 0, s>>>(logits, E, k, ids, weights, err_flags, r, p, slots_out)
+    if (p.rotary && small) TL_LAUNCH(true, 4);
+    else if (p.rotary) TL_LAUNCH(true, PTL);
+    else if (small) TL_LAUNCH(false, 4);
+    else TL_LAUNCH(false, PTL);
+#undef TL_LAUNCH
     return hipGetLastError();
 }
 

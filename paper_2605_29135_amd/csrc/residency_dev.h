@@ -9,30 +9,33 @@ namespace moe {
 namespace devres {
 
 constexpr int kDevThreads = 256;
-constexpr int kDevPerThread = kDevMaxSlots / kDevThreads;  // slots each thread stages
+constexpr int kDevPerThread = kDevMaxSlots / kDevThreads;  // slots each thread stages, at most
+// PT = slots each thread stages (ceil(C / kDevThreads) <= PT): 4 up to 1024 slots, else kDevPerThread.
+constexpr int dev_pt(int C) { return C <= 4 * kDevThreads ? 4 : kDevPerThread; }
 constexpr int kWaveDev = 64;
 constexpr int kFastVictims = 8;  // LRU: up to this many victims per step are chosen in one pass
 
 // The lookup's global reads that do not depend on the step's ids, held in registers: each thread's share of
 // the slot keys and their stamps or charges, one entry of the layer's row of the slot table, one counter and
 // the step number.  Issued first, so that a caller can overlap them with forming the ids.
+template <int PT>
 struct DevStaged {
     int32_t row;
     int step_v;
     unsigned long long sc0;
-    int32_t kv[kDevPerThread];
-    uint64_t sv[kDevPerThread];
+    int32_t kv[PT];
+    uint64_t sv[PT];
 };
 
-template <bool ROTARY>
-__device__ __forceinline__ void dev_stage_issue(const DevResidency &r, const DevLookup &p, DevStaged &st) {
+template <bool ROTARY, int PT>
+__device__ __forceinline__ void dev_stage_issue(const DevResidency &r, const DevLookup &p, DevStaged<PT> &st) {
     const int tid = threadIdx.x;
     // clamped indices, no branches: every read is in flight at once
     st.row = r.slot_of_key[p.layer * p.E + min(tid, p.E - 1)];
     st.step_v = p.step_dev ? p.step_dev[0] : p.step;
     st.sc0 = r.scal[min(tid, kDevScalars - 1)];
 #pragma unroll
-    for (int u = 0; u < kDevPerThread; ++u) {
+    for (int u = 0; u < PT; ++u) {
         const int sc = min(tid + u * kDevThreads, p.C - 1);
         st.kv[u] = r.key_of_slot[sc];
         if constexpr (ROTARY) st.sv[u] = r.charge[sc];
@@ -40,13 +43,13 @@ __device__ __forceinline__ void dev_stage_issue(const DevResidency &r, const Dev
     }
 }
 
-template <bool ROTARY>
-__device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const DevLookup &p, const DevStaged &st,
+template <bool ROTARY, int PT>
+__device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const DevLookup &p, const DevStaged<PT> &st,
                                                 const int32_t *ids, int n, int32_t *__restrict__ slots_out,
                                                 int *err) {
-    __shared__ int32_t key_of[kDevMaxSlots];
-    __shared__ uint64_t stamp[ROTARY ? 1 : kDevMaxSlots];
-    __shared__ uint16_t charge[ROTARY ? kDevMaxSlots : 1];
+    __shared__ int32_t key_of[PT * kDevThreads];
+    __shared__ uint64_t stamp[ROTARY ? 1 : PT * kDevThreads];
+    __shared__ uint16_t charge[ROTARY ? PT * kDevThreads : 1];
     __shared__ uint32_t present[MOE_MAX_EXPERTS / 32];
     __shared__ int32_t R[MOE_MAX_EXPERTS];
     __shared__ int32_t slot_of_e[MOE_MAX_EXPERTS];  // slot of each expert of the step, by expert id
@@ -64,7 +67,7 @@ __device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const Dev
     {
         const int32_t id0 = ids[min(tid, max(n - 1, 0))];
 #pragma unroll
-        for (int u = 0; u < kDevPerThread; ++u) {
+        for (int u = 0; u < PT; ++u) {
             if (u * kDevThreads >= C) break;  // uniform
             const int s = tid + u * kDevThreads;
             if (s < C) {
@@ -164,25 +167,32 @@ __device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const Dev
             const int n_need = n_need_sh;
             if (n_need <= kFastVictims) {
                 if (n_need > 0) {
-                    // candidates: occupied slots (0 .. next_free - 1) outside the step, keyed (stamp << 12) | slot
-                    unsigned long long cand[kDevPerThread];
+                    // candidates: occupied slots (0 .. next_free - 1) outside the step, keyed (stamp << 12) |
+                    // slot; each thread's sorted ascending, so that its head is its least recent
+                    unsigned long long cand[PT];
 #pragma unroll
-                    for (int u = 0; u < kDevPerThread; ++u) {
+                    for (int u = 0; u < PT; ++u) {
                         const long long s = tid + u * kDevThreads;
                         cand[u] = ~0ull;
-                        if (u * kDevThreads < (long long)nf0 && s < (long long)nf0 && !pinned(key_of[s]))
+                        if (s < (long long)nf0 && !pinned(key_of[s]))
                             cand[u] = (stamp[s] << 12) | (unsigned long long)s;
                     }
+#pragma unroll
+                    for (int a = 1; a < PT; ++a)  // insertion sort, unrolled
+#pragma unroll
+                        for (int b = a; b > 0; --b) {
+                            const unsigned long long x = cand[b - 1], y = cand[b];
+                            cand[b - 1] = x < y ? x : y;
+                            cand[b] = x < y ? y : x;
+                        }
                     for (int q = 0; q < n_need; ++q) {
-                        unsigned long long best = ~0ull;
-#pragma unroll
-                        for (int u = 0; u < kDevPerThread; ++u)
-                            if (u * kDevThreads < (long long)nf0) best = cand[u] < best ? cand[u] : best;
-                        best = dev::wave_reduce_u64<false>(best);
+                        const unsigned long long best = dev::wave_reduce_u64<false>(cand[0]);
                         if (lane == 0) vic_w[wave][q] = best;
+                        if (cand[0] == best) {  // unique keys: only the owner matches
 #pragma unroll
-                        for (int u = 0; u < kDevPerThread; ++u)
-                            if (u * kDevThreads < (long long)nf0 && cand[u] == best) cand[u] = ~0ull;  // unique keys
+                            for (int u = 0; u + 1 < PT; ++u) cand[u] = cand[u + 1];
+                            cand[PT - 1] = ~0ull;
+                        }
                     }
                     __syncthreads();
                     if (tid == 0) {

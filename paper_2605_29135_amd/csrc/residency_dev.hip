@@ -21,13 +21,13 @@ namespace {
 using namespace devres;
 constexpr int kFillUnrollDev = 4;
 
-template <bool ROTARY>
+template <bool ROTARY, int PT>
 __global__ __launch_bounds__(kDevThreads) void dev_lookup_kernel(DevResidency r, DevLookup p,
                                                                  const int32_t *__restrict__ ids, int n,
                                                                  int32_t *__restrict__ slots_out, int *err) {
-    DevStaged st;
-    dev_stage_issue<ROTARY>(r, p, st);
-    dev_lookup_body<ROTARY>(r, p, st, ids, n, slots_out, err);
+    DevStaged<PT> st;
+    dev_stage_issue<ROTARY, PT>(r, p, st);
+    dev_lookup_body<ROTARY, PT>(r, p, st, ids, n, slots_out, err);
 }
 
 // Block (x, f) streams its share of fill f; blocks past the lookup's fill count exit.
@@ -72,8 +72,11 @@ hipError_t launch_dev_lookup(const DevResidency &r, const DevLookup &p, const in
                              int *err, hipStream_t s) {
     if (p.C < 1 || p.C > kDevMaxSlots || p.E < 1 || p.E > MOE_MAX_EXPERTS || p.layer < 0 || p.layer >= p.L || n < 0)
         return hipErrorInvalidValue;
-    if (p.rotary) dev_lookup_kernel<true><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
-    else dev_lookup_kernel<false><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
+    const bool small = dev_pt(p.C) == 4;
+    if (p.rotary && small) dev_lookup_kernel<true, 4><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
+    else if (p.rotary) dev_lookup_kernel<true, kDevPerThread><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
+    else if (small) dev_lookup_kernel<false, 4><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
+    else dev_lookup_kernel<false, kDevPerThread><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
     return hipGetLastError();
 }
 
