@@ -809,9 +809,11 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const float *__restrict
 // Expert fills as one kernel: each block streams a share of one expert blob
 // from pinned host memory (read over PCIe) into its HBM slot; block (0, 0) also
 // writes the slot-table changes of the batch.  Later kernels on the stream see
-// both.  Reads of host memory need many bytes in flight: each thread keeps
-// kFillUnroll 16-byte loads outstanding.
-constexpr int kFillUnroll = 4;
+// both.  Each thread keeps kFillUnroll 16-byte loads of host memory
+// outstanding; with 32 blocks per 9 MiB blob that is 256 KiB in flight per
+// fill, which measured faster than 1 or 2 MiB (the device-decision fill kernel
+// has the same shape).
+constexpr int kFillUnroll = 2;
 __global__ __launch_bounds__(kBlock) void fill_slots_kernel(FillBatch b) {
     const int f = blockIdx.y;
     if (f == 0 && blockIdx.x == 0)
@@ -1086,9 +1088,8 @@ hipError_t launch_hbm_read(const void *buf, size_t bytes, float *sink, hipStream
 hipError_t launch_fill_slots(const FillBatch &b, hipStream_t s) {
     if (b.n < 1 || b.n > kMaxFillBatch || b.n_tab < 0 || b.n_tab > 2 * kMaxFillBatch || b.bytes <= 0 || b.bytes % 16)
         return hipErrorInvalidValue;
-    // about 64 blocks keep a 9 MiB blob's PCIe reads at full rate; smaller blobs take fewer
-    long long bpf = b.bytes / (128 << 10);
-    bpf = bpf < 4 ? 4 : (bpf > 64 ? 64 : bpf);
+    long long bpf = b.bytes / (64 << 10);  // 32 blocks for a 9 MiB blob; smaller blobs take fewer
+    bpf = bpf < 4 ? 4 : (bpf > 32 ? 32 : bpf);
     fill_slots_kernel<<<dim3(unsigned(bpf), unsigned(b.n)), kBlock, 0, s>>>(b);
     return hipGetLastError();
 }
