@@ -472,6 +472,45 @@ def test_device_lookups_match_oracle(rotary, Q, C, L, E, nmax, steps):
     buf.close()
 
 
+@pytest.mark.parametrize("case", ["all_free", "free_then_victims", "eight_victims", "nine_victims", "m64", "m65"])
+def test_device_lookup_one_pass_boundaries(case):
+    """The device LRU's one-pass placement (at most 64 experts and 8 victims in a step) and the lane walk beyond
+    it, at their boundaries, against the oracle event for event: misses into free slots only; free slots then
+    victims in one step; exactly 8 and 9 victims; 64 and 65 experts in one step."""
+    L, E, eb = 2, 160, 256
+    C = {"all_free": 40, "free_then_victims": 10, "eight_victims": 16, "nine_victims": 16, "m64": 100,
+         "m65": 100}[case]
+    steps = {"all_free": [list(range(8)), list(range(8, 20))],
+             "free_then_victims": [list(range(8)), list(range(20, 26))],        # 2 free + 4 victims
+             "eight_victims": [list(range(16)), list(range(30, 38))],           # 8 victims
+             "nine_victims": [list(range(16)), list(range(30, 39))],            # 9 victims: the lane walk
+             "m64": [list(range(64)), list(range(30, 94)), list(range(100, 110))],
+             "m65": [list(range(65)), list(range(30, 95)), list(range(100, 110))]}[case]
+    buf = moe.PinnedBuffer(L * E * eb)
+    buf.array.view(np.int32).reshape(L * E, eb // 4)[:] = np.arange(L * E, dtype=np.int32)[:, None]
+    cache = moe.ExpertCache(L, E, eb, C * eb, buf.ptr, E * eb, eb, device=True)
+    o = oracle.LRU(C, L, E)
+    rng = np.random.default_rng(len(case))
+    for t, ids in enumerate(steps):
+        ids = np.array(rng.permutation(ids), np.int32)  # any order: decisions follow ascending ids
+        slots = torch.empty(ids.size, dtype=torch.int32, device=DEV)
+        cache.lookup_device(t, 1, dev(ids), slots)
+        assert o.lookup(t, 1, ids) == oracle.OK
+        moe.moe_sync_check()
+        assert slots.cpu().tolist() == [o.slot_of(1, int(e)) for e in ids]
+    ev, oev = cache.trace(), o.events()
+    assert len(ev) == len(oev) and (ev.view(np.int32).reshape(-1, 6) == oev.view(np.int32).reshape(-1, 6)).all()
+    st, so = cache.stats(), o.stats()
+    assert (st["hits"], st["misses"], st["evictions"]) == (so["hits"], so["misses"], so["evictions"])
+    pool = _d2h(cache.slot_table()[1], C * eb).view(np.int32).reshape(C, eb // 4)
+    for e in range(E):
+        s_ = o.slot_of(1, e)
+        if s_ >= 0:
+            assert (pool[s_] == E + e).all()
+    cache.close()
+    buf.close()
+
+
 def test_device_lookup_errors_change_nothing():
     L, E, C, eb = 2, 16, 4, 256
     buf = moe.PinnedBuffer(L * E * eb)
