@@ -153,22 +153,21 @@ __global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__res
 // ranks the experts and writes ids and weights while they are in flight, then
 // the whole block takes the slot table's decisions for them -- one launch and
 // one global round trip before the decisions.
-template <bool ROTARY, int PT>
-__global__ __launch_bounds__(kBlock) void topk_lookup_kernel(const float *__restrict__ logits, int E, int k,
+template <bool ROTARY, int NT>
+__global__ __launch_bounds__(NT) void topk_lookup_kernel(const float *__restrict__ logits, int E, int k,
                                                              int32_t *__restrict__ ids, float *__restrict__ wout,
                                                              int *err, DevResidency r, DevLookup p,
                                                              int32_t *__restrict__ slots_out) {
-    static_assert(kBlock == devres::kDevThreads, "the lookup body runs on the whole block");
     __shared__ TopkScratch sc;
     __shared__ int32_t ids_l[MOE_MAX_TOPK];
-    devres::DevStaged<PT> st;
-    devres::dev_stage_issue<ROTARY, PT>(r, p, st);
+    devres::DevStaged st;
+    devres::dev_stage_issue<ROTARY, NT>(r, p, st);
     if (threadIdx.x < kWave) {
         topk_wave<false>(logits, E, k, ids, wout, err, &sc);
         if (int(threadIdx.x) < k) ids_l[threadIdx.x] = sc.rid[threadIdx.x];  // the ranked ids (-1 if non-finite)
     }
     __syncthreads();
-    devres::dev_lookup_body<ROTARY, PT>(r, p, st, ids_l, k, slots_out, err);
+    devres::dev_lookup_body<ROTARY, NT>(r, p, st, ids_l, k, slots_out, err);
 }
 
 // --------------------------------------------------------------- router ---
@@ -953,14 +952,13 @@ hipError_t launch_topk_lookup(const float *logits, int E, int k, int32_t *ids, f
     if (p.C < 1 || p.C > kDevMaxSlots || p.E != E || E > MOE_MAX_EXPERTS || k < 1 || k > MOE_MAX_TOPK ||
         p.layer < 0 || p.layer >= p.L)
         return hipErrorInvalidValue;
-    constexpr int PTL = devres::kDevPerThread;
-    const bool small = devres::dev_pt(p.C) == 4;
-#define TL_LAUNCH(RT, PTV) \
-    topk_lookup_kernel<RT, PTV><<<1, kBlock, 0, s>>>(logits, E, k, ids, weights, err_flags, r, p, slots_out)
-    if (p.rotary && small) TL_LAUNCH(true, 4);
-    else if (p.rotary) TL_LAUNCH(true, PTL);
-    else if (small) TL_LAUNCH(false, 4);
-    else TL_LAUNCH(false, PTL);
+    const bool small = devres::dev_threads(p.C) == 256;
+#define TL_LAUNCH(RT, NTV) \
+    topk_lookup_kernel<RT, NTV><<<1, NTV, 0, s>>>(logits, E, k, ids, weights, err_flags, r, p, slots_out)
+    if (p.rotary && small) TL_LAUNCH(true, 256);
+    else if (p.rotary) TL_LAUNCH(true, 1024);
+    else if (small) TL_LAUNCH(false, 256);
+    else TL_LAUNCH(false, 1024);
 #undef TL_LAUNCH
     return hipGetLastError();
 }

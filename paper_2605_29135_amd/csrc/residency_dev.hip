@@ -23,18 +23,18 @@ using namespace devres;
 // per fill: a sweep of blocks x loads (256 KiB to 2 MiB per fill) over the decode stack measured the
 // smallest in flight fastest (2 MiB: 75 tokens/s, 1 MiB: 77.8, 256 KiB: 80.0).
 constexpr int kFillUnrollDev = 2;
+constexpr int kFillThreads = 256;
 
-template <bool ROTARY, int PT>
-__global__ __launch_bounds__(kDevThreads) void dev_lookup_kernel(DevResidency r, DevLookup p,
-                                                                 const int32_t *__restrict__ ids, int n,
-                                                                 int32_t *__restrict__ slots_out, int *err) {
-    DevStaged<PT> st;
-    dev_stage_issue<ROTARY, PT>(r, p, st);
-    dev_lookup_body<ROTARY, PT>(r, p, st, ids, n, slots_out, err);
+template <bool ROTARY, int NT>
+__global__ __launch_bounds__(NT) void dev_lookup_kernel(DevResidency r, DevLookup p, const int32_t *__restrict__ ids,
+                                                        int n, int32_t *__restrict__ slots_out, int *err) {
+    DevStaged st;
+    dev_stage_issue<ROTARY, NT>(r, p, st);
+    dev_lookup_body<ROTARY, NT>(r, p, st, ids, n, slots_out, err);
 }
 
 // Block (x, f) streams its share of fill f; blocks past the lookup's fill count exit.
-__global__ __launch_bounds__(kDevThreads) void dev_fill_kernel(const long long *__restrict__ src_off,
+__global__ __launch_bounds__(kFillThreads) void dev_fill_kernel(const long long *__restrict__ src_off,
                                                                const int32_t *__restrict__ slot,
                                                                const int32_t *__restrict__ n_fill,
                                                                const uint8_t *__restrict__ host_dev,
@@ -47,16 +47,16 @@ __global__ __launch_bounds__(kDevThreads) void dev_fill_kernel(const long long *
     const size_t end = beg + per < n16 ? beg + per : n16;
     const uint4 *src = reinterpret_cast<const uint4 *>(host_dev + src_off[f]);
     uint4 *dst = reinterpret_cast<uint4 *>(pool + size_t(slot[f]) * size_t(bytes));
-    for (size_t i = beg + threadIdx.x; i < end; i += size_t(kDevThreads) * kFillUnrollDev) {
+    for (size_t i = beg + threadIdx.x; i < end; i += size_t(kFillThreads) * kFillUnrollDev) {
         uint4 v[kFillUnrollDev];
 #pragma unroll
         for (int u = 0; u < kFillUnrollDev; ++u) {
-            const size_t j = i + size_t(u) * kDevThreads;
+            const size_t j = i + size_t(u) * kFillThreads;
             v[u] = j < end ? src[j] : make_uint4(0u, 0u, 0u, 0u);
         }
 #pragma unroll
         for (int u = 0; u < kFillUnrollDev; ++u) {
-            const size_t j = i + size_t(u) * kDevThreads;
+            const size_t j = i + size_t(u) * kFillThreads;
             if (j < end) dst[j] = v[u];
         }
     }
@@ -75,11 +75,11 @@ hipError_t launch_dev_lookup(const DevResidency &r, const DevLookup &p, const in
                              int *err, hipStream_t s) {
     if (p.C < 1 || p.C > kDevMaxSlots || p.E < 1 || p.E > MOE_MAX_EXPERTS || p.layer < 0 || p.layer >= p.L || n < 0)
         return hipErrorInvalidValue;
-    const bool small = dev_pt(p.C) == 4;
-    if (p.rotary && small) dev_lookup_kernel<true, 4><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
-    else if (p.rotary) dev_lookup_kernel<true, kDevPerThread><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
-    else if (small) dev_lookup_kernel<false, 4><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
-    else dev_lookup_kernel<false, kDevPerThread><<<1, kDevThreads, 0, s>>>(r, p, ids, n, slots_out, err);
+    const bool small = dev_threads(p.C) == 256;
+    if (p.rotary && small) dev_lookup_kernel<true, 256><<<1, 256, 0, s>>>(r, p, ids, n, slots_out, err);
+    else if (p.rotary) dev_lookup_kernel<true, 1024><<<1, 1024, 0, s>>>(r, p, ids, n, slots_out, err);
+    else if (small) dev_lookup_kernel<false, 256><<<1, 256, 0, s>>>(r, p, ids, n, slots_out, err);
+    else dev_lookup_kernel<false, 1024><<<1, 1024, 0, s>>>(r, p, ids, n, slots_out, err);
     return hipGetLastError();
 }
 
@@ -89,7 +89,7 @@ hipError_t launch_dev_fill(const DevResidency &r, const uint8_t *host_dev, uint8
     if (expert_bytes <= 0 || expert_bytes % 16) return hipErrorInvalidValue;
     long long bpf = expert_bytes / (64 << 10);  // 32 blocks for a 9 MiB blob
     bpf = bpf < 4 ? 4 : (bpf > 32 ? 32 : bpf);
-    dev_fill_kernel<<<dim3(unsigned(bpf), unsigned(max_fills)), kDevThreads, 0, s>>>(r.fill_src, r.fill_slot,
+    dev_fill_kernel<<<dim3(unsigned(bpf), unsigned(max_fills)), kFillThreads, 0, s>>>(r.fill_src, r.fill_slot,
                                                                                      r.n_fill, host_dev, pool,
                                                                                      expert_bytes);
     return hipGetLastError();
