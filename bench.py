@@ -496,8 +496,8 @@ def main():
     if (args.prefetch or args.recall) and args.residency == "device":
         args.residency = "host"  # prefetch and recall decide on the host
     if args.gpus != 1:
-        print(f"bench.py measures one GPU: this build runs on a single MI355X and has no multi-GPU path "
-              f"(asked for --gpus {args.gpus})", file=sys.stderr)
+        print(f"bench.py measures one GPU: the library has no multi-GPU path (asked for --gpus {args.gpus})",
+              file=sys.stderr)
         sys.exit(2)
     import torch
 

@@ -8,11 +8,12 @@
 // (rotary) in LDS, forms the step's ascending unique experts from a presence
 // bitmap, and takes the same decisions, in the same order, as the host runtime:
 // a hit refreshes its slot; a miss takes the lowest free slot, else the least
-// recently used slot (LRU: a block-wide arg-min over the stamps of slots whose
-// expert the step does not need) or the slot where the forward rotation stops
-// (rotary: one lane turns the hand over the LDS copy).  Each decision is logged,
-// the slot table is updated in place, and the misses form a fill list that the
-// fill kernel then streams from pinned host memory.
+// recently used slot whose expert the step does not need (LRU: every expert of
+// the step decided at once by its own thread, the victims picked first) or the
+// slot where the forward rotation stops (rotary: one lane turns the hand over the
+// LDS copy).  Each decision is logged, the slot table is updated in place, and
+// the misses form a fill list that the fill kernel then streams from pinned host
+// memory.
 #include "residency_dev.h"
 
 namespace moe {
