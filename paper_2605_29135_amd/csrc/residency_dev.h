@@ -178,18 +178,15 @@ __device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const Dev
                     }
                 }
                 __syncthreads();
-                if (tid == 0) {
-                    int pos[NW] = {};
+                if (wave == 0) {  // the n_need smallest of the waves' NW * n_need picks, by wave minima
+                    unsigned long long c0 = ~0ull, c1 = ~0ull;
+                    if (lane < NW * n_need) c0 = vic_w[lane / n_need][lane % n_need];
+                    if (lane + kWaveDev < NW * n_need) c1 = vic_w[(lane + kWaveDev) / n_need][(lane + kWaveDev) % n_need];
                     for (int k2 = 0; k2 < n_need; ++k2) {
-                        int bw = 0;
-                        unsigned long long bv = ~0ull;
-                        for (int w = 0; w < NW; ++w)
-                            if (pos[w] < n_need && vic_w[w][pos[w]] < bv) {
-                                bv = vic_w[w][pos[w]];
-                                bw = w;
-                            }
-                        vic[k2] = int(bv & 4095ull);
-                        ++pos[bw];
+                        const unsigned long long best = dev::wave_reduce_u64<false>(c0 < c1 ? c0 : c1);
+                        if (lane == 0) vic[k2] = int(best & 4095ull);
+                        if (c0 == best) c0 = ~0ull;  // unique keys: one lane owns it
+                        if (c1 == best) c1 = ~0ull;
                     }
                 }
             } else {
@@ -247,6 +244,8 @@ __device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const Dev
                 r.fill_slot[q] = s;
             }
             stamp[s] = ctr + 1 + (unsigned long long)tid;
+            r.stamp[s] = ctr + 1 + (unsigned long long)tid;  // the only slots the step changes
+            if (miss) r.key_of_slot[s] = layer * E + e;
             slot_of_e[e] = s;
             const unsigned long long ev = n_ev + (unsigned long long)tid;
             if (ev < (unsigned long long)r.cap_events)
@@ -322,11 +321,11 @@ __device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const Dev
     __syncthreads();
     if (slots_out)
         for (int i = tid; i < n; i += NT) slots_out[i] = slot_of_e[ids[i]];
-    for (int s = tid; s < C; s += NT) {
-        r.key_of_slot[s] = key_of[s];
-        if constexpr (ROTARY) r.charge[s] = charge[s];
-        else r.stamp[s] = stamp[s];
-    }
+    if constexpr (ROTARY)  // the hand's turn changes charges along its path
+        for (int s = tid; s < C; s += NT) {
+            r.key_of_slot[s] = key_of[s];
+            r.charge[s] = charge[s];
+        }
 }
 
 }  // namespace devres
