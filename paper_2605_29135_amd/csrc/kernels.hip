@@ -150,9 +150,9 @@ __global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__res
 
 // One token's top-k fused with the device lookup of its experts (MOE_CACHE_DEVICE
 // decode): every thread first issues its reads of the slot state, then wave 0
-// ranks the experts and writes ids and weights while they are in flight, then
-// the whole block takes the slot table's decisions for them -- one launch and
-// one global round trip before the decisions.
+// ranks the experts and writes ids and weights while the other waves stage the
+// slot state in LDS, then the whole block takes the slot table's decisions for
+// them -- one launch and one global round trip before the decisions.
 template <bool ROTARY, int NT>
 __global__ __launch_bounds__(NT) void topk_lookup_kernel(const float *__restrict__ logits, int E, int k,
                                                              int32_t *__restrict__ ids, float *__restrict__ wout,
@@ -160,14 +160,16 @@ __global__ __launch_bounds__(NT) void topk_lookup_kernel(const float *__restrict
                                                              int32_t *__restrict__ slots_out) {
     __shared__ TopkScratch sc;
     __shared__ int32_t ids_l[MOE_MAX_TOPK];
+    __shared__ devres::DevLds<ROTARY, NT> L;
     devres::DevStaged st;
     devres::dev_stage_issue<ROTARY, NT>(r, p, st);
     if (threadIdx.x < kWave) {
         topk_wave<false>(logits, E, k, ids, wout, err, &sc);
         if (int(threadIdx.x) < k) ids_l[threadIdx.x] = sc.rid[threadIdx.x];  // the ranked ids (-1 if non-finite)
     }
+    devres::dev_stage_lds<ROTARY, NT>(L, p, st);  // the other waves stage while wave 0 ranks
     __syncthreads();
-    devres::dev_lookup_body<ROTARY, NT>(r, p, st, ids_l, k, slots_out, err);
+    devres::dev_lookup_body<ROTARY, NT>(L, r, p, ids_l, k, slots_out, err);
 }
 
 // --------------------------------------------------------------- router ---

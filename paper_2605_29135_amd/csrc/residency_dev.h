@@ -56,49 +56,71 @@ __device__ __forceinline__ int wave_prefix(const int *cnt, int wave, int &total)
     return pre;
 }
 
+// The lookup's LDS: the staged slot state and the step's working sets.
 template <bool ROTARY, int NT>
-__device__ __forceinline__ void dev_lookup_body(const DevResidency &r, const DevLookup &p, const DevStaged &st,
+struct DevLds {
+    static constexpr int NS = kDevPT * NT;  // slots staged (a power of two)
+    static constexpr int NW = NT / kWaveDev;
+    int32_t key_of[NS];
+    uint64_t stamp[ROTARY ? 1 : NS];  // LRU: recency stamps; also the sort buffer of the victims
+    uint16_t charge[ROTARY ? NS : 1];
+    uint32_t present[MOE_MAX_EXPERTS / 32];
+    int32_t R[MOE_MAX_EXPERTS];
+    int32_t slot_of_e[MOE_MAX_EXPERTS];  // slot of each expert of the step, by expert id
+    int32_t pre[MOE_MAX_EXPERTS];        // slot of each expert of the layer before the step
+    unsigned long long scal_sh[kDevScalars];
+    int step_sh;
+    int bad_sh;
+    int wcnt[NW];
+    unsigned long long vic_w[ROTARY ? 1 : NW][kFastVictims];
+    int vic[ROTARY ? 1 : MOE_MAX_EXPERTS];
+};
+
+// The staged registers into LDS (no ids needed: a caller may do this while the ids are formed).  A block
+// barrier must follow before dev_lookup_body.
+template <bool ROTARY, int NT>
+__device__ __forceinline__ void dev_stage_lds(DevLds<ROTARY, NT> &L, const DevLookup &p, const DevStaged &st) {
+    const int tid = threadIdx.x;
+#pragma unroll
+    for (int u = 0; u < kDevPT; ++u) {
+        if (u * NT >= p.C) break;  // uniform
+        const int s = tid + u * NT;
+        if (s < p.C) {
+            L.key_of[s] = st.kv[u];
+            if constexpr (ROTARY) L.charge[s] = uint16_t(st.sv[u]);
+            else L.stamp[s] = st.sv[u];
+        }
+    }
+    if (tid < p.E) L.pre[tid] = st.row;
+    if (tid < kDevScalars) L.scal_sh[tid] = st.sc0;
+    if (tid < MOE_MAX_EXPERTS / 32) L.present[tid] = 0u;
+    if (tid == 0) {
+        L.bad_sh = 0;
+        L.step_sh = st.step_v;
+    }
+}
+
+template <bool ROTARY, int NT>
+__device__ __forceinline__ void dev_lookup_body(DevLds<ROTARY, NT> &L, const DevResidency &r, const DevLookup &p,
                                                 const int32_t *ids, int n, int32_t *__restrict__ slots_out,
                                                 int *err) {
-    constexpr int NS = kDevPT * NT;  // slots staged (a power of two)
-    constexpr int NW = NT / kWaveDev;
-    __shared__ int32_t key_of[NS];
-    __shared__ uint64_t stamp[ROTARY ? 1 : NS];  // LRU: recency stamps; also the sort buffer of the victims
-    __shared__ uint16_t charge[ROTARY ? NS : 1];
-    __shared__ uint32_t present[MOE_MAX_EXPERTS / 32];
-    __shared__ int32_t R[MOE_MAX_EXPERTS];
-    __shared__ int32_t slot_of_e[MOE_MAX_EXPERTS];  // slot of each expert of the step, by expert id
-    __shared__ int32_t pre[MOE_MAX_EXPERTS];        // slot of each expert of the layer before the step
-    __shared__ unsigned long long scal_sh[kDevScalars];
-    __shared__ int step_sh;
-    __shared__ int bad_sh;
-    __shared__ int wcnt[NW];
-    __shared__ unsigned long long vic_w[ROTARY ? 1 : NW][kFastVictims];
-    __shared__ int vic[ROTARY ? 1 : MOE_MAX_EXPERTS];
+    constexpr int NS = DevLds<ROTARY, NT>::NS;
+    constexpr int NW = DevLds<ROTARY, NT>::NW;
+    int32_t *key_of = L.key_of;
+    uint64_t *stamp = L.stamp;
+    uint16_t *charge = L.charge;
+    uint32_t *present = L.present;
+    int32_t *R = L.R, *slot_of_e = L.slot_of_e, *pre = L.pre;
+    unsigned long long *scal_sh = L.scal_sh;
+    int &step_sh = L.step_sh, &bad_sh = L.bad_sh;
+    int *wcnt = L.wcnt;
+    auto &vic_w = L.vic_w;
+    int *vic = L.vic;
     const int tid = threadIdx.x, lane = tid & (kWaveDev - 1), wave = tid / kWaveDev;
     const int C = p.C, E = p.E, layer = p.layer;
     {
-        const int32_t id0 = ids[min(tid, max(n - 1, 0))];
-#pragma unroll
-        for (int u = 0; u < kDevPT; ++u) {
-            if (u * NT >= C) break;  // uniform
-            const int s = tid + u * NT;
-            if (s < C) {
-                key_of[s] = st.kv[u];
-                if constexpr (ROTARY) charge[s] = uint16_t(st.sv[u]);
-                else stamp[s] = st.sv[u];
-            }
-        }
-        if (tid < E) pre[tid] = st.row;
-        if (tid < kDevScalars) scal_sh[tid] = st.sc0;
-        if (tid < MOE_MAX_EXPERTS / 32) present[tid] = 0u;
-        if (tid == 0) {
-            bad_sh = 0;
-            step_sh = st.step_v;
-        }
-        __syncthreads();
         for (int i = tid; i < n; i += NT) {
-            const int e = i == tid ? id0 : ids[i];  // steps of more than one block of ids read the rest here
+            const int e = ids[i];
             if (e < 0 || e >= E) atomicOr(&bad_sh, 1);
             else atomicOr(&present[e >> 5], 1u << (e & 31));
         }

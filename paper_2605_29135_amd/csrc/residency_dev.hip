@@ -29,9 +29,12 @@ constexpr int kFillThreads = 256;
 template <bool ROTARY, int NT>
 __global__ __launch_bounds__(NT) void dev_lookup_kernel(DevResidency r, DevLookup p, const int32_t *__restrict__ ids,
                                                         int n, int32_t *__restrict__ slots_out, int *err) {
+    __shared__ DevLds<ROTARY, NT> L;
     DevStaged st;
     dev_stage_issue<ROTARY, NT>(r, p, st);
-    dev_lookup_body<ROTARY, NT>(r, p, st, ids, n, slots_out, err);
+    dev_stage_lds<ROTARY, NT>(L, p, st);
+    __syncthreads();
+    dev_lookup_body<ROTARY, NT>(L, r, p, ids, n, slots_out, err);
 }
 
 // Block (x, f) streams its share of fill f; blocks past the lookup's fill count exit.
