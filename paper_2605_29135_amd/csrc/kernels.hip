@@ -163,13 +163,29 @@ __global__ __launch_bounds__(NT) void topk_lookup_kernel(const float *__restrict
     __shared__ devres::DevLds<ROTARY, NT> L;
     devres::DevStaged st;
     devres::dev_stage_issue<ROTARY, NT>(r, p, st);
+    const int lane = threadIdx.x & (kWave - 1);
     if (threadIdx.x < kWave) {
         topk_wave<false>(logits, E, k, ids, wout, err, &sc);
-        if (int(threadIdx.x) < k) ids_l[threadIdx.x] = sc.rid[threadIdx.x];  // the ranked ids (-1 if non-finite)
+        const int id = lane < k ? sc.rid[lane] : 0;  // the ranked ids (-1 if non-finite)
+        if (lane < k) ids_l[lane] = id;
+        devres::dev_stage_lds<ROTARY, NT>(L, p, st);  // wave 0's share (it clears the presence bits)
+        // the step's ascending experts and presence bits from the k distinct ids
+        int rank = 0;
+        for (int j = 0; j < k; ++j) rank += __builtin_amdgcn_readlane(id, j) < id;
+        const bool bad = lane < k && (id < 0 || id >= E);
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup");  // the cleared bits before the new ones
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup");
+        if (lane < k && !bad) {
+            L.R[rank] = id;
+            atomicOr(&L.present[id >> 5], 1u << (id & 31));
+        }
+        if (__any(bad) && lane == 0) L.bad_sh = 1;
+    } else {
+        devres::dev_stage_lds<ROTARY, NT>(L, p, st);  // the other waves stage while wave 0 ranks
     }
-    devres::dev_stage_lds<ROTARY, NT>(L, p, st);  // the other waves stage while wave 0 ranks
     __syncthreads();
-    devres::dev_lookup_body<ROTARY, NT>(L, r, p, ids_l, k, slots_out, err);
+    devres::dev_lookup_body<ROTARY, NT, true>(L, r, p, ids_l, k, slots_out, err);
 }
 
 // --------------------------------------------------------------- router ---

@@ -100,7 +100,9 @@ __device__ __forceinline__ void dev_stage_lds(DevLds<ROTARY, NT> &L, const DevLo
     }
 }
 
-template <bool ROTARY, int NT>
+// FORMED: the caller has already set the step's presence bits and its ascending experts R (with bad_sh set
+// for an id out of range), before the barrier that precedes this call.
+template <bool ROTARY, int NT, bool FORMED = false>
 __device__ __forceinline__ void dev_lookup_body(DevLds<ROTARY, NT> &L, const DevResidency &r, const DevLookup &p,
                                                 const int32_t *ids, int n, int32_t *__restrict__ slots_out,
                                                 int *err) {
@@ -118,14 +120,14 @@ __device__ __forceinline__ void dev_lookup_body(DevLds<ROTARY, NT> &L, const Dev
     int *vic = L.vic;
     const int tid = threadIdx.x, lane = tid & (kWaveDev - 1), wave = tid / kWaveDev;
     const int C = p.C, E = p.E, layer = p.layer;
-    {
+    if constexpr (!FORMED) {
         for (int i = tid; i < n; i += NT) {
             const int e = ids[i];
             if (e < 0 || e >= E) atomicOr(&bad_sh, 1);
             else atomicOr(&present[e >> 5], 1u << (e & 31));
         }
+        __syncthreads();
     }
-    __syncthreads();
     // the step's unique experts: every thread counts them; thread w writes word w's experts at its offset
     const int nw = (E + 31) / 32;
     int m = 0;
@@ -137,12 +139,14 @@ __device__ __forceinline__ void dev_lookup_body(DevLds<ROTARY, NT> &L, const Dev
         }
         return;
     }
-    if (tid < nw) {
-        int off = 0;
-        for (int w = 0; w < tid; ++w) off += __popc(present[w]);
-        for (uint32_t b = present[tid]; b; b &= b - 1u) R[off++] = tid * 32 + __builtin_ctz(b);
+    if constexpr (!FORMED) {
+        if (tid < nw) {
+            int off = 0;
+            for (int w = 0; w < tid; ++w) off += __popc(present[w]);
+            for (uint32_t b = present[tid]; b; b &= b - 1u) R[off++] = tid * 32 + __builtin_ctz(b);
+        }
+        __syncthreads();
     }
-    __syncthreads();
     auto pinned = [&](int k2) {  // is slot key k2 an expert of this step?
         const int e2 = k2 - layer * E;
         return e2 >= 0 && e2 < E && ((present[e2 >> 5] >> (e2 & 31)) & 1u);
