@@ -78,7 +78,10 @@ hipError_t launch_fill_slots(const FillBatch &b, hipStream_t s);
 // needs no host round trip.  Decisions are those of the host runtime (LRU or
 // rotary), event for event.
 constexpr int kDevMaxSlots = 4096;
-enum : int { kScalCtr, kScalHand, kScalNextFree, kScalHits, kScalMisses, kScalEvictions, kScalEvents, kDevScalars };
+enum : int {
+    kScalCtr, kScalHand, kScalNextFree, kScalHits, kScalMisses, kScalEvictions, kScalEvents, kScalPrefetches,
+    kDevScalars
+};
 struct DevResidency {
     int32_t *key_of_slot = nullptr;      // [C] layer*E + expert, -1 = free
     uint64_t *stamp = nullptr;           // [C] LRU: recency stamp
@@ -95,6 +98,7 @@ struct DevLookup {
     int C, L, E, layer, step, rotary, charge_max;
     long long layer_stride, expert_stride;
     const int *step_dev = nullptr;  // when set, the step tag of the decisions is read here instead of `step`
+    int prefetch = 0;               // 1: insert the non-resident ids only, as expert_cache_prefetch does
 };
 // Sets *p = v on the stream (a one-lane kernel: a graph replay reads the step tag from device memory).
 hipError_t launch_set_int(int *p, int v, hipStream_t s);
@@ -152,6 +156,12 @@ size_t cache_expert_bytes(const struct ::moe_cache *c);
 bool cache_preloaded(const struct ::moe_cache *c);
 bool cache_resident(const struct ::moe_cache *c, int layer, int expert);  // host mirror
 bool cache_device(const struct ::moe_cache *c);  // lookups run on the device (MOE_CACHE_DEVICE)
+int cache_capacity(const struct ::moe_cache *c);  // slots
+bool cache_rotary(const struct ::moe_cache *c);   // MOE_POLICY_ROTARY
+// MOE_CACHE_DEVICE: enqueue on `s` the prefetch of ids_dev[0..n) at `layer` (non-resident ones inserted, logged
+// as prefetches; resident ones untouched), its fills on the cache's copy stream; the next device lookup waits
+// for those fills.  Returns an MOE_ERR_* code.
+int cache_prefetch_device(struct ::moe_cache *c, int step, int layer, const int32_t *ids_dev, int n, hipStream_t s);
 // MOE_CACHE_DEVICE, one token: enqueue top-k of `logits` fused with the lookup of the chosen experts, then
 // the fills of its misses.  Returns an MOE_ERR_* code.
 int cache_topk_lookup(struct ::moe_cache *c, int step, int layer, const float *logits, int k, int32_t *ids,

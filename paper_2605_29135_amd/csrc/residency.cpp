@@ -116,6 +116,9 @@ struct moe_cache {
 
     bool dev_mode = false;   // MOE_CACHE_DEVICE: decisions and log on the device
     moe::DevResidency dr;
+    // MOE_CACHE_DEVICE prefetch: its decisions on the caller's stream, its fills on the copy stream
+    hipEvent_t pf_issued = nullptr, pf_done = nullptr;
+    bool pf_pending = false;  // a prefetch's fills may still run: the next lookup waits for pf_done
 };
 
 namespace {
@@ -377,6 +380,40 @@ bool moe::cache_resident(const moe_cache *c, int layer, int expert) {
     return c->slot_of_key[size_t(layer) * c->E + expert] >= 0;
 }
 bool moe::cache_device(const moe_cache *c) { return c->dev_mode; }
+int moe::cache_capacity(const moe_cache *c) { return c->C; }
+bool moe::cache_rotary(const moe_cache *c) { return c->d.policy == MOE_POLICY_ROTARY; }
+
+namespace {
+// A device lookup rewrites the fill list and may evict: an earlier device prefetch's fills come first.
+hipError_t after_device_prefetch(moe_cache *c, hipStream_t s) {
+    if (!c->pf_pending) return hipSuccess;
+    c->pf_pending = false;
+    return hipStreamWaitEvent(s, c->pf_done, 0);
+}
+}  // namespace
+
+int moe::cache_prefetch_device(moe_cache *c, int step, int layer, const int32_t *ids_dev, int n, hipStream_t s) {
+    if (!c || !c->dev_mode || layer < 0 || layer >= c->L || n < 0 || (n > 0 && !ids_dev))
+        return moe::fail(MOE_ERR_INVALID_ARG, "device prefetch needs a MOE_CACHE_DEVICE cache, a valid layer and ids");
+    if (n == 0) return MOE_OK;
+    int *err = moe::device_error_flags();
+    if (!err) return moe::fail(MOE_ERR_HIP, "device error flags unavailable");
+    moe::DevLookup p{c->C, c->L, c->E, layer, step, c->d.policy == MOE_POLICY_ROTARY ? 1 : 0, c->charge_max,
+                     (long long)c->d.host_layer_stride, (long long)c->d.host_expert_stride};
+    p.prefetch = 1;
+    hipError_t e = after_device_prefetch(c, s);
+    if (e == hipSuccess) e = moe::launch_dev_lookup(c->dr, p, ids_dev, n, nullptr, err, s);
+    // the fills go to the copy stream, so that work the caller queues next on `s` overlaps them
+    if (e == hipSuccess) e = hipEventRecord(c->pf_issued, s);
+    if (e == hipSuccess) e = hipStreamWaitEvent(c->copy, c->pf_issued, 0);
+    if (e == hipSuccess)
+        e = moe::launch_dev_fill(c->dr, c->host_dev, c->pool, (long long)c->d.expert_bytes, std::min(n, c->E),
+                                 c->copy);
+    if (e == hipSuccess) e = hipEventRecord(c->pf_done, c->copy);
+    if (e != hipSuccess) return moe::fail_hip(e, "device prefetch");
+    c->pf_pending = true;
+    return MOE_OK;
+}
 
 int moe::cache_topk_lookup(moe_cache *c, int step, int layer, const float *logits, int k, int32_t *ids,
                            float *weights, int32_t *slots_out, int *err_flags, hipStream_t s, const int *step_dev) {
@@ -384,7 +421,8 @@ int moe::cache_topk_lookup(moe_cache *c, int step, int layer, const float *logit
         return moe::fail(MOE_ERR_INVALID_ARG, "fused top-k lookup needs a MOE_CACHE_DEVICE cache and a valid layer");
     moe::DevLookup p{c->C, c->L, c->E, layer, step, c->d.policy == MOE_POLICY_ROTARY ? 1 : 0, c->charge_max,
                      (long long)c->d.host_layer_stride, (long long)c->d.host_expert_stride, step_dev};
-    hipError_t e = moe::launch_topk_lookup(logits, c->E, k, ids, weights, err_flags, c->dr, p, slots_out, s);
+    hipError_t e = after_device_prefetch(c, s);
+    if (e == hipSuccess) e = moe::launch_topk_lookup(logits, c->E, k, ids, weights, err_flags, c->dr, p, slots_out, s);
     if (e == hipSuccess)
         e = moe::launch_dev_fill(c->dr, c->host_dev, c->pool, (long long)c->d.expert_bytes, std::min(k, c->E), s);
     return e == hipSuccess ? MOE_OK : moe::fail_hip(e, "fused top-k lookup");
@@ -519,6 +557,9 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
         if ((e = hipStreamCreateWithFlags(&c->copy, hipStreamNonBlocking)) != hipSuccess)
             return cleanup(moe::fail_hip(e, "creating the copy stream"));
         if ((e = c->ring.init()) != hipSuccess) return cleanup(moe::fail_hip(e, "creating events"));
+        if (dev_mode && ((e = hipEventCreateWithFlags(&c->pf_issued, hipEventDisableTiming)) != hipSuccess ||
+                         (e = hipEventCreateWithFlags(&c->pf_done, hipEventDisableTiming)) != hipSuccess))
+            return cleanup(moe::fail_hip(e, "creating events"));
     }
     if (preload) {
         for (int l = 0; l < c->L; ++l)
@@ -565,6 +606,8 @@ int expert_cache_destroy(moe_cache *c) {
         if (c->have_last_compute) (void)hipStreamSynchronize(c->last_compute);
         c->ring.destroy();
         dev_state_destroy(c);
+        if (c->pf_issued) (void)hipEventDestroy(c->pf_issued);
+        if (c->pf_done) (void)hipEventDestroy(c->pf_done);
         if (c->copy) (void)hipStreamDestroy(c->copy);
         if (c->pool) (void)hipFree(c->pool);
         if (c->dev_slot_of) (void)hipFree(c->dev_slot_of);
@@ -585,7 +628,8 @@ int expert_cache_lookup_device(moe_cache *c, int step, int layer, const int32_t 
     moe::DevLookup p{c->C, c->L, c->E, layer, step, c->d.policy == MOE_POLICY_ROTARY ? 1 : 0, c->charge_max,
                      (long long)c->d.host_layer_stride, (long long)c->d.host_expert_stride};
     auto s = static_cast<hipStream_t>(stream);
-    hipError_t e = moe::launch_dev_lookup(c->dr, p, ids_dev, n, slots_out_dev, err, s);
+    hipError_t e = after_device_prefetch(c, s);
+    if (e == hipSuccess) e = moe::launch_dev_lookup(c->dr, p, ids_dev, n, slots_out_dev, err, s);
     if (e == hipSuccess)
         e = moe::launch_dev_fill(c->dr, c->host_dev, c->pool, (long long)c->d.expert_bytes, std::min(n, c->E), s);
     if (e != hipSuccess) return moe::fail_hip(e, "device lookup");
@@ -628,9 +672,10 @@ int expert_cache_stats(moe_cache *c, moe_cache_stats *out) {
         *out = moe_cache_stats{};
         out->hits = v[moe::kScalHits];
         out->misses = v[moe::kScalMisses];
+        out->prefetches = v[moe::kScalPrefetches];
         out->lookups = out->hits + out->misses;
         out->evictions = v[moe::kScalEvictions];
-        out->h2d_bytes = out->misses * c->d.expert_bytes;
+        out->h2d_bytes = (out->misses + out->prefetches) * c->d.expert_bytes;
         out->capacity = c->C;
         out->occupancy = int32_t(std::min<unsigned long long>(v[moe::kScalNextFree], (unsigned long long)c->C));
         return MOE_OK;

@@ -154,14 +154,17 @@ __device__ __forceinline__ void dev_lookup_body(DevLds<ROTARY, NT> &L, const Dev
     int n_fill = 0;
     unsigned long long ctr = scal_sh[kScalCtr], hand = scal_sh[kScalHand], next_free = scal_sh[kScalNextFree],
                        hits = scal_sh[kScalHits], misses = scal_sh[kScalMisses],
-                       evictions = scal_sh[kScalEvictions], n_ev = scal_sh[kScalEvents];
+                       evictions = scal_sh[kScalEvictions], n_ev = scal_sh[kScalEvents],
+                       prefetches = scal_sh[kScalPrefetches];
+    // a prefetch inserts the step's non-resident experts (events PREFETCH) and leaves resident ones untouched
+    const bool pf = p.prefetch != 0;
     if constexpr (!ROTARY) {
         // LRU in closed form.  Every expert of the step takes the next stamp in ascending-id order, and no slot
         // outside the step changes while the step is decided (hits and new entries are the step's own slots,
         // which are never victims).  So expert j takes stamp ctr + 1 + j and event n_ev + j; a resident one
         // keeps its slot; the q-th miss takes free slot next_free + q while free slots last, and after that the
         // least recently used slots outside the step in ascending stamp order.  Thread j decides expert j
-        // (m <= MOE_MAX_EXPERTS <= NT).
+        // (m <= MOE_MAX_EXPERTS <= NT).  A prefetch takes stamps and events for its misses only, in order.
         const bool act = tid < m;
         const int e = act ? R[tid] : 0;
         const int spre = act ? pre[e] : 0;
@@ -269,20 +272,28 @@ __device__ __forceinline__ void dev_lookup_body(DevLds<ROTARY, NT> &L, const Dev
                 r.fill_src[q] = (long long)layer * p.layer_stride + (long long)e * p.expert_stride;
                 r.fill_slot[q] = s;
             }
-            stamp[s] = ctr + 1 + (unsigned long long)tid;
-            r.stamp[s] = ctr + 1 + (unsigned long long)tid;  // the only slots the step changes
-            if (miss) r.key_of_slot[s] = layer * E + e;
             slot_of_e[e] = s;
-            const unsigned long long ev = n_ev + (unsigned long long)tid;
-            if (ev < (unsigned long long)r.cap_events)
-                r.events[ev] = moe_cache_event{step_sh, layer, e, miss ? MOE_EVENT_MISS : MOE_EVENT_HIT, s, victim};
+            if (miss || !pf) {
+                const unsigned long long rank = (unsigned long long)(pf ? q : tid);
+                stamp[s] = ctr + 1 + rank;
+                r.stamp[s] = ctr + 1 + rank;  // the only slots the step changes
+                if (miss) r.key_of_slot[s] = layer * E + e;
+                const unsigned long long ev = n_ev + rank;
+                const int kind = miss ? (pf ? MOE_EVENT_PREFETCH : MOE_EVENT_MISS) : MOE_EVENT_HIT;
+                if (ev < (unsigned long long)r.cap_events) r.events[ev] = moe_cache_event{step_sh, layer, e, kind, s, victim};
+            }
         }
-        ctr += (unsigned long long)m;
+        const int n_dec = pf ? nm : m;  // decisions logged
+        ctr += (unsigned long long)n_dec;
+        n_ev += (unsigned long long)n_dec;
         next_free += (unsigned long long)(nm < nfree ? nm : nfree);
-        hits += (unsigned long long)(m - nm);
-        misses += (unsigned long long)nm;
+        if (pf) {
+            prefetches += (unsigned long long)nm;
+        } else {
+            hits += (unsigned long long)(m - nm);
+            misses += (unsigned long long)nm;
+        }
         evictions += (unsigned long long)n_need;  // free slots held no expert
-        n_ev += (unsigned long long)m;
         n_fill = nm;
     } else {
         // Rotary: lane 0 walks the step's experts in order.  A hit adds a charge; a miss takes the lowest free
@@ -295,6 +306,8 @@ __device__ __forceinline__ void dev_lookup_body(DevLds<ROTARY, NT> &L, const Dev
                 int s = pre[e], victim = -1;
                 const bool miss = s < 0;
                 if (!miss) {
+                    slot_of_e[e] = s;
+                    if (pf) continue;
                     if (charge[s] < p.charge_max) ++charge[s];
                     ++hits;
                 } else {
@@ -321,15 +334,16 @@ __device__ __forceinline__ void dev_lookup_body(DevLds<ROTARY, NT> &L, const Dev
                     key_of[s] = key;
                     r.slot_of_key[key] = s;
                     charge[s] = 0;
-                    ++misses;
+                    if (pf) ++prefetches;
+                    else ++misses;
                     r.fill_src[n_fill] = (long long)layer * p.layer_stride + (long long)e * p.expert_stride;
                     r.fill_slot[n_fill] = s;
                     ++n_fill;
                 }
                 slot_of_e[e] = s;
+                const int kind = miss ? (pf ? MOE_EVENT_PREFETCH : MOE_EVENT_MISS) : MOE_EVENT_HIT;
                 if (n_ev < (unsigned long long)r.cap_events)
-                    r.events[n_ev] =
-                        moe_cache_event{step_sh, layer, e, miss ? MOE_EVENT_MISS : MOE_EVENT_HIT, s, victim};
+                    r.events[n_ev] = moe_cache_event{step_sh, layer, e, kind, s, victim};
                 ++n_ev;
             }
         }
@@ -342,6 +356,7 @@ __device__ __forceinline__ void dev_lookup_body(DevLds<ROTARY, NT> &L, const Dev
         r.scal[kScalMisses] = misses;
         r.scal[kScalEvictions] = evictions;
         r.scal[kScalEvents] = n_ev;
+        r.scal[kScalPrefetches] = prefetches;
         r.n_fill[0] = n_fill;
     }
     __syncthreads();

@@ -60,6 +60,7 @@ struct moe_stack {
     int32_t *slots_host = nullptr; // [Tmax x k] slot of each id after the lookup
     int32_t *dev_slots = nullptr;  // device [L x max_tokens x k]: slot of each id after each layer's device lookup
     int *dev_step = nullptr;       // device: step tag of a replayed decode graph's decisions
+    int32_t *all_experts = nullptr;  // device [E]: 0..E-1, the prefill's prefetch of a whole layer
     bool attn = false;             // a self-attention block before each MoE block
     moe_attention_desc ad{};       // its shapes (the arrays below hold its per-layer buffers)
     std::vector<const void *> a_wqkv, a_wo;
@@ -195,6 +196,7 @@ int moe_stack_destroy(moe_stack *s) {
     if (s->scratch_y) (void)hipFree(s->scratch_y);
     if (s->dev_slots) (void)hipFree(s->dev_slots);
     if (s->dev_step) (void)hipFree(s->dev_step);
+    if (s->all_experts) (void)hipFree(s->all_experts);
     if (s->attn_ws) (void)hipFree(s->attn_ws);
     if (s->graph_exec) (void)hipGraphExecDestroy(s->graph_exec);
     delete s;
@@ -268,6 +270,14 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
         ((e = hipMalloc(&s->dev_slots, sizeof(int32_t) * size_t(d->n_layers) * d->max_tokens * d->k)) != hipSuccess ||
          (e = hipMalloc(&s->dev_step, sizeof(int))) != hipSuccess))
         return bail(e, "stack buffers");
+    if (moe::cache_device(d->cache) && d->max_prefill_tokens > 0) {
+        std::vector<int32_t> iota(size_t(d->E));
+        for (int i = 0; i < d->E; ++i) iota[size_t(i)] = i;
+        if ((e = hipMalloc(&s->all_experts, sizeof(int32_t) * size_t(d->E))) != hipSuccess ||
+            (e = hipMemcpy(s->all_experts, iota.data(), sizeof(int32_t) * size_t(d->E), hipMemcpyHostToDevice)) !=
+                hipSuccess)
+            return bail(e, "stack buffers");
+    }
     if (const moe_attention_desc *a = d->attention) {
         s->attn = true;
         s->ad = *a;
@@ -480,6 +490,19 @@ int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out,
     if (!eflags) return moe::fail(MOE_ERR_HIP, "device error flags unavailable");
     const auto &d = s->d;
     const moe::PrefillWorkspace ws = moe::prefill_workspace(s->pws, T, d.k, d.E, d.H, d.I);
+    // Device LRU residency, a chunk long enough to use nearly every expert (T k >= 8 E) and room for two
+    // whole layers: each layer's experts are prefetched (decisions on this stream, fills on the cache's copy
+    // stream) right after the previous layer's lookup, so that they stream in while that layer's expert FFN
+    // and the next routing run.  The previous layer's experts hold the most recent stamps, and with 2 E
+    // slots or more at least E slots are older, so no prefetch victim is a slot that FFN still reads.  (A
+    // rotary hand may stop at any slot outside the step: rotary stacks do not pipeline.)
+    const bool dev_lookup = s->budgeted && moe::cache_device(d.cache);
+    const bool pipe = dev_lookup && s->all_experts && moe::cache_capacity(d.cache) >= 2 * d.E &&
+                      size_t(T) * d.k >= size_t(8) * d.E && !moe::cache_rotary(d.cache);
+    if (pipe) {
+        int st = moe::cache_prefetch_device(d.cache, step, 0, s->all_experts, d.E, strm);
+        if (st != MOE_OK) return st;
+    }
     for (int l = 0; l < d.n_layers; ++l) {
         int32_t *ids = ids_out ? ids_out + size_t(l) * T * d.k : s->ids;
         float *w = weights_out ? weights_out + size_t(l) * T * d.k : s->weights;
@@ -489,9 +512,10 @@ int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out,
         if (e != hipSuccess) return moe::fail_hip(e, "stack prefill: routing");
         const int32_t *slot_of = s->slot_table + size_t(l) * d.E;
         const uint8_t *pool = static_cast<const uint8_t *>(s->pool);
-        const bool dev_lookup = s->budgeted && moe::cache_device(d.cache);
         if (dev_lookup) {
             int st = expert_cache_lookup_device(d.cache, step, l, ids, T * d.k, nullptr, strm);
+            if (st == MOE_OK && pipe && l + 1 < d.n_layers)
+                st = moe::cache_prefetch_device(d.cache, step, l + 1, s->all_experts, d.E, strm);
             if (st != MOE_OK) return st;
         } else if (s->budgeted) {
             e = hipMemcpyAsync(s->ids_host, ids, sizeof(int32_t) * T * d.k, hipMemcpyDeviceToHost, strm);

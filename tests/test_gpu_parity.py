@@ -725,6 +725,67 @@ def test_stack_prefill_then_decode_budgeted(dtype, shared):
     buf.close()
 
 
+@pytest.mark.parametrize("dtype", [synth.BF16, synth.INT4G128])
+def test_stack_prefill_pipelined_device_prefetch(dtype):
+    """Device LRU residency with room for two layers and a chunk that uses nearly every expert: the stack
+    prefetches each layer's experts (fills on the copy stream) while the previous layer's FFN runs.  The
+    decision log equals the oracle LRU's for the same sequence (prefetch layer 0; per layer: demand lookup,
+    then prefetch of the next layer), outputs match the oracle chain, and decode steps continue on the cache."""
+    H = 2048 if dtype == synth.INT4G128 else 512
+    wl = synth.Workload("prefill pipe", H=H, E=16, k=4, I=256, L=4, dtype=dtype, shared=True,
+                        routing="zipf_overlap", cfg_id=130 + dtype)
+    capacity, T = 40, 64  # 2E <= 40 < L E: layers evict each other; T k = 256 >= 8 E
+    buf = _pinned_store(wl)
+    eb = wl.expert_bytes
+    reserved = wl.L * eb
+    cache = moe.ExpertCache(wl.L, wl.E, eb, capacity * eb + reserved, buf.ptr, wl.E * eb, eb,
+                            reserved_bytes=reserved, device=True)
+    routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
+    shw = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)]
+    stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shw, max_tokens=1,
+                         max_prefill_tokens=T)
+    x0 = np.random.default_rng(dtype + 3).standard_normal((T, wl.H)).astype(np.float32)
+    x = dev(x0)
+    ids = torch.empty((wl.L, T, wl.k), dtype=torch.int32, device=DEV)
+    w = torch.empty((wl.L, T, wl.k), dtype=torch.float32, device=DEV)
+    stack.prefill(0, x, ids, w)
+    moe.moe_sync_check()
+    g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
+    o = oracle.LRU(capacity, wl.L, wl.E)
+    every = np.arange(wl.E, dtype=np.int32)
+    assert o.lookup(0, 0, every, prefetch=True) == oracle.OK
+    for l in range(wl.L):
+        assert o.lookup(0, l, g_ids[l].reshape(-1)) == oracle.OK
+        if l + 1 < wl.L:
+            assert o.lookup(0, l + 1, every, prefetch=True) == oracle.OK
+    host_layers = {}
+    xr = _oracle_chain(wl, x0, g_ids, g_w, host_layers)
+    assert normwise(x.cpu().numpy() - x0, xr - x0) <= PREFILL_TOL[dtype]
+    sets = synth.routing_sets(wl, steps=3)
+    for t in range(3):
+        xd0 = synth.hidden_states(wl, t)
+        bias = np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)])
+        xd = dev(xd0)
+        di = torch.empty((wl.L, 1, wl.k), dtype=torch.int32, device=DEV)
+        dw = torch.empty((wl.L, 1, wl.k), dtype=torch.float32, device=DEV)
+        stack.decode_step(1 + t, xd, dev(bias), di, dw)
+        moe.moe_sync_check()
+        for l in range(wl.L):
+            assert o.lookup(1 + t, l, di.cpu().numpy()[l].reshape(-1)) == oracle.OK
+        xr = _oracle_chain(wl, xd0, di.cpu().numpy(), dw.cpu().numpy(), host_layers)
+        assert normwise(xd.cpu().numpy() - xd0, xr - xd0) <= TOL[dtype]
+    ev, oev = cache.trace(), o.events()
+    assert len(ev) == len(oev)
+    assert (ev.view(np.int32).reshape(-1, 6) == oev.view(np.int32).reshape(-1, 6)).all()
+    s, so = cache.stats(), o.stats()
+    assert (s["hits"], s["misses"], s["prefetches"], s["evictions"]) == \
+        (so["hits"], so["misses"], so["prefetches"], so["evictions"])
+    assert so["prefetches"] > 0 and so["evictions"] > 0
+    stack.close()
+    cache.close()
+    buf.close()
+
+
 def test_stack_prefill_config5_two_layers_sampled():
     """Config 5's full 2048-token chunk through two of its layers (6 GiB budget: 3923 slots), checked on
     sampled tokens against the oracle chain."""
