@@ -421,7 +421,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     rows = Tp * k + Tp
     pf_flop = 2.0 * rows * (2 * I) * H + 2.0 * rows * H * I
 
-    d_pf = {f: st1[f] - st0[f] for f in ("lookups", "hits", "misses", "evictions", "h2d_bytes")}
+    d_pf = {f: st1[f] - st0[f] for f in ("lookups", "hits", "misses", "evictions", "prefetches", "h2d_bytes")}
     d_dec = {f: st3[f] - st2[f] for f in ("lookups", "hits", "misses", "evictions", "h2d_bytes")}
     ceil = max(pcie_ceiling_gbps(torch, moe, eb, 256 * eb), pcie_ceiling_gbps(torch, moe, 64 << 20, 1 << 30))
     h2d_tok = d_dec["h2d_bytes"] / steps
@@ -468,6 +468,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
                     "ffn_us": ktimes["ffn"] * 1e3, "ffn_GBps": (gu_bytes + dn_bytes) / (ktimes["ffn"] * 1e-3) / 1e9},
         "prefill": {"tokens": Tp, "tokens_per_s": Tp / t_prefill, "ms": t_prefill * 1e3,
                     "h2d_bytes": d_pf["h2d_bytes"], "misses": d_pf["misses"],
+                    "prefetches": d_pf["prefetches"],
                     "h2d_GBps": d_pf["h2d_bytes"] / t_prefill / 1e9,
                     "layer_ffn_ms": pf_ms, "layer_ffn_flop": pf_flop,
                     "roofline": {"bound": "mfma", "kernel": "one layer's prompt-chunk expert FFN (grouping, "

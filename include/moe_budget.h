@@ -290,8 +290,9 @@ MOE_API int expert_cache_create(const moe_cache_desc *desc, moe_cache **out);
  * kernel that streams the misses from the host store: a decode step needs no
  * host round trip.  Needs capacity <= 4096 and n_experts <= 256; cannot be
  * combined with MOE_CACHE_HOST_SIM.  In this mode expert_cache_lookup and
- * expert_cache_prefetch return MOE_ERR_INVALID_ARG, expert_cache_release does
- * nothing, and expert_cache_stats / expert_cache_trace synchronise the device. */
+ * expert_cache_prefetch return MOE_ERR_INVALID_ARG (their _device forms take
+ * their place), expert_cache_release does nothing, and expert_cache_stats /
+ * expert_cache_trace synchronise the device. */
 
 /* Device lookup (MOE_CACHE_DEVICE only): enqueues on `stream` the lookup of the
  * experts ids_dev[0..n) (device int32, e.g. as written by moe_route_topk) of
@@ -303,6 +304,23 @@ MOE_API int expert_cache_create(const moe_cache_desc *desc, moe_cache **out);
  * ordered: issue them on one stream. */
 MOE_API int expert_cache_lookup_device(moe_cache *c, int step, int layer, const int32_t *ids_dev, int n,
                                        int32_t *slots_out_dev, void *stream);
+
+/* Device prefetch (MOE_CACHE_DEVICE only): the speculative insert of
+ * expert_cache_prefetch with device ids (int32 [n], e.g. a routing result or
+ * a fixed list): non-resident ids are placed like misses, counted as
+ * prefetches and logged with MOE_EVENT_PREFETCH; resident ids are left
+ * untouched.  The decisions are enqueued on `stream`; the fills run on the
+ * cache's copy stream after everything queued on `stream` before this call,
+ * so work queued next on `stream` overlaps them, and the next device lookup
+ * or prefetch waits for them.  A victim may be any slot outside this call's
+ * set: work queued on `stream` after this call must not read slots returned
+ * by an earlier lookup, unless LRU cannot evict them (no lookup in between
+ * and capacity >= that lookup's distinct experts + this call's: the earlier
+ * set's stamps are newer than every victim's).  Errors as for
+ * expert_cache_lookup_device (range and budget errors in the device flags,
+ * changing nothing). */
+MOE_API int expert_cache_prefetch_device(moe_cache *c, int step, int layer, const int32_t *ids_dev, int n,
+                                         void *stream);
 
 /* Wait for the cache's copies and free everything it owns. */
 MOE_API int expert_cache_destroy(moe_cache *c);

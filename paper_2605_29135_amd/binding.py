@@ -90,6 +90,7 @@ def lib() -> C.CDLL:
             "expert_cache_destroy": [P],
             "expert_cache_lookup": [P, I, I, P, I, P, P, P],
             "expert_cache_lookup_device": [P, I, I, P, I, P, P],
+            "expert_cache_prefetch_device": [P, I, I, P, I, P],
             "expert_cache_prefetch": [P, I, I, P, I],
             "expert_cache_release": [P, P],
             "expert_cache_slot_table": [P, C.POINTER(P), C.POINTER(P)],
@@ -348,6 +349,12 @@ class ExpertCache:
         _check(lib().expert_cache_lookup_device(self._h, step, layer, _dev(ids, "ids", torch.int32), ids.numel(),
                                                 _dev(slots_out, "slots_out", torch.int32), _stream(stream)),
                "expert_cache_lookup_device")
+
+    def prefetch_device(self, step: int, layer: int, ids, stream=None):
+        """Device prefetch (MOE_CACHE_DEVICE): decisions on `stream`, fills on the cache's copy stream."""
+        import torch
+        _check(lib().expert_cache_prefetch_device(self._h, step, layer, _dev(ids, "ids", torch.int32), ids.numel(),
+                                                  _stream(stream)), "expert_cache_prefetch_device")
 
     def prefetch(self, step: int, layer: int, ids):
         a = np.ascontiguousarray(np.asarray(ids).reshape(-1), dtype=np.int32)

@@ -831,27 +831,31 @@ __global__ __launch_bounds__(kBlock) void combine_kernel(const float *__restrict
 // fill, which measured faster than 1 or 2 MiB (the device-decision fill kernel
 // has the same shape).
 constexpr int kFillUnroll = 2;
+constexpr int kHostFillsInFlight = 4;  // fills streamed at once
 __global__ __launch_bounds__(kBlock) void fill_slots_kernel(FillBatch b) {
-    const int f = blockIdx.y;
-    if (f == 0 && blockIdx.x == 0)
+    if (blockIdx.y == 0 && blockIdx.x == 0)
         for (int i = threadIdx.x; i < b.n_tab; i += kBlock) b.table[b.tab_idx[i]] = b.tab_val[i];
     const size_t n16 = size_t(b.bytes) / 16;
     const size_t per = (n16 + gridDim.x - 1) / gridDim.x;
     const size_t beg = size_t(blockIdx.x) * per;
     const size_t end = beg + per < n16 ? beg + per : n16;
-    const uint4 *src = reinterpret_cast<const uint4 *>(b.src[f]);
-    uint4 *dst = reinterpret_cast<uint4 *>(b.dst[f]);
-    for (size_t i = beg + threadIdx.x; i < end; i += size_t(kBlock) * kFillUnroll) {
-        uint4 v[kFillUnroll];
+    // A bounded grid walks the batch: a few fills saturate the link, and the rest of the chip stays free
+    // for the compute a prefetch overlaps.
+    for (int f = blockIdx.y; f < b.n; f += gridDim.y) {
+        const uint4 *src = reinterpret_cast<const uint4 *>(b.src[f]);
+        uint4 *dst = reinterpret_cast<uint4 *>(b.dst[f]);
+        for (size_t i = beg + threadIdx.x; i < end; i += size_t(kBlock) * kFillUnroll) {
+            uint4 v[kFillUnroll];
 #pragma unroll
-        for (int u = 0; u < kFillUnroll; ++u) {
-            const size_t j = i + size_t(u) * kBlock;
-            v[u] = j < end ? src[j] : make_uint4(0u, 0u, 0u, 0u);
-        }
+            for (int u = 0; u < kFillUnroll; ++u) {
+                const size_t j = i + size_t(u) * kBlock;
+                v[u] = j < end ? src[j] : make_uint4(0u, 0u, 0u, 0u);
+            }
 #pragma unroll
-        for (int u = 0; u < kFillUnroll; ++u) {
-            const size_t j = i + size_t(u) * kBlock;
-            if (j < end) dst[j] = v[u];
+            for (int u = 0; u < kFillUnroll; ++u) {
+                const size_t j = i + size_t(u) * kBlock;
+                if (j < end) dst[j] = v[u];
+            }
         }
     }
 }
@@ -1109,7 +1113,8 @@ hipError_t launch_fill_slots(const FillBatch &b, hipStream_t s) {
         return hipErrorInvalidValue;
     long long bpf = b.bytes / (64 << 10);  // 32 blocks for a 9 MiB blob; smaller blobs take fewer
     bpf = bpf < 4 ? 4 : (bpf > 32 ? 32 : bpf);
-    fill_slots_kernel<<<dim3(unsigned(bpf), unsigned(b.n)), kBlock, 0, s>>>(b);
+    const int ny = b.n < kHostFillsInFlight ? b.n : kHostFillsInFlight;
+    fill_slots_kernel<<<dim3(unsigned(bpf), unsigned(ny)), kBlock, 0, s>>>(b);
     return hipGetLastError();
 }
 

@@ -637,6 +637,16 @@ int expert_cache_lookup_device(moe_cache *c, int step, int layer, const int32_t 
     return MOE_OK;
 }
 
+int expert_cache_prefetch_device(moe_cache *c, int step, int layer, const int32_t *ids_dev, int n, void *stream) {
+    if (!c) return moe::fail(MOE_ERR_INVALID_ARG, "cache is NULL");
+    if (!c->dev_mode) return moe::fail(MOE_ERR_INVALID_ARG, "device prefetches need a MOE_CACHE_DEVICE cache");
+    if (layer < 0 || layer >= c->L) return moe::fail(MOE_ERR_INVALID_ARG, "layer %d outside [0, %d)", layer, c->L);
+    if (n < 0 || (n > 0 && !ids_dev)) return moe::fail(MOE_ERR_INVALID_ARG, "bad ids");
+    const int st = moe::cache_prefetch_device(c, step, layer, ids_dev, n, static_cast<hipStream_t>(stream));
+    if (st == MOE_OK) moe::clear_error();
+    return st;
+}
+
 int expert_cache_lookup(moe_cache *c, int step, int layer, const int32_t *ids_host, int n,
                         int32_t *slots_out, uint8_t *hit_out, void *compute_stream) {
     if (c && c->dev_mode) return moe::fail(MOE_ERR_INVALID_ARG, "a MOE_CACHE_DEVICE cache looks up on the device");
@@ -645,7 +655,7 @@ int expert_cache_lookup(moe_cache *c, int step, int layer, const int32_t *ids_ho
 }
 
 int expert_cache_prefetch(moe_cache *c, int step, int layer, const int32_t *ids_host, int n) {
-    if (c && c->dev_mode) return moe::fail(MOE_ERR_INVALID_ARG, "a MOE_CACHE_DEVICE cache does not prefetch");
+    if (c && c->dev_mode) return moe::fail(MOE_ERR_INVALID_ARG, "a MOE_CACHE_DEVICE cache prefetches on the device (expert_cache_prefetch_device)");
     return lookup_impl(c, step, layer, ids_host, n, true, nullptr, nullptr, nullptr);
 }
 

@@ -472,6 +472,60 @@ def test_device_lookups_match_oracle(rotary, Q, C, L, E, nmax, steps):
     buf.close()
 
 
+@pytest.mark.parametrize("rotary,Q,C,L,E,nmax,steps", [(False, 0, 24, 3, 32, 8, 300), (True, 3, 24, 3, 32, 8, 300),
+                                                       (False, 0, 700, 40, 128, 40, 300),
+                                                       (True, 32, 700, 40, 128, 40, 300),
+                                                       (False, 0, 4096, 48, 256, 600, 80)])
+def test_device_prefetches_and_lookups_match_oracle(rotary, Q, C, L, E, nmax, steps):
+    """Device prefetches (decisions on the stream, fills on the copy stream) interleaved with device lookups:
+    every decision, the counters, the slot table and every slot's contents against the oracle replaying the
+    same calls, prefetches included."""
+    eb = 256
+    buf = moe.PinnedBuffer(L * E * eb)
+    buf.array.view(np.int32).reshape(L * E, eb // 4)[:] = np.arange(L * E, dtype=np.int32)[:, None]
+    cache = moe.ExpertCache(L, E, eb, C * eb, buf.ptr, E * eb, eb, device=True,
+                            policy=moe.MOE_POLICY_ROTARY if rotary else moe.MOE_POLICY_LRU, charge_max=Q)
+    o = oracle.Rotary(C, L, E, Q) if rotary else oracle.LRU(C, L, E)
+    rng = np.random.default_rng(11 * C + Q + int(rotary))
+    ids = [rng.integers(0, E, size=int(rng.integers(1, nmax + 1))).astype(np.int32) for _ in range(steps)]
+    layers = rng.integers(0, L, size=steps)
+    pf = rng.random(steps) < 0.4
+    ids_d = [dev(a) for a in ids]
+    slots_d = [torch.empty(a.size, dtype=torch.int32, device=DEV) for a in ids]
+    want_slots = {}
+    torch.cuda.synchronize()
+    for t in range(steps):
+        if pf[t]:
+            cache.prefetch_device(t, int(layers[t]), ids_d[t])
+        else:
+            cache.lookup_device(t, int(layers[t]), ids_d[t], slots_d[t])
+        assert o.lookup(t, int(layers[t]), ids[t], prefetch=bool(pf[t])) == oracle.OK
+        if not pf[t]:
+            want_slots[t] = [o.slot_of(int(layers[t]), int(e)) for e in ids[t]]
+    torch.cuda.synchronize()
+    moe.moe_sync_check()
+    assert all(slots_d[t].cpu().tolist() == w for t, w in want_slots.items())
+    ev, oev = cache.trace(), o.events()
+    assert len(ev) == len(oev)
+    assert (ev.view(np.int32).reshape(-1, 6) == oev.view(np.int32).reshape(-1, 6)).all()
+    st, so = cache.stats(), o.stats()
+    assert st["prefetches"] > 0
+    assert ((st["hits"], st["misses"], st["prefetches"], st["evictions"])
+            == (so["hits"], so["misses"], so["prefetches"], so["evictions"]))
+    assert st["occupancy"] == o.occupancy() and st["h2d_bytes"] == (st["misses"] + st["prefetches"]) * eb
+    table_p, pool_p = cache.slot_table()
+    table = _d2h(table_p, 4 * L * E).view(np.int32)
+    pool = _d2h(pool_p, C * eb).view(np.int32).reshape(C, eb // 4)
+    for l in range(L):
+        for e in range(E):
+            s = o.slot_of(l, e)
+            assert table[l * E + e] == s
+            if s >= 0:
+                assert (pool[s] == l * E + e).all()
+    cache.close()
+    buf.close()
+
+
 @pytest.mark.parametrize("case", ["all_free", "free_then_victims", "eight_victims", "nine_victims", "m64", "m65"])
 def test_device_lookup_one_pass_boundaries(case):
     """The device LRU's one-pass placement (at most 64 experts and 8 victims in a step) and the lane walk beyond
@@ -533,6 +587,18 @@ def test_device_lookup_errors_change_nothing():
         cache.prefetch(3, 0, np.array([1], np.int32))
     with pytest.raises(moe.MoeError):
         cache.lookup_device(3, 2, dev(np.array([1], np.int32)))
+    with pytest.raises(moe.MoeError):
+        cache.prefetch_device(3, 2, dev(np.array([1], np.int32)))
+    cache.prefetch_device(3, 0, dev(np.array([-1], np.int32)))
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_sync_check()
+    assert ei.value.code == -2
+    cache.prefetch_device(4, 0, dev(np.arange(5, dtype=np.int32)))
+    with pytest.raises(moe.MoeError) as ei:
+        moe.moe_sync_check()
+    assert ei.value.code == -4
+    st = cache.stats()
+    assert len(cache.trace()) == 2 and st["misses"] == 2 and st["prefetches"] == 0
     cache.close()
     with pytest.raises(moe.MoeError):
         moe.ExpertCache(L, E, eb, 5000 * eb, buf.ptr, E * eb, eb, device=True)
@@ -852,6 +918,58 @@ def test_cache_prefetch_and_demand_fills_on_device():
             ws.numel(), 0, stream.cuda_stream)
         assert rc == 0, moe.lib().moe_last_error()
         cache.release(stream)
+    moe.moe_sync_check()
+    y = y_d.cpu().numpy()
+    for t in range(steps):
+        ref = oracle.moe_ffn(x_np[t], ids_np[t], w_np[t].astype(np.float64), host[t % 2], wl.H, wl.I, wl.dtype)
+        assert normwise(y[t], ref) <= TOL[wl.dtype], t
+    ev, oev = cache.trace(), o.events()
+    assert len(ev) == len(oev)
+    assert (ev.view(np.int32).reshape(-1, 6) == oev.view(np.int32).reshape(-1, 6)).all()
+    s = cache.stats()
+    assert s["prefetches"] > 0 and s["evictions"] > 0
+    cache.close()
+    buf.close()
+
+
+def test_cache_device_prefetch_and_demand_fills():
+    """Device residency with device prefetches, no host synchronisation between steps: each step prefetches
+    three experts of the other layer (fills on the copy stream, overlapping the FFN queued next), then looks up
+    its own experts on the device (waiting for those fills) and runs the FFN through the device slot table.
+    With 6 slots, prefetches evict slots earlier FFNs read and lookups evict prefetched slots. Every FFN
+    output matches the oracle on the experts it asked for; the residency log matches the oracle's."""
+    wl = synth.Workload("cache order", H=256, E=16, k=4, I=128, L=2, dtype=synth.BF16, cfg_id=121)
+    C, steps = 6, 40
+    buf = _pinned_store(wl)
+    eb = wl.expert_bytes
+    cache = moe.ExpertCache(wl.L, wl.E, eb, C * eb, buf.ptr, wl.E * eb, eb, device=True)
+    table, pool = cache.slot_table()
+    o = oracle.LRU(C, wl.L, wl.E)
+    rng = np.random.default_rng(1)
+    host = {l: synth.layer_experts(wl, l) for l in range(wl.L)}
+    ids_np = np.stack([rng.choice(wl.E, wl.k, replace=False) for _ in range(steps)]).astype(np.int32)[:, None, :]
+    pf_np = np.stack([rng.choice(wl.E, 3, replace=False) for _ in range(steps)]).astype(np.int32)
+    w_np = rng.random((steps, 1, wl.k)).astype(np.float32)
+    w_np /= w_np.sum(axis=2, keepdims=True)
+    x_np = rng.standard_normal((steps, 1, wl.H)).astype(np.float32)
+    ids_d, pf_d, w_d, x_d = dev(ids_np), dev(pf_np), dev(w_np), dev(x_np)
+    y_d = torch.zeros((steps, 1, wl.H), dtype=torch.float32, device=DEV)
+    ws = torch.empty(moe.moe_ffn_workspace_bytes(1, wl.k, wl.I), dtype=torch.uint8, device=DEV)
+    stream = torch.cuda.current_stream()
+    torch.cuda.synchronize()
+    for t in range(steps):
+        l = t % 2
+        if t % 3 != 2:
+            cache.prefetch_device(t, 1 - l, pf_d[t], stream)
+            assert o.lookup(t, 1 - l, pf_np[t], prefetch=True) == oracle.OK
+        cache.lookup_device(t, l, ids_d[t].reshape(-1), None, stream)
+        assert o.lookup(t, l, ids_np[t].reshape(-1)) == oracle.OK
+        rc = moe.lib().moe_expert_ffn_grouped(
+            x_d[t].data_ptr(), 1, wl.H, wl.I, wl.E, wl.k, ids_d[t].data_ptr(), w_d[t].data_ptr(),
+            table + 4 * l * wl.E, pool, eb, wl.dtype, None, y_d[t].data_ptr(), ws.data_ptr(),
+            ws.numel(), 0, stream.cuda_stream)
+        assert rc == 0, moe.lib().moe_last_error()
+    torch.cuda.synchronize()
     moe.moe_sync_check()
     y = y_d.cpu().numpy()
     for t in range(steps):
