@@ -41,12 +41,30 @@ hipError_t launch_topk_softmax(const float *logits, int T, int E, int k, int32_t
 // Which expert kernels launch_expert_ffn enqueues (grouping goes with gate/up).
 enum : int { kFfnGateUp = 1, kFfnDown = 2, kFfnBoth = 3 };
 
+// A single-token step's missing experts streamed in by its gate/up launch
+// (device residency): the blocks of a rank whose slot is in the lookup's fill
+// list read that expert's gate/up rows from the host store, use them and
+// store them into the slot; one more row of blocks copies each missing blob's
+// down part.  The host link then carries the misses while the resident
+// experts' gate/up runs, and no separate fill launch sits on the step's path.
+struct FfnFill {
+    const int32_t *n = nullptr;      // device: number of fills (nullptr: this launch fills nothing)
+    const long long *src = nullptr;  // device [n]: byte offset of each blob in the host store
+    const int32_t *slot = nullptr;   // device [n]: its slot
+    const uint8_t *host = nullptr;   // device address of the host store
+    uint8_t *pool = nullptr;         // the slot pool, written
+    long long doff = 0;              // byte offset of the down part in a blob
+    int blocks = 32;                 // blocks streaming one missing expert's gate/up rows
+    int slices = 32;                 // pieces of one missing blob's down part (one block each)
+};
+
 // Slots of a single-token step known on the host (after a residency lookup):
 // off[j] = byte offset from the pool of the expert of rank j.  n = k when
 // valid, 0 when the kernels must read ids and the slot table on the device.
 struct FfnPlan {
     int n = 0;
     long long off[16];
+    FfnFill fill;  // one token, slots read on the device: the fills this launch performs
 };
 
 hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, const int32_t *ids,
@@ -163,10 +181,14 @@ bool cache_rotary(const struct ::moe_cache *c);   // MOE_POLICY_ROTARY
 // for those fills.  Returns an MOE_ERR_* code.
 int cache_prefetch_device(struct ::moe_cache *c, int step, int layer, const int32_t *ids_dev, int n, hipStream_t s);
 // MOE_CACHE_DEVICE, one token: enqueue top-k of `logits` fused with the lookup of the chosen experts, then
-// the fills of its misses.  Returns an MOE_ERR_* code.
+// the fills of its misses, unless fill_in_ffn (the step's gate/up launch then performs them, see FfnFill).
+// Returns an MOE_ERR_* code.
 int cache_topk_lookup(struct ::moe_cache *c, int step, int layer, const float *logits, int k, int32_t *ids,
                       float *weights, int32_t *slots_out, int *err_flags, hipStream_t s,
-                      const int *step_dev = nullptr);
+                      const int *step_dev = nullptr, bool fill_in_ffn = false);
+// The fill list of the cache's last device lookup, for a gate/up launch that performs its fills
+// (cache_topk_lookup with fill_in_ffn; that launch must follow the lookup on its stream).
+FfnFill cache_ffn_fill(struct ::moe_cache *c, long long down_off);
 
 // Sticky error-flag word of the current device (set up on first use).
 int *device_error_flags();

@@ -437,11 +437,50 @@ __global__ __launch_bounds__(kBlock) void group_pairs_kernel(const int32_t *__re
     }
 }
 
+// A missing expert streamed by a gate/up launch: kFillGuBlocks blocks stream its rows (128 waves, each
+// with a row pair in flight per pass: 1 MiB for bf16 rows of 2048, 256 KiB for int4) and kFillSlices
+// blocks copy its down part.  Swept on both benchmark shapes (8-48 blocks, 16-64 pieces): 32 and 32 were
+// the fastest or within noise of it on each.
+constexpr int kFillGuBlocks = 32;
+constexpr int kFillSlices = 32;
+
+// 16-byte store with the nontemporal hint (a filled slot is not read again by this launch).
+__device__ __forceinline__ void store16_stream(uint8_t *p, uint4 v) {
+    const u32x4 t = {v.x, v.y, v.z, v.w};
+    __builtin_nontemporal_store(t, reinterpret_cast<u32x4 *>(p));
+}
+
+// Copies the down part of every blob in the fill list from the host store to its slot: fl.slices pieces
+// per blob, one block each, two 16-byte loads per thread in flight.
+__device__ __forceinline__ void copy_down_parts(const FfnFill &fl, size_t expert_bytes) {
+    const int nf = min(fl.n[0], MOE_MAX_TOPK);  // a one-token step fills at most k <= MOE_MAX_TOPK blobs
+    const size_t n16 = (expert_bytes - size_t(fl.doff)) / 16;
+    const size_t per = (n16 + size_t(fl.slices) - 1) / size_t(fl.slices);
+    for (int it = blockIdx.x; it < nf * fl.slices; it += gridDim.x) {
+        const int f = it / fl.slices, piece = it - f * fl.slices;
+        const size_t beg = size_t(piece) * per;
+        const size_t end = beg + per < n16 ? beg + per : n16;
+        const uint4 *src = reinterpret_cast<const uint4 *>(fl.host + fl.src[f] + fl.doff);
+        uint4 *dst = reinterpret_cast<uint4 *>(fl.pool + size_t(fl.slot[f]) * expert_bytes + size_t(fl.doff));
+        for (size_t i = beg + threadIdx.x; i < end; i += size_t(2 * kBlock)) {
+            const size_t j = i + kBlock;
+            const uint4 a = src[i];
+            const uint4 b = j < end ? src[j] : make_uint4(0u, 0u, 0u, 0u);
+            dst[i] = a;
+            if (j < end) dst[j] = b;
+        }
+    }
+}
+
 // -------------------------------------------------------------- gate/up ---
 // act[p, i] = w_p * silu(W_g[i] . x_t) * (W_u[i] . x_t) for every pair p of one
 // expert group.  One wave per row pair (gate row 2i, up row 2i+1): the pair's
 // weights are loaded once into registers and applied to each token of the
-// group.  ONE_TOKEN: T == 1, groups are the k ranks (+ shared), no table.
+// group.  ONE_TOKEN: T == 1, groups are the k ranks (+ shared), no table;
+// with plan.fill it also performs the step's fills (FfnFill): a missing
+// expert's rows come from the host store, plan.fill.blocks blocks stream them
+// (each wave a row pair per pass) and store them into the slot, and one more
+// row of blocks copies the blobs' down parts.
 template <int DT, int NCH, bool ONE_TOKEN>
 __global__ __launch_bounds__(kBlock) void gateup_kernel(
     const float *__restrict__ x, int T, int H, int I, int E, int k, const int32_t *__restrict__ ids,
@@ -456,9 +495,15 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     const int lane = threadIdx.x & (kWave - 1);
     const int g = blockIdx.y;
     const uint8_t *blob;
+    uint8_t *dst = nullptr;  // a missing expert streamed in by this launch: its rows are stored here too
+    int istride = 0;         // then the wave's row pairs lie this far apart (0: one row pair per wave)
     int pstart = 0, pcount = 1, single = 0;
     const int *pairs = nullptr;
     if constexpr (ONE_TOKEN) {
+        if (plan.fill.n && g == int(gridDim.y) - 1) {
+            copy_down_parts(plan.fill, expert_bytes);
+            return;
+        }
         if (g < k && plan.n) {
             blob = pool + plan.off[g];  // slots known on the host: no device lookups
         } else if (g < k) {
@@ -473,6 +518,19 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
                 return;
             }
             blob = pool + size_t(s) * expert_bytes;
+            if (plan.fill.n) {
+                const int nf = min(plan.fill.n[0], MOE_MAX_TOPK);
+                for (int f = 0; f < nf; ++f)
+                    if (plan.fill.slot[f] == s) {
+                        dst = plan.fill.pool + size_t(s) * expert_bytes;
+                        blob = plan.fill.host + plan.fill.src[f];
+                        break;
+                    }
+                if (dst) {
+                    if (int(blockIdx.x) >= plan.fill.blocks) return;
+                    istride = plan.fill.blocks * (kBlock / kWave);
+                }
+            }
         } else {
             blob = shared_w;
         }
@@ -485,7 +543,7 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
         pairs = group_pairs(groups, T, k);
         blob = s == -2 ? shared_w : pool + size_t(s) * expert_bytes;
     }
-    const int i = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
+    int i = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
     if (!STAGE_X && i >= I) return;  // when x is staged, every wave joins the block's staging below
     const int P = T * k;
     float xv[NCH][EPC];
@@ -508,8 +566,9 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
         }
     }
     const size_t rb = row_bytes_of(DT, H);
+    for (bool first = true;; first = false) {
     const int iw = i < I ? i : I - 1;  // staging x: a wave past I loads a valid row and stores nothing
-    const uint8_t *gate = blob + size_t(2 * iw) * rb;
+    const uint8_t *gate = blob + size_t(2 * iw) * rb + row_bytes_of(DT, lane * EPC);  // this lane's first chunk
     const uint8_t *up = gate + rb;
     uint4 wg[NCH], wu[NCH];
     float sg[NCH], su[NCH];
@@ -517,8 +576,8 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     for (int c = 0; c < NCH; ++c) {
         const int col0 = (c * kWave + lane) * EPC;
         const bool in = col0 < H;
-        wg[c] = in ? load16_stream(gate + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
-        wu[c] = in ? load16_stream(up + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
+        wg[c] = in ? load16_stream(gate + size_t(c) * 16 * kWave) : make_uint4(0, 0, 0, 0);
+        wu[c] = in ? load16_stream(up + size_t(c) * 16 * kWave) : make_uint4(0, 0, 0, 0);
         if constexpr (DT == INT4) {
             const uint16_t *sc = reinterpret_cast<const uint16_t *>(blob + size_t(I) * H);
             const int groups_per_row = H / 128;
@@ -526,7 +585,27 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
             su[c] = in ? bf16_bits_to_float(sc[size_t(2 * iw + 1) * groups_per_row + col0 / 128]) : 0.f;
         }
     }
+    if (dst && i < I) {  // the missing expert's row pair (and int4 scales) into its slot
+        uint8_t *dg = dst + (gate - blob);  // the same place in the slot
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+            const int col0 = (c * kWave + lane) * EPC;
+            if (col0 < H) {
+                store16_stream(dg + size_t(c) * 16 * kWave, wg[c]);
+                store16_stream(dg + rb + size_t(c) * 16 * kWave, wu[c]);
+                if constexpr (DT == INT4) {
+                    if (col0 % 128 == 0) {  // one lane per quantisation group; bf16 -> float -> bf16 is exact
+                        uint16_t *sc = reinterpret_cast<uint16_t *>(dst + size_t(I) * H);
+                        const int groups_per_row = H / 128;
+                        sc[size_t(2 * iw) * groups_per_row + col0 / 128] = uint16_t(__float_as_uint(sg[c]) >> 16);
+                        sc[size_t(2 * iw + 1) * groups_per_row + col0 / 128] = uint16_t(__float_as_uint(su[c]) >> 16);
+                    }
+                }
+            }
+        }
+    }
     if constexpr (STAGE_X) {
+      if (first) {
         // The token row is the same for every wave of the block: it is staged in LDS once, behind the
         // weight loads, transposed to [chunk][quarter][lane] so that each read of a quarter is 64
         // consecutive 16-byte words.
@@ -552,6 +631,7 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
                 xv[c][4 * q + 3] = v.w;
             }
         }
+      }
     }
     for (int q = 0; q < pcount; ++q) {
         const int p = ONE_TOKEN ? single : pairs[pstart + q];
@@ -579,6 +659,10 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
         // the pair's combine weight is folded in here
         const float wp = q == 0 ? wp0 : (p < P ? weights[p] : 1.f);
         if (lane == 0) act[size_t(p) * I + i] = wp * (ga / (1.f + expf(-ga)) * ua);
+    }
+    if (!istride) break;  // block-uniform; no barrier follows the first pass
+    i += istride;
+    if (i >= I) break;
     }
 }
 
@@ -999,7 +1083,23 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
                              bool accumulate, const FfnWorkspace &ws, int *err_flags, hipStream_t s,
                              const FfnPlan *plan, int parts) {
     FfnPlan pl1;
-    if (plan && T == 1 && plan->n == k) pl1 = *plan;
+    if (plan && T == 1) {
+        if (plan->n == k) {
+            pl1 = *plan;
+            pl1.fill = FfnFill{};  // slots known on the host: nothing left to fill
+        } else {
+            pl1.fill = plan->fill;
+        }
+    }
+    if (pl1.fill.n) {  // fills performed by the gate/up launch
+        const size_t doff = size_t(pl1.fill.doff);
+        if (!slot_of || !(parts & kFfnGateUp) || doff != down_offset(H, I, dtype) || doff % 16 ||
+            (expert_bytes - doff) % 16 || !pl1.fill.host || !pl1.fill.pool)
+            return hipErrorInvalidValue;
+        const int nbx = (I + 3) / 4;
+        pl1.fill.blocks = kFillGuBlocks < nbx ? kFillGuBlocks : nbx;
+        pl1.fill.slices = kFillSlices;
+    }
     if (T == 0) return hipSuccess;
     const bool one = T == 1;
     const int has_shared = shared_w != nullptr;
@@ -1011,7 +1111,7 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
         if (e != hipSuccess) return e;
     }
     const int groups = one ? k + has_shared : (T * k < E ? T * k : E) + has_shared;
-    const dim3 ggrid((I + 3) / 4, groups);
+    const dim3 ggrid((I + 3) / 4, groups + (pl1.fill.n ? 1 : 0));  // + the blocks copying down parts
     const int nch = chunks_per_row(H, dtype);
     // One-token int4 x staging covers every lane's chunk slots, [nch][EPC/4][64] float4, not just H floats.
     const size_t x_lds = dtype == INT4 ? sizeof(float) * size_t(nch) * kWave * elems_per_chunk(dtype) : 0;

@@ -415,15 +415,27 @@ int moe::cache_prefetch_device(moe_cache *c, int step, int layer, const int32_t 
     return MOE_OK;
 }
 
+moe::FfnFill moe::cache_ffn_fill(moe_cache *c, long long down_off) {
+    moe::FfnFill f;
+    f.n = c->dr.n_fill;
+    f.src = c->dr.fill_src;
+    f.slot = c->dr.fill_slot;
+    f.host = c->host_dev;
+    f.pool = c->pool;
+    f.doff = down_off;
+    return f;
+}
+
 int moe::cache_topk_lookup(moe_cache *c, int step, int layer, const float *logits, int k, int32_t *ids,
-                           float *weights, int32_t *slots_out, int *err_flags, hipStream_t s, const int *step_dev) {
+                           float *weights, int32_t *slots_out, int *err_flags, hipStream_t s, const int *step_dev,
+                           bool fill_in_ffn) {
     if (!c || !c->dev_mode || layer < 0 || layer >= c->L)
         return moe::fail(MOE_ERR_INVALID_ARG, "fused top-k lookup needs a MOE_CACHE_DEVICE cache and a valid layer");
     moe::DevLookup p{c->C, c->L, c->E, layer, step, c->d.policy == MOE_POLICY_ROTARY ? 1 : 0, c->charge_max,
                      (long long)c->d.host_layer_stride, (long long)c->d.host_expert_stride, step_dev};
     hipError_t e = after_device_prefetch(c, s);
     if (e == hipSuccess) e = moe::launch_topk_lookup(logits, c->E, k, ids, weights, err_flags, c->dr, p, slots_out, s);
-    if (e == hipSuccess)
+    if (e == hipSuccess && !fill_in_ffn)
         e = moe::launch_dev_fill(c->dr, c->host_dev, c->pool, (long long)c->d.expert_bytes, std::min(k, c->E), s);
     return e == hipSuccess ? MOE_OK : moe::fail_hip(e, "fused top-k lookup");
 }

@@ -361,7 +361,8 @@ int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_b
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: routing");
         if (fused) {
             int st = moe::cache_topk_lookup(d.cache, step, l, s->logits, d.k, ids, w,
-                                            s->dev_slots + size_t(l) * d.max_tokens * d.k, eflags, strm, step_dev);
+                                            s->dev_slots + size_t(l) * d.max_tokens * d.k, eflags, strm, step_dev,
+                                            true);
             if (st != MOE_OK) return st;
         } else if (dev_lookup) {
             int st = expert_cache_lookup_device(d.cache, step, l, ids, T * d.k,
@@ -398,9 +399,13 @@ int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_b
             pool += size_t(l) * d.E * s->expert_bytes;
             slot_of = nullptr;
         }
+        // One token with device lookups: the gate/up launch streams the lookup's misses itself (their rows
+        // from the host store while the resident experts' gate/up runs), so no fill launch precedes it.
+        moe::FfnPlan fplan;
+        if (fused) fplan.fill = moe::cache_ffn_fill(d.cache, (long long)moe::down_offset(d.H, d.I, d.w_dtype));
         e = moe::launch_expert_ffn(s->h, T, d.H, d.I, d.E, d.k, ids, w, slot_of, pool, s->expert_bytes, d.w_dtype,
                                    s->shared_w.empty() ? nullptr : s->shared_w[l], x, true, ws, eflags, strm,
-                                   plan.n ? &plan : nullptr);
+                                   fused ? &fplan : plan.n ? &plan : nullptr);
         s->last[l] = LastLayer{true, T, l, ids, w, slot_of, pool, plan};
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: expert FFN");
         if (s->budgeted && !dev_lookup) {

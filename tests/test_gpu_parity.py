@@ -323,6 +323,17 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
     assert (ev.view(np.int32).reshape(-1, 6) == oev.view(np.int32).reshape(-1, 6)).all()
     s = cache.stats()
     assert s["occupancy"] <= capacity and s["misses"] == o.stats()["misses"]
+    if capacity * eb <= 64 << 20:  # every resident expert's slot holds its whole blob, byte for byte
+        table_p, pool_p = cache.slot_table()
+        table = _d2h(table_p, 4 * wl.L * wl.E).view(np.int32)
+        pool = _d2h(pool_p, capacity * eb).reshape(capacity, eb)
+        store = buf.array.reshape(-1, eb)
+        for l in range(wl.L):
+            for e in range(wl.E):
+                sl = o.slot_of(l, e)
+                assert table[l * wl.E + e] == sl
+                if sl >= 0:
+                    assert np.array_equal(pool[sl], store[e if layers_alias else l * wl.E + e]), (l, e)
     stack.close()
     cache.close()
     buf.close()
@@ -404,6 +415,17 @@ def test_budgeted_stack_tokens_and_shared_int4():
     wl = synth.Workload("int4 stack", H=2048, E=64, k=8, I=256, L=3, dtype=synth.INT4G128, shared=True,
                         routing="zipf_overlap", cfg_id=98)
     s = run_stack_and_check(wl, steps=12, capacity=40, T=4, check_steps=[0, 5, 11])
+    assert s["evictions"] > 0
+
+
+@pytest.mark.parametrize("graph", [False, True])
+def test_budgeted_stack_int4_shared_device_one_token(graph):
+    """One-token int4 steps with a shared expert under device residency: the gate/up launch streams each
+    step's missing experts itself (rows, group scales and the down parts); outputs, decisions and every
+    resident slot's bytes against the oracle and the host store."""
+    wl = synth.Workload("int4 stack", H=2048, E=64, k=8, I=256, L=3, dtype=synth.INT4G128, shared=True,
+                        routing="zipf_overlap", cfg_id=92)
+    s = run_stack_and_check(wl, steps=16, capacity=30, device=True, graph=graph)
     assert s["evictions"] > 0
 
 
