@@ -417,8 +417,13 @@ MOE_API int moe_stack_destroy(moe_stack *s);
 /* One decode step over every layer, in place on x (device fp32 [T x H]):
  * x <- x + MoE_l(rmsnorm(x)) for l = 0..L-1 (unit-gain RMS norm, eps 1e-6).  logit_bias is device fp32 [L x T x E]
  * added to each layer's router logits, or NULL.  Unless the cache was created
- * with PRELOAD, each layer copies its ids to the host (one synchronisation per
- * layer), runs the lookup, then enqueues the FFN and releases the slots.
+ * with PRELOAD or DEVICE, each layer copies its ids to the host (one
+ * synchronisation per layer), runs the lookup, then enqueues the FFN and
+ * releases the slots.  With a DEVICE cache nothing waits for the host: each
+ * layer enqueues its routing, the fused top-k + lookup and the FFN; for one
+ * token the FFN's gate/up launch also streams the layer's missing experts from
+ * the host store into their slots (the resident experts' gate/up runs
+ * meanwhile), for more tokens a fill launch precedes the FFN.
  * ids_out (device int32 [L x T x k]) and weights_out (device fp32 [L x T x k])
  * receive each layer's routing when non-NULL. */
 MOE_API int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *logit_bias,
@@ -427,7 +432,7 @@ MOE_API int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const
 /* moe_stack_decode_step for one token (T = 1), as a replayed HIP graph.  With a
  * MOE_CACHE_DEVICE cache nothing in a step waits for the host, so the first call
  * captures the step's launches (every layer's routing, fused top-k + lookup,
- * fills and expert FFN) and later calls replay them after setting the step tag
+ * and expert FFN with its fills) and later calls replay them after setting the step tag
  * on the device; a call with other x / logit_bias / ids_out / weights_out
  * pointers captures again (keep the buffers fixed and refill them).  Results
  * and residency decisions are those of moe_stack_decode_step.  Without a device
