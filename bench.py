@@ -458,8 +458,9 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
         "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU (int4 decode)", "achieved": gu_gbps,
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gu_gbps / HBM_PEAK_GBPS,
                      "bytes_per_launch": gu_bytes, "mean_launch_us": gu_ms * 1e3,
-                     "timing": f"the last step's {L} launches (one per layer, same arguments) in one HIP graph, "
-                               f"replayed {args.replays}x between HIP events",
+                     "timing": f"the last step's {L} launches (one per layer, same arguments, every expert resident: "
+                               f"the replays fill nothing, while a budgeted step's own gate/up launch also streams "
+                               f"its misses) in one HIP graph, replayed {args.replays}x between HIP events",
                      "traffic": traffic, "traffic_source": traffic_src, "practical_ceiling_GBps": hbm["launch_GBps"],
                      "frac_of_practical": gu_gbps / hbm["launch_GBps"]},
         "hbm_ceiling": hbm,
@@ -692,8 +693,9 @@ def main():
                      "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": gu_gbps / HBM_PEAK_GBPS if gu_gbps else None,
                      "bytes_per_launch": gu_bytes, "mean_launch_us": gu_ms * 1e3,
-                     "timing": f"the last step's {L} launches (one per layer, same arguments) in one HIP graph, "
-                               f"replayed {args.replays}x between HIP events",
+                     "timing": f"the last step's {L} launches (one per layer, same arguments, every expert resident: "
+                               f"the replays fill nothing, while a budgeted step's own gate/up launch also streams "
+                               f"its misses) in one HIP graph, replayed {args.replays}x between HIP events",
                      "traffic": traffic, "traffic_source": traffic_src,
                      "practical_ceiling_GBps": hbm["launch_GBps"],
                      "frac_of_practical": gu_gbps / hbm["launch_GBps"] if gu_gbps else None},
