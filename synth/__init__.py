@@ -9,14 +9,19 @@ residency) lives here.
 Recipe (every draw comes from NumPy PCG64 keyed by ``SeedSequence(seed,
 spawn_key=...)`` so any tensor can be rebuilt on its own):
 
-* Weights.  Every weight tensor of a workload is a consecutive window of one
-  stream of N(0, sigma_w) draws that repeats with period ``P`` elements
-  (``P = min(2**26, total elements rounded up to 128)``), in the enumeration
-  order: for each layer, the router ``[E x H]``, then routed experts 0..E-1
-  (``W_gu`` then ``W_d``), then the shared expert if the workload has one.
-  Small workloads therefore get fully independent draws; the large stacks
-  re-use the stream with shifting windows, which keeps generation of 48 GB
-  host stores to memcpy speed.  fp32 draws are stored as fp32, bf16 by
+* Weights.  Every weight tensor of a workload is a window of one stream of
+  N(0, sigma_w) draws that repeats with period ``P`` elements
+  (``P = min(2**26, total elements rounded up to 128)``).  The tensors are
+  enumerated per layer: the router ``[E x H]``, then routed experts 0..E-1
+  (each ``W_gu`` then ``W_d``), then the shared expert if the workload has
+  one.  When the whole workload fits in one period (small workloads) the
+  windows are consecutive, so every draw is independent.  The large stacks
+  re-use the stream, which keeps generation of 48 GB host stores to memcpy
+  speed; there tensor number q of the enumeration starts at element
+  ``128 * ((q * 0x9E3779B1) mod P/128)`` of the stream.  The multiplier is
+  odd, so q -> start is a bijection on the P/128 group-aligned starts: no two
+  tensors (up to P/128 = 524 288 of them) start at the same place, and no two
+  expert blobs are byte-identical.  fp32 draws are stored as fp32, bf16 by
   round-to-nearest-even, int4 by the group-128 symmetric quantizer below.
 * Hidden states: fresh N(0, 1) fp32 per decode step (and per token).
 * Routing for the Zipf workloads: per layer a seeded permutation maps Zipf
@@ -267,8 +272,35 @@ def _window(pool: np.ndarray, off: int, n: int, unit: int = 1) -> np.ndarray:
     return out
 
 
+_START_MULT = 0x9E3779B1  # odd: tensor number -> window start is a bijection modulo P/128
+
+
+def _stream_repeats(wl: Workload) -> bool:
+    return wl.L * _elements_per_layer(wl) > _pool_size(wl)
+
+
+def _tensor_number(wl: Workload, layer: int, which: str, expert: int = 0) -> int:
+    """Position of a weight tensor in the enumeration (router, experts 0..E-1, shared) per layer."""
+    base = layer * (wl.E + 2)
+    if which == "router":
+        return base
+    if which == "expert":
+        if not 0 <= expert < wl.E:
+            raise ValueError(f"expert {expert} outside [0, {wl.E})")
+        return base + 1 + expert
+    if which == "shared":
+        return base + 1 + wl.E
+    raise ValueError(which)
+
+
 def _tensor_offset(wl: Workload, layer: int, which: str, expert: int = 0) -> int:
-    """Element offset of a weight tensor in the enumeration order."""
+    """Element offset of a weight tensor in the (periodic) stream."""
+    if _stream_repeats(wl):
+        groups = _pool_size(wl) // GROUP
+        q = _tensor_number(wl, layer, which, expert)
+        if q >= groups:
+            raise ValueError("more tensors than distinct window starts")
+        return GROUP * ((q * _START_MULT) % groups)
     base = layer * _elements_per_layer(wl)
     if which == "router":
         return base
@@ -298,26 +330,41 @@ def router_weights(wl: Workload, layer: int = 0) -> np.ndarray:
     return np.array(w).reshape(wl.E, wl.H)
 
 
-def expert_blob(wl: Workload, layer: int, expert: int | None) -> np.ndarray:
-    """One expert's blob as uint8 bytes.  ``expert=None`` = the layer's shared expert."""
+def _blob_parts(wl: Workload, layer: int, expert: int | None, prefix: int | None = None) -> dict:
+    """The encoded parts of one expert blob (name in :func:`blob_layout` -> uint8 bytes), or with
+    ``prefix`` only the encoding of each matrix's first ``prefix`` elements (a multiple of 128)."""
     off = _tensor_offset(wl, layer, "shared" if expert is None else "expert", expert or 0)
     H, I = wl.H, wl.I
-    out = np.empty(wl.expert_bytes, dtype=np.uint8)
-    lay = blob_layout(H, I, wl.dtype)
-    if wl.dtype in (F32, BF16):
-        n_gu = 2 * I * H
-        for name, o, n in (("gu", off, n_gu), ("d", off + n_gu, H * I)):
-            b, _, nb = lay[name]
-            out[b:b + nb] = np.asarray(_encode_window(wl, wl.dtype, o, n)).view(np.uint8)
-    else:
-        n_gu = 2 * I * H
-        for name, o, n in (("gu", off, n_gu), ("d", off + n_gu, H * I)):
+    n_gu = 2 * I * H
+    parts = {}
+    for name, o, n in (("gu", off, n_gu), ("d", off + n_gu, H * I)):
+        if prefix is not None:
+            n = min(n, prefix)
+        if wl.dtype in (F32, BF16):
+            parts[name] = np.asarray(_encode_window(wl, wl.dtype, o, n)).view(np.uint8)
+        else:
             q, s = _encode_window(wl, wl.dtype, o, n)
-            bq, _, nq = lay[name + "_q"]
-            bs, _, ns = lay[name + "_s"]
-            out[bq:bq + nq] = q
-            out[bs:bs + ns] = np.asarray(s).view(np.uint8)
+            parts[name + "_q"] = np.asarray(q)
+            parts[name + "_s"] = np.asarray(s).view(np.uint8)
+    return parts
+
+
+def expert_blob(wl: Workload, layer: int, expert: int | None) -> np.ndarray:
+    """One expert's blob as uint8 bytes.  ``expert=None`` = the layer's shared expert."""
+    out = np.empty(wl.expert_bytes, dtype=np.uint8)
+    lay = blob_layout(wl.H, wl.I, wl.dtype)
+    for name, part in _blob_parts(wl, layer, expert).items():
+        b, _, nb = lay[name]
+        out[b:b + nb] = part
     return out
+
+
+def expert_blob_prefixes(wl: Workload, layer: int, expert: int | None, n: int = 4096) -> dict:
+    """The first bytes of each part of an expert blob: the encoding of each matrix's first ``n`` elements
+    (packed nibbles and scales separately for int4).  Distinct prefixes prove distinct blobs."""
+    if n % GROUP:
+        raise ValueError("prefix must be a multiple of 128 elements")
+    return _blob_parts(wl, layer, expert, prefix=n)
 
 
 def layer_experts(wl: Workload, layer: int, out: np.ndarray | None = None) -> np.ndarray:
@@ -326,7 +373,7 @@ def layer_experts(wl: Workload, layer: int, out: np.ndarray | None = None) -> np
     if out is None:
         out = np.empty((wl.E, eb), dtype=np.uint8)
     out = out.reshape(wl.E, eb)
-    if wl.dtype in (F32, BF16):
+    if wl.dtype in (F32, BF16) and not _stream_repeats(wl):
         # consecutive experts are consecutive windows, so the layout of
         # [E x (gu | d)] is one contiguous window of the encoded stream
         off = _tensor_offset(wl, layer, "expert", 0)
