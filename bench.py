@@ -122,13 +122,14 @@ def pcie_ceiling_gbps(torch, moe, chunk: int, total: int) -> float:
     return best
 
 
-def hbm_ceiling(torch, moe, launch_bytes: int, n_launch: int = 40, stream_bytes: int = 4 << 30):
+def hbm_ceiling(torch, moe, launch_sizes, n_launch: int = 40, stream_bytes: int = 4 << 30):
     """HBM read rate of the library's streaming probe (the expert kernels' 16-byte nontemporal loads):
-    one pass over `stream_bytes`, and `n_launch` launches of `launch_bytes` each over distinct memory
-    (so the 256 MB last-level cache cannot serve repeats), replayed from a graph so that host launch
-    cost is out of the picture.  Also runs one 256 MiB device copy: the known-size kernels the HBM
-    byte counters are calibrated against."""
-    launch_bytes = (launch_bytes // 16) * 16
+    one pass over `stream_bytes`, and `n_launch` groups of back-to-back launches of `launch_sizes` bytes
+    (the expert FFN's two launches) over distinct memory (so the 256 MB last-level cache cannot serve
+    repeats), replayed from a graph so that host launch cost is out of the picture.  Also runs one 256 MiB
+    device copy: the known-size kernels the HBM byte counters are calibrated against."""
+    sizes = [(b // 16) * 16 for b in launch_sizes]
+    launch_bytes = sum(sizes)
     total = max(stream_bytes, launch_bytes * n_launch)
     buf = torch.zeros(total, dtype=torch.uint8, device="cuda")
     sink = torch.zeros(1, dtype=torch.float32, device="cuda")
@@ -147,7 +148,10 @@ def hbm_ceiling(torch, moe, launch_bytes: int, n_launch: int = 40, stream_bytes:
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         for i in range(n_launch):
-            moe.moe_hbm_read_probe(buf[i * launch_bytes:(i + 1) * launch_bytes], sink)
+            off = i * launch_bytes
+            for b in sizes:
+                moe.moe_hbm_read_probe(buf[off:off + b], sink)
+                off += b
     g.replay()
     torch.cuda.synchronize()
     a, b = ev(), ev()
@@ -161,32 +165,41 @@ def hbm_ceiling(torch, moe, launch_bytes: int, n_launch: int = 40, stream_bytes:
     del g, buf, cp_src, cp_dst
     return {"stream_GBps": best_stream, "stream_bytes": stream_bytes,
             "launch_GBps": launch_bytes / (us * 1e-6) / 1e9, "launch_us": us, "launch_bytes": launch_bytes,
-            "method": f"moe_hbm_read_probe: one {stream_bytes >> 30} GiB pass; {n_launch} launches of "
-                      f"{launch_bytes} B over distinct memory replayed from a graph"}
+            "method": f"moe_hbm_read_probe: one {stream_bytes >> 30} GiB pass; {n_launch} groups of launches of "
+                      f"{'+'.join(str(b) for b in sizes)} B over distinct memory replayed from a graph"}
 
 
-TRAFFIC_FILES = {4: os.path.join(ROOT, "profiles", "cfg4_gateup_hbm_traffic.txt"),
-                 5: os.path.join(ROOT, "profiles", "cfg5_gateup_hbm_traffic.txt")}
+TRAFFIC_FILES = {4: os.path.join(ROOT, "profiles", "cfg4_expert_ffn_hbm_traffic.txt"),
+                 5: os.path.join(ROOT, "profiles", "cfg5_expert_ffn_hbm_traffic.txt")}
 CSRC = os.path.join(ROOT, "paper_2605_29135_amd", "csrc")
+FFN_KERNELS = ("gateup_kernel", "down_combine_lds_kernel")
 
 
-def gateup_source_hash() -> str:
-    """sha256 of the gate/up kernel's own source text and of the device helpers it uses."""
+def kernel_source(src: str, name: str) -> str:
+    """The source text of one kernel template (from its `template` line to its closing brace)."""
+    i0 = src.index(f"void {name}(")
+    i0 = src.rindex("template", 0, i0)
+    return src[i0:src.index("\n}\n", i0) + 3]
+
+
+def ffn_source_hash() -> str:
+    """sha256 of the expert FFN kernels' own source text and of the device helpers they use."""
     import hashlib
     with open(os.path.join(CSRC, "kernels.hip")) as fh:
         src = fh.read()
-    i0 = src.index("void gateup_kernel(")
-    i0 = src.rindex("template", 0, i0)
-    i1 = src.index("\n}\n", i0) + 3
-    h = hashlib.sha256(src[i0:i1].encode())
-    with open(os.path.join(CSRC, "device_common.h"), "rb") as fh:
-        h.update(fh.read())
+    h = hashlib.sha256()
+    for name in FFN_KERNELS:
+        h.update(kernel_source(src, name).encode())
+    for helper in ("device_common.h", "residency_dev.h"):
+        with open(os.path.join(CSRC, helper), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()
 
 
 def measured_traffic(cfg=4):
-    """HBM bytes per gate/up launch from the committed counter summary (FETCH_SIZE + WRITE_SIZE, each
-    calibrated by a known-size kernel), or None when the kernel source changed since they were taken."""
+    """HBM bytes per launch of the gate/up and of the down + combine kernel from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE passes, each calibrated by a known-size kernel): a dict, or None when
+    the kernels' source changed since the counters were taken."""
     path = TRAFFIC_FILES[cfg]
     if not os.path.exists(path):
         return None, "no counter summary"
@@ -196,9 +209,47 @@ def measured_traffic(cfg=4):
             if ":" in line and not line.startswith("#"):
                 key, val = line.split(":", 1)
                 kv[key.strip()] = val.strip()
-    if kv.get("kernel_source_sha256") != gateup_source_hash():
+    if kv.get("kernel_source_sha256") != ffn_source_hash():
         return None, "kernel source changed since the counters were taken"
-    return float(kv["hbm_bytes_per_launch"]), path[len(ROOT) + 1:]
+    return {"gateup": float(kv["gateup_hbm_bytes_per_launch"]),
+            "down": float(kv["down_hbm_bytes_per_launch"])}, path[len(ROOT) + 1:]
+
+
+def ffn_roofline(gu_bytes, dn_bytes, ktimes, hbm, traffic, traffic_src, replays, n_launch, label):
+    """The expert FFN's HBM roofline: algorithmic bytes of its two launches (gate/up + SwiGLU, down +
+    combine) over their device time per layer, with each launch's own figure beside it."""
+    gu_s, dn_s, ffn_s = ktimes["gateup"] * 1e-3, ktimes["down"] * 1e-3, ktimes["ffn"] * 1e-3
+    ffn_bytes = gu_bytes + dn_bytes
+    ach = ffn_bytes / ffn_s / 1e9
+    tr = None if traffic is None else traffic["gateup"] + traffic["down"]
+    sub = lambda b, t, tb: {"achieved": b / t / 1e9, "frac": b / t / 1e9 / HBM_PEAK_GBPS, "bytes_per_launch": b,
+                            "mean_launch_us": t * 1e6, "traffic": tb,
+                            "traffic_over_algorithmic": None if tb is None else tb / b}
+    return {"bound": "hbm", "kernel": f"expert FFN ({label}): gate/up + SwiGLU, then down + combine",
+            "achieved": ach, "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": ach / HBM_PEAK_GBPS,
+            "traffic": tr, "traffic_over_algorithmic": None if tr is None else tr / ffn_bytes,
+            "traffic_source": traffic_src, "bytes_per_launch": ffn_bytes, "mean_launch_us": ffn_s * 1e6,
+            "timing": f"the last step's {n_launch} layers' gate/up and down launches (same arguments, every expert "
+                      f"resident: the replays fill nothing, while a budgeted step's own gate/up launch also streams "
+                      f"its misses) in one HIP graph, replayed {replays}x between HIP events; per layer",
+            "practical_ceiling_GBps": hbm["launch_GBps"], "frac_of_practical": ach / hbm["launch_GBps"],
+            "gateup": sub(gu_bytes, gu_s, None if traffic is None else traffic["gateup"]),
+            "down": sub(dn_bytes, dn_s, None if traffic is None else traffic["down"])}
+
+
+def link_overlap(d, elapsed, steps):
+    """Stall and overlap of the demand fills over the timed region (device fill clock): per token the link's
+    busy time (copy), the time the fills held the step up (stall), the rest of the step (compute = wall -
+    stall), and overlap = 1 - (wall - max(copy, compute)) / min(copy, compute)."""
+    wall = elapsed * 1e3 / steps
+    copy = d["fill_ns"] * 1e-6 / steps
+    stall = d["stall_ns"] * 1e-6 / steps
+    compute = wall - stall
+    lo = min(copy, compute)
+    return {"stall_ms_per_token": stall, "fill_ms_per_token": copy, "compute_ms_per_token": compute,
+            "wall_ms_per_token": wall, "overlap": 1.0 - (wall - max(copy, compute)) / lo if lo > 0 else None,
+            "method": "device wall-clock stamps of the filling launches: first to last filling block (copy); how "
+                      "long the fills ran past the launch's computing blocks (stall)"}
 
 
 def expert_kernel_bytes(wl, n_exp, T):
@@ -311,6 +362,26 @@ def cpu_baseline(wl, store, steps, bias_np, x_np, budget_s, shared=None, attenti
     return len(outs) / dt, outs, dt
 
 
+def cpu_baseline_line(wl, store, steps, bias_np, x_np, budget_s, bytes_per_token, shared=None, attention=None):
+    """The oracle timed on every host core it is given, then on one thread (a third of the budget, at least
+    one token); returns the bench line's cpu_baseline object and the all-core run's outputs."""
+    import oracle
+    cores = oracle.threads_used()
+    tps, outs, dt = cpu_baseline(wl, store, steps, bias_np, x_np, budget_s, shared, attention)
+    oracle.set_threads(1)
+    try:
+        tps1, outs1, dt1 = cpu_baseline(wl, store, steps, bias_np, x_np, budget_s / 3, shared, attention)
+    finally:
+        oracle.set_threads(cores)
+    line = {"value": round(tps, 4), "unit": "tokens/s", "cores": cores, "kind": "oracle",
+            "cpu_model": oracle.cpu_model(), "GBps": tps * bytes_per_token / 1e9,
+            "sample": f"{len(outs)} timed tokens x {wl.L} layers, fp64 C oracle, no budget ({dt:.1f} s)",
+            "single_thread": {"value": round(tps1, 4), "unit": "tokens/s", "cores": 1,
+                              "GBps": tps1 * bytes_per_token / 1e9,
+                              "sample": f"{len(outs1)} timed tokens x {wl.L} layers ({dt1:.1f} s)"}}
+    return line, outs
+
+
 def prefill_ffn_time(torch, moe, synth, wl, layer_blob, shared_blob, router, reps=10):
     """Device time of one layer's expert FFN over the prompt chunk (moe_prefill_grouped: grouping, grouped
     GEMMs, combine) with that layer's experts resident, routed by its router; events around `reps` calls."""
@@ -409,10 +480,9 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
 
     tok_s = steps / t_decode
     gu_bytes, dn_bytes = expert_kernel_bytes(wl, k + 1, 1)
-    gu_ms, dn_ms = ktimes["gateup"], ktimes["down"]
-    gu_gbps = gu_bytes / (gu_ms * 1e-3) / 1e9
-    hbm = hbm_ceiling(torch, moe, gu_bytes)
+    hbm = hbm_ceiling(torch, moe, [gu_bytes, dn_bytes])
     traffic, traffic_src = measured_traffic(5)
+    roof = ffn_roofline(gu_bytes, dn_bytes, ktimes, hbm, traffic, traffic_src, args.replays, L, "int4 decode")
 
     # the prompt chunk's expert FFN on the matrix cores, one layer with its experts resident
     layer_blob = torch.from_numpy(np.ascontiguousarray(store[L - 1]).reshape(-1)).to(dev)
@@ -422,13 +492,14 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     pf_flop = 2.0 * rows * (2 * I) * H + 2.0 * rows * H * I
 
     d_pf = {f: st1[f] - st0[f] for f in ("lookups", "hits", "misses", "evictions", "prefetches", "h2d_bytes")}
-    d_dec = {f: st3[f] - st2[f] for f in ("lookups", "hits", "misses", "evictions", "h2d_bytes")}
+    d_dec = {f: st3[f] - st2[f] for f in ("lookups", "hits", "misses", "evictions", "h2d_bytes", "stall_ns",
+                                          "fill_ns")}
     ceil = max(pcie_ceiling_gbps(torch, moe, eb, 256 * eb), pcie_ceiling_gbps(torch, moe, 64 << 20, 1 << 30))
     h2d_tok = d_dec["h2d_bytes"] / steps
 
     sample = list(range(args.warmup, n_steps))
-    cpu_tps, outs, cpu_dt = cpu_baseline(wl, lambda l: store[l], sample, bias_np, x_np, args.cpu_seconds,
-                                         shared=shared_np)
+    cpu_line, outs = cpu_baseline_line(wl, lambda l: store[l], sample, bias_np, x_np, args.cpu_seconds,
+                                       L * (k + 1) * eb + L * wl.router_bytes, shared=shared_np)
     gpu_x = xs[sample[0]:sample[0] + len(outs)].cpu().numpy().astype(np.float64)
     err = 0.0
     for i, o in enumerate(outs):
@@ -455,18 +526,10 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
                    "prefetch_per_layer": args.prefetch, "policy": args.policy, "residency": args.residency,
                    "decode_graph": use_graph,
                    **({"charge_max": args.charge_max} if args.policy == "rotary" else {})},
-        "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU (int4 decode)", "achieved": gu_gbps,
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s", "frac": gu_gbps / HBM_PEAK_GBPS,
-                     "bytes_per_launch": gu_bytes, "mean_launch_us": gu_ms * 1e3,
-                     "timing": f"the last step's {L} launches (one per layer, same arguments, every expert resident: "
-                               f"the replays fill nothing, while a budgeted step's own gate/up launch also streams "
-                               f"its misses) in one HIP graph, replayed {args.replays}x between HIP events",
-                     "traffic": traffic, "traffic_source": traffic_src, "practical_ceiling_GBps": hbm["launch_GBps"],
-                     "frac_of_practical": gu_gbps / hbm["launch_GBps"]},
+        "roofline": roof,
         "hbm_ceiling": hbm,
-        "kernels": {"route_us": ktimes["route"] * 1e3, "gateup_us": gu_ms * 1e3, "down_us": dn_ms * 1e3,
-                    "down_bytes_per_launch": dn_bytes, "down_GBps": dn_bytes / (dn_ms * 1e-3) / 1e9,
-                    "ffn_us": ktimes["ffn"] * 1e3, "ffn_GBps": (gu_bytes + dn_bytes) / (ktimes["ffn"] * 1e-3) / 1e9},
+        "kernels": {"route_us": ktimes["route"] * 1e3, "gateup_us": ktimes["gateup"] * 1e3,
+                    "down_us": ktimes["down"] * 1e3, "ffn_us": ktimes["ffn"] * 1e3},
         "prefill": {"tokens": Tp, "tokens_per_s": Tp / t_prefill, "ms": t_prefill * 1e3,
                     "h2d_bytes": d_pf["h2d_bytes"], "misses": d_pf["misses"],
                     "prefetches": d_pf["prefetches"],
@@ -480,11 +543,9 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
                       "misses_per_token": d_dec["misses"] / steps, "bound": bound},
         "pcie": {"h2d_bytes_per_token": h2d_tok, "achieved_GBps": d_dec["h2d_bytes"] / t_decode / 1e9,
                  "ceiling_GBps": ceil, "frac": d_dec["h2d_bytes"] / t_decode / 1e9 / ceil,
-                 "tokens_per_s_bound": ceil * 1e9 / h2d_tok if h2d_tok else None},
-        "cpu_baseline": {"value": round(cpu_tps, 4), "unit": "tokens/s", "cores": oracle.threads_used(),
-                         "kind": "oracle",
-                         "sample": f"{len(outs)} timed decode tokens x {L} layers, fp64 C oracle, no budget "
-                                   f"({cpu_dt:.1f} s)"},
+                 "tokens_per_s_bound": ceil * 1e9 / h2d_tok if h2d_tok else None,
+                 **(link_overlap(d_dec, t_decode, steps) if args.residency == "device" else {})},
+        "cpu_baseline": cpu_line,
         "parity": {"sampled_tokens": len(outs), "max_normwise_err": err},
         "setup_s": round(t_setup, 1),
         "paper_context": "21.06 decode tokens/s and 74.2 prompt tokens/s at ~6.3 GB VRAM, RTX 4060 Laptop 8 GB, "
@@ -621,12 +682,9 @@ def main():
         unique = float(np.mean([len(np.unique(sets[t, 0])) for t in range(args.warmup, n_steps)]))
     n_exp = unique + (1 if wl.shared else 0)
     gu_bytes, dn_bytes = expert_kernel_bytes(wl, n_exp, T)
-    gu_ms, dn_ms, rt_ms = ktimes["gateup"], ktimes["down"], ktimes["route"]
-    gu_gbps = gu_bytes / (gu_ms * 1e-3) / 1e9 if gu_ms else None
-    dn_gbps = dn_bytes / (dn_ms * 1e-3) / 1e9 if dn_ms else None
 
     # ---- residency and PCIe
-    d = {f: st1[f] - st0[f] for f in ("lookups", "hits", "misses", "evictions", "h2d_bytes")}
+    d = {f: st1[f] - st0[f] for f in ("lookups", "hits", "misses", "evictions", "h2d_bytes", "stall_ns", "fill_ns")}
     h2d_per_tok = d["h2d_bytes"] / (args.steps * T)
     pcie = None
     if budgeted:
@@ -637,10 +695,13 @@ def main():
                 "ceiling_GBps": ceil, "ceiling_expert_chunks_GBps": ceil_expert,
                 "frac": d["h2d_bytes"] / elapsed / 1e9 / ceil,
                 "tokens_per_s_bound": ceil * 1e9 / h2d_per_tok if h2d_per_tok else None,
-                "ceiling_method": "hipMemcpyAsync from hipHostMalloc memory, 64 MiB and expert-size chunks"}
+                "ceiling_method": "hipMemcpyAsync from hipHostMalloc memory, 64 MiB and expert-size chunks",
+                **(link_overlap(d, elapsed, args.steps) if args.residency == "device" else {})}
 
-    hbm = hbm_ceiling(torch, moe, gu_bytes)
-    traffic, traffic_src = measured_traffic(4)
+    hbm = hbm_ceiling(torch, moe, [gu_bytes, dn_bytes])
+    traffic, traffic_src = measured_traffic(4) if args.config == 4 else (None, "no counter summary")
+    roof = ffn_roofline(gu_bytes, dn_bytes, ktimes, hbm, traffic, traffic_src, args.replays, L,
+                        f"{synth.DTYPE_NAMES[wl.dtype]} decode, T={T}")
 
     bound = residency_bound(moe, cache, E, st1["capacity"], policy=args.policy) if budgeted else None
 
@@ -651,9 +712,12 @@ def main():
         att_hook = lambda l, t, x: oracle.attention_decode(x.astype(np.float32), att_host["wq"][l], att_host["wo"][l],
                                                            att_host["kc"][l], att_host["vc"][l], att["start_pos"] + t,
                                                            att["n_heads"], att["n_kv"], theta=att["theta"])
-    cpu_tps, outs, cpu_dt = cpu_baseline(wl, lambda l: store[0 if alias else l], sample, bias_np
-                                         if bias_np is not None else np.zeros((n_steps, L, T, E), np.float32),
-                                         x_np, args.cpu_seconds, attention=att_hook)
+    cpu_bytes = L * T * (n_exp * eb + wl.router_bytes)
+    cpu_line, outs = cpu_baseline_line(wl, lambda l: store[0 if alias else l], sample, bias_np
+                                       if bias_np is not None else np.zeros((n_steps, L, T, E), np.float32),
+                                       x_np, args.cpu_seconds, cpu_bytes,
+                                       shared=[synth.expert_blob(wl, l, None) for l in range(L)] if wl.shared
+                                       else None, attention=att_hook)
     gpu_x = xs[sample[0]:sample[0] + len(outs)].cpu().numpy().astype(np.float64)
     err = 0.0
     for i, o in enumerate(outs):
@@ -689,29 +753,15 @@ def main():
                    **({"attention": {"n_heads": att["n_heads"], "n_kv": att["n_kv"], "head_dim": att["head_dim"],
                                      "kv_positions": att["max_pos"], "first_position": att["start_pos"]}}
                       if att is not None else {})},
-        "roofline": {"bound": "hbm", "kernel": "expert gate/up + SwiGLU", "achieved": gu_gbps,
-                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": gu_gbps / HBM_PEAK_GBPS if gu_gbps else None,
-                     "bytes_per_launch": gu_bytes, "mean_launch_us": gu_ms * 1e3,
-                     "timing": f"the last step's {L} launches (one per layer, same arguments, every expert resident: "
-                               f"the replays fill nothing, while a budgeted step's own gate/up launch also streams "
-                               f"its misses) in one HIP graph, replayed {args.replays}x between HIP events",
-                     "traffic": traffic, "traffic_source": traffic_src,
-                     "practical_ceiling_GBps": hbm["launch_GBps"],
-                     "frac_of_practical": gu_gbps / hbm["launch_GBps"] if gu_gbps else None},
+        "roofline": roof,
         "hbm_ceiling": hbm,
-        "kernels": {"route_us": rt_ms * 1e3, "gateup_us": gu_ms * 1e3, "down_us": dn_ms * 1e3,
-                    "down_GBps": dn_gbps, "down_bytes_per_launch": dn_bytes,
-                    "ffn_us": ktimes["ffn"] * 1e3,
-                    "ffn_GBps": (gu_bytes + dn_bytes) / (ktimes["ffn"] * 1e-3) / 1e9 if ktimes["ffn"] else None,
+        "kernels": {"route_us": ktimes["route"] * 1e3, "gateup_us": ktimes["gateup"] * 1e3,
+                    "down_us": ktimes["down"] * 1e3, "ffn_us": ktimes["ffn"] * 1e3,
                     **(attention_kernel_line(att, H, ktimes["attention"], n_steps) if att is not None else {})},
         "residency": {**d, "miss_rate": d["misses"] / d["lookups"] if d["lookups"] else 0.0,
                       "misses_per_token": d["misses"] / (args.steps * T), "bound": bound},
         "pcie": pcie,
-        "cpu_baseline": {"value": round(cpu_tps, 4), "unit": "tokens/s", "cores": oracle.threads_used(),
-                         "kind": "oracle",
-                         "sample": f"{len(outs)} timed tokens x {L} layers, fp64 C oracle, no budget "
-                                   f"({cpu_dt:.1f} s)"},
+        "cpu_baseline": cpu_line,
         "parity": {"sampled_tokens": len(outs), "max_normwise_err": err},
         "setup_s": round(t_setup, 1),
         "paper_context": "21.06 decode tokens/s at ~6.3 GB VRAM, RTX 4060 Laptop 8 GB, Qwen3.6-35B-A3B Q4_K_M",

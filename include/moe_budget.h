@@ -263,6 +263,14 @@ typedef struct {
     uint64_t h2d_bytes;   /* bytes filled from the host store */
     int32_t capacity;     /* slots: floor((budget - reserved) / expert_bytes) */
     int32_t occupancy;    /* slots holding an expert */
+    /* MOE_CACHE_DEVICE (0 otherwise), device wall-clock time of the demand fills (sec. 4's selective load
+     * on the step's path; a prefetch's fills are not counted):
+     *   fill_ns:  per filling launch, from its first filling block's start to its last one's end, summed;
+     *   stall_ns: per filling launch, how long its fills ran past both their start and the end of the
+     *             launch's computing blocks (the resident experts' work), summed: the time the misses held
+     *             up the step. */
+    uint64_t stall_ns;
+    uint64_t fill_ns;
 } moe_cache_stats;
 
 /* One residency decision.  victim_key = layer * E + expert of the evicted
@@ -424,21 +432,22 @@ MOE_API int moe_stack_destroy(moe_stack *s);
  * token the FFN's gate/up launch also streams the layer's missing experts from
  * the host store into their slots (the resident experts' gate/up runs
  * meanwhile), for more tokens a fill launch precedes the FFN.
- * ids_out (device int32 [L x T x k]) and weights_out (device fp32 [L x T x k])
- * receive each layer's routing when non-NULL. */
+ * ids_out (device int32 [L x T x k]), weights_out (device fp32 [L x T x k]) and
+ * logits_out (device fp32 [L x T x E]: each layer's router logits, bias
+ * included, as the top-k saw them) receive each layer's routing when non-NULL. */
 MOE_API int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *logit_bias,
-                          int32_t *ids_out, float *weights_out, void *stream);
+                          int32_t *ids_out, float *weights_out, float *logits_out, void *stream);
 
 /* moe_stack_decode_step for one token (T = 1), as a replayed HIP graph.  With a
  * MOE_CACHE_DEVICE cache nothing in a step waits for the host, so the first call
  * captures the step's launches (every layer's routing, fused top-k + lookup,
  * and expert FFN with its fills) and later calls replay them after setting the step tag
- * on the device; a call with other x / logit_bias / ids_out / weights_out
- * pointers captures again (keep the buffers fixed and refill them).  Results
+ * on the device; a call with other x / logit_bias / ids_out / weights_out /
+ * logits_out pointers captures again (keep the buffers fixed and refill them).  Results
  * and residency decisions are those of moe_stack_decode_step.  Without a device
  * cache it is moe_stack_decode_step. */
 MOE_API int moe_stack_decode_graph(moe_stack *s, int step, float *x, const float *logit_bias, int32_t *ids_out,
-                                   float *weights_out, void *stream);
+                                   float *weights_out, float *logits_out, void *stream);
 
 /* Prompt evaluation (prefill; its rate is reported beside decode in the table
  * of sec. 8.1) over every layer, in place on x (device fp32 [T x H]):
@@ -447,10 +456,10 @@ MOE_API int moe_stack_decode_graph(moe_stack *s, int step, float *x, const float
  * moe_prefill_grouped (bf16 activations on the matrix cores; w_dtype MOE_BF16 or
  * MOE_INT4G128).  Under a budget each layer copies its T*k ids to the host and
  * runs one lookup for the chunk's distinct experts, which must fit in the cache
- * (MOE_ERR_BUDGET otherwise).  1 <= T <= max_prefill_tokens; ids_out / weights_out
- * as for moe_stack_decode_step; `step` is the residency step of the chunk. */
+ * (MOE_ERR_BUDGET otherwise).  1 <= T <= max_prefill_tokens; ids_out / weights_out /
+ * logits_out as for moe_stack_decode_step; `step` is the residency step of the chunk. */
 MOE_API int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out, float *weights_out,
-                              void *stream);
+                              float *logits_out, void *stream);
 
 /* Mean device time (ms) of one launch of kernel `which` (0 = router logits and
  * top-k, 1 = expert gate/up + SwiGLU, 2 = expert down + combine, 3 = the whole

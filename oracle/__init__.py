@@ -87,9 +87,27 @@ def _c(a, dtype) -> np.ndarray:
 
 
 def threads_used() -> int:
-    """OpenMP threads the oracle's parallel loops run on."""
-    n = os.environ.get("OMP_NUM_THREADS")
-    return int(n) if n else (len(os.sched_getaffinity(0)) if hasattr(os, "sched_getaffinity") else os.cpu_count())
+    """OpenMP threads the oracle's parallel loops run on (OpenMP's own count, as set or defaulted)."""
+    return int(lib().omp_get_max_threads())
+
+
+def set_threads(n: int) -> None:
+    """Run the oracle's parallel loops on n threads from now on (OpenMP's omp_set_num_threads); the results
+    do not depend on it, since every output row is summed by one thread in a fixed order."""
+    lib().omp_set_num_threads(C.c_int(int(n)))
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (from /proc/cpuinfo), for reporting the oracle's timings."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
 
 
 def expert_bytes(H: int, I: int, dtype: int) -> int:

@@ -45,7 +45,8 @@ class CacheDesc(C.Structure):
 class CacheStats(C.Structure):
     _fields_ = [("lookups", C.c_uint64), ("hits", C.c_uint64), ("misses", C.c_uint64),
                 ("prefetches", C.c_uint64), ("evictions", C.c_uint64), ("h2d_bytes", C.c_uint64),
-                ("capacity", C.c_int32), ("occupancy", C.c_int32)]
+                ("capacity", C.c_int32), ("occupancy", C.c_int32), ("stall_ns", C.c_uint64),
+                ("fill_ns", C.c_uint64)]
 
 
 EVENT_DTYPE = np.dtype([("t", "<i4"), ("layer", "<i4"), ("expert", "<i4"),
@@ -98,10 +99,10 @@ def lib() -> C.CDLL:
             "expert_cache_trace": [P, SZ, P, SZ, C.POINTER(SZ)],
             "moe_stack_create": [C.POINTER(StackDesc), C.POINTER(P)],
             "moe_stack_destroy": [P],
-            "moe_stack_decode_step": [P, I, P, I, P, P, P, P],
-            "moe_stack_decode_graph": [P, I, P, P, P, P, P],
+            "moe_stack_decode_step": [P, I, P, I, P, P, P, P, P],
+            "moe_stack_decode_graph": [P, I, P, P, P, P, P, P],
             "moe_stack_kernel_time": [P, I, I, P, C.POINTER(C.c_double)],
-            "moe_stack_prefill": [P, I, P, I, P, P, P],
+            "moe_stack_prefill": [P, I, P, I, P, P, P, P],
             "moe_hbm_read_probe": [P, SZ, P, P],
             "moe_opt_fills": [P, P, I, I, I, U64P],
         }
@@ -429,17 +430,20 @@ class MoeStack:
 
     __del__ = close
 
-    def decode_step(self, step: int, x, logit_bias=None, ids_out=None, weights_out=None, stream=None):
+    def decode_step(self, step: int, x, logit_bias=None, ids_out=None, weights_out=None, logits_out=None,
+                    stream=None):
         """x <- x + MoE_l(x) over every layer, in place on the device tensor x [T x H]."""
         import torch
         T = x.shape[0]
         _check(lib().moe_stack_decode_step(self._h, step, _dev(x, "x", torch.float32), T,
                                            _dev(logit_bias, "logit_bias", torch.float32),
                                            _dev(ids_out, "ids_out", torch.int32),
-                                           _dev(weights_out, "weights_out", torch.float32), _stream(stream)),
+                                           _dev(weights_out, "weights_out", torch.float32),
+                                           _dev(logits_out, "logits_out", torch.float32), _stream(stream)),
                "moe_stack_decode_step")
 
-    def decode_graph(self, step: int, x, logit_bias=None, ids_out=None, weights_out=None, stream=None):
+    def decode_graph(self, step: int, x, logit_bias=None, ids_out=None, weights_out=None, logits_out=None,
+                     stream=None):
         """One-token decode step as a replayed HIP graph (device residency); keep the tensors fixed."""
         import torch
         if x.shape[0] != 1:
@@ -447,17 +451,19 @@ class MoeStack:
         _check(lib().moe_stack_decode_graph(self._h, step, _dev(x, "x", torch.float32),
                                             _dev(logit_bias, "logit_bias", torch.float32),
                                             _dev(ids_out, "ids_out", torch.int32),
-                                            _dev(weights_out, "weights_out", torch.float32), _stream(stream)),
+                                            _dev(weights_out, "weights_out", torch.float32),
+                                            _dev(logits_out, "logits_out", torch.float32), _stream(stream)),
                "moe_stack_decode_graph")
         return x
 
-    def prefill(self, step: int, x, ids_out=None, weights_out=None, stream=None):
+    def prefill(self, step: int, x, ids_out=None, weights_out=None, logits_out=None, stream=None):
         """Prompt chunk: x <- x + MoE_l(rmsnorm(x)) over every layer, in place on the device tensor x [T x H]."""
         import torch
         T = x.shape[0]
         _check(lib().moe_stack_prefill(self._h, step, _dev(x, "x", torch.float32), T,
                                        _dev(ids_out, "ids_out", torch.int32),
-                                       _dev(weights_out, "weights_out", torch.float32), _stream(stream)),
+                                       _dev(weights_out, "weights_out", torch.float32),
+                                       _dev(logits_out, "logits_out", torch.float32), _stream(stream)),
                "moe_stack_prefill")
         return x
 

@@ -48,6 +48,7 @@ enum : int { kFfnGateUp = 1, kFfnDown = 2, kFfnBoth = 3 };
 // down part.  The host link then carries the misses while the resident
 // experts' gate/up runs, and no separate fill launch sits on the step's path.
 struct FfnFill {
+    unsigned long long *clk = nullptr;  // device fill clock of the cache (DevResidency::clk), or nullptr
     const int32_t *n = nullptr;      // device: number of fills (nullptr: this launch fills nothing)
     const long long *src = nullptr;  // device [n]: byte offset of each blob in the host store
     const int32_t *slot = nullptr;   // device [n]: its slot
@@ -100,7 +101,16 @@ enum : int {
     kScalCtr, kScalHand, kScalNextFree, kScalHits, kScalMisses, kScalEvictions, kScalEvents, kScalPrefetches,
     kDevScalars
 };
+// Fill clock of a device-residency cache, in device wall-clock ticks: a launch that performs demand fills
+// records when its filling blocks started (minimum) and ended (maximum) and when its other, computing blocks
+// ended (maximum), each spread over kClkLanes words to keep the atomics apart; the cache's next lookup kernel
+// folds the record into the stall and fill-time totals and clears it.  Stall = how long the fills outlasted
+// both their own start and the launch's compute, i.e. the time they held up the step.
+constexpr int kClkLanes = 8;
+enum : int { kClkFillStart = 0, kClkFillEnd = kClkLanes, kClkComputeEnd = 2 * kClkLanes, kClkStall = 3 * kClkLanes,
+             kClkFill, kClkFolds, kClkWords };
 struct DevResidency {
+    unsigned long long *clk = nullptr;   // [kClkWords] fill clock (above)
     int32_t *key_of_slot = nullptr;      // [C] layer*E + expert, -1 = free
     uint64_t *stamp = nullptr;           // [C] LRU: recency stamp
     uint16_t *charge = nullptr;          // [C] rotary: charge
@@ -126,9 +136,10 @@ hipError_t launch_dev_lookup(const DevResidency &r, const DevLookup &p, const in
 // One token: top-k of its logits fused with the device lookup of the selected experts (one block).
 hipError_t launch_topk_lookup(const float *logits, int E, int k, int32_t *ids, float *weights, int *err_flags,
                               const DevResidency &r, const DevLookup &p, int32_t *slots_out, hipStream_t s);
-// Streams the last lookup's fills (at most max_fills) from the host store into their slots.
+// Streams the last lookup's fills (at most max_fills) from the host store into their slots.  Demand fills
+// (`demand`) record their span in the fill clock; a prefetch's fills, off the step's path, do not.
 hipError_t launch_dev_fill(const DevResidency &r, const uint8_t *host_dev, uint8_t *pool, long long expert_bytes,
-                           int max_fills, hipStream_t s);
+                           int max_fills, hipStream_t s, bool demand = true);
 hipError_t launch_hbm_read(const void *buf, size_t bytes, float *sink, hipStream_t s);
 
 // Prefill (any T): pairs grouped by expert, grouped bf16 MFMA GEMMs, rank-order combine.

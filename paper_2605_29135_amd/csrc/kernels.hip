@@ -163,6 +163,7 @@ __global__ __launch_bounds__(NT) void topk_lookup_kernel(const float *__restrict
     __shared__ devres::DevLds<ROTARY, NT> L;
     devres::DevStaged st;
     devres::dev_stage_issue<ROTARY, NT>(r, p, st);
+    if (threadIdx.x == NT - 1 && r.clk) devres::clk_fold(r.clk);  // the previous filling launch's record
     const int lane = threadIdx.x & (kWave - 1);
     if (threadIdx.x < kWave) {
         topk_wave<false>(logits, E, k, ids, wout, err, &sc);
@@ -499,9 +500,15 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     int istride = 0;         // then the wave's row pairs lie this far apart (0: one row pair per wave)
     int pstart = 0, pcount = 1, single = 0;
     const int *pairs = nullptr;
+    unsigned long long *clk = nullptr;  // a filling launch: its blocks stamp the fill clock
+    unsigned long long t_fill = 0;      // when this block began filling
     if constexpr (ONE_TOKEN) {
+        clk = plan.fill.n ? plan.fill.clk : nullptr;
         if (plan.fill.n && g == int(gridDim.y) - 1) {
+            const bool busy = int(blockIdx.x) < min(plan.fill.n[0], MOE_MAX_TOPK) * plan.fill.slices;
+            const unsigned long long t0 = clk && busy ? devres::clk_now() : 0ull;
             copy_down_parts(plan.fill, expert_bytes);
+            if (t0) devres::clk_record_fill(clk, t0, devres::clk_now());
             return;
         }
         if (g < k && plan.n) {
@@ -529,6 +536,7 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
                 if (dst) {
                     if (int(blockIdx.x) >= plan.fill.blocks) return;
                     istride = plan.fill.blocks * (kBlock / kWave);
+                    if (clk) t_fill = devres::clk_now();
                 }
             }
         } else {
@@ -663,6 +671,10 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     if (!istride) break;  // block-uniform; no barrier follows the first pass
     i += istride;
     if (i >= I) break;
+    }
+    if (clk) {  // (wave 0 of the block records: waves past I returned early only when not staging x)
+        if (t_fill) devres::clk_record_fill(clk, t_fill, devres::clk_now());
+        else devres::clk_record_compute(clk, devres::clk_now());
     }
 }
 

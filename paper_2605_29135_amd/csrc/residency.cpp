@@ -115,6 +115,7 @@ struct moe_cache {
     moe_cache_stats st{};
 
     bool dev_mode = false;   // MOE_CACHE_DEVICE: decisions and log on the device
+    int clk_khz = 0;         // MOE_CACHE_DEVICE: rate of the device wall clock the fill clock counts in
     moe::DevResidency dr;
     // MOE_CACHE_DEVICE prefetch: its decisions on the caller's stream, its fills on the copy stream
     hipEvent_t pf_issued = nullptr, pf_done = nullptr;
@@ -408,7 +409,7 @@ int moe::cache_prefetch_device(moe_cache *c, int step, int layer, const int32_t 
     if (e == hipSuccess) e = hipStreamWaitEvent(c->copy, c->pf_issued, 0);
     if (e == hipSuccess)
         e = moe::launch_dev_fill(c->dr, c->host_dev, c->pool, (long long)c->d.expert_bytes, std::min(n, c->E),
-                                 c->copy);
+                                 c->copy, false);
     if (e == hipSuccess) e = hipEventRecord(c->pf_done, c->copy);
     if (e != hipSuccess) return moe::fail_hip(e, "device prefetch");
     c->pf_pending = true;
@@ -417,6 +418,7 @@ int moe::cache_prefetch_device(moe_cache *c, int step, int layer, const int32_t 
 
 moe::FfnFill moe::cache_ffn_fill(moe_cache *c, long long down_off) {
     moe::FfnFill f;
+    f.clk = c->dr.clk;
     f.n = c->dr.n_fill;
     f.src = c->dr.fill_src;
     f.slot = c->dr.fill_slot;
@@ -455,7 +457,13 @@ int dev_state_create(moe_cache *c, bool preload) {
     if (e == hipSuccess) e = hipMalloc(&r.fill_src, sizeof(long long) * size_t(c->E));
     if (e == hipSuccess) e = hipMalloc(&r.fill_slot, sizeof(int32_t) * size_t(c->E));
     if (e == hipSuccess) e = hipMalloc(&r.n_fill, sizeof(int32_t));
+    if (e == hipSuccess) e = hipMalloc(&r.clk, sizeof(unsigned long long) * moe::kClkWords);
     if (e != hipSuccess) return moe::fail_hip(e, "allocating the device residency state");
+    int dev = 0, khz = 0;
+    if ((e = hipGetDevice(&dev)) == hipSuccess)
+        e = hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev);
+    if (e != hipSuccess || khz <= 0) return moe::fail_hip(e, "reading the device wall-clock rate");
+    c->clk_khz = khz;
     r.cap_events = kDevEvents;
     r.slot_of_key = c->dev_slot_of;
     std::vector<uint64_t> stamp(C, 0);
@@ -472,6 +480,10 @@ int dev_state_create(moe_cache *c, bool preload) {
     if (e == hipSuccess)
         e = hipMemcpy(r.scal, scal.data(), sizeof(unsigned long long) * scal.size(), hipMemcpyHostToDevice);
     if (e == hipSuccess) e = hipMemset(r.n_fill, 0, sizeof(int32_t));
+    std::vector<unsigned long long> clk(moe::kClkWords, 0ull);
+    for (int i = 0; i < moe::kClkLanes; ++i) clk[size_t(moe::kClkFillStart + i)] = ~0ull;
+    if (e == hipSuccess)
+        e = hipMemcpy(r.clk, clk.data(), sizeof(unsigned long long) * clk.size(), hipMemcpyHostToDevice);
     return e == hipSuccess ? MOE_OK : moe::fail_hip(e, "initialising the device residency state");
 }
 
@@ -479,7 +491,7 @@ void dev_state_destroy(moe_cache *c) {
     moe::DevResidency &r = c->dr;
     for (void *p : {static_cast<void *>(r.key_of_slot), static_cast<void *>(r.stamp), static_cast<void *>(r.charge),
                     static_cast<void *>(r.scal), static_cast<void *>(r.events), static_cast<void *>(r.fill_src),
-                    static_cast<void *>(r.fill_slot), static_cast<void *>(r.n_fill)})
+                    static_cast<void *>(r.fill_slot), static_cast<void *>(r.n_fill), static_cast<void *>(r.clk)})
         if (p) (void)hipFree(p);
     r = moe::DevResidency{};
 }
@@ -700,6 +712,25 @@ int expert_cache_stats(moe_cache *c, moe_cache_stats *out) {
         out->h2d_bytes = (out->misses + out->prefetches) * c->d.expert_bytes;
         out->capacity = c->C;
         out->occupancy = int32_t(std::min<unsigned long long>(v[moe::kScalNextFree], (unsigned long long)c->C));
+        // fill clock: the folded totals plus the record of the last filling launch, not folded yet
+        unsigned long long k[moe::kClkWords];
+        if ((e = hipMemcpy(k, c->dr.clk, sizeof k, hipMemcpyDeviceToHost)) != hipSuccess)
+            return moe::fail_hip(e, "reading the fill clock");
+        unsigned long long stall = k[moe::kClkStall], fill = k[moe::kClkFill];
+        unsigned long long fs = ~0ull, fe = 0, ce = 0;
+        for (int i = 0; i < moe::kClkLanes; ++i) {
+            fs = std::min(fs, k[moe::kClkFillStart + i]);
+            fe = std::max(fe, k[moe::kClkFillEnd + i]);
+            ce = std::max(ce, k[moe::kClkComputeEnd + i]);
+        }
+        if (fe > 0 && fe > fs) {
+            const unsigned long long from = std::max(fs, ce);
+            if (fe > from) stall += fe - from;
+            fill += fe - fs;
+        }
+        const double ns_per_tick = 1.0e6 / double(c->clk_khz);
+        out->stall_ns = uint64_t(double(stall) * ns_per_tick + 0.5);
+        out->fill_ns = uint64_t(double(fill) * ns_per_tick + 0.5);
         return MOE_OK;
     }
     *out = c->st;

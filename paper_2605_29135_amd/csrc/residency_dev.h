@@ -43,6 +43,49 @@ __device__ __forceinline__ void dev_stage_issue(const DevResidency &r, const Dev
     }
 }
 
+// ---- fill clock (DevResidency::clk) ----
+__device__ __forceinline__ unsigned long long clk_now() { return (unsigned long long)wall_clock64(); }
+
+__device__ __forceinline__ int clk_lane() { return int(blockIdx.x + blockIdx.y) & (kClkLanes - 1); }
+
+// A block that filled from t0 to t1 (called by every thread; lane 0 of wave 0 records).
+__device__ __forceinline__ void clk_record_fill(unsigned long long *clk, unsigned long long t0, unsigned long long t1) {
+    if (threadIdx.x == 0) {
+        atomicMin(clk + kClkFillStart + clk_lane(), t0);
+        atomicMax(clk + kClkFillEnd + clk_lane(), t1);
+    }
+}
+
+// A block of a filling launch that computed and ended at t1.
+__device__ __forceinline__ void clk_record_compute(unsigned long long *clk, unsigned long long t1) {
+    if (threadIdx.x == 0) atomicMax(clk + kClkComputeEnd + clk_lane(), t1);
+}
+
+// Folds the last filling launch's record into the totals and clears it (one thread; the launch has ended,
+// being earlier on the stream).
+__device__ __forceinline__ void clk_fold(unsigned long long *clk) {
+    unsigned long long fs = ~0ull, fe = 0, ce = 0;
+#pragma unroll
+    for (int i = 0; i < kClkLanes; ++i) {
+        fs = min(fs, clk[kClkFillStart + i]);
+        fe = max(fe, clk[kClkFillEnd + i]);
+        ce = max(ce, clk[kClkComputeEnd + i]);
+    }
+    if (fe == 0 && ce == 0) return;  // nothing recorded since the last fold
+    if (fe > 0 && fe > fs) {
+        const unsigned long long from = fs > ce ? fs : ce;
+        if (fe > from) clk[kClkStall] += fe - from;
+        clk[kClkFill] += fe - fs;
+        clk[kClkFolds] += 1;
+    }
+#pragma unroll
+    for (int i = 0; i < kClkLanes; ++i) {
+        clk[kClkFillStart + i] = ~0ull;
+        clk[kClkFillEnd + i] = 0;
+        clk[kClkComputeEnd + i] = 0;
+    }
+}
+
 // One int per wave in cnt[]: the block total, and the sum over the waves ahead of `wave`.
 template <int NW>
 __device__ __forceinline__ int wave_prefix(const int *cnt, int wave, int &total) {

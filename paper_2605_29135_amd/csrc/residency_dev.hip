@@ -33,6 +33,7 @@ __global__ __launch_bounds__(NT) void dev_lookup_kernel(DevResidency r, DevLooku
     __shared__ DevLds<ROTARY, NT> L;
     DevStaged st;
     dev_stage_issue<ROTARY, NT>(r, p, st);
+    if (threadIdx.x == NT - 1 && r.clk) clk_fold(r.clk);
     dev_stage_lds<ROTARY, NT>(L, p, st);
     __syncthreads();
     dev_lookup_body<ROTARY, NT>(L, r, p, ids, n, slots_out, err);
@@ -41,12 +42,15 @@ __global__ __launch_bounds__(NT) void dev_lookup_kernel(DevResidency r, DevLooku
 // Block (x, y) streams its share of fills y, y + gridDim.y, ...; blocks past the lookup's fill count exit.
 // The grid covers a few fills at a time: a prefetch of a whole layer (hundreds of fills) then keeps the
 // same bytes in flight as a decode step's fills and leaves most compute units to the kernels it overlaps.
+// With clk (demand fills) each block that streamed something records its span in the fill clock.
 __global__ __launch_bounds__(kFillThreads) void dev_fill_kernel(const long long *__restrict__ src_off,
                                                                const int32_t *__restrict__ slot,
                                                                const int32_t *__restrict__ n_fill,
                                                                const uint8_t *__restrict__ host_dev,
-                                                               uint8_t *__restrict__ pool, long long bytes) {
+                                                               uint8_t *__restrict__ pool, long long bytes,
+                                                               unsigned long long *clk) {
     const int nf = n_fill[0];
+    const unsigned long long t0 = clk && int(blockIdx.y) < nf ? clk_now() : 0ull;
     const size_t n16 = size_t(bytes) / 16;
     const size_t per = (n16 + gridDim.x - 1) / gridDim.x;
     const size_t beg = size_t(blockIdx.x) * per;
@@ -68,6 +72,7 @@ __global__ __launch_bounds__(kFillThreads) void dev_fill_kernel(const long long 
             }
         }
     }
+    if (t0) clk_record_fill(clk, t0, clk_now());
 }
 
 __global__ void set_int_kernel(int *p, int v) { *p = v; }
@@ -92,7 +97,7 @@ hipError_t launch_dev_lookup(const DevResidency &r, const DevLookup &p, const in
 }
 
 hipError_t launch_dev_fill(const DevResidency &r, const uint8_t *host_dev, uint8_t *pool, long long expert_bytes,
-                           int max_fills, hipStream_t s) {
+                           int max_fills, hipStream_t s, bool demand) {
     if (max_fills < 1) return hipSuccess;
     if (expert_bytes <= 0 || expert_bytes % 16) return hipErrorInvalidValue;
     long long bpf = expert_bytes / (64 << 10);  // 32 blocks for a 9 MiB blob
@@ -100,7 +105,8 @@ hipError_t launch_dev_fill(const DevResidency &r, const uint8_t *host_dev, uint8
     const int ny = max_fills < kFillsInFlight ? max_fills : kFillsInFlight;
     dev_fill_kernel<<<dim3(unsigned(bpf), unsigned(ny)), kFillThreads, 0, s>>>(r.fill_src, r.fill_slot,
                                                                                      r.n_fill, host_dev, pool,
-                                                                                     expert_bytes);
+                                                                                     expert_bytes,
+                                                                                     demand ? r.clk : nullptr);
     return hipGetLastError();
 }
 

@@ -29,8 +29,10 @@ struct Snapshot {
 struct GraphKey {
     const float *x = nullptr, *bias = nullptr;
     const int32_t *ids = nullptr;
-    const float *w = nullptr;
-    bool operator==(const GraphKey &o) const { return x == o.x && bias == o.bias && ids == o.ids && w == o.w; }
+    const float *w = nullptr, *logits = nullptr;
+    bool operator==(const GraphKey &o) const {
+        return x == o.x && bias == o.bias && ids == o.ids && w == o.w && logits == o.logits;
+    }
 };
 
 struct LastLayer {
@@ -327,7 +329,7 @@ namespace {
 // cache, one token: nothing waits for the host) the decisions take their step tag
 // from device memory, so that the enqueued work can be captured once and replayed.
 int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_bias, int32_t *ids_out,
-                   float *weights_out, hipStream_t strm, const int *step_dev) {
+                   float *weights_out, float *logits_out, hipStream_t strm, const int *step_dev) {
     int *eflags = moe::device_error_flags();
     if (!eflags) return moe::fail(MOE_ERR_HIP, "device error flags unavailable");
     const auto &d = s->d;
@@ -346,21 +348,21 @@ int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_b
         }
         int32_t *ids = ids_out ? ids_out + size_t(l) * T * d.k : s->ids;
         float *w = weights_out ? weights_out + size_t(l) * T * d.k : s->weights;
+        float *lg = logits_out ? logits_out + size_t(l) * T * d.E : s->logits;
         const float *bias = logit_bias ? logit_bias + size_t(l) * T * d.E : nullptr;
         // lookups on the device need no ids on the host; otherwise one token under a budget has the
         // top-k kernel publish its ids straight to host memory
         const bool dev_lookup = s->budgeted && moe::cache_device(d.cache);
         const bool mailbox = s->budgeted && T == 1 && !dev_lookup;
         const uint32_t seq = mailbox ? ++s->mbox_seq : 0;
-        hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, bias, s->logits,
-                                                 true, s->h, strm);
+        hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, bias, lg, true,
+                                                 s->h, strm);
         const bool fused = dev_lookup && T == 1;  // one token: top-k and the lookup in one kernel
         if (e == hipSuccess && !fused)
-            e = moe::launch_topk_softmax(s->logits, T, d.E, d.k, ids, w, eflags, strm, mailbox ? s->mbox_dev : nullptr,
-                                         seq);
+            e = moe::launch_topk_softmax(lg, T, d.E, d.k, ids, w, eflags, strm, mailbox ? s->mbox_dev : nullptr, seq);
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: routing");
         if (fused) {
-            int st = moe::cache_topk_lookup(d.cache, step, l, s->logits, d.k, ids, w,
+            int st = moe::cache_topk_lookup(d.cache, step, l, lg, d.k, ids, w,
                                             s->dev_slots + size_t(l) * d.max_tokens * d.k, eflags, strm, step_dev,
                                             true);
             if (st != MOE_OK) return st;
@@ -433,20 +435,21 @@ int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_b
 extern "C" {
 
 int moe_stack_decode_step(moe_stack *s, int step, float *x, int T, const float *logit_bias,
-                          int32_t *ids_out, float *weights_out, void *stream) {
+                          int32_t *ids_out, float *weights_out, float *logits_out, void *stream) {
     if (!s || !x) return moe::fail(MOE_ERR_INVALID_ARG, "stack step: NULL argument");
     if (T < 1 || T > s->d.max_tokens)
         return moe::fail(MOE_ERR_INVALID_ARG, "stack step: T=%d outside [1, %d]", T, s->d.max_tokens);
-    return enqueue_decode(s, step, x, T, logit_bias, ids_out, weights_out, static_cast<hipStream_t>(stream), nullptr);
+    return enqueue_decode(s, step, x, T, logit_bias, ids_out, weights_out, logits_out,
+                          static_cast<hipStream_t>(stream), nullptr);
 }
 
 int moe_stack_decode_graph(moe_stack *s, int step, float *x, const float *logit_bias, int32_t *ids_out,
-                           float *weights_out, void *stream) {
+                           float *weights_out, float *logits_out, void *stream) {
     if (!s || !x) return moe::fail(MOE_ERR_INVALID_ARG, "stack step: NULL argument");
     auto strm = static_cast<hipStream_t>(stream);
     if (!s->budgeted || !moe::cache_device(s->d.cache) || s->attn)  // host waits, or a moving position: no graph
-        return enqueue_decode(s, step, x, 1, logit_bias, ids_out, weights_out, strm, nullptr);
-    const GraphKey key{x, logit_bias, ids_out, weights_out};
+        return enqueue_decode(s, step, x, 1, logit_bias, ids_out, weights_out, logits_out, strm, nullptr);
+    const GraphKey key{x, logit_bias, ids_out, weights_out, logits_out};
     hipError_t e = hipSuccess;
     if (!s->graph_exec || !(s->graph_key == key)) {
         if (s->graph_exec) (void)hipGraphExecDestroy(s->graph_exec);
@@ -462,7 +465,7 @@ int moe_stack_decode_graph(moe_stack *s, int step, float *x, const float *logit_
         int st = MOE_OK;
         if (e == hipSuccess) e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
         if (e == hipSuccess) {
-            st = enqueue_decode(s, step, x, 1, logit_bias, ids_out, weights_out, cs, s->dev_step);
+            st = enqueue_decode(s, step, x, 1, logit_bias, ids_out, weights_out, logits_out, cs, s->dev_step);
             hipError_t e2 = hipStreamEndCapture(cs, &g);
             if (e == hipSuccess) e = e2;
         }
@@ -485,7 +488,7 @@ int moe_stack_decode_graph(moe_stack *s, int step, float *x, const float *logit_
 }
 
 int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out, float *weights_out,
-                      void *stream) {
+                      float *logits_out, void *stream) {
     if (!s || !x) return moe::fail(MOE_ERR_INVALID_ARG, "stack prefill: NULL argument");
     if (s->d.max_prefill_tokens < 1) return moe::fail(MOE_ERR_INVALID_ARG, "stack prefill: created without prefill");
     if (T < 1 || T > s->d.max_prefill_tokens)
@@ -511,9 +514,10 @@ int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out,
     for (int l = 0; l < d.n_layers; ++l) {
         int32_t *ids = ids_out ? ids_out + size_t(l) * T * d.k : s->ids;
         float *w = weights_out ? weights_out + size_t(l) * T * d.k : s->weights;
-        hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, nullptr, s->logits,
-                                                 true, s->h, strm);
-        if (e == hipSuccess) e = moe::launch_topk_softmax(s->logits, T, d.E, d.k, ids, w, eflags, strm);
+        float *lg = logits_out ? logits_out + size_t(l) * T * d.E : s->logits;
+        hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, nullptr, lg, true,
+                                                 s->h, strm);
+        if (e == hipSuccess) e = moe::launch_topk_softmax(lg, T, d.E, d.k, ids, w, eflags, strm);
         if (e != hipSuccess) return moe::fail_hip(e, "stack prefill: routing");
         const int32_t *slot_of = s->slot_table + size_t(l) * d.E;
         const uint8_t *pool = static_cast<const uint8_t *>(s->pool);

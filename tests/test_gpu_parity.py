@@ -255,6 +255,60 @@ def _pinned_store(wl, layers_alias=False):
     return buf
 
 
+class _Layers:
+    """Host copies of a workload's per-layer weights for the oracle chains (built on first use)."""
+
+    def __init__(self, wl, layers_alias=False):
+        self.wl, self.alias, self._ex, self._sh, self._rt = wl, layers_alias, {}, {}, {}
+
+    def experts(self, l):
+        src = 0 if self.alias else l
+        if src not in self._ex:
+            self._ex[src] = synth.layer_experts(self.wl, src)
+        return self._ex[src]
+
+    def shared(self, l):
+        if not self.wl.shared:
+            return None
+        if l not in self._sh:
+            self._sh[l] = synth.expert_blob(self.wl, l, None)
+        return self._sh[l]
+
+    def router(self, l):
+        if l not in self._rt:
+            self._rt[l] = synth.router_weights(self.wl, l)
+        return self._rt[l]
+
+
+def oracle_routed_chain(wl, x0, g_logits, g_ids, g_w, layers, bias=None, logit_tol=1e-5, attention=None,
+                        logit_tol0=1e-5):
+    """The fp64 oracle chain x <- x + MoE_l(rmsnorm(x)), l = 0..L-1, routed by the oracle itself.
+
+    At each layer the oracle recomputes the router logits from its own chain state; the GPU's logits (bias
+    taken off) must match them normwise per token (`logit_tol0` at layer 0, `logit_tol` later, where the chain
+    states may have drifted apart by the kernels' own rounding).  The oracle's top-k of the GPU's fp32 logits must
+    give the GPU's ids bit for bit and its weights within 1e-5 (the decision is taken on the same fp32 values),
+    and the chain continues with the oracle's ids and weights.  A stack that routed a layer with the wrong
+    router, an input that was not normalised, or the wrong experts fails here.  attention(l, x) -> x, when
+    given, is each layer's attention block before its MoE block."""
+    xr = np.atleast_2d(x0).astype(np.float64)
+    for l in range(wl.L):
+        if attention is not None:
+            xr = np.atleast_2d(attention(l, xr))
+        hr = oracle.rmsnorm(xr.astype(np.float32)).astype(np.float32)
+        zr = oracle.router_logits(hr, layers.router(l), wl.router_dtype)
+        gz = np.atleast_2d(g_logits[l]).astype(np.float64) - (0.0 if bias is None else np.atleast_2d(bias[l]))
+        err = normwise(gz, zr)
+        assert err <= (logit_tol0 if l == 0 else logit_tol), f"layer {l}: router logits off by {err:.2e}"
+        o_ids, o_w, st = oracle.topk_softmax(np.atleast_2d(g_logits[l]).astype(np.float32), wl.k)
+        assert st == oracle.OK
+        assert (o_ids == np.atleast_2d(g_ids[l])).all(), f"layer {l}: top-k ids differ from the oracle's"
+        gw = np.atleast_2d(g_w[l])
+        assert (np.abs(gw - o_w) <= 1e-5 * np.maximum(1.0, np.abs(o_w))).all(), f"layer {l}: top-k weights"
+        xr = xr + oracle.moe_ffn(hr, o_ids, o_w, layers.experts(l), wl.H, wl.I, wl.dtype, layers.shared(l))
+    return xr
+
+
 def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=None, T=1, charge_max=None,
                         recall=0, recall_overlap=0, device=False, graph=False):
     """Decode `steps` steps through the stack; check events exactly and outputs within tolerance.  With
@@ -273,27 +327,29 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
     sets = synth.routing_sets(wl, steps=steps, T=T)
     o = oracle.LRU(capacity, wl.L, wl.E) if charge_max is None else oracle.Rotary(capacity, wl.L, wl.E, charge_max)
     check_steps = set(range(steps) if check_steps is None else check_steps)
-    host_layers = {}
+    layers = _Layers(wl, layers_alias)
     if graph:  # a replayed graph reads and writes the same buffers every step
         x_buf = torch.empty((T, wl.H), dtype=torch.float32, device=DEV)
         b_buf = torch.empty((wl.L, T, wl.E), dtype=torch.float32, device=DEV)
         ids_buf = torch.empty((wl.L, T, wl.k), dtype=torch.int32, device=DEV)
         w_buf = torch.empty((wl.L, T, wl.k), dtype=torch.float32, device=DEV)
+        z_buf = torch.empty((wl.L, T, wl.E), dtype=torch.float32, device=DEV)
     for t in range(steps):
         x0 = synth.hidden_states(wl, t, T=T)
         bias = np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)])
         if graph:
-            x, ids, w = x_buf, ids_buf, w_buf
+            x, ids, w, z = x_buf, ids_buf, w_buf, z_buf
             x.copy_(dev(x0))
             b_buf.copy_(dev(bias))
-            stack.decode_graph(t, x, b_buf, ids, w)
+            stack.decode_graph(t, x, b_buf, ids, w, z)
         else:
             x = dev(x0)
             ids = torch.empty((wl.L, T, wl.k), dtype=torch.int32, device=DEV)
             w = torch.empty((wl.L, T, wl.k), dtype=torch.float32, device=DEV)
-            stack.decode_step(t, x, dev(bias), ids, w)
+            z = torch.empty((wl.L, T, wl.E), dtype=torch.float32, device=DEV)
+            stack.decode_step(t, x, dev(bias), ids, w, z)
         moe.moe_sync_check()
-        g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
+        g_ids, g_w, g_z = ids.cpu().numpy(), w.cpu().numpy(), z.cpu().numpy()
         calls = dict(rec.step(t, [g_ids[l].reshape(-1) for l in range(wl.L)])[1]) if rec else {}
         for l in range(wl.L):
             assert (np.sort(g_ids[l], axis=1) == sets[t, l]).all()
@@ -301,16 +357,8 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
             if l + 1 in calls:
                 assert o.lookup(t, l + 1, calls[l + 1], prefetch=True) == oracle.OK
         if t in check_steps:
-            # oracle chain in fp64 from the same input, routed by the GPU's ids and weights:
-            # x <- x + MoE(rmsnorm(x)) per layer
-            xr = x0.astype(np.float64)
-            for l in range(wl.L):
-                lsrc = 0 if layers_alias else l
-                if lsrc not in host_layers:
-                    host_layers[lsrc] = synth.layer_experts(wl, lsrc)
-                sh = synth.expert_blob(wl, l, None) if wl.shared else None
-                hr = oracle.rmsnorm(xr.astype(np.float32)).astype(np.float32)
-                xr = xr + oracle.moe_ffn(hr, g_ids[l], g_w[l], host_layers[lsrc], wl.H, wl.I, wl.dtype, sh)
+            # the fp64 oracle chain from the same input, routed by the oracle itself
+            xr = oracle_routed_chain(wl, x0, g_z, g_ids, g_w, layers, bias=bias)
             assert normwise(x.cpu().numpy() - x0, xr - x0) <= TOL[wl.dtype]
     n_ev = len(cache.trace())
     for which in range(4):  # re-launch timing leaves the residency state alone
@@ -746,16 +794,12 @@ def test_prefill_rejects_fp32_weights():
 
 
 # ---------------------------------------------------------- stack prefill ---
-def _oracle_chain(wl, x0, g_ids, g_w, host_layers):
-    """x <- x + MoE_l(rmsnorm(x)) per layer in fp64, routed by the given ids and weights."""
-    xr = x0.astype(np.float64)
-    for l in range(wl.L):
-        if l not in host_layers:
-            host_layers[l] = synth.layer_experts(wl, l)
-        sh = synth.expert_blob(wl, l, None) if wl.shared else None
-        hr = oracle.rmsnorm(xr.astype(np.float32)).astype(np.float32)
-        xr = xr + oracle.moe_ffn(hr, g_ids[l], g_w[l].astype(np.float64), host_layers[l], wl.H, wl.I, wl.dtype, sh)
-    return xr
+# A prompt chunk's expert FFN rounds x and the activations to bf16 for the matrix cores (a normwise error of
+# up to PREFILL_TOL in each layer's increment), so after layer 0 the oracle's chain state and the GPU's have
+# drifted apart by up to that much of each increment so far, and the logits with them: later layers' logits
+# are compared within half that tolerance (layer 0 within 1e-5).  A layer routed with another layer's router
+# is off by O(1).
+PREFILL_LOGIT_TOL = {synth.BF16: 5e-3, synth.INT4G128: 1.5e-2}
 
 
 @pytest.mark.parametrize("dtype,shared", [(synth.BF16, False), (synth.INT4G128, True)])
@@ -776,19 +820,18 @@ def test_stack_prefill_then_decode_budgeted(dtype, shared):
     stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shw, max_tokens=1,
                          max_prefill_tokens=T)
     o = oracle.LRU(capacity, wl.L, wl.E)
-    host_layers = {}
+    layers = _Layers(wl)
     x0 = np.random.default_rng(dtype).standard_normal((T, wl.H)).astype(np.float32)
     x = dev(x0)
     ids = torch.empty((wl.L, T, wl.k), dtype=torch.int32, device=DEV)
     w = torch.empty((wl.L, T, wl.k), dtype=torch.float32, device=DEV)
-    stack.prefill(0, x, ids, w)
+    z = torch.empty((wl.L, T, wl.E), dtype=torch.float32, device=DEV)
+    stack.prefill(0, x, ids, w, z)
     moe.moe_sync_check()
     g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
     for l in range(wl.L):
-        assert ((g_ids[l] >= 0) & (g_ids[l] < wl.E)).all()
-        assert np.allclose(g_w[l].sum(axis=1), 1.0, atol=1e-5)
         assert o.lookup(0, l, g_ids[l].reshape(-1)) == oracle.OK
-    xr = _oracle_chain(wl, x0, g_ids, g_w, host_layers)
+    xr = oracle_routed_chain(wl, x0, z.cpu().numpy(), g_ids, g_w, layers, logit_tol=PREFILL_LOGIT_TOL[wl.dtype])
     assert normwise(x.cpu().numpy() - x0, xr - x0) <= PREFILL_TOL[dtype]
     sets = synth.routing_sets(wl, steps=steps)
     for t in range(steps):
@@ -797,11 +840,12 @@ def test_stack_prefill_then_decode_budgeted(dtype, shared):
         xd = dev(xd0)
         di = torch.empty((wl.L, 1, wl.k), dtype=torch.int32, device=DEV)
         dw = torch.empty((wl.L, 1, wl.k), dtype=torch.float32, device=DEV)
-        stack.decode_step(1 + t, xd, dev(bias), di, dw)
+        dz = torch.empty((wl.L, 1, wl.E), dtype=torch.float32, device=DEV)
+        stack.decode_step(1 + t, xd, dev(bias), di, dw, dz)
         moe.moe_sync_check()
         for l in range(wl.L):
             assert o.lookup(1 + t, l, di.cpu().numpy()[l].reshape(-1)) == oracle.OK
-        xr = _oracle_chain(wl, xd0, di.cpu().numpy(), dw.cpu().numpy(), host_layers)
+        xr = oracle_routed_chain(wl, xd0, dz.cpu().numpy(), di.cpu().numpy(), dw.cpu().numpy(), layers, bias=bias)
         assert normwise(xd.cpu().numpy() - xd0, xr - xd0) <= TOL[dtype]
     ev, oev = cache.trace(), o.events()
     assert len(ev) == len(oev)
@@ -836,7 +880,8 @@ def test_stack_prefill_pipelined_device_prefetch(dtype):
     x = dev(x0)
     ids = torch.empty((wl.L, T, wl.k), dtype=torch.int32, device=DEV)
     w = torch.empty((wl.L, T, wl.k), dtype=torch.float32, device=DEV)
-    stack.prefill(0, x, ids, w)
+    z = torch.empty((wl.L, T, wl.E), dtype=torch.float32, device=DEV)
+    stack.prefill(0, x, ids, w, z)
     moe.moe_sync_check()
     g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
     o = oracle.LRU(capacity, wl.L, wl.E)
@@ -846,8 +891,8 @@ def test_stack_prefill_pipelined_device_prefetch(dtype):
         assert o.lookup(0, l, g_ids[l].reshape(-1)) == oracle.OK
         if l + 1 < wl.L:
             assert o.lookup(0, l + 1, every, prefetch=True) == oracle.OK
-    host_layers = {}
-    xr = _oracle_chain(wl, x0, g_ids, g_w, host_layers)
+    layers = _Layers(wl)
+    xr = oracle_routed_chain(wl, x0, z.cpu().numpy(), g_ids, g_w, layers, logit_tol=PREFILL_LOGIT_TOL[wl.dtype])
     assert normwise(x.cpu().numpy() - x0, xr - x0) <= PREFILL_TOL[dtype]
     sets = synth.routing_sets(wl, steps=3)
     for t in range(3):
@@ -856,11 +901,12 @@ def test_stack_prefill_pipelined_device_prefetch(dtype):
         xd = dev(xd0)
         di = torch.empty((wl.L, 1, wl.k), dtype=torch.int32, device=DEV)
         dw = torch.empty((wl.L, 1, wl.k), dtype=torch.float32, device=DEV)
-        stack.decode_step(1 + t, xd, dev(bias), di, dw)
+        dz = torch.empty((wl.L, 1, wl.E), dtype=torch.float32, device=DEV)
+        stack.decode_step(1 + t, xd, dev(bias), di, dw, dz)
         moe.moe_sync_check()
         for l in range(wl.L):
             assert o.lookup(1 + t, l, di.cpu().numpy()[l].reshape(-1)) == oracle.OK
-        xr = _oracle_chain(wl, xd0, di.cpu().numpy(), dw.cpu().numpy(), host_layers)
+        xr = oracle_routed_chain(wl, xd0, dz.cpu().numpy(), di.cpu().numpy(), dw.cpu().numpy(), layers, bias=bias)
         assert normwise(xd.cpu().numpy() - xd0, xr - xd0) <= TOL[dtype]
     ev, oev = cache.trace(), o.events()
     assert len(ev) == len(oev)
@@ -890,11 +936,12 @@ def test_stack_prefill_config5_two_layers_sampled():
     x = dev(x0)
     ids = torch.empty((wl.L, wl.prefill, wl.k), dtype=torch.int32, device=DEV)
     w = torch.empty((wl.L, wl.prefill, wl.k), dtype=torch.float32, device=DEV)
-    stack.prefill(0, x, ids, w)
+    z = torch.empty((wl.L, wl.prefill, wl.E), dtype=torch.float32, device=DEV)
+    stack.prefill(0, x, ids, w, z)
     moe.moe_sync_check()
     sample = np.random.default_rng(5).choice(wl.prefill, 12, replace=False)
-    g_ids, g_w = ids.cpu().numpy()[:, sample], w.cpu().numpy()[:, sample]
-    xr = _oracle_chain(wl, x0[sample], g_ids, g_w, {})
+    g_ids, g_w, g_z = ids.cpu().numpy()[:, sample], w.cpu().numpy()[:, sample], z.cpu().numpy()[:, sample]
+    xr = oracle_routed_chain(wl, x0[sample], g_z, g_ids, g_w, _Layers(wl), logit_tol=PREFILL_LOGIT_TOL[wl.dtype])
     assert normwise(x.cpu().numpy()[sample] - x0[sample], xr - x0[sample]) <= PREFILL_TOL[wl.dtype]
     s = cache.stats()
     assert s["misses"] == len(np.unique(ids.cpu().numpy()[0])) + len(np.unique(ids.cpu().numpy()[1]))
@@ -1019,17 +1066,18 @@ def test_stack_decode_with_prefetch():
     routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
     stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, None, prefetch=P)
     sets = synth.routing_sets(wl, steps=steps)
-    host_layers = {}
+    layers = _Layers(wl)
     for t in range(steps):
         x0 = synth.hidden_states(wl, t)
         bias = np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)])
         x = dev(x0)
         ids = torch.empty((wl.L, 1, wl.k), dtype=torch.int32, device=DEV)
         w = torch.empty((wl.L, 1, wl.k), dtype=torch.float32, device=DEV)
-        stack.decode_step(t, x, dev(bias), ids, w)
+        z = torch.empty((wl.L, 1, wl.E), dtype=torch.float32, device=DEV)
+        stack.decode_step(t, x, dev(bias), ids, w, z)
         moe.moe_sync_check()
         if t % 7 == 0:
-            xr = _oracle_chain(wl, x0, ids.cpu().numpy(), w.cpu().numpy(), host_layers)
+            xr = oracle_routed_chain(wl, x0, z.cpu().numpy(), ids.cpu().numpy(), w.cpu().numpy(), layers, bias=bias)
             assert normwise(x.cpu().numpy() - x0, xr - x0) <= TOL[wl.dtype]
     ev = cache.trace()
     # replay: consecutive events of one call share (t, layer) and demand-or-prefetch kind
@@ -1064,6 +1112,7 @@ def test_stack_decode_with_prefetch():
 # ------------------------------------------------------------- decoder attention ---
 # bf16 weights and caches, fp32 arithmetic: the attention block's output (x + W_o Attn) is compared as its
 # increment over x, normwise against the fp64 oracle.
+ATTN_LOGIT_TOL = 2e-3  # logits after attention blocks whose new key or value may round to another bf16 value
 ATTN_TOL = 1e-2
 
 
@@ -1154,7 +1203,9 @@ def test_attention_decode_rejects_bad_arguments():
 
 def test_stack_with_attention_blocks_matches_oracle_chain():
     """Each layer x <- x + Attn(rmsnorm(x)), then the MoE block, over a budgeted device cache; the oracle
-    chain (its own caches, the GPU's routing) token by token."""
+    chain (its own caches, routed by the oracle) token by token.  A new key or value may round to a
+    neighbouring bf16 value on one side only, so the chain states (and the logits) may differ by that much of
+    an attention increment."""
     wl = synth.Workload("attn stack", H=256, E=16, k=2, I=128, L=3, dtype=synth.BF16, routing="zipf_overlap",
                         cfg_id=94)
     nh, nkv, d, max_pos, start = 4, 2, 64, 40, 20
@@ -1170,23 +1221,23 @@ def test_stack_with_attention_blocks_matches_oracle_chain():
                k_cache=[_i16(moe.key_cache_layout(b[2])) for b in blocks], v_cache=[_i16(b[3]) for b in blocks])
     stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, None, attention=att)
     sets = synth.routing_sets(wl, steps=6)
-    experts = [synth.layer_experts(wl, l) for l in range(wl.L)]
+    layers = _Layers(wl)
     for t in range(6):
         x0 = synth.hidden_states(wl, t)
         bias = np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)])
         x = dev(x0)
         ids = torch.empty((wl.L, 1, wl.k), dtype=torch.int32, device=DEV)
         w = torch.empty((wl.L, 1, wl.k), dtype=torch.float32, device=DEV)
-        stack.decode_step(t, x, dev(bias), ids, w)
+        z = torch.empty((wl.L, 1, wl.E), dtype=torch.float32, device=DEV)
+        stack.decode_step(t, x, dev(bias), ids, w, z)
         moe.moe_sync_check()
         g_ids, g_w = ids.cpu().numpy(), w.cpu().numpy()
-        xr = x0.astype(np.float64).reshape(-1)
         for l in range(wl.L):
             assert (np.sort(g_ids[l], axis=1) == sets[t, l]).all()
-            xr = oracle.attention_decode(xr.astype(np.float32), blocks[l][0], blocks[l][1], kc_o[l], vc_o[l],
-                                         start + t, nh, nkv)
-            hr = oracle.rmsnorm(xr.astype(np.float32)).astype(np.float32)
-            xr = xr + oracle.moe_ffn(hr, g_ids[l], g_w[l], experts[l], wl.H, wl.I, wl.dtype)[0]
+        attn = lambda l, xr: oracle.attention_decode(xr.reshape(-1).astype(np.float32), blocks[l][0], blocks[l][1],
+                                                     kc_o[l], vc_o[l], start + t, nh, nkv)
+        xr = oracle_routed_chain(wl, x0, z.cpu().numpy(), g_ids, g_w, layers, bias=bias, attention=attn,
+                                 logit_tol0=ATTN_LOGIT_TOL, logit_tol=ATTN_LOGIT_TOL).reshape(-1)
         assert normwise(x.cpu().numpy().reshape(-1) - x0.reshape(-1), xr - x0.reshape(-1)) <= ATTN_TOL, t
     assert stack.kernel_time(4, 2) > 0
     moe.moe_sync_check()
