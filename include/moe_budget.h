@@ -154,6 +154,25 @@ MOE_API int moe_expert_ffn_grouped(const float *x, int T, int H, int I, int E, i
                            size_t expert_bytes, int w_dtype, const void *shared_w, float *y_out,
                            void *workspace, size_t workspace_bytes, int flags, void *stream);
 
+/* moe_expert_ffn_grouped without a workspace argument, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc): the workspace is a fixed array of
+ * MOE_NOALLOC_SCRATCH_BYTES in the library, one per device, held until the
+ * process ends.  This call allocates nothing (no hipMalloc, no hipFree, no
+ * allocating library routine); moe_init(device) must have run on the device
+ * first (MOE_ERR_INVALID_ARG otherwise), since it looks up the array's address.
+ * Needs moe_ffn_workspace_bytes(T, k, I) <= MOE_NOALLOC_SCRATCH_BYTES
+ * (MOE_ERR_INVALID_ARG otherwise, with nothing enqueued); other arguments,
+ * results and errors as for moe_expert_ffn_grouped.  Every call on a device
+ * shares that device's array: calls whose work overlaps on one device (other
+ * streams, other threads) race and must be serialised by the caller.  No part
+ * of the array needs to start at zero (each call writes what it reads first). */
+#define MOE_NOALLOC_SCRATCH_BYTES (4 << 20)
+MOE_API int moe_expert_ffn_grouped_noalloc(const float *x, int T, int H, int I, int E, int k, const int32_t *ids,
+                                           const float *weights, const int32_t *slot_of, const void *pool,
+                                           size_t expert_bytes, int w_dtype, const void *shared_w, float *y_out,
+                                           int flags, void *stream);
+
 /* Device workspace bytes moe_prefill_grouped needs. */
 MOE_API size_t moe_prefill_workspace_bytes(int T, int k, int E, int H, int I);
 

@@ -83,6 +83,7 @@ def lib() -> C.CDLL:
             "moe_route_topk": [P, P, I, I, I, I, I, P, P, P, P, I, P, P],
             "moe_ffn_workspace_bytes": [I, I, I],
             "moe_expert_ffn_grouped": [P, I, I, I, I, I, P, P, P, P, SZ, I, P, P, P, SZ, I, P],
+            "moe_expert_ffn_grouped_noalloc": [P, I, I, I, I, I, P, P, P, P, SZ, I, P, P, I, P],
             "moe_combine": [P, P, P, I, I, I, P, I, P],
             "moe_attention_decode": [P, I, I, I, I, P, P, P, P, I, I, C.c_float, P, SZ, P],
             "moe_prefill_workspace_bytes": [I, I, I, I, I],
@@ -202,6 +203,22 @@ def moe_expert_ffn_grouped(x, ids, weights, pool, expert_bytes: int, w_dtype: in
         expert_bytes, w_dtype, _dev(shared_w, "shared_w"), _dev(y_out, "y_out", torch.float32),
         _dev(workspace, "workspace"), workspace.numel() * workspace.element_size(),
         MOE_ACCUMULATE if accumulate else 0, _stream(stream)), "moe_expert_ffn_grouped")
+    return y_out
+
+
+def moe_expert_ffn_grouped_noalloc(x, ids, weights, pool, expert_bytes: int, w_dtype: int, I: int, E: int, *,
+                                   slot_of=None, shared_w=None, y_out=None, accumulate: bool = False, stream=None):
+    """moe_expert_ffn_grouped on the library's fixed per-device scratch (the call allocates nothing; pass
+    y_out to keep this wrapper from allocating it); returns y_out [T x H]."""
+    import torch
+    T, H = x.shape
+    k = ids.shape[1]
+    y_out = torch.empty((T, H), dtype=torch.float32, device=x.device) if y_out is None else y_out
+    _check(lib().moe_expert_ffn_grouped_noalloc(
+        _dev(x, "x", torch.float32), T, H, I, E, k, _dev(ids, "ids", torch.int32),
+        _dev(weights, "weights", torch.float32), _dev(slot_of, "slot_of", torch.int32), _dev(pool, "pool"),
+        expert_bytes, w_dtype, _dev(shared_w, "shared_w"), _dev(y_out, "y_out", torch.float32),
+        MOE_ACCUMULATE if accumulate else 0, _stream(stream)), "moe_expert_ffn_grouped_noalloc")
     return y_out
 
 

@@ -51,6 +51,13 @@ int *device_error_flags() {
     return g_flags[dev];
 }
 
+int *device_error_flags_ready() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lk(g_dev_mu);
+    return g_flags[dev];
+}
+
 }  // namespace moe
 
 using moe::fail;
@@ -74,6 +81,8 @@ int moe_init(int device) {
     hipError_t e = hipSetDevice(device);
     if (e != hipSuccess) return fail_hip(e, "hipSetDevice");
     if (!moe::device_error_flags()) return fail(MOE_ERR_HIP, "allocating device error flags failed");
+    const int st = moe::noalloc_scratch_setup();
+    if (st != MOE_OK) return st;
     moe::clear_error();
     return MOE_OK;
 }
@@ -161,6 +170,25 @@ int moe_expert_ffn_grouped(const float *x, int T, int H, int I, int E, int k, co
                                                 w_dtype, shared_w, y_out, flags & MOE_ACCUMULATE, ws, eflags,
                                                 static_cast<hipStream_t>(stream)),
                          "ffn launch");
+}
+
+int moe_expert_ffn_grouped_noalloc(const float *x, int T, int H, int I, int E, int k, const int32_t *ids,
+                                   const float *weights, const int32_t *slot_of, const void *pool, size_t expert_bytes,
+                                   int w_dtype, const void *shared_w, float *y_out, int flags, void *stream) {
+    // Nothing here allocates: the error flags and the scratch address come from moe_init's set-up.
+    int *eflags = moe::device_error_flags_ready();
+    void *ws = moe::noalloc_scratch();
+    if (!eflags || !ws)
+        return fail(MOE_ERR_INVALID_ARG, "ffn (no allocation): call moe_init on this device first");
+    if (T < 0 || T > MOE_MAX_DECODE_TOKENS || k < 1 || k > MOE_MAX_TOPK || I < 0)
+        return fail(MOE_ERR_INVALID_ARG, "ffn (no allocation): T=%d or k=%d out of range", T, k);
+    const size_t need = moe::ffn_workspace_bytes(T, k, I);
+    if (need > size_t(MOE_NOALLOC_SCRATCH_BYTES))
+        return fail(MOE_ERR_INVALID_ARG,
+                    "ffn (no allocation): T=%d k=%d I=%d needs %zu bytes of workspace, the fixed scratch holds %d",
+                    T, k, I, need, MOE_NOALLOC_SCRATCH_BYTES);
+    return moe_expert_ffn_grouped(x, T, H, I, E, k, ids, weights, slot_of, pool, expert_bytes, w_dtype, shared_w,
+                                  y_out, ws, size_t(MOE_NOALLOC_SCRATCH_BYTES), flags, stream);
 }
 
 size_t moe_prefill_workspace_bytes(int T, int k, int E, int H, int I) {

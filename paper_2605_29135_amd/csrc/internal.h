@@ -203,5 +203,12 @@ FfnFill cache_ffn_fill(struct ::moe_cache *c, long long down_off);
 
 // Sticky error-flag word of the current device (set up on first use).
 int *device_error_flags();
+// The same, or nullptr when the current device has not been set up yet (allocates nothing).
+int *device_error_flags_ready();
+
+// Allocation-free FFN workspace (kernels.hip): noalloc_scratch_setup() looks up the current device's copy of
+// the fixed array once (an MOE_* code); noalloc_scratch() returns its device address, or nullptr before set-up.
+int noalloc_scratch_setup();
+void *noalloc_scratch();
 
 }  // namespace moe

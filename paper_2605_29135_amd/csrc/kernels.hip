@@ -991,7 +991,38 @@ hipError_t launch(void (*kernel)(Params...), dim3 grid, dim3 block, size_t shmem
 
 }  // namespace
 
+// ---------------------------------------------- allocation-free workspace ---
+// The expert FFN's workspace for callers that cannot allocate (moe_expert_ffn_grouped_noalloc): one fixed
+// array per device, held until the process ends.  In host code `scratch` names a host-side stand-in, not
+// device memory: its device address is looked up once per device (noalloc_scratch_setup) and only that
+// address is ever handed to kernels.
+__device__ __align__(256) unsigned char scratch[MOE_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+constexpr int kScratchDevices = 64;
+void *g_scratch[kScratchDevices] = {};
+}  // namespace
+
 // ===================================================================== host
+
+int noalloc_scratch_setup() {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return fail_hip(e, "scratch: hipGetDevice");
+    if (dev < 0 || dev >= kScratchDevices) return fail(MOE_ERR_INVALID_ARG, "scratch: device %d out of range", dev);
+    if (g_scratch[dev]) return MOE_OK;
+    void *ptr = nullptr;
+    e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !ptr) return fail_hip(e, "scratch: hipGetSymbolAddress");
+    g_scratch[dev] = ptr;
+    return MOE_OK;
+}
+
+void *noalloc_scratch() {
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kScratchDevices) return nullptr;
+    return g_scratch[dev];
+}
 
 size_t expert_blob_bytes(int H, int I, int dtype) {
     if (dtype == INT4) return size_t(3) * H * I / 2 + size_t(3) * H * I / 128 * 2;
