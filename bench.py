@@ -71,6 +71,14 @@ def parse():
                          "(--topics contexts, a token keeps its context with --topic-stay)")
     ap.add_argument("--topics", type=int, default=8)
     ap.add_argument("--topic-stay", type=float, default=0.9)
+    ap.add_argument("--host-quota", type=int, default=0,
+                    help="host tier: per lookup, up to this many non-resident experts computed on host cores from "
+                         "the pinned store instead of filled over the link (the layer's previous host share first); "
+                         "0 = off")
+    ap.add_argument("--host-layers", type=int, default=0,
+                    help="host tier: layers below this one computed wholly on host cores (the paper's n-cpu-moe "
+                         "recipe); 0 = off")
+    ap.add_argument("--host-threads", type=int, default=0, help="host tier threads (0 = every core)")
     ap.add_argument("--replays", type=int, default=5,
                     help="replays of the last step's launches (one per layer) for the per-launch device time")
     return ap.parse_args()
@@ -237,19 +245,38 @@ def ffn_roofline(gu_bytes, dn_bytes, ktimes, hbm, traffic, traffic_src, replays,
             "down": sub(dn_bytes, dn_s, None if traffic is None else traffic["down"])}
 
 
-def link_overlap(d, elapsed, steps):
-    """Stall and overlap of the demand fills over the timed region (device fill clock): per token the link's
-    busy time (copy), the time the fills held the step up (stall), the rest of the step (compute = wall -
-    stall), and overlap = 1 - (wall - max(copy, compute)) / min(copy, compute)."""
+def hit_step_ms(torch, dec, xs, t_last, reps=16):
+    """Device time of one decode token whose every expert is resident: the last timed token's routing
+    replayed (its experts were just used, so every lookup hits), from copies of its input, after the timed
+    region.  This is the step's compute with no fill on its path."""
+    x_save = xs[t_last].clone()
+    dec(t_last + 1, t_last)  # warm, and sets the token's experts most recent
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(reps):
+        xs[t_last].copy_(x_save)
+        dec(t_last + 2 + i, t_last)
+    torch.cuda.synchronize()
+    ms = (time.perf_counter() - t0) * 1e3 / reps
+    xs[t_last].copy_(x_save)
+    return ms
+
+
+def link_overlap(d, elapsed, steps, compute_ms):
+    """Stall and overlap of the demand fills over the timed region, per token: copy = the link's busy time
+    (device fill clock: first to last filling block of each filling launch), compute = a step whose experts
+    are all resident (hit_step_ms), stall = wall - compute (the time the step spent waiting for the link), and
+    overlap = 1 - (wall - max(copy, compute)) / min(copy, compute)."""
     wall = elapsed * 1e3 / steps
     copy = d["fill_ns"] * 1e-6 / steps
-    stall = d["stall_ns"] * 1e-6 / steps
-    compute = wall - stall
-    lo = min(copy, compute)
-    return {"stall_ms_per_token": stall, "fill_ms_per_token": copy, "compute_ms_per_token": compute,
-            "wall_ms_per_token": wall, "overlap": 1.0 - (wall - max(copy, compute)) / lo if lo > 0 else None,
-            "method": "device wall-clock stamps of the filling launches: first to last filling block (copy); how "
-                      "long the fills ran past the launch's computing blocks (stall)"}
+    lo = min(copy, compute_ms)
+    return {"stall_ms_per_token": max(0.0, wall - compute_ms), "fill_ms_per_token": copy,
+            "compute_ms_per_token": compute_ms, "wall_ms_per_token": wall,
+            "overlap": 1.0 - (wall - max(copy, compute_ms)) / lo if lo > 0 else None,
+            "fill_tail_ms_per_token": d["stall_ns"] * 1e-6 / steps,
+            "method": "copy: device wall-clock stamps of the filling launches; compute: 16 steps repeating the last "
+                      "token's routing (every expert resident, no fill); fill_tail: how long each launch's fills ran "
+                      "past its computing blocks (the library's stall_ns), which the fills' own traffic stretches"}
 
 
 def expert_kernel_bytes(wl, n_exp, T):
@@ -472,6 +499,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     t_decode = time.perf_counter() - t0
     moe.moe_sync_check()
     st3 = cache.stats()
+    compute_ms = hit_step_ms(torch, dec, xs, n_steps - 1)
     ktimes = {name: stack.kernel_time(w, args.replays) for w, name in enumerate(["route", "gateup", "down", "ffn"])}
     moe.moe_sync_check()
     bound = residency_bound(moe, cache, E, st3["capacity"], policy=args.policy)
@@ -544,7 +572,7 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
         "pcie": {"h2d_bytes_per_token": h2d_tok, "achieved_GBps": d_dec["h2d_bytes"] / t_decode / 1e9,
                  "ceiling_GBps": ceil, "frac": d_dec["h2d_bytes"] / t_decode / 1e9 / ceil,
                  "tokens_per_s_bound": ceil * 1e9 / h2d_tok if h2d_tok else None,
-                 **(link_overlap(d_dec, t_decode, steps) if args.residency == "device" else {})},
+                 **(link_overlap(d_dec, t_decode, steps, compute_ms) if args.residency == "device" else {})},
         "cpu_baseline": cpu_line,
         "parity": {"sampled_tokens": len(outs), "max_normwise_err": err},
         "setup_s": round(t_setup, 1),
@@ -556,8 +584,8 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
 
 def main():
     args = parse()
-    if (args.prefetch or args.recall) and args.residency == "device":
-        args.residency = "host"  # prefetch and recall decide on the host
+    if (args.prefetch or args.recall or args.host_quota or args.host_layers) and args.residency == "device":
+        args.residency = "host"  # prefetch, recall and the host tier decide on the host
     if args.gpus != 1:
         print(f"bench.py measures one GPU: the library has no multi-GPU path (asked for --gpus {args.gpus})",
               file=sys.stderr)
@@ -615,7 +643,10 @@ def main():
     budget = wl.budget_bytes if budgeted else L * E * eb + reserved
     cache = moe.ExpertCache(L, E, eb, budget, buf.ptr, 0 if alias else E * eb, eb, reserved_bytes=reserved,
                             preload=not budgeted, policy=POLICIES[args.policy], charge_max=args.charge_max,
-                            device=budgeted and args.residency == "device")
+                            device=budgeted and args.residency == "device",
+                            host_layers=args.host_layers if budgeted else 0,
+                            host_quota=args.host_quota if budgeted else 0)
+    hybrid = budgeted and (args.host_layers > 0 or args.host_quota > 0)
     att = None
     if args.attention:
         # synthetic, seeded: N(0, 0.02) projection weights, an N(0, 1) cache prefix; the timed tokens take the
@@ -637,7 +668,7 @@ def main():
         torch.cuda.synchronize()
     stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T,
                          prefetch=args.prefetch if budgeted else 0, recall=args.recall if budgeted else 0,
-                         recall_overlap=args.recall_overlap, attention=att)
+                         recall_overlap=args.recall_overlap, attention=att, host_threads=args.host_threads)
     t_setup = time.perf_counter() - t_setup
 
     stream = torch.cuda.current_stream()
@@ -660,6 +691,7 @@ def main():
     elapsed = time.perf_counter() - t0
     moe.moe_sync_check(stream)
     st1 = cache.stats()
+    compute_ms = hit_step_ms(torch, dec, xs, n_steps - 1) if budgeted and att is None else None
     # the oracle leg's copy of the attention state, taken before the attention timing rewrites the last position
     att_host = None
     if att is not None:
@@ -684,7 +716,8 @@ def main():
     gu_bytes, dn_bytes = expert_kernel_bytes(wl, n_exp, T)
 
     # ---- residency and PCIe
-    d = {f: st1[f] - st0[f] for f in ("lookups", "hits", "misses", "evictions", "h2d_bytes", "stall_ns", "fill_ns")}
+    d = {f: st1[f] - st0[f] for f in ("lookups", "hits", "misses", "evictions", "h2d_bytes", "stall_ns", "fill_ns",
+                                      "host_computed")}
     h2d_per_tok = d["h2d_bytes"] / (args.steps * T)
     pcie = None
     if budgeted:
@@ -696,14 +729,24 @@ def main():
                 "frac": d["h2d_bytes"] / elapsed / 1e9 / ceil,
                 "tokens_per_s_bound": ceil * 1e9 / h2d_per_tok if h2d_per_tok else None,
                 "ceiling_method": "hipMemcpyAsync from hipHostMalloc memory, 64 MiB and expert-size chunks",
-                **(link_overlap(d, elapsed, args.steps) if args.residency == "device" else {})}
+                **(link_overlap(d, elapsed, args.steps, compute_ms) if compute_ms and args.residency == "device"
+                   else {})}
 
     hbm = hbm_ceiling(torch, moe, [gu_bytes, dn_bytes])
     traffic, traffic_src = measured_traffic(4) if args.config == 4 else (None, "no counter summary")
     roof = ffn_roofline(gu_bytes, dn_bytes, ktimes, hbm, traffic, traffic_src, args.replays, L,
                         f"{synth.DTYPE_NAMES[wl.dtype]} decode, T={T}")
 
-    bound = residency_bound(moe, cache, E, st1["capacity"], policy=args.policy) if budgeted else None
+    bound = residency_bound(moe, cache, E, st1["capacity"], policy=args.policy) if budgeted and not hybrid else None
+    host_tier = None
+    if hybrid:
+        hb = d["host_computed"] * eb
+        host_tier = {"host_layers": args.host_layers, "host_quota": args.host_quota,
+                     "threads": args.host_threads or len(os.sched_getaffinity(0)),
+                     "experts_per_token": d["host_computed"] / (args.steps * T),
+                     "bytes_per_token": hb / (args.steps * T), "achieved_GBps": hb / elapsed / 1e9,
+                     "note": "experts computed on host cores from the pinned store (not filled); achieved_GBps is "
+                             "their weight bytes over the timed wall time"}
 
     # ---- oracle on the host cores (bounded sample of the timed tokens), with a parity check
     sample = list(range(args.warmup, n_steps))
@@ -726,6 +769,9 @@ def main():
         err = max(err, float(np.abs(delta - delta_ref).max() / np.abs(delta_ref).max()))
 
     wl_name = wl.name if T == 1 else f"{wl.name} (T={T})"
+    if hybrid:
+        wl_name = (f"{wl_name}; with a host tier (host_layers {args.host_layers}, host_quota {args.host_quota}: those "
+                   f"experts computed on host cores from the pinned store)")
     if att is not None:
         wl_name = (f"{wl_name}; with a decoder self-attention block per layer ({att['n_heads']}/{att['n_kv']} heads "
                    f"of {att['head_dim']}, positions {att['start_pos']}..{att['start_pos'] + n_steps - 1} of a "
@@ -761,6 +807,7 @@ def main():
         "residency": {**d, "miss_rate": d["misses"] / d["lookups"] if d["lookups"] else 0.0,
                       "misses_per_token": d["misses"] / (args.steps * T), "bound": bound},
         "pcie": pcie,
+        **({"host_tier": host_tier} if host_tier else {}),
         "cpu_baseline": cpu_line,
         "parity": {"sampled_tokens": len(outs), "max_normwise_err": err},
         "setup_s": round(t_setup, 1),

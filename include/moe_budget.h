@@ -80,6 +80,10 @@ extern "C" {
 #define MOE_EVENT_HIT 0
 #define MOE_EVENT_MISS 1
 #define MOE_EVENT_PREFETCH 2
+#define MOE_EVENT_HOST 3 /* served by the host tier: computed on host cores, not filled (slot -1) */
+
+/* expert_cache_lookup's slots_out for an id the host tier serves */
+#define MOE_SLOT_HOST (-2)
 
 /* Limits of the decode kernels. */
 #define MOE_MAX_EXPERTS 256   /* router top-k holds at most 4 logits per lane of a 64-wide wave */
@@ -271,6 +275,18 @@ typedef struct {
     int policy;                /* MOE_POLICY_LRU or MOE_POLICY_ROTARY */
     int flags;                 /* MOE_CACHE_PRELOAD | MOE_CACHE_HOST_SIM */
     int charge_max;            /* MOE_POLICY_ROTARY: most charge a slot holds, 0..65535 (0 = cyclic FIFO) */
+    /* Host tier (the paper's run recipe keeps experts of some layers in host memory and computes them on
+     * host cores, sec. 6 and Fig. 3): demand lookups may leave experts in the host store, to be computed there
+     * (moe_host_expert_ffn) instead of filled over the link.  Both 0 = no host tier.  Not with
+     * MOE_CACHE_DEVICE or MOE_CACHE_PRELOAD.  The rule, per demand lookup of layer l (prefetches ignore it):
+     *   l < host_layers: every expert of the step is served by the host (no slot is touched);
+     *   otherwise, of the step's non-resident experts, those the host served at layer l's previous demand
+     *   lookup stay with the host, then further ones in ascending id order while the lookup's host count is
+     *   below host_quota (the sticky ones count too, so a lookup serves at most max(host_quota, sticky) on
+     *   the host, and by induction at most host_quota); the rest miss and are filled as usual.
+     * Host-served experts log MOE_EVENT_HOST (slot -1, victim -1), take no recency stamp and no slot. */
+    int host_layers;           /* 0..L */
+    int host_quota;            /* 0..E */
 } moe_cache_desc;
 
 typedef struct {
@@ -286,10 +302,12 @@ typedef struct {
      * on the step's path; a prefetch's fills are not counted):
      *   fill_ns:  per filling launch, from its first filling block's start to its last one's end, summed;
      *   stall_ns: per filling launch, how long its fills ran past both their start and the end of the
-     *             launch's computing blocks (the resident experts' work), summed: the time the misses held
-     *             up the step. */
+     *             launch's computing blocks (the resident experts' work), summed.  The fills' own traffic
+     *             slows the computing blocks beside them, so this is a lower bound on what the misses add
+     *             to the step. */
     uint64_t stall_ns;
     uint64_t fill_ns;
+    uint64_t host_computed;  /* lookups served by the host tier (counted in lookups too) */
 } moe_cache_stats;
 
 /* One residency decision.  victim_key = layer * E + expert of the evicted
@@ -395,6 +413,32 @@ MOE_API int expert_cache_trace(moe_cache *c, size_t first, moe_cache_event *buf,
 /* with fused residual x += MoE(rmsnorm(x)); attention is the identity       */
 /* ======================================================================= */
 
+/* ======================================================================= */
+/* Host tier: expert FFN on host cores, from the host store (the paper's    */
+/* run recipe computes the experts it keeps in host memory on the CPU,      */
+/* sec. 6, Fig. 3)                                                          */
+/* ======================================================================= */
+
+typedef struct moe_host_tier moe_host_tier;
+
+/* A pool of `threads` host threads (the calling thread is one of them; 0 = every core the process may run
+ * on).  Idle threads spin briefly, then sleep. */
+MOE_API int moe_host_tier_create(int threads, moe_host_tier **out);
+MOE_API int moe_host_tier_destroy(moe_host_tier *t);
+
+/* y_out[h] = sum_j weights[j] * (W_d^j silu(W_g^j x) * (W_u^j x))[h], j = 0..n-1 in that order, for one
+ * token, on the pool's threads (synchronous; host memory only; fp32 accumulation):
+ *   x        host fp32 [H]
+ *   blobs    host array [n] of host expert blobs (layout above), e.g. in the pinned host store
+ *   weights  host fp32 [n]
+ *   y_out    host fp32 [H], overwritten
+ * The gate/up rows are split over the threads, then (after all have finished) the output rows; each output
+ * row is summed by one thread in rank order, so the result does not depend on the thread count.
+ * w_dtype MOE_F32, MOE_BF16 or MOE_INT4G128; H, I multiples of 128; 0 <= n <= MOE_MAX_TOPK
+ * (MOE_ERR_INVALID_ARG otherwise; n = 0 writes zeros). */
+MOE_API int moe_host_expert_ffn(moe_host_tier *t, const float *x, int H, int I, int w_dtype, int n,
+                                const void *const *blobs, const float *weights, float *y_out);
+
 typedef struct moe_stack moe_stack;
 
 /* A decoder self-attention block before each MoE block (moe_attention_decode),
@@ -436,6 +480,13 @@ typedef struct {
                                        x <- x + Attn(rmsnorm(x)) then the MoE block; one-token steps only,
                                        the position advancing by one per step from start_pos; copied at
                                        creation (the arrays, not the device buffers they point to) */
+    int host_threads;               /* a cache with a host tier (moe_cache_desc.host_layers / host_quota): the
+                                       stack's moe_host_tier threads (0 = every core).  Each one-token step
+                                       then publishes its ids, weights and normalised input to host memory,
+                                       the host looks up, the GPU runs the fills and the GPU-resident experts
+                                       while the host tier computes the host-served ones from the store, and a
+                                       small kernel adds their sum to x.  One-token decode only (max_tokens 1,
+                                       no prefill, no attention block) */
 } moe_stack_desc;
 
 MOE_API int moe_stack_create(const moe_stack_desc *desc, moe_stack **out);

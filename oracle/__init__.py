@@ -21,7 +21,7 @@ _LIB = os.path.join(_HERE, "libmoe_oracle.so")
 
 F32, BF16, INT4G128 = 0, 1, 2
 OK, ERR_ARG, ERR_RANGE, ERR_NONFINITE, ERR_BUDGET = 0, -1, -2, -3, -4
-HIT, MISS, PREFETCH = 0, 1, 2
+HIT, MISS, PREFETCH, HOST = 0, 1, 2, 3
 
 EVENT_DTYPE = np.dtype([("t", "<i4"), ("layer", "<i4"), ("expert", "<i4"),
                         ("kind", "<i4"), ("slot", "<i4"), ("victim_key", "<i4")])
@@ -238,6 +238,75 @@ class Rotary(LRU):
         if not self._h:
             raise ValueError("oracle_rotary_new: invalid arguments")
         self.C, self.L, self.E = capacity, L, E
+
+class HostTier:
+    """A slot table with a host tier (the paper's run recipe keeps the experts of some layers in host memory
+    and computes them on host cores, sec. 6 and Fig. 3; this is the rule the library's cache applies, which
+    the paper leaves open).  Each demand lookup of a step's experts R (ascending, distinct) at layer l:
+
+    1. an id outside [0, E) is a range error, a step needing more experts than there are slots a budget
+       error; either changes nothing;
+    2. the host's share: all of R when l < host_layers; otherwise, of the experts of R that hold no slot,
+       first those the host served at layer l's previous demand lookup, then the others in ascending order
+       while the share is smaller than host_quota;
+    3. the rest of R goes through the slot table's own policy (the LRU or rotary object `table`), exactly as
+       a lookup of that subset; the host's share takes no slot and no recency stamp;
+    4. layer l remembers its share for its next demand lookup.
+
+    Prefetches pass straight to the table.  The decision log is the table's events with one event
+    (t, l, e, HOST, -1, -1) per host-served expert, merged in ascending expert order within each lookup."""
+
+    def __init__(self, table: LRU, host_layers: int, host_quota: int):
+        self.table, self.N, self.Q = table, int(host_layers), int(host_quota)
+        self.prev = [set() for _ in range(table.L)]
+        self._log = []
+        self._seen = 0  # table events already merged into the log
+        self.host = 0
+
+    def _take_table_events(self):
+        ev = self.table.events(self._seen)
+        self._seen += ev.size
+        return ev
+
+    def lookup(self, t: int, layer: int, ids, prefetch: bool = False) -> int:
+        R = sorted({int(i) for i in np.atleast_1d(ids)})
+        if prefetch:
+            st = self.table.lookup(t, layer, np.array(R, np.int32), prefetch=True)
+            self._log.extend(self._take_table_events().tolist())
+            return st
+        if any(e < 0 or e >= self.table.E for e in R):
+            return ERR_RANGE
+        if len(R) > self.table.C:
+            return ERR_BUDGET
+        if layer < self.N:
+            host = set(R)
+        else:
+            absent = [e for e in R if self.table.slot_of(layer, e) < 0]
+            host = {e for e in absent if e in self.prev[layer]}
+            for e in absent:
+                if len(host) >= self.Q:
+                    break
+                host.add(e)
+        self.prev[layer] = host
+        rest = [e for e in R if e not in host]
+        st = self.table.lookup(t, layer, np.array(rest, np.int32)) if rest else OK
+        if st != OK:
+            return st
+        table_ev = {int(ev[2]): tuple(ev) for ev in self._take_table_events().tolist()}
+        for e in R:
+            self._log.append((t, layer, e, HOST, -1, -1) if e in host else table_ev[e])
+        self.host += len(host)
+        return OK
+
+    def events(self, first: int = 0) -> np.ndarray:
+        return np.array(self._log[first:], dtype=EVENT_DTYPE)
+
+    def stats(self) -> dict:
+        return dict(self.table.stats(), host=self.host)
+
+    def slot_of(self, layer: int, expert: int) -> int:
+        return self.table.slot_of(layer, expert)
+
 
 class Recall:
     """Reverse rotation of the slot group (paper sec. 4, Fig. 2: when an earlier context recurs the

@@ -25,7 +25,8 @@ MOE_ROUTE_RMSNORM = 1
 MOE_POLICY_LRU = 0
 MOE_POLICY_ROTARY = 1
 MOE_CACHE_PRELOAD, MOE_CACHE_HOST_SIM, MOE_CACHE_DEVICE = 1, 2, 4
-EVENT_HIT, EVENT_MISS, EVENT_PREFETCH = 0, 1, 2
+EVENT_HIT, EVENT_MISS, EVENT_PREFETCH, EVENT_HOST = 0, 1, 2, 3
+MOE_SLOT_HOST = -2
 MAX_DECODE_TOKENS = 16
 
 
@@ -39,14 +40,15 @@ class CacheDesc(C.Structure):
     _fields_ = [("n_layers", C.c_int), ("n_experts", C.c_int), ("expert_bytes", C.c_size_t),
                 ("budget_bytes", C.c_size_t), ("reserved_bytes", C.c_size_t), ("host_base", C.c_void_p),
                 ("host_layer_stride", C.c_size_t), ("host_expert_stride", C.c_size_t),
-                ("policy", C.c_int), ("flags", C.c_int), ("charge_max", C.c_int)]
+                ("policy", C.c_int), ("flags", C.c_int), ("charge_max", C.c_int), ("host_layers", C.c_int),
+                ("host_quota", C.c_int)]
 
 
 class CacheStats(C.Structure):
     _fields_ = [("lookups", C.c_uint64), ("hits", C.c_uint64), ("misses", C.c_uint64),
                 ("prefetches", C.c_uint64), ("evictions", C.c_uint64), ("h2d_bytes", C.c_uint64),
                 ("capacity", C.c_int32), ("occupancy", C.c_int32), ("stall_ns", C.c_uint64),
-                ("fill_ns", C.c_uint64)]
+                ("fill_ns", C.c_uint64), ("host_computed", C.c_uint64)]
 
 
 EVENT_DTYPE = np.dtype([("t", "<i4"), ("layer", "<i4"), ("expert", "<i4"),
@@ -64,7 +66,7 @@ class StackDesc(C.Structure):
                 ("w_dtype", C.c_int), ("router_dtype", C.c_int), ("router_w", C.POINTER(C.c_void_p)),
                 ("shared_w", C.POINTER(C.c_void_p)), ("cache", C.c_void_p), ("max_tokens", C.c_int),
                 ("max_prefill_tokens", C.c_int), ("prefetch", C.c_int), ("recall", C.c_int),
-                ("recall_overlap", C.c_int), ("attention", C.POINTER(AttentionDesc))]
+                ("recall_overlap", C.c_int), ("attention", C.POINTER(AttentionDesc)), ("host_threads", C.c_int)]
 
 
 _lib = None
@@ -99,6 +101,9 @@ def lib() -> C.CDLL:
             "expert_cache_stats": [P, C.POINTER(CacheStats)],
             "expert_cache_trace": [P, SZ, P, SZ, C.POINTER(SZ)],
             "moe_stack_create": [C.POINTER(StackDesc), C.POINTER(P)],
+            "moe_host_tier_create": [I, C.POINTER(P)],
+            "moe_host_tier_destroy": [P],
+            "moe_host_expert_ffn": [P, P, I, I, I, I, P, P, P],
             "moe_stack_destroy": [P],
             "moe_stack_decode_step": [P, I, P, I, P, P, P, P, P],
             "moe_stack_decode_graph": [P, I, P, P, P, P, P, P],
@@ -323,17 +328,44 @@ def moe_combine(y_partial, weights, y_shared=None, y_out=None, accumulate: bool 
     return y_out
 
 
+class HostTier:
+    """Owner of one moe_host_tier (a pool of host threads computing experts from host memory)."""
+
+    def __init__(self, threads: int = 0):
+        h = C.c_void_p()
+        _check(lib().moe_host_tier_create(threads, C.byref(h)), "moe_host_tier_create")
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().moe_host_tier_destroy(self._h)
+            self._h = None
+
+    __del__ = close
+
+    def expert_ffn(self, x, blobs, weights, H: int, I: int, w_dtype: int):
+        """y = sum_j weights[j] FFN_j(x) over host blobs (numpy uint8 arrays or addresses); numpy in and out."""
+        xa = np.ascontiguousarray(x, dtype=np.float32).reshape(-1)
+        keep = [b if isinstance(b, int) else np.ascontiguousarray(b) for b in blobs]
+        ptrs = (C.c_void_p * max(1, len(keep)))(*[b if isinstance(b, int) else b.ctypes.data for b in keep])
+        wa = np.ascontiguousarray(weights, dtype=np.float32).reshape(-1)
+        y = np.empty(H, np.float32)
+        _check(lib().moe_host_expert_ffn(self._h, xa.ctypes.data, H, I, w_dtype, len(keep), ptrs, wa.ctypes.data,
+                                         y.ctypes.data), "moe_host_expert_ffn")
+        return y
+
+
 class ExpertCache:
     """Owner of one expert_cache (slot table in HBM over a pinned host store; LRU or rotary replacement)."""
 
     def __init__(self, n_layers: int, n_experts: int, expert_bytes: int, budget_bytes: int, host_base: int,
                  host_layer_stride: int, host_expert_stride: int, reserved_bytes: int = 0,
                  preload: bool = False, host_sim: bool = False, policy: int = MOE_POLICY_LRU,
-                 charge_max: int = 0, device: bool = False):
+                 charge_max: int = 0, device: bool = False, host_layers: int = 0, host_quota: int = 0):
         d = CacheDesc(n_layers, n_experts, expert_bytes, budget_bytes, reserved_bytes, host_base,
                       host_layer_stride, host_expert_stride, policy,
                       (MOE_CACHE_PRELOAD if preload else 0) | (MOE_CACHE_HOST_SIM if host_sim else 0) |
-                      (MOE_CACHE_DEVICE if device else 0), charge_max)
+                      (MOE_CACHE_DEVICE if device else 0), charge_max, host_layers, host_quota)
         h = C.c_void_p()
         _check(lib().expert_cache_create(C.byref(d), C.byref(h)), "expert_cache_create")
         self._h = h
@@ -415,7 +447,8 @@ class MoeStack:
 
     def __init__(self, cache: ExpertCache, H: int, I: int, E: int, k: int, w_dtype: int, router_dtype: int,
                  router_w: list, shared_w: list | None = None, max_tokens: int = 1, max_prefill_tokens: int = 0,
-                 prefetch: int = 0, recall: int = 0, recall_overlap: int = 0, attention: dict | None = None):
+                 prefetch: int = 0, recall: int = 0, recall_overlap: int = 0, attention: dict | None = None,
+                 host_threads: int = 0):
         self._router = (C.c_void_p * len(router_w))(*[_dev(w, "router_w") for w in router_w])
         self._shared = None
         if shared_w is not None:
@@ -434,7 +467,7 @@ class MoeStack:
                       C.cast(self._router, C.POINTER(C.c_void_p)),
                       C.cast(self._shared, C.POINTER(C.c_void_p)) if self._shared is not None else None,
                       cache.handle, max_tokens, max_prefill_tokens, prefetch, recall, recall_overlap,
-                      C.pointer(att) if att is not None else None)
+                      C.pointer(att) if att is not None else None, host_threads)
         h = C.c_void_p()
         _check(lib().moe_stack_create(C.byref(d), C.byref(h)), "moe_stack_create")
         self._h = h

@@ -31,12 +31,18 @@ hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int 
                                 const float *bias, float *logits, bool norm, float *h_out, hipStream_t s);
 // Host-visible mailbox for one token's ids (coherent pinned memory): the top-k
 // kernel writes ids[0..k), then, after a system-scope fence, seq.
+// With a host tier the wave also publishes the weights, and copies the token's normalised input h (H
+// floats, from h_src in device memory) to h_pub (host memory), before the fence.
 struct IdsMailbox {
     uint32_t seq;
     int32_t ids[MOE_MAX_TOPK];
+    float w[MOE_MAX_TOPK];
 };
 hipError_t launch_topk_softmax(const float *logits, int T, int E, int k, int32_t *ids, float *weights,
-                               int *err_flags, hipStream_t s, IdsMailbox *pub = nullptr, uint32_t seq = 0);
+                               int *err_flags, hipStream_t s, IdsMailbox *pub = nullptr, uint32_t seq = 0,
+                               const float *h_src = nullptr, float *h_pub = nullptr, int H = 0);
+// x[i] += y[i], i < n (y may be host memory: the host tier's output).
+hipError_t launch_add(float *x, const float *y, int n, hipStream_t s);
 
 // Which expert kernels launch_expert_ffn enqueues (grouping goes with gate/up).
 enum : int { kFfnGateUp = 1, kFfnDown = 2, kFfnBoth = 3 };
@@ -60,8 +66,9 @@ struct FfnFill {
 };
 
 // Slots of a single-token step known on the host (after a residency lookup):
-// off[j] = byte offset from the pool of the expert of rank j.  n = k when
-// valid, 0 when the kernels must read ids and the slot table on the device.
+// off[j] = byte offset from the pool of the expert of rank j, or -1 for a rank
+// the host tier computes (the kernels skip it).  n = k when valid, 0 when the
+// kernels must read ids and the slot table on the device.
 struct FfnPlan {
     int n = 0;
     long long off[16];
@@ -187,6 +194,8 @@ bool cache_resident(const struct ::moe_cache *c, int layer, int expert);  // hos
 bool cache_device(const struct ::moe_cache *c);  // lookups run on the device (MOE_CACHE_DEVICE)
 int cache_capacity(const struct ::moe_cache *c);  // slots
 bool cache_rotary(const struct ::moe_cache *c);   // MOE_POLICY_ROTARY
+bool cache_host_tier(const struct ::moe_cache *c);  // demand lookups may leave experts to the host tier
+const uint8_t *cache_host_blob(const struct ::moe_cache *c, int layer, int expert);  // host address in the store
 // MOE_CACHE_DEVICE: enqueue on `s` the prefetch of ids_dev[0..n) at `layer` (non-resident ones inserted, logged
 // as prefetches; resident ones untouched), its fills on the cache's copy stream; the next device lookup waits
 // for those fills.  Returns an MOE_ERR_* code.

@@ -134,7 +134,9 @@ __device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wou
 __global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__restrict__ logits, int T,
                                                               int E, int k, int32_t *__restrict__ ids,
                                                               float *__restrict__ wout, int *err,
-                                                              IdsMailbox *pub, uint32_t seq) {
+                                                              IdsMailbox *pub, uint32_t seq,
+                                                              const float *__restrict__ h_src, float *h_pub,
+                                                              int H) {
     __shared__ TopkScratch sc[kBlock / kWave];
     const int wave = threadIdx.x / kWave;
     const int t = blockIdx.x * (kBlock / kWave) + wave;
@@ -142,7 +144,13 @@ __global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__res
     topk_wave<false>(logits + size_t(t) * E, E, k, ids + size_t(t) * k, wout + size_t(t) * k, err, &sc[wave]);
     if (pub && t == 0) {
         const int lane = threadIdx.x & (kWave - 1);
-        if (lane < k) pub->ids[lane] = ids[lane];  // this lane wrote ids[lane] itself
+        if (lane < k) {  // this lane wrote ids[lane] and wout[lane] itself
+            pub->ids[lane] = ids[lane];
+            pub->w[lane] = wout[lane];
+        }
+        if (h_pub)
+            for (int i = 4 * lane; i < H; i += 4 * kWave)
+                *reinterpret_cast<float4 *>(h_pub + i) = *reinterpret_cast<const float4 *>(h_src + i);
         __threadfence_system();
         if (lane == 0) __hip_atomic_store(&pub->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
     }
@@ -512,7 +520,8 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
             return;
         }
         if (g < k && plan.n) {
-            blob = pool + plan.off[g];  // slots known on the host: no device lookups
+            if (plan.off[g] < 0) return;  // a rank the host tier computes
+            blob = pool + plan.off[g];    // slots known on the host: no device lookups
         } else if (g < k) {
             const int e = ids[g];
             if (e < 0 || e >= E) {
@@ -819,8 +828,8 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
         long long off = 0;
         if (j < k) {
             if (plan.n) {
-                ok = 1;
-                off = plan.off[j];
+                ok = plan.off[j] >= 0;  // (a rank the host tier computes is skipped)
+                off = ok ? plan.off[j] : 0;
             } else {
                 const int e = ids[t * k + j];
                 if (e >= 0 && e < E) {
@@ -1113,10 +1122,26 @@ hipError_t launch_topk_lookup(const float *logits, int E, int k, int32_t *ids, f
 }
 
 hipError_t launch_topk_softmax(const float *logits, int T, int E, int k, int32_t *ids, float *weights,
-                               int *err_flags, hipStream_t s, IdsMailbox *pub, uint32_t seq) {
+                               int *err_flags, hipStream_t s, IdsMailbox *pub, uint32_t seq, const float *h_src,
+                               float *h_pub, int H) {
     if (T == 0) return hipSuccess;
     if (pub && T != 1) return hipErrorInvalidValue;
-    topk_softmax_kernel<<<(T + 3) / 4, kBlock, 0, s>>>(logits, T, E, k, ids, weights, err_flags, pub, seq);
+    if (h_pub && (!pub || !h_src || H % 4)) return hipErrorInvalidValue;
+    topk_softmax_kernel<<<(T + 3) / 4, kBlock, 0, s>>>(logits, T, E, k, ids, weights, err_flags, pub, seq, h_src,
+                                                       h_pub, H);
+    return hipGetLastError();
+}
+
+namespace {
+__global__ __launch_bounds__(kBlock) void add_kernel(float *__restrict__ x, const float *__restrict__ y, int n) {
+    const int i = blockIdx.x * kBlock + threadIdx.x;
+    if (i < n) x[i] += y[i];
+}
+}  // namespace
+
+hipError_t launch_add(float *x, const float *y, int n, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    add_kernel<<<(n + kBlock - 1) / kBlock, kBlock, 0, s>>>(x, y, n);
     return hipGetLastError();
 }
 

@@ -114,6 +114,10 @@ struct moe_cache {
     std::vector<moe_cache_event> log;
     moe_cache_stats st{};
 
+    // host tier (moe_cache_desc.host_layers / host_quota)
+    int host_layers = 0, host_quota = 0;
+    std::vector<uint8_t> host_prev;  // [L*E]: 1 if the host served the key at its layer's last demand lookup
+
     bool dev_mode = false;   // MOE_CACHE_DEVICE: decisions and log on the device
     int clk_khz = 0;         // MOE_CACHE_DEVICE: rate of the device wall clock the fill clock counts in
     moe::DevResidency dr;
@@ -321,10 +325,40 @@ int lookup_impl(moe_cache *c, int step, int layer, const int32_t *ids, int n, bo
     for (int e : R) c->step_mark[layer * c->E + e] = c->epoch;
     std::vector<int32_t> chg_idx, chg_val;
     std::vector<uint8_t> hit_of(R.size(), 0);
+    // The host tier's share of a demand lookup: the whole step in a host layer; otherwise the non-resident
+    // experts the host served at this layer's previous demand lookup, then more in ascending order while
+    // fewer than host_quota are served.
+    std::vector<uint8_t> to_host(R.size(), 0);
+    if (!prefetch && (c->host_layers > 0 || c->host_quota > 0)) {
+        uint8_t *prev = c->host_prev.data() + size_t(layer) * c->E;
+        if (layer < c->host_layers) {
+            std::fill(to_host.begin(), to_host.end(), uint8_t(1));
+        } else {
+            int served = 0;
+            for (size_t r = 0; r < R.size(); ++r)
+                if (c->slot_of_key[layer * c->E + R[r]] < 0 && prev[R[r]]) {
+                    to_host[r] = 1;
+                    ++served;
+                }
+            for (size_t r = 0; r < R.size() && served < c->host_quota; ++r)
+                if (!to_host[r] && c->slot_of_key[layer * c->E + R[r]] < 0) {
+                    to_host[r] = 1;
+                    ++served;
+                }
+        }
+        std::fill(prev, prev + c->E, uint8_t(0));
+        for (size_t r = 0; r < R.size(); ++r) prev[R[r]] = to_host[r];
+    }
     st = MOE_OK;
     for (size_t r = 0; r < R.size(); ++r) {
         const int e = R[r];
         const int32_t key = layer * c->E + e;
+        if (to_host[r]) {
+            ++c->st.host_computed;
+            ++c->st.lookups;
+            c->log.push_back({step, layer, e, MOE_EVENT_HOST, -1, -1});
+            continue;
+        }
         int s = c->slot_of_key[key];
         if (s >= 0) {
             if (prefetch) continue;  // a prefetch leaves resident experts untouched
@@ -366,7 +400,7 @@ int lookup_impl(moe_cache *c, int step, int layer, const int32_t *ids, int n, bo
         c->have_last_compute = true;
         for (int i = 0; i < n; ++i) {
             const size_t r = size_t(std::lower_bound(R.begin(), R.end(), ids[i]) - R.begin());
-            if (slots_out) slots_out[i] = c->slot_of_key[layer * c->E + ids[i]];
+            if (slots_out) slots_out[i] = to_host[r] ? MOE_SLOT_HOST : c->slot_of_key[layer * c->E + ids[i]];
             if (hit_out) hit_out[i] = hit_of[r];
         }
     }
@@ -383,6 +417,8 @@ bool moe::cache_resident(const moe_cache *c, int layer, int expert) {
 bool moe::cache_device(const moe_cache *c) { return c->dev_mode; }
 int moe::cache_capacity(const moe_cache *c) { return c->C; }
 bool moe::cache_rotary(const moe_cache *c) { return c->d.policy == MOE_POLICY_ROTARY; }
+bool moe::cache_host_tier(const moe_cache *c) { return c->host_layers > 0 || c->host_quota > 0; }
+const uint8_t *moe::cache_host_blob(const moe_cache *c, int layer, int expert) { return host_blob(c, layer, expert); }
 
 namespace {
 // A device lookup rewrites the fill list and may evict: an earlier device prefetch's fills come first.
@@ -522,6 +558,12 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
     if (keys > size_t(INT32_MAX)) return moe::fail(MOE_ERR_INVALID_ARG, "too many experts");
 
     const bool dev_mode = d->flags & MOE_CACHE_DEVICE;
+    const bool host_tier = d->host_layers != 0 || d->host_quota != 0;
+    if (d->host_layers < 0 || d->host_layers > d->n_layers || d->host_quota < 0 || d->host_quota > d->n_experts)
+        return moe::fail(MOE_ERR_INVALID_ARG, "host tier: host_layers %d / host_quota %d outside [0, L] / [0, E]",
+                         d->host_layers, d->host_quota);
+    if (host_tier && (d->flags & (MOE_CACHE_DEVICE | MOE_CACHE_PRELOAD)))
+        return moe::fail(MOE_ERR_INVALID_ARG, "host tier: not with MOE_CACHE_DEVICE or MOE_CACHE_PRELOAD");
     if (dev_mode && (d->flags & MOE_CACHE_HOST_SIM))
         return moe::fail(MOE_ERR_INVALID_ARG, "MOE_CACHE_DEVICE cannot be combined with MOE_CACHE_HOST_SIM");
     if (dev_mode && (std::min(cap, preload ? keys : cap) > size_t(moe::kDevMaxSlots) || d->n_experts > MOE_MAX_EXPERTS))
@@ -546,6 +588,9 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
     c->rotary = d->policy == MOE_POLICY_ROTARY;
     c->charge_max = c->rotary ? d->charge_max : 0;
     c->charge.assign(c->C, 0);
+    c->host_layers = d->host_layers;
+    c->host_quota = d->host_quota;
+    if (host_tier) c->host_prev.assign(keys, 0);
 
     auto cleanup = [&](int code) {
         expert_cache_destroy(c);

@@ -11,6 +11,7 @@
 #include <chrono>
 #include <vector>
 
+#include "host_ffn.h"
 #include "internal.h"
 #include "../../include/moe_budget.h"
 
@@ -86,6 +87,14 @@ struct moe_stack {
     std::vector<int32_t> cur_sets;         // [L x k] the current token's expert sets
     int recalled = -1;                     // snapshot recalled for the current token, or -1
     uint64_t tokens = 0;                   // one-token decode steps so far (snapshot stamps)
+    moe_host_tier *host = nullptr;  // the host tier, when the cache has one
+    float *h_pub = nullptr;         // coherent pinned [H]: the layer's normalised input, published by the top-k
+    float *h_pub_dev = nullptr;     // its device address
+    float *y_pub = nullptr;         // coherent pinned [H]: the host tier's output for the layer
+    float *y_pub_dev = nullptr;     // its device address
+    std::vector<const void *> host_blobs;  // [k] blobs the host tier computes this layer
+    std::vector<float> host_w;             // [k] their combine weights
+    uint64_t host_calls = 0;               // layers whose experts the host tier computed (some or all)
     float *scratch_x = nullptr;  // device [Tmax x H] scratch input/output of kernel re-launches
     float *scratch_y = nullptr;  // device [Tmax x H]
     std::vector<LastLayer> last;  // per layer, arguments of the last decode step
@@ -111,6 +120,10 @@ int wait_published_ids(moe_stack *s, uint32_t seq, hipStream_t strm) {
     std::atomic_thread_fence(std::memory_order_acquire);
     const volatile int32_t *src = s->mbox->ids;
     for (int j = 0; j < s->d.k; ++j) s->ids_host[j] = src[j];
+    if (s->host) {
+        const volatile float *w = s->mbox->w;
+        for (int j = 0; j < s->d.k; ++j) s->host_w[size_t(j)] = w[j];
+    }
     return MOE_OK;
 }
 
@@ -200,6 +213,9 @@ int moe_stack_destroy(moe_stack *s) {
     if (s->dev_step) (void)hipFree(s->dev_step);
     if (s->all_experts) (void)hipFree(s->all_experts);
     if (s->attn_ws) (void)hipFree(s->attn_ws);
+    if (s->host) moe_host_tier_destroy(s->host);
+    if (s->h_pub) (void)hipHostFree(s->h_pub);
+    if (s->y_pub) (void)hipHostFree(s->y_pub);
     if (s->graph_exec) (void)hipGraphExecDestroy(s->graph_exec);
     delete s;
     return MOE_OK;
@@ -230,6 +246,11 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
         if (d->max_prefill_tokens > 0 || d->max_tokens != 1)
             return moe::fail(MOE_ERR_INVALID_ARG, "stack: an attention block decodes one token per step (no prefill)");
     }
+    if (d->cache && moe::cache_host_tier(d->cache) &&
+        (d->max_tokens != 1 || d->max_prefill_tokens > 0 || d->attention || d->prefetch > 0 || d->recall > 0))
+        return moe::fail(MOE_ERR_INVALID_ARG, "stack: a host-tier cache runs one-token decode steps only (max_tokens 1, "
+                                              "no prefill, attention, prefetch or recall)");
+    if (d->host_threads < 0) return moe::fail(MOE_ERR_INVALID_ARG, "stack: host_threads must be >= 0");
     if (d->max_prefill_tokens > 0 && !moe::prefill_dtype_supported(d->w_dtype))
         return moe::fail(MOE_ERR_INVALID_ARG, "stack: prefill needs MOE_BF16 or MOE_INT4G128 experts");
     if (!moe::ffn_shape_supported(d->H, d->I, d->w_dtype) || !moe::router_shape_supported(d->H, d->router_dtype))
@@ -314,6 +335,21 @@ int moe_stack_create(const moe_stack_desc *d, moe_stack **out) {
     memset(s->mbox, 0, sizeof(moe::IdsMailbox));
     if ((e = hipHostGetDevicePointer(reinterpret_cast<void **>(&s->mbox_dev), s->mbox, 0)) != hipSuccess)
         return bail(e, "stack ids mailbox");
+    if (moe::cache_host_tier(d->cache)) {
+        int st2 = moe_host_tier_create(d->host_threads, &s->host);
+        if (st2 != MOE_OK) {
+            moe_stack_destroy(s);
+            return st2;
+        }
+        const unsigned fl = hipHostMallocCoherent | hipHostMallocMapped;
+        if ((e = hipHostMalloc(reinterpret_cast<void **>(&s->h_pub), sizeof(float) * d->H, fl)) != hipSuccess ||
+            (e = hipHostMalloc(reinterpret_cast<void **>(&s->y_pub), sizeof(float) * d->H, fl)) != hipSuccess ||
+            (e = hipHostGetDevicePointer(reinterpret_cast<void **>(&s->h_pub_dev), s->h_pub, 0)) != hipSuccess ||
+            (e = hipHostGetDevicePointer(reinterpret_cast<void **>(&s->y_pub_dev), s->y_pub, 0)) != hipSuccess)
+            return bail(e, "stack host tier buffers");
+        s->host_blobs.assign(size_t(d->k), nullptr);
+        s->host_w.assign(size_t(d->k), 0.f);
+    }
     const size_t Td = size_t(d->max_tokens);
     if ((e = hipMalloc(&s->scratch_x, sizeof(float) * Td * d->H)) != hipSuccess) return bail(e, "stack buffers");
     if ((e = hipMalloc(&s->scratch_y, sizeof(float) * Td * d->H)) != hipSuccess) return bail(e, "stack buffers");
@@ -358,8 +394,10 @@ int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_b
         hipError_t e = moe::launch_router_logits(x, s->router_w[l], d.router_dtype, T, d.H, d.E, bias, lg, true,
                                                  s->h, strm);
         const bool fused = dev_lookup && T == 1;  // one token: top-k and the lookup in one kernel
+        // with a host tier the top-k also publishes the weights and h_l for the host's share of the layer
         if (e == hipSuccess && !fused)
-            e = moe::launch_topk_softmax(lg, T, d.E, d.k, ids, w, eflags, strm, mailbox ? s->mbox_dev : nullptr, seq);
+            e = moe::launch_topk_softmax(lg, T, d.E, d.k, ids, w, eflags, strm, mailbox ? s->mbox_dev : nullptr, seq,
+                                         s->h, mailbox ? s->h_pub_dev : nullptr, d.H);
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: routing");
         if (fused) {
             int st = moe::cache_topk_lookup(d.cache, step, l, lg, d.k, ids, w,
@@ -394,9 +432,19 @@ int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_b
         moe::FfnPlan plan;
         const int32_t *slot_of = s->slot_table + size_t(l) * d.E;
         const uint8_t *pool = static_cast<const uint8_t *>(s->pool);
+        int n_host = 0;
         if (s->budgeted && T == 1 && !dev_lookup) {
             plan.n = d.k;
-            for (int j = 0; j < d.k; ++j) plan.off[j] = (long long)s->slots_host[j] * (long long)s->expert_bytes;
+            for (int j = 0; j < d.k; ++j) {
+                if (s->slots_host[j] == MOE_SLOT_HOST) {  // computed by the host tier, skipped by the kernels
+                    plan.off[j] = -1;
+                    s->host_blobs[size_t(n_host)] = moe::cache_host_blob(d.cache, l, s->ids_host[j]);
+                    s->host_w[size_t(n_host)] = s->host_w[size_t(j)];  // (n_host <= j: compacting in place)
+                    ++n_host;
+                } else {
+                    plan.off[j] = (long long)s->slots_host[j] * (long long)s->expert_bytes;
+                }
+            }
         } else if (!s->budgeted) {
             pool += size_t(l) * d.E * s->expert_bytes;
             slot_of = nullptr;
@@ -405,10 +453,28 @@ int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_b
         // from the host store while the resident experts' gate/up runs), so no fill launch precedes it.
         moe::FfnPlan fplan;
         if (fused) fplan.fill = moe::cache_ffn_fill(d.cache, (long long)moe::down_offset(d.H, d.I, d.w_dtype));
-        e = moe::launch_expert_ffn(s->h, T, d.H, d.I, d.E, d.k, ids, w, slot_of, pool, s->expert_bytes, d.w_dtype,
-                                   s->shared_w.empty() ? nullptr : s->shared_w[l], x, true, ws, eflags, strm,
-                                   fused ? &fplan : plan.n ? &plan : nullptr);
+        // the host tier starts on its share at once; the GPU's share (every rank when no host tier, none when
+        // the host computes them all and there is no shared expert) is enqueued meanwhile, so that it and the
+        // fills run while the host computes
+        if (n_host > 0) {
+            int st = moe::host_ffn_begin(s->host, s->h_pub, d.H, d.I, d.w_dtype, n_host, s->host_blobs.data(),
+                                         s->host_w.data(), s->y_pub);
+            if (st != MOE_OK) return st;
+        }
+        if (n_host < d.k || !s->shared_w.empty())
+            e = moe::launch_expert_ffn(s->h, T, d.H, d.I, d.E, d.k, ids, w, slot_of, pool, s->expert_bytes, d.w_dtype,
+                                       s->shared_w.empty() ? nullptr : s->shared_w[l], x, true, ws, eflags, strm,
+                                       fused ? &fplan : plan.n ? &plan : nullptr);
         s->last[l] = LastLayer{true, T, l, ids, w, slot_of, pool, plan};
+        if (n_host > 0) {
+            const int st = moe::host_ffn_finish(s->host);  // (also when the launch failed: the tier must end)
+            if (e != hipSuccess) return moe::fail_hip(e, "stack step: expert FFN");
+            if (st != MOE_OK) return st;
+            // x += the host's share; the next layer's top-k, which rewrites h_pub, runs after this on the stream
+            e = moe::launch_add(x, s->y_pub_dev, d.H, strm);
+            if (e != hipSuccess) return moe::fail_hip(e, "stack step: adding the host tier's output");
+            ++s->host_calls;
+        }
         if (e != hipSuccess) return moe::fail_hip(e, "stack step: expert FFN");
         if (s->budgeted && !dev_lookup) {
             int st = expert_cache_release(d.cache, strm);

@@ -310,22 +310,27 @@ def oracle_routed_chain(wl, x0, g_logits, g_ids, g_w, layers, bias=None, logit_t
 
 
 def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=None, T=1, charge_max=None,
-                        recall=0, recall_overlap=0, device=False, graph=False):
+                        recall=0, recall_overlap=0, device=False, graph=False, host_layers=0, host_quota=0,
+                        host_threads=0):
     """Decode `steps` steps through the stack; check events exactly and outputs within tolerance.  With
-    charge_max the slots use the rotary policy (else LRU); with recall the stack recalls prior slot sets."""
+    charge_max the slots use the rotary policy (else LRU); with recall the stack recalls prior slot sets; with
+    host_layers / host_quota a host tier computes its share of the experts on host cores."""
     buf = _pinned_store(wl, layers_alias)
     eb = wl.expert_bytes
     policy = moe.MOE_POLICY_LRU if charge_max is None else moe.MOE_POLICY_ROTARY
     cache = moe.ExpertCache(wl.L, wl.E, eb, capacity * eb + (wl.L * eb if wl.shared else 0), buf.ptr,
                             0 if layers_alias else wl.E * eb, eb, reserved_bytes=wl.L * eb if wl.shared else 0,
-                            policy=policy, charge_max=charge_max or 0, device=device)
+                            policy=policy, charge_max=charge_max or 0, device=device, host_layers=host_layers,
+                            host_quota=host_quota)
     routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
     shared = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)] if wl.shared else None
     stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T,
-                         recall=recall, recall_overlap=recall_overlap)
+                         recall=recall, recall_overlap=recall_overlap, host_threads=host_threads)
     rec = oracle.Recall(recall, wl.k, recall_overlap) if recall else None
     sets = synth.routing_sets(wl, steps=steps, T=T)
     o = oracle.LRU(capacity, wl.L, wl.E) if charge_max is None else oracle.Rotary(capacity, wl.L, wl.E, charge_max)
+    if host_layers or host_quota:
+        o = oracle.HostTier(o, host_layers, host_quota)
     check_steps = set(range(steps) if check_steps is None else check_steps)
     layers = _Layers(wl, layers_alias)
     if graph:  # a replayed graph reads and writes the same buffers every step
@@ -475,6 +480,35 @@ def test_budgeted_stack_int4_shared_device_one_token(graph):
                         routing="zipf_overlap", cfg_id=92)
     s = run_stack_and_check(wl, steps=16, capacity=30, device=True, graph=graph)
     assert s["evictions"] > 0
+
+
+@pytest.mark.parametrize("dtype,shared,N,Q,threads", [(synth.BF16, False, 1, 1, 0), (synth.BF16, False, 0, 2, 3),
+                                                      (synth.INT4G128, True, 1, 2, 0)])
+def test_budgeted_stack_host_tier(dtype, shared, N, Q, threads):
+    """A host tier beside the slot table: layers below N, and up to Q non-resident experts per lookup elsewhere,
+    are computed on host cores from the pinned store while the GPU runs the fills and the resident experts.
+    Decisions event for event against the oracle's model of the rule, outputs against the oracle chain (routed
+    by the oracle), and every resident slot byte for byte against the store."""
+    H = 2048 if dtype == synth.INT4G128 else 512
+    wl = synth.Workload("host tier stack", H=H, E=32, k=4, I=256, L=4, dtype=dtype, shared=shared,
+                        routing="zipf_overlap", cfg_id=160 + dtype)
+    s = run_stack_and_check(wl, steps=24, capacity=16, host_layers=N, host_quota=Q, host_threads=threads)
+    assert s["host_computed"] > 0 and s["misses"] > 0 and s["evictions"] > 0
+
+
+def test_host_tier_stack_rejects_what_it_cannot_run():
+    wl = synth.Workload("host tier stack", H=512, E=16, k=2, I=128, L=2, dtype=synth.BF16, cfg_id=170)
+    buf = _pinned_store(wl)
+    eb = wl.expert_bytes
+    routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
+    cache = moe.ExpertCache(wl.L, wl.E, eb, 8 * eb, buf.ptr, wl.E * eb, eb, host_quota=1)
+    for kw in (dict(max_tokens=2), dict(max_prefill_tokens=16), dict(prefetch=1)):
+        with pytest.raises(moe.MoeError):
+            moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, None, **kw)
+    cache.close()
+    with pytest.raises(moe.MoeError):  # a host tier decides on the host
+        moe.ExpertCache(wl.L, wl.E, eb, 8 * eb, buf.ptr, wl.E * eb, eb, host_quota=1, device=True)
+    buf.close()
 
 
 @pytest.mark.parametrize("device", [False, True])
