@@ -18,7 +18,10 @@ namespace {
 using namespace dev;
 
 
-constexpr int kDownRows = 2; // output rows per wave in the down projection
+constexpr int kDownRows = 2; // output rows per wave in the down projection (fallback kernel)
+// Output rows per wave of down_combine_lds_kernel: one (two, sharing the LDS reads of the activations,
+// measured slower on config 4: 6.62 against 6.39 us).
+constexpr int kDownWaveRows = 1;
 constexpr int kDownSlots = 4; // 16-byte chunks per lane per pass of the down projection
 constexpr float kRmsEps = 1e-6f;
 constexpr int kRouterMfmaMinTokens = 16;  // from this many tokens on, bf16 routers run on the matrix cores
@@ -205,7 +208,7 @@ __global__ __launch_bounds__(NT) void topk_lookup_kernel(const float *__restrict
 // stores h_t for the expert FFN.  The same GEMV serves the attention block's
 // projections; `bias` may be `logits` itself (an in-place residual add: each
 // element is read and then written by the same lane).
-template <int DT, int NCH, bool NORM>
+template <int DT, int NCH, bool NORM, bool FULL>
 __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__restrict__ x,
                                                                const uint8_t *__restrict__ w, int H,
                                                                int E, const float *bias, float *logits,
@@ -222,7 +225,7 @@ __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__re
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {  // x first: waiting for it never waits for the weight loads
         const int col0 = (c * kWave + lane) * EPC;
-        if (col0 < H) {
+        if ((FULL || col0 < H)) {
             load_x<DT>(xt, col0, xv[c]);
         } else {
 #pragma unroll
@@ -232,7 +235,7 @@ __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__re
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         const int col0 = (c * kWave + lane) * EPC;
-        wv[c] = (col0 < H && e < E) ? load16(row + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
+        wv[c] = ((FULL || col0 < H) && e < E) ? load16(row + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
     }
     if constexpr (NORM) {
         float ss = 0.f;
@@ -249,7 +252,7 @@ __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__re
 #pragma unroll
             for (int c = 0; c < NCH; ++c) {
                 const int col0 = (c * kWave + lane) * EPC;
-                if (col0 < H) {
+                if ((FULL || col0 < H)) {
                     float4 *o = reinterpret_cast<float4 *>(h_out + size_t(t) * H + col0);
 #pragma unroll
                     for (int q = 0; q < EPC / 4; ++q)
@@ -490,7 +493,7 @@ __device__ __forceinline__ void copy_down_parts(const FfnFill &fl, size_t expert
 // expert's rows come from the host store, plan.fill.blocks blocks stream them
 // (each wave a row pair per pass) and store them into the slot, and one more
 // row of blocks copies the blobs' down parts.
-template <int DT, int NCH, bool ONE_TOKEN>
+template <int DT, int NCH, bool ONE_TOKEN, bool FULL>
 __global__ __launch_bounds__(kBlock) void gateup_kernel(
     const float *__restrict__ x, int T, int H, int I, int E, int k, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ slot_of, const uint8_t *__restrict__ pool, size_t expert_bytes,
@@ -574,7 +577,7 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const int col0 = (c * kWave + lane) * EPC;
-            if (col0 < H) {
+            if ((FULL || col0 < H)) {
                 load_x<DT>(xt, col0, xv[c]);
             } else {
 #pragma unroll
@@ -592,7 +595,7 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         const int col0 = (c * kWave + lane) * EPC;
-        const bool in = col0 < H;
+        const bool in = (FULL || col0 < H);
         wg[c] = in ? load16_stream(gate + size_t(c) * 16 * kWave) : make_uint4(0, 0, 0, 0);
         wu[c] = in ? load16_stream(up + size_t(c) * 16 * kWave) : make_uint4(0, 0, 0, 0);
         if constexpr (DT == INT4) {
@@ -607,7 +610,7 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
             const int col0 = (c * kWave + lane) * EPC;
-            if (col0 < H) {
+            if ((FULL || col0 < H)) {
                 store16_stream(dg + size_t(c) * 16 * kWave, wg[c]);
                 store16_stream(dg + rb + size_t(c) * 16 * kWave, wu[c]);
                 if constexpr (DT == INT4) {
@@ -641,7 +644,7 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
             const int col0 = (c * kWave + lane) * EPC;
 #pragma unroll
             for (int q = 0; q < Q; ++q) {
-                const float4 v = col0 < H ? xsh[(c * Q + q) * kWave + lane] : make_float4(0.f, 0.f, 0.f, 0.f);
+                const float4 v = (FULL || col0 < H) ? xsh[(c * Q + q) * kWave + lane] : make_float4(0.f, 0.f, 0.f, 0.f);
                 xv[c][4 * q] = v.x;
                 xv[c][4 * q + 1] = v.y;
                 xv[c][4 * q + 2] = v.z;
@@ -657,7 +660,7 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
 #pragma unroll
             for (int c = 0; c < NCH; ++c) {
                 const int col0 = (c * kWave + lane) * EPC;
-                if (col0 < H) load_x<DT>(xt, col0, xv[c]);
+                if ((FULL || col0 < H)) load_x<DT>(xt, col0, xv[c]);
             }
         }
         float ga = 0.f, ua = 0.f;
@@ -794,7 +797,7 @@ __global__ __launch_bounds__(kBlock) void down_combine_kernel(
 // back without branches (an invalid chunk loads from the pool base and is
 // masked), and only then are the staged values written to LDS.
 // One output row per wave, four per block, one block per (row tile, token).
-template <int DT, int NS>
+template <int DT, int NS, int R>
 __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
     int T, int H, int I, int E, int k, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ slot_of, const uint8_t *__restrict__ pool, size_t expert_bytes,
@@ -848,19 +851,17 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
         ent_ok[j] = ok;
     }
     __syncthreads();
-    // 3. weight loads of this wave's output row.  Workgroup b runs on XCD b mod 8: consecutive row tiles
+    // 3. weight loads of this wave's R output rows.  Workgroup b runs on XCD b mod 8: consecutive row tiles
     // go to the same XCD, so the blocks that share a cache line of int4 row scales share one L2.
     const int lane = threadIdx.x & (kWave - 1);
     const int nb = gridDim.x;
     const int tile = (nb & 7) ? int(blockIdx.x) : int(blockIdx.x & 7) * (nb >> 3) + int(blockIdx.x >> 3);
-    const int h = min(tile * (kBlock / kWave) + (threadIdx.x / kWave), H - 1);
+    const int h0 = (tile * (kBlock / kWave) + (threadIdx.x / kWave)) * R;  // the wave's first row
     const size_t rb = row_bytes_of(DT, I);
     const unsigned cpr = unsigned(rb / 16);  // chunks per expert row
     const unsigned total = unsigned(NE) * cpr;
-    const size_t row_off = d_off + size_t(h) * rb;
-    const size_t sc_off = d_off + size_t(H) * rb + size_t(h) * (I / 128) * 2;  // int4: this row's scales
-    uint4 wv[NS];
-    float sv[NS];
+    uint4 wv[R][NS];
+    float sv[R][NS];
     bool ok[NS];
     unsigned j = unsigned(lane) / cpr, c = unsigned(lane) - j * cpr;  // chunk lane + 64 s = entry j, column chunk c
 #pragma unroll
@@ -869,10 +870,17 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
         const unsigned jj = in ? j : 0u;
         ok[s] = in && ent_ok[jj];
         const uint8_t *blob = pool + (ok[s] ? ent_off[jj] : 0);
-        wv[s] = load16_stream(ok[s] ? blob + row_off + size_t(c) * 16 : pool);
-        if constexpr (DT == INT4)
-            sv[s] = bf16_bits_to_float(*reinterpret_cast<const uint16_t *>(
-                ok[s] ? blob + sc_off + size_t(c * EPC / 128) * 2 : pool));
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+            const int h = min(h0 + r, H - 1);
+            const size_t row_off = d_off + size_t(h) * rb;
+            wv[r][s] = load16_stream(ok[s] ? blob + row_off + size_t(c) * 16 : pool);
+            if constexpr (DT == INT4) {
+                const size_t sc_off = d_off + size_t(H) * rb + size_t(h) * (I / 128) * 2;  // this row's scales
+                sv[r][s] = bf16_bits_to_float(*reinterpret_cast<const uint16_t *>(
+                    ok[s] ? blob + sc_off + size_t(c * EPC / 128) * 2 : pool));
+            }
+        }
         c += kWave;
         while (c >= cpr) {
             c -= cpr;
@@ -886,7 +894,9 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
         if (i < n4) aw4[i] = stage[m];
     }
     __syncthreads();
-    float acc = 0.f;
+    float acc[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) acc[r] = 0.f;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
         if (ok[s]) {
@@ -900,16 +910,22 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
                 av[4 * q + 2] = a4.z;
                 av[4 * q + 3] = a4.w;
             }
-            float d = chunk_dot<DT>(wv[s], av);
-            if constexpr (DT == INT4) d *= sv[s];
-            acc += d;
+#pragma unroll
+            for (int r = 0; r < R; ++r) {
+                float d = chunk_dot<DT>(wv[r][s], av);
+                if constexpr (DT == INT4) d *= sv[r][s];
+                acc[r] += d;
+            }
         }
     }
-    const float v = wave_sum(acc);
-    const int hrow = tile * (kBlock / kWave) + (threadIdx.x / kWave);
-    if (lane == 0 && hrow < H) {
-        float *o = y + size_t(t) * H + hrow;
-        *o = accumulate ? *o + v : v;
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+        const float v = wave_sum(acc[r]);
+        const int hrow = h0 + r;
+        if (lane == 0 && hrow < H) {
+            float *o = y + size_t(t) * H + hrow;
+            *o = accumulate ? *o + v : v;
+        }
     }
 }
 
@@ -1095,13 +1111,17 @@ hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int 
     const auto *wp = static_cast<const uint8_t *>(w);
     const int nch = chunks_per_row(H, w_dtype);
     float *hp = norm ? h_out : nullptr;
+    // FULL: every lane's chunk slots lie inside the row (H = nch * 64 * elements per chunk), no bound checks
+    const bool full = H == nch * kWave * elems_per_chunk(w_dtype);
+#define ROUTER_LAUNCH(DT, N, F)                                                                     \
+    (norm ? launch(router_logits_kernel<DT, N, true, F>, grid, kBlock, 0, s, x, wp, H, E, bias, logits, hp) \
+          : launch(router_logits_kernel<DT, N, false, F>, grid, kBlock, 0, s, x, wp, H, E, bias, logits, hp))
 #define ROUTER_CASE(DT, N)                                                                          \
-    if (w_dtype == DT && nch == N)                                                                  \
-        return norm ? launch(router_logits_kernel<DT, N, true>, grid, kBlock, 0, s, x, wp, H, E, bias, logits, hp) \
-                    : launch(router_logits_kernel<DT, N, false>, grid, kBlock, 0, s, x, wp, H, E, bias, logits, hp);
+    if (w_dtype == DT && nch == N) return full ? ROUTER_LAUNCH(DT, N, true) : ROUTER_LAUNCH(DT, N, false);
     ROUTER_CASE(F32, 1) ROUTER_CASE(F32, 2) ROUTER_CASE(F32, 4) ROUTER_CASE(F32, 8)
     ROUTER_CASE(BF16, 1) ROUTER_CASE(BF16, 2) ROUTER_CASE(BF16, 4) ROUTER_CASE(BF16, 8)
 #undef ROUTER_CASE
+#undef ROUTER_LAUNCH
     return hipErrorInvalidValue;
 }
 
@@ -1183,13 +1203,29 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
     const int nch = chunks_per_row(H, dtype);
     // One-token int4 x staging covers every lane's chunk slots, [nch][EPC/4][64] float4, not just H floats.
     const size_t x_lds = dtype == INT4 ? sizeof(float) * size_t(nch) * kWave * elems_per_chunk(dtype) : 0;
+    // The down kernel: the LDS form when a token's k (+1) activation rows fit in LDS and NS chunks per lane
+    // cover them, else the plain one.
+    const size_t doff = down_offset(H, I, dtype);
+    const int acc = accumulate ? 1 : 0;
+    const int NE = k + has_shared;
+    const int epc = elems_per_chunk(dtype);
+    const int need = (NE * (I / epc) + kWave - 1) / kWave;
+    const size_t lds = sizeof(float) * size_t(NE) * I;
+    int ns = 0;
+    for (int n : {1, 2, 3, 4, 6, 8, 9, 12, 16})
+        if (!ns && need <= n) ns = n;
+    const bool lds_down = ns && lds <= 64 * 1024;
     bool launched = !(parts & kFfnGateUp);
+    // FULL: every lane's chunk slots lie inside the row (H = nch * 64 * elements per chunk), no bound checks
+    const bool full = H == nch * kWave * elems_per_chunk(dtype);
+#define GU_LAUNCH(DT, N, F)                                                                         \
+    (one ? launch(gateup_kernel<DT, N, true, F>, ggrid, kBlock, x_lds, s, x, T, H, I, E, k, ids,    \
+                  slot_of, pl, expert_bytes, sw, weights, ws.groups, ws.act, err_flags, pl1)        \
+         : launch(gateup_kernel<DT, N, false, F>, ggrid, kBlock, 0, s, x, T, H, I, E, k, ids,       \
+                  slot_of, pl, expert_bytes, sw, weights, ws.groups, ws.act, err_flags, FfnPlan{}))
 #define GU_CASE(DT, N)                                                                              \
     if (!launched && dtype == DT && nch == N) {                                                     \
-        e = one ? launch(gateup_kernel<DT, N, true>, ggrid, kBlock, x_lds, s, x, T, H, I, E, k, ids, \
-                         slot_of, pl, expert_bytes, sw, weights, ws.groups, ws.act, err_flags, pl1) \
-                : launch(gateup_kernel<DT, N, false>, ggrid, kBlock, 0, s, x, T, H, I, E, k, ids, \
-                         slot_of, pl, expert_bytes, sw, weights, ws.groups, ws.act, err_flags, FfnPlan{}); \
+        e = full ? GU_LAUNCH(DT, N, true) : GU_LAUNCH(DT, N, false);                                \
         launched = true;                                                                            \
     }
     hipError_t e = hipSuccess;
@@ -1197,24 +1233,16 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
     GU_CASE(BF16, 1) GU_CASE(BF16, 2) GU_CASE(BF16, 4) GU_CASE(BF16, 8)
     GU_CASE(INT4, 1) GU_CASE(INT4, 2) GU_CASE(INT4, 4) GU_CASE(INT4, 8)
 #undef GU_CASE
+#undef GU_LAUNCH
     if (!launched) return hipErrorInvalidValue;
     if (e != hipSuccess) return e;
     if (!(parts & kFfnDown)) return hipSuccess;
-    const size_t doff = down_offset(H, I, dtype);
-    const int acc = accumulate ? 1 : 0;
-    const int NE = k + has_shared;
-    const int epc = dtype == F32 ? 4 : dtype == BF16 ? 8 : 32;
-    const int need = (NE * (I / epc) + kWave - 1) / kWave;
-    const size_t lds = sizeof(float) * size_t(NE) * I;
-    int ns = 0;
-    for (int n : {1, 2, 3, 4, 6, 8, 9, 12, 16})
-        if (!ns && need <= n) ns = n;
-    if (ns && lds <= 64 * 1024) {
-        const dim3 grid((H + 3) / 4, T);
+    if (lds_down) {
+        const dim3 grid((H + 4 * kDownWaveRows - 1) / (4 * kDownWaveRows), T);
 #define DN_CASE(DT, N)                                                                               \
         if (dtype == DT && ns == N)                                                                  \
-            return launch(down_combine_lds_kernel<DT, N>, grid, kBlock, lds, s, T, H, I, E, k, ids, \
-                          slot_of, pl, expert_bytes, sw, doff, ws.act, y, acc, pl1);
+            return launch(down_combine_lds_kernel<DT, N, kDownWaveRows>, grid, kBlock, lds, s, T, H, I, E, k, \
+                          ids, slot_of, pl, expert_bytes, sw, doff, ws.act, y, acc, pl1);
 #define DN_ALL(N) DN_CASE(F32, N) DN_CASE(BF16, N) DN_CASE(INT4, N)
         DN_ALL(1) DN_ALL(2) DN_ALL(3) DN_ALL(4) DN_ALL(6) DN_ALL(8) DN_ALL(9) DN_ALL(12) DN_ALL(16)
 #undef DN_ALL
