@@ -136,7 +136,7 @@ def hbm_ceiling(torch, moe, launch_sizes, n_launch: int = 40, stream_bytes: int 
     (the expert FFN's two launches) over distinct memory (so the 256 MB last-level cache cannot serve
     repeats), replayed from a graph so that host launch cost is out of the picture.  Also runs one 256 MiB
     device copy: the known-size kernels the HBM byte counters are calibrated against."""
-    sizes = [(b // 16) * 16 for b in launch_sizes]
+    sizes = [int(b) // 16 * 16 for b in launch_sizes]
     launch_bytes = sum(sizes)
     total = max(stream_bytes, launch_bytes * n_launch)
     buf = torch.zeros(total, dtype=torch.uint8, device="cuda")
@@ -262,21 +262,48 @@ def hit_step_ms(torch, dec, xs, t_last, reps=16):
     return ms
 
 
-def link_overlap(d, elapsed, steps, compute_ms):
-    """Stall and overlap of the demand fills over the timed region, per token: copy = the link's busy time
-    (device fill clock: first to last filling block of each filling launch), compute = a step whose experts
-    are all resident (hit_step_ms), stall = wall - compute (the time the step spent waiting for the link), and
-    overlap = 1 - (wall - max(copy, compute)) / min(copy, compute)."""
+def link_overlap(d, elapsed, steps, compute_ms, ceil_gbps):
+    """Stall and overlap of the demand fills over the timed region, per token: copy = the link's busy time, as
+    the filled bytes over the link's measured ceiling; compute = a step whose experts are all resident
+    (hit_step_ms); stall = wall - compute (the time the step spent waiting for the link); overlap =
+    1 - (wall - max(copy, compute)) / min(copy, compute)."""
     wall = elapsed * 1e3 / steps
-    copy = d["fill_ns"] * 1e-6 / steps
+    copy = d["h2d_bytes"] / (ceil_gbps * 1e9) * 1e3 / steps
     lo = min(copy, compute_ms)
-    return {"stall_ms_per_token": max(0.0, wall - compute_ms), "fill_ms_per_token": copy,
+    return {"stall_ms_per_token": max(0.0, wall - compute_ms), "copy_ms_per_token": copy,
             "compute_ms_per_token": compute_ms, "wall_ms_per_token": wall,
             "overlap": 1.0 - (wall - max(copy, compute_ms)) / lo if lo > 0 else None,
-            "fill_tail_ms_per_token": d["stall_ns"] * 1e-6 / steps,
-            "method": "copy: device wall-clock stamps of the filling launches; compute: 16 steps repeating the last "
-                      "token's routing (every expert resident, no fill); fill_tail: how long each launch's fills ran "
-                      "past its computing blocks (the library's stall_ns), which the fills' own traffic stretches"}
+            "method": "copy: filled bytes / the link's measured ceiling; compute: 16 steps repeating the last token's "
+                      "routing after the timed region (every expert resident, no fill); stall = wall - compute"}
+
+
+def clocked_fills(torch, moe, make_stack, dec_factory, n_tokens, first, warmup=64):
+    """The demand fills timed on the device (MOE_CACHE_FILL_CLOCK) in a separate run of `n_tokens` decode tokens
+    on a fresh cache (after `warmup` untimed ones): the stamps cost each filling launch and lookup a few
+    microseconds, so this run is not the timed one."""
+    cache, stack = make_stack()
+    dec = dec_factory(stack)
+    for t in range(first, first + warmup):
+        dec(10_000_000 + t, t)
+    moe.moe_sync_check()
+    s0 = cache.stats()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for t in range(first + warmup, first + warmup + n_tokens):
+        dec(10_000_000 + t, t)
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    moe.moe_sync_check()
+    s1 = cache.stats()
+    stack.close()
+    cache.close()
+    fill = (s1["fill_ns"] - s0["fill_ns"]) * 1e-6 / n_tokens
+    return {"tokens": n_tokens, "tokens_per_s": n_tokens / el, "wall_ms_per_token": el * 1e3 / n_tokens,
+            "fill_ms_per_token": fill, "link_GBps_while_filling":
+                (s1["h2d_bytes"] - s0["h2d_bytes"]) / n_tokens / (fill * 1e-3) / 1e9 if fill else None,
+            "fill_tail_ms_per_token": (s1["stall_ns"] - s0["stall_ns"]) * 1e-6 / n_tokens,
+            "method": "device wall-clock stamps of each filling launch: first to last filling block (fill), and how "
+                      "long the fills ran past the launch's computing blocks (fill_tail, the library's stall_ns)"}
 
 
 def expert_kernel_bytes(wl, n_exp, T):
@@ -457,10 +484,10 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     xp_np = synth.prefill_states(wl)
     t_setup = time.perf_counter() - t_setup
 
-    def make():
+    def make(fill_clock=False):
         cache = moe.ExpertCache(L, E, eb, wl.budget_bytes, buf.ptr, E * eb, eb, reserved_bytes=L * eb,
                                 policy=POLICIES[args.policy], charge_max=args.charge_max,
-                                device=args.residency == "device")
+                                device=args.residency == "device", fill_clock=fill_clock)
         stack = moe.MoeStack(cache, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=1,
                              max_prefill_tokens=Tp, prefetch=args.prefetch)
         return cache, stack
@@ -500,6 +527,12 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
     moe.moe_sync_check()
     st3 = cache.stats()
     compute_ms = hit_step_ms(torch, dec, xs, n_steps - 1)
+    clocked = None
+    if args.residency == "device" and n_steps >= 96:
+        xs_c = xs.clone()  # the clocked run works on its own copy of the inputs
+        clocked = clocked_fills(torch, moe, lambda: make(fill_clock=True),
+                                lambda st: decoder(torch, st, xs_c, bias, use_graph), min(256, n_steps - 64), 0)
+        del xs_c
     ktimes = {name: stack.kernel_time(w, args.replays) for w, name in enumerate(["route", "gateup", "down", "ffn"])}
     moe.moe_sync_check()
     bound = residency_bound(moe, cache, E, st3["capacity"], policy=args.policy)
@@ -572,7 +605,8 @@ def run_prefill_decode(args, torch, moe, oracle, synth):
         "pcie": {"h2d_bytes_per_token": h2d_tok, "achieved_GBps": d_dec["h2d_bytes"] / t_decode / 1e9,
                  "ceiling_GBps": ceil, "frac": d_dec["h2d_bytes"] / t_decode / 1e9 / ceil,
                  "tokens_per_s_bound": ceil * 1e9 / h2d_tok if h2d_tok else None,
-                 **(link_overlap(d_dec, t_decode, steps, compute_ms) if args.residency == "device" else {})},
+                 **(link_overlap(d_dec, t_decode, steps, compute_ms, ceil) if args.residency == "device" else {}),
+                 "clocked_fills": clocked},
         "cpu_baseline": cpu_line,
         "parity": {"sampled_tokens": len(outs), "max_normwise_err": err},
         "setup_s": round(t_setup, 1),
@@ -641,11 +675,13 @@ def main():
     bias = None if bias_np is None else torch.from_numpy(bias_np).to(dev)
     reserved = L * eb if wl.shared else 0
     budget = wl.budget_bytes if budgeted else L * E * eb + reserved
-    cache = moe.ExpertCache(L, E, eb, budget, buf.ptr, 0 if alias else E * eb, eb, reserved_bytes=reserved,
-                            preload=not budgeted, policy=POLICIES[args.policy], charge_max=args.charge_max,
-                            device=budgeted and args.residency == "device",
-                            host_layers=args.host_layers if budgeted else 0,
-                            host_quota=args.host_quota if budgeted else 0)
+    def make_cache(fill_clock=False):
+        return moe.ExpertCache(L, E, eb, budget, buf.ptr, 0 if alias else E * eb, eb, reserved_bytes=reserved,
+                               preload=not budgeted, policy=POLICIES[args.policy], charge_max=args.charge_max,
+                               device=budgeted and args.residency == "device",
+                               host_layers=args.host_layers if budgeted else 0,
+                               host_quota=args.host_quota if budgeted else 0, fill_clock=fill_clock)
+    cache = make_cache()
     hybrid = budgeted and (args.host_layers > 0 or args.host_quota > 0)
     att = None
     if args.attention:
@@ -692,6 +728,15 @@ def main():
     moe.moe_sync_check(stream)
     st1 = cache.stats()
     compute_ms = hit_step_ms(torch, dec, xs, n_steps - 1) if budgeted and att is None else None
+    clocked = None
+    if budgeted and args.residency == "device" and att is None and not hybrid and T == 1 and n_steps >= 96:
+        def make_clocked():
+            c = make_cache(fill_clock=True)
+            return c, moe.MoeStack(c, H, I, E, k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T)
+        xs_c = xs.clone()  # the clocked run works on its own copy of the inputs
+        clocked = clocked_fills(torch, moe, make_clocked, lambda st: decoder(torch, st, xs_c, bias, use_graph),
+                                min(256, n_steps - 64), 0)
+        del xs_c
     # the oracle leg's copy of the attention state, taken before the attention timing rewrites the last position
     att_host = None
     if att is not None:
@@ -712,6 +757,10 @@ def main():
     unique = k if T == 1 else None
     if unique is None:
         unique = float(np.mean([len(np.unique(sets[t, 0])) for t in range(args.warmup, n_steps)]))
+    if hybrid:  # the timing re-launches skip the ranks the host tier computed in the last step
+        ev_all = cache.trace()
+        last = ev_all[ev_all["t"] == ev_all["t"].max()]
+        unique = k - float((last["kind"] == moe.EVENT_HOST).sum()) / L
     n_exp = unique + (1 if wl.shared else 0)
     gu_bytes, dn_bytes = expert_kernel_bytes(wl, n_exp, T)
 
@@ -729,8 +778,8 @@ def main():
                 "frac": d["h2d_bytes"] / elapsed / 1e9 / ceil,
                 "tokens_per_s_bound": ceil * 1e9 / h2d_per_tok if h2d_per_tok else None,
                 "ceiling_method": "hipMemcpyAsync from hipHostMalloc memory, 64 MiB and expert-size chunks",
-                **(link_overlap(d, elapsed, args.steps, compute_ms) if compute_ms and args.residency == "device"
-                   else {})}
+                **(link_overlap(d, elapsed, args.steps, compute_ms, ceil) if compute_ms and args.residency == "device"
+                   else {}), "clocked_fills": clocked}
 
     hbm = hbm_ceiling(torch, moe, [gu_bytes, dn_bytes])
     traffic, traffic_src = measured_traffic(4) if args.config == 4 else (None, "no counter summary")

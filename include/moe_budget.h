@@ -76,6 +76,8 @@ extern "C" {
 #define MOE_CACHE_PRELOAD 1  /* start with every expert resident at slot layer*E + expert */
 #define MOE_CACHE_HOST_SIM 2 /* no device: slots live in host memory and fills are memcpy */
 #define MOE_CACHE_DEVICE 4   /* decisions on the device: lookups are kernels (expert_cache_lookup_device) */
+#define MOE_CACHE_FILL_CLOCK 8 /* MOE_CACHE_DEVICE: time the demand fills on the device (stats stall_ns, fill_ns);
+                                  the stamps add a few microseconds to each filling launch and lookup */
 
 #define MOE_EVENT_HIT 0
 #define MOE_EVENT_MISS 1
@@ -273,7 +275,7 @@ typedef struct {
     size_t host_layer_stride;  /* 0 lets layers alias one host copy (keys stay distinct) */
     size_t host_expert_stride;
     int policy;                /* MOE_POLICY_LRU or MOE_POLICY_ROTARY */
-    int flags;                 /* MOE_CACHE_PRELOAD | MOE_CACHE_HOST_SIM */
+    int flags;                 /* MOE_CACHE_PRELOAD | MOE_CACHE_HOST_SIM | MOE_CACHE_DEVICE | MOE_CACHE_FILL_CLOCK */
     int charge_max;            /* MOE_POLICY_ROTARY: most charge a slot holds, 0..65535 (0 = cyclic FIFO) */
     /* Host tier (the paper's run recipe keeps experts of some layers in host memory and computes them on
      * host cores, sec. 6 and Fig. 3): demand lookups may leave experts in the host store, to be computed there
@@ -298,8 +300,8 @@ typedef struct {
     uint64_t h2d_bytes;   /* bytes filled from the host store */
     int32_t capacity;     /* slots: floor((budget - reserved) / expert_bytes) */
     int32_t occupancy;    /* slots holding an expert */
-    /* MOE_CACHE_DEVICE (0 otherwise), device wall-clock time of the demand fills (sec. 4's selective load
-     * on the step's path; a prefetch's fills are not counted):
+    /* MOE_CACHE_DEVICE with MOE_CACHE_FILL_CLOCK (0 otherwise), device wall-clock time of the demand fills
+     * (sec. 4's selective load on the step's path; a prefetch's fills are not counted):
      *   fill_ns:  per filling launch, from its first filling block's start to its last one's end, summed;
      *   stall_ns: per filling launch, how long its fills ran past both their start and the end of the
      *             launch's computing blocks (the resident experts' work), summed.  The fills' own traffic

@@ -24,7 +24,7 @@ MOE_ACCUMULATE = 1
 MOE_ROUTE_RMSNORM = 1
 MOE_POLICY_LRU = 0
 MOE_POLICY_ROTARY = 1
-MOE_CACHE_PRELOAD, MOE_CACHE_HOST_SIM, MOE_CACHE_DEVICE = 1, 2, 4
+MOE_CACHE_PRELOAD, MOE_CACHE_HOST_SIM, MOE_CACHE_DEVICE, MOE_CACHE_FILL_CLOCK = 1, 2, 4, 8
 EVENT_HIT, EVENT_MISS, EVENT_PREFETCH, EVENT_HOST = 0, 1, 2, 3
 MOE_SLOT_HOST = -2
 MAX_DECODE_TOKENS = 16
@@ -361,11 +361,13 @@ class ExpertCache:
     def __init__(self, n_layers: int, n_experts: int, expert_bytes: int, budget_bytes: int, host_base: int,
                  host_layer_stride: int, host_expert_stride: int, reserved_bytes: int = 0,
                  preload: bool = False, host_sim: bool = False, policy: int = MOE_POLICY_LRU,
-                 charge_max: int = 0, device: bool = False, host_layers: int = 0, host_quota: int = 0):
+                 charge_max: int = 0, device: bool = False, host_layers: int = 0, host_quota: int = 0,
+                 fill_clock: bool = False):
         d = CacheDesc(n_layers, n_experts, expert_bytes, budget_bytes, reserved_bytes, host_base,
                       host_layer_stride, host_expert_stride, policy,
                       (MOE_CACHE_PRELOAD if preload else 0) | (MOE_CACHE_HOST_SIM if host_sim else 0) |
-                      (MOE_CACHE_DEVICE if device else 0), charge_max, host_layers, host_quota)
+                      (MOE_CACHE_DEVICE if device else 0) | (MOE_CACHE_FILL_CLOCK if fill_clock else 0),
+                      charge_max, host_layers, host_quota)
         h = C.c_void_p()
         _check(lib().expert_cache_create(C.byref(d), C.byref(h)), "expert_cache_create")
         self._h = h

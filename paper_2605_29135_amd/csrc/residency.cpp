@@ -493,7 +493,9 @@ int dev_state_create(moe_cache *c, bool preload) {
     if (e == hipSuccess) e = hipMalloc(&r.fill_src, sizeof(long long) * size_t(c->E));
     if (e == hipSuccess) e = hipMalloc(&r.fill_slot, sizeof(int32_t) * size_t(c->E));
     if (e == hipSuccess) e = hipMalloc(&r.n_fill, sizeof(int32_t));
-    if (e == hipSuccess) e = hipMalloc(&r.clk, sizeof(unsigned long long) * moe::kClkWords);
+    // the fill clock costs its launches a few microseconds (stamps, atomics, the fold): only when asked for
+    if (e == hipSuccess && (c->d.flags & MOE_CACHE_FILL_CLOCK))
+        e = hipMalloc(&r.clk, sizeof(unsigned long long) * moe::kClkWords);
     if (e != hipSuccess) return moe::fail_hip(e, "allocating the device residency state");
     int dev = 0, khz = 0;
     if ((e = hipGetDevice(&dev)) == hipSuccess)
@@ -518,7 +520,7 @@ int dev_state_create(moe_cache *c, bool preload) {
     if (e == hipSuccess) e = hipMemset(r.n_fill, 0, sizeof(int32_t));
     std::vector<unsigned long long> clk(moe::kClkWords, 0ull);
     for (int i = 0; i < moe::kClkLanes; ++i) clk[size_t(moe::kClkFillStart + i)] = ~0ull;
-    if (e == hipSuccess)
+    if (e == hipSuccess && r.clk)
         e = hipMemcpy(r.clk, clk.data(), sizeof(unsigned long long) * clk.size(), hipMemcpyHostToDevice);
     return e == hipSuccess ? MOE_OK : moe::fail_hip(e, "initialising the device residency state");
 }
@@ -564,6 +566,8 @@ int expert_cache_create(const moe_cache_desc *d, moe_cache **out) {
                          d->host_layers, d->host_quota);
     if (host_tier && (d->flags & (MOE_CACHE_DEVICE | MOE_CACHE_PRELOAD)))
         return moe::fail(MOE_ERR_INVALID_ARG, "host tier: not with MOE_CACHE_DEVICE or MOE_CACHE_PRELOAD");
+    if ((d->flags & MOE_CACHE_FILL_CLOCK) && !dev_mode)
+        return moe::fail(MOE_ERR_INVALID_ARG, "MOE_CACHE_FILL_CLOCK needs MOE_CACHE_DEVICE");
     if (dev_mode && (d->flags & MOE_CACHE_HOST_SIM))
         return moe::fail(MOE_ERR_INVALID_ARG, "MOE_CACHE_DEVICE cannot be combined with MOE_CACHE_HOST_SIM");
     if (dev_mode && (std::min(cap, preload ? keys : cap) > size_t(moe::kDevMaxSlots) || d->n_experts > MOE_MAX_EXPERTS))
@@ -758,8 +762,9 @@ int expert_cache_stats(moe_cache *c, moe_cache_stats *out) {
         out->capacity = c->C;
         out->occupancy = int32_t(std::min<unsigned long long>(v[moe::kScalNextFree], (unsigned long long)c->C));
         // fill clock: the folded totals plus the record of the last filling launch, not folded yet
-        unsigned long long k[moe::kClkWords];
-        if ((e = hipMemcpy(k, c->dr.clk, sizeof k, hipMemcpyDeviceToHost)) != hipSuccess)
+        unsigned long long k[moe::kClkWords] = {};
+        for (int i = 0; i < moe::kClkLanes; ++i) k[moe::kClkFillStart + i] = ~0ull;
+        if (c->dr.clk && (e = hipMemcpy(k, c->dr.clk, sizeof k, hipMemcpyDeviceToHost)) != hipSuccess)
             return moe::fail_hip(e, "reading the fill clock");
         unsigned long long stall = k[moe::kClkStall], fill = k[moe::kClkFill];
         unsigned long long fs = ~0ull, fe = 0, ce = 0;

@@ -311,7 +311,7 @@ def oracle_routed_chain(wl, x0, g_logits, g_ids, g_w, layers, bias=None, logit_t
 
 def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=None, T=1, charge_max=None,
                         recall=0, recall_overlap=0, device=False, graph=False, host_layers=0, host_quota=0,
-                        host_threads=0):
+                        host_threads=0, fill_clock=False):
     """Decode `steps` steps through the stack; check events exactly and outputs within tolerance.  With
     charge_max the slots use the rotary policy (else LRU); with recall the stack recalls prior slot sets; with
     host_layers / host_quota a host tier computes its share of the experts on host cores."""
@@ -321,7 +321,7 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
     cache = moe.ExpertCache(wl.L, wl.E, eb, capacity * eb + (wl.L * eb if wl.shared else 0), buf.ptr,
                             0 if layers_alias else wl.E * eb, eb, reserved_bytes=wl.L * eb if wl.shared else 0,
                             policy=policy, charge_max=charge_max or 0, device=device, host_layers=host_layers,
-                            host_quota=host_quota)
+                            host_quota=host_quota, fill_clock=fill_clock)
     routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
     shared = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)] if wl.shared else None
     stack = moe.MoeStack(cache, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shared, max_tokens=T,
@@ -480,6 +480,18 @@ def test_budgeted_stack_int4_shared_device_one_token(graph):
                         routing="zipf_overlap", cfg_id=92)
     s = run_stack_and_check(wl, steps=16, capacity=30, device=True, graph=graph)
     assert s["evictions"] > 0
+
+
+@pytest.mark.parametrize("graph", [False, True])
+def test_fill_clock_times_the_fills_and_changes_nothing(graph):
+    """MOE_CACHE_FILL_CLOCK: the demand fills of one-token device steps are timed (fill_ns > 0, stall_ns within
+    it); decisions and outputs still match the oracle; without the flag both stay 0."""
+    wl = synth.Workload("clock stack", H=512, E=32, k=4, I=256, L=4, dtype=synth.BF16, routing="zipf_overlap",
+                        cfg_id=97)
+    s = run_stack_and_check(wl, steps=16, capacity=24, device=True, graph=graph, fill_clock=True)
+    assert s["misses"] > 0 and s["fill_ns"] > 0 and 0 <= s["stall_ns"] <= s["fill_ns"]
+    s0 = run_stack_and_check(wl, steps=4, capacity=24, device=True)
+    assert s0["fill_ns"] == 0 and s0["stall_ns"] == 0
 
 
 @pytest.mark.parametrize("dtype,shared,N,Q,threads", [(synth.BF16, False, 1, 1, 0), (synth.BF16, False, 0, 2, 3),

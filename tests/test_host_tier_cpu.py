@@ -188,6 +188,12 @@ def test_library_host_tier_matches_oracle(seed, L, E, n, C_slots, N, Q):
             assert table[l * E + e] == o.slot_of(l, e)
 
 
+def test_fill_clock_needs_device_residency():
+    st = _Store(2, 8)
+    with pytest.raises(moe.MoeError):
+        moe.ExpertCache(2, 8, 256, 4 * 256, st.buf.ctypes.data, 8 * 256, 256, host_sim=True, fill_clock=True)
+
+
 def test_library_host_tier_rejects_bad_settings():
     st = _Store(2, 8)
     for N, Q in [(-1, 0), (3, 0), (0, -1), (0, 9)]:
