@@ -560,9 +560,9 @@ MOE_API int moe_opt_fills(const int32_t *keys, const int32_t *offsets, int n_ste
 
 /* Measurement aid, not part of the method: streams `bytes` of device memory
  * once, with the 16-byte nontemporal loads the expert kernels use for weight
- * rows (each wave issues eight 1 KiB pieces before consuming any), so that a
+ * rows (each wave issues four 1 KiB pieces before consuming any), so that a
  * caller timing it gets the HBM read rate those kernels can reach.  buf: device
- * memory, 16-byte aligned, bytes a multiple of 16 (< 2^31 * 32 KiB); sink:
+ * memory, 16-byte aligned, bytes a multiple of 16 (< 2^31 * 16 KiB); sink:
  * device float [1], written only in the unlikely case that the data xor to a
  * fixed pattern.  Enqueued on `stream`. */
 MOE_API int moe_hbm_read_probe(const void *buf, size_t bytes, float *sink, void *stream);

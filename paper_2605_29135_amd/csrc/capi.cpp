@@ -269,7 +269,7 @@ int moe_hbm_read_probe(const void *buf, size_t bytes, float *sink, void *stream)
     if (!buf || !sink) return fail(MOE_ERR_INVALID_ARG, "hbm read probe: NULL pointer");
     if (bytes % 16 || reinterpret_cast<uintptr_t>(buf) % 16)
         return fail(MOE_ERR_INVALID_ARG, "hbm read probe: buffer and size must be multiples of 16 bytes");
-    if (bytes / 16 / (8 * 256) >= (size_t(1) << 31))
+    if (bytes / 16 / (4 * 256) >= (size_t(1) << 31))
         return fail(MOE_ERR_INVALID_ARG, "hbm read probe: buffer too large for one launch");
     return finish_launch(moe::launch_hbm_read(buf, bytes, sink, static_cast<hipStream_t>(stream)), "read probe launch");
 }

@@ -1300,6 +1300,7 @@ hipError_t launch_hbm_read(const void *buf, size_t bytes, float *sink, hipStream
     if (n16 == 0) return hipSuccess;
     const size_t per_block = size_t(kReadLoads) * kBlock;  // 16-byte words per block
     const size_t blocks = (n16 + per_block - 1) / per_block;
+    if (blocks >= (size_t(1) << 31)) return hipErrorInvalidValue;
     hbm_read_kernel<<<unsigned(blocks), kBlock, 0, s>>>(static_cast<const uint8_t *>(buf), n16, sink);
     return hipGetLastError();
 }
