@@ -134,6 +134,74 @@ __device__ __forceinline__ float chunk_dot(uint4 w, const float *xv) {
     return acc;
 }
 
+// ---- int4 x fp16 dot products (the one-token int4 kernels) ----
+// The activations of a 32-element chunk (one lane's 16 bytes of nibbles) are held as fp16 pairs, scaled by
+// a power of two 2^sh that puts the chunk's largest magnitude in [2^13, 2^14): fp16 then keeps 11
+// significant bits of every element (elements below 2^-27 of the chunk's largest become subnormal), and
+// no element can overflow.  Dword i of the chunk (elements 8i .. 8i+7, nibble e at bits 4e) pairs with
+// the 16-byte word {(x0, x4), (x1, x5), (x2, x6), (x3, x7)} of those elements.
+typedef _Float16 half2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ half2_t as_half2(uint32_t v) { return __builtin_bit_cast(half2_t, v); }
+
+// A signed nibble q becomes the fp16 value bias + q with one three-input bit operation: its sign bit is
+// flipped (q + 8 as an unsigned nibble) and the result is dropped into the mantissa of 1024 (nibble at
+// bits 0-3 of a half: 1024 + q + 8) or of 64 (bits 4-7, sixteen times the weight of a mantissa step:
+// 64 + q + 8).  So every nibble is exact, and the sum carries sum_x (1032 x) over the elements at even
+// nibble positions and sum_x (72 x) over the odd ones: int4_bias_sum gives that term for the chunk,
+// which the caller subtracts once per chunk.
+constexpr uint32_t kNibLo = 0x000F000Fu, kMagicLo = 0x64086408u;  // 1024 + (q ^ 8) per half
+constexpr uint32_t kNibHi = 0x00F000F0u, kMagicHi = 0x54805480u;  // 64 + (q ^ 8) per half
+constexpr float kBiasLo = 1032.f, kBiasHi = 72.f;
+
+// sum of q * x over the eight nibbles of d, added to acc (x pairs as above, unscaled by the bias).
+__device__ __forceinline__ float dot8_i4h(uint32_t d, uint4 xq, float acc) {
+    const uint32_t t = d >> 8;
+    acc = __builtin_amdgcn_fdot2(as_half2((d & kNibLo) ^ kMagicLo), as_half2(xq.x), acc, false);
+    acc = __builtin_amdgcn_fdot2(as_half2((d & kNibHi) ^ kMagicHi), as_half2(xq.y), acc, false);
+    acc = __builtin_amdgcn_fdot2(as_half2((t & kNibLo) ^ kMagicLo), as_half2(xq.z), acc, false);
+    acc = __builtin_amdgcn_fdot2(as_half2((t & kNibHi) ^ kMagicHi), as_half2(xq.w), acc, false);
+    return acc;
+}
+
+// One 16-byte chunk of 32 nibbles against its four words of fp16 pairs: sum of (q + bias) * x.
+__device__ __forceinline__ float chunk_dot_i4h(uint4 w, const uint4 *xq) {
+    float acc = dot8_i4h(w.x, xq[0], 0.f);
+    acc = dot8_i4h(w.y, xq[1], acc);
+    acc = dot8_i4h(w.z, xq[2], acc);
+    return dot8_i4h(w.w, xq[3], acc);
+}
+
+// The staging side, run by the four consecutive lanes (a quad) that hold one chunk's four dwords of
+// activations, v[0..7] each: returns this lane's word of fp16 pairs; sh_out gets the chunk's exponent
+// shift (the dot's result is scaled back by 2^-sh) and bias_out the chunk's bias term (same in the four
+// lanes).  Every lane of the wave must call it (quad DPP exchanges).
+__device__ __forceinline__ uint4 stage8_i4h(const float *v, int &sh_out, float &bias_out) {
+    float m = 0.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) m = fmaxf(m, fabsf(v[e]));
+    m = fmaxf(m, dpp<0xB1>(m));  // quad_perm [1,0,3,2]
+    m = fmaxf(m, dpp<0x4E>(m));  // quad_perm [2,3,0,1]
+    int ex;
+    (void)frexpf(m, &ex);  // m = f * 2^ex, f in [0.5, 1) (ex = 0 for m = 0)
+    const int sh = 14 - ex;
+    uint32_t p[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const half2_t h = {(_Float16)ldexpf(v[e], sh), (_Float16)ldexpf(v[e + 4], sh)};
+        p[e] = __builtin_bit_cast(uint32_t, h);
+    }
+    const half2_t lo = {(_Float16)kBiasLo, (_Float16)kBiasLo}, hi = {(_Float16)kBiasHi, (_Float16)kBiasHi};
+    float b = __builtin_amdgcn_fdot2(as_half2(p[0]), lo, 0.f, false);
+    b = __builtin_amdgcn_fdot2(as_half2(p[1]), hi, b, false);
+    b = __builtin_amdgcn_fdot2(as_half2(p[2]), lo, b, false);
+    b = __builtin_amdgcn_fdot2(as_half2(p[3]), hi, b, false);
+    b += dpp<0xB1>(b);
+    b += dpp<0x4E>(b);
+    sh_out = sh;
+    bias_out = b;
+    return make_uint4(p[0], p[1], p[2], p[3]);
+}
 
 }  // namespace dev
 }  // namespace moe

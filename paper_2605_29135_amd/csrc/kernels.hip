@@ -566,7 +566,10 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     int i = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
     if (!STAGE_X && i >= I) return;  // when x is staged, every wave joins the block's staging below
     const int P = T * k;
-    float xv[NCH][EPC];
+    float xv[STAGE_X ? 1 : NCH][EPC];
+    uint4 xq[STAGE_X ? NCH : 1][4];       // staged int4 path: the chunk's activations as fp16 pairs
+    float xbias[NCH];                     // ... the chunk's bias term
+    int xsh_[NCH];                        // ... and its exponent shift
     float wp0;  // combine weight of the first pair (1 for the shared expert)
     if constexpr (!STAGE_X) {
         // The first pair's activations are loaded before the weight stream: loads
@@ -583,6 +586,19 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
 #pragma unroll
                 for (int q = 0; q < EPC; ++q) xv[c][q] = 0.f;
             }
+        }
+    }
+    // Staged int4 token: this thread's share of x (eight elements per round) is loaded before the weight
+    // stream, so that packing it waits only for these loads.
+    float4 xa[STAGE_X ? NCH : 1][2];
+    if constexpr (STAGE_X) {
+        const float4 *xt4 = reinterpret_cast<const float4 *>(x + size_t(single < P ? single / k : single - P) * H);
+#pragma unroll
+        for (int r = 0; r < NCH; ++r) {
+            const int f = r * kBlock + threadIdx.x;
+            const bool in = FULL || (f >> 2) * EPC < H;  // (H is a multiple of 128: a chunk is in or out whole)
+            xa[r][0] = in ? xt4[2 * f] : make_float4(0.f, 0.f, 0.f, 0.f);
+            xa[r][1] = in ? xt4[2 * f + 1] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     }
     const size_t rb = row_bytes_of(DT, H);
@@ -605,6 +621,40 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
             su[c] = in ? bf16_bits_to_float(sc[size_t(2 * iw + 1) * groups_per_row + col0 / 128]) : 0.f;
         }
     }
+    if constexpr (STAGE_X) {
+      if (first) {
+        // The token row is the same for every wave of the block: it is staged in LDS once, while the
+        // weight loads are in flight, as fp16 pairs (stage8_i4h: thread f packs the eight elements of dword f % 4 of
+        // chunk slot f / 4), transposed to [chunk][dword][lane] so that each read of a dword's word is 64
+        // consecutive 16-byte words; each chunk slot's exponent shift and bias term follow.
+        extern __shared__ uint4 xsh[];
+        int2 *xaux = reinterpret_cast<int2 *>(xsh + NCH * 4 * kWave);
+        wp0 = single < P ? weights[single] : 1.f;
+#pragma unroll
+        for (int r = 0; r < NCH; ++r) {  // NCH * 64 chunk slots x 4 dwords = NCH rounds of the block
+            const int f = r * kBlock + threadIdx.x, gs = f >> 2, q = f & 3;
+            float v[8];
+            const float4 a = xa[r][0], b = xa[r][1];
+            v[0] = a.x; v[1] = a.y; v[2] = a.z; v[3] = a.w;
+            v[4] = b.x; v[5] = b.y; v[6] = b.z; v[7] = b.w;
+            int sh;
+            float bias;
+            const uint4 w = stage8_i4h(v, sh, bias);
+            xsh[((gs / kWave) * 4 + q) * kWave + (gs % kWave)] = w;
+            if (q == 0) xaux[gs] = make_int2(__float_as_int(bias), sh);
+        }
+        __syncthreads();
+        if (i >= I) return;
+#pragma unroll
+        for (int c = 0; c < NCH; ++c) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) xq[c][q] = xsh[(c * 4 + q) * kWave + lane];
+            const int2 au = xaux[c * kWave + lane];
+            xbias[c] = __int_as_float(au.x);
+            xsh_[c] = -au.y;
+        }
+      }
+    }
     if (dst && i < I) {  // the missing expert's row pair (and int4 scales) into its slot
         uint8_t *dg = dst + (gate - blob);  // the same place in the slot
 #pragma unroll
@@ -624,55 +674,31 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
             }
         }
     }
-    if constexpr (STAGE_X) {
-      if (first) {
-        // The token row is the same for every wave of the block: it is staged in LDS once, behind the
-        // weight loads, transposed to [chunk][quarter][lane] so that each read of a quarter is 64
-        // consecutive 16-byte words.
-        extern __shared__ float4 xsh[];
-        constexpr int Q = EPC / 4;
-        wp0 = single < P ? weights[single] : 1.f;
-        const float4 *xt4 = reinterpret_cast<const float4 *>(x + size_t(single < P ? single / k : single - P) * H);
-        for (int f = threadIdx.x; f < H / 4; f += kBlock) {
-            const int l = (f / Q) % kWave, cc = f / Q / kWave, q = f % Q;
-            xsh[(cc * Q + q) * kWave + l] = xt4[f];
-        }
-        __syncthreads();
-        if (i >= I) return;
-#pragma unroll
-        for (int c = 0; c < NCH; ++c) {
-            const int col0 = (c * kWave + lane) * EPC;
-#pragma unroll
-            for (int q = 0; q < Q; ++q) {
-                const float4 v = (FULL || col0 < H) ? xsh[(c * Q + q) * kWave + lane] : make_float4(0.f, 0.f, 0.f, 0.f);
-                xv[c][4 * q] = v.x;
-                xv[c][4 * q + 1] = v.y;
-                xv[c][4 * q + 2] = v.z;
-                xv[c][4 * q + 3] = v.w;
-            }
-        }
-      }
-    }
     for (int q = 0; q < pcount; ++q) {
         const int p = ONE_TOKEN ? single : pairs[pstart + q];
-        if (q > 0) {
+        if (!STAGE_X && q > 0) {  // (a staged token is one pair)
             const float *xt = x + size_t(p < P ? p / k : p - P) * H;
 #pragma unroll
             for (int c = 0; c < NCH; ++c) {
                 const int col0 = (c * kWave + lane) * EPC;
-                if ((FULL || col0 < H)) load_x<DT>(xt, col0, xv[c]);
+                if ((FULL || col0 < H)) load_x<DT>(xt, col0, xv[STAGE_X ? 0 : c]);
             }
         }
         float ga = 0.f, ua = 0.f;
 #pragma unroll
         for (int c = 0; c < NCH; ++c) {
-            float dg = chunk_dot<DT>(wg[c], xv[c]), du = chunk_dot<DT>(wu[c], xv[c]);
-            if constexpr (DT == INT4) {
-                dg *= sg[c];
-                du *= su[c];
+            if constexpr (STAGE_X) {
+                ga += ldexpf((chunk_dot_i4h(wg[c], xq[c]) - xbias[c]) * sg[c], xsh_[c]);
+                ua += ldexpf((chunk_dot_i4h(wu[c], xq[c]) - xbias[c]) * su[c], xsh_[c]);
+            } else {
+                float dg = chunk_dot<DT>(wg[c], xv[c]), du = chunk_dot<DT>(wu[c], xv[c]);
+                if constexpr (DT == INT4) {
+                    dg *= sg[c];
+                    du *= su[c];
+                }
+                ga += dg;
+                ua += du;
             }
-            ga += dg;
-            ua += du;
         }
         ga = wave_sum(ga);
         ua = wave_sum(ua);
@@ -804,14 +830,14 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
     const uint8_t *__restrict__ shared_w, size_t d_off, const float *__restrict__ act,
     float *__restrict__ y, int accumulate, FfnPlan plan) {
     constexpr int EPC = Fmt<DT>::EPC;
+    // int4 weights: the activations are staged as fp16 pairs (stage8_i4h), [4][chunks] words then an
+    // (exponent shift, bias term) pair per chunk; thread f of staging round m = f / 256 packs dword f % 4
+    // of chunk f / 4.  Otherwise as fp32, [(k+1) x I / 4] float4.
+    constexpr bool HALF = DT == INT4;
     // float4 staging loads per thread: (k+1) I <= NS * 64 * EPC = SM * 4 * 256
     constexpr int SM = (NS * EPC + 15) / 16;
-    extern __shared__ float4 aw4[];  // [(k+1) x I / 4] activations of this token
-    // Entry j: byte offset of its blob from `pool` (the shared expert's too, so
-    // that every address derives from a kernel argument and stays a global
-    // load) and whether it contributes.
-    __shared__ long long ent_off[MOE_MAX_TOPK + 1];
-    __shared__ int ent_ok[MOE_MAX_TOPK + 1];
+    static_assert(!HALF || SM == 2 * NS, "int4 staging: two float4 per thread per round");
+    extern __shared__ float4 aw4[];
     const int t = blockIdx.y;
     const int NE = k + (shared_w != nullptr);
     // 1. staging loads (independent of everything else)
@@ -819,12 +845,26 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
     const float4 *src_routed = reinterpret_cast<const float4 *>(act) + size_t(t) * routed4;
     const float4 *src_shared = reinterpret_cast<const float4 *>(act) + (size_t(T) * k + t) * (I / 4) - routed4;
     float4 stage[SM];
+    if constexpr (HALF) {
 #pragma unroll
-    for (int m = 0; m < SM; ++m) {
-        const int i = threadIdx.x + m * kBlock;
-        stage[m] = i < n4 ? (i < routed4 ? src_routed[i] : src_shared[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
+        for (int m = 0; m < NS; ++m) {
+            const int i = 2 * (threadIdx.x + m * kBlock);  // (routed4 is even: a pair lies on one side)
+            const bool in = i < n4;
+            stage[2 * m] = in ? (i < routed4 ? src_routed[i] : src_shared[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
+            stage[2 * m + 1] = in ? (i < routed4 ? src_routed[i + 1] : src_shared[i + 1]) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+    } else {
+#pragma unroll
+        for (int m = 0; m < SM; ++m) {
+            const int i = threadIdx.x + m * kBlock;
+            stage[m] = i < n4 ? (i < routed4 ? src_routed[i] : src_shared[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
     }
-    // 2. where the entries live
+    // 2. where the entries live.  Entry j: byte offset of its blob from `pool` (the shared expert's too, so
+    // that every address derives from a kernel argument and stays a global load) and whether it contributes.
+    // (Vector loads: the ids and the slot table are written by earlier kernels on the stream.)
+    __shared__ long long ent_off[MOE_MAX_TOPK + 1];
+    __shared__ int ent_ok[MOE_MAX_TOPK + 1];
     if (threadIdx.x < NE) {
         const int j = threadIdx.x;
         int ok = 0;
@@ -851,9 +891,9 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
         ent_ok[j] = ok;
     }
     __syncthreads();
+    const int lane = threadIdx.x & (kWave - 1);
     // 3. weight loads of this wave's R output rows.  Workgroup b runs on XCD b mod 8: consecutive row tiles
     // go to the same XCD, so the blocks that share a cache line of int4 row scales share one L2.
-    const int lane = threadIdx.x & (kWave - 1);
     const int nb = gridDim.x;
     const int tile = (nb & 7) ? int(blockIdx.x) : int(blockIdx.x & 7) * (nb >> 3) + int(blockIdx.x >> 3);
     const int h0 = (tile * (kBlock / kWave) + (threadIdx.x / kWave)) * R;  // the wave's first row
@@ -887,11 +927,29 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
             ++j;
         }
     }
-    // 4. staged activations to LDS; chunk g of the virtual row covers aw[g * EPC, +EPC)
+    // 4. staged activations to LDS; chunk g of the virtual row covers elements [g * EPC, +EPC)
+    uint4 *xs = reinterpret_cast<uint4 *>(aw4);
+    int2 *xaux = reinterpret_cast<int2 *>(xs + 4 * total);
+    if constexpr (HALF) {
 #pragma unroll
-    for (int m = 0; m < SM; ++m) {
-        const int i = threadIdx.x + m * kBlock;
-        if (i < n4) aw4[i] = stage[m];
+        for (int m = 0; m < NS; ++m) {
+            const unsigned f = threadIdx.x + m * kBlock, g = f >> 2, q = f & 3u;
+            const float v[8] = {stage[2 * m].x, stage[2 * m].y, stage[2 * m].z, stage[2 * m].w,
+                                stage[2 * m + 1].x, stage[2 * m + 1].y, stage[2 * m + 1].z, stage[2 * m + 1].w};
+            int sh;
+            float bias;
+            const uint4 w = stage8_i4h(v, sh, bias);  // (every lane: quad exchanges)
+            if (g < total) {
+                xs[q * total + g] = w;
+                if (q == 0) xaux[g] = make_int2(__float_as_int(bias), sh);
+            }
+        }
+    } else {
+#pragma unroll
+        for (int m = 0; m < SM; ++m) {
+            const int i = threadIdx.x + m * kBlock;
+            if (i < n4) aw4[i] = stage[m];
+        }
     }
     __syncthreads();
     float acc[R];
@@ -899,7 +957,16 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
     for (int r = 0; r < R; ++r) acc[r] = 0.f;
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
-        if (ok[s]) {
+        if (HALF && ok[s]) {
+            const unsigned g = s * kWave + lane;
+            uint4 xq[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) xq[q] = xs[q * total + g];
+            const int2 au = xaux[g];
+#pragma unroll
+            for (int r = 0; r < R; ++r)
+                acc[r] += ldexpf((chunk_dot_i4h(wv[r][s], xq) - __int_as_float(au.x)) * sv[r][s], -au.y);
+        } else if (!HALF && ok[s]) {
             const int g = s * kWave + lane;
             float av[EPC];
 #pragma unroll
@@ -1201,8 +1268,9 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
     const int groups = one ? k + has_shared : (T * k < E ? T * k : E) + has_shared;
     const dim3 ggrid((I + 3) / 4, groups + (pl1.fill.n ? 1 : 0));  // + the blocks copying down parts
     const int nch = chunks_per_row(H, dtype);
-    // One-token int4 x staging covers every lane's chunk slots, [nch][EPC/4][64] float4, not just H floats.
-    const size_t x_lds = dtype == INT4 ? sizeof(float) * size_t(nch) * kWave * elems_per_chunk(dtype) : 0;
+    // One-token int4 x staging covers every lane's chunk slot: [nch][4][64] words of fp16 pairs, then an
+    // (exponent shift, bias term) pair per slot.
+    const size_t x_lds = dtype == INT4 ? size_t(nch) * kWave * (4 * 16 + 8) : 0;
     // The down kernel: the LDS form when a token's k (+1) activation rows fit in LDS and NS chunks per lane
     // cover them, else the plain one.
     const size_t doff = down_offset(H, I, dtype);
@@ -1210,7 +1278,8 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
     const int NE = k + has_shared;
     const int epc = elems_per_chunk(dtype);
     const int need = (NE * (I / epc) + kWave - 1) / kWave;
-    const size_t lds = sizeof(float) * size_t(NE) * I;
+    // (int4: per chunk of 32 activations, four 16-byte words of fp16 pairs and an 8-byte shift and bias)
+    const size_t lds = dtype == INT4 ? size_t(NE) * (I / 32) * 72 : sizeof(float) * size_t(NE) * I;
     int ns = 0;
     for (int n : {1, 2, 3, 4, 6, 8, 9, 12, 16})
         if (!ns && need <= n) ns = n;
