@@ -347,7 +347,8 @@ MOE_API int expert_cache_create(const moe_cache_desc *desc, moe_cache **out);
  * `stream` see the updated slot table.  slots_out_dev (device int32 [n], or
  * NULL) receives the slot of each id after the lookup.  Ids outside [0, E) raise MOE_ERR_RANGE
  * and a step with more distinct experts than slots MOE_ERR_BUDGET in the device
- * flags (moe_sync_check); such a lookup changes nothing.  Lookups must be
+ * flags (moe_sync_check); such a lookup changes nothing in the cache and writes
+ * -1 to every slots_out_dev entry.  Lookups must be
  * ordered: issue them on one stream. */
 MOE_API int expert_cache_lookup_device(moe_cache *c, int step, int layer, const int32_t *ids_dev, int n,
                                        int32_t *slots_out_dev, void *stream);

@@ -68,11 +68,14 @@ struct FfnFill {
 // Slots of a single-token step known on the host (after a residency lookup):
 // off[j] = byte offset from the pool of the expert of rank j, or -1 for a rank
 // the host tier computes (the kernels skip it).  n = k when valid, 0 when the
-// kernels must read ids and the slot table on the device.
+// kernels must read ids and the slot table on the device -- or, with
+// rank_slot, the slot of each rank as a device lookup wrote it (one read
+// instead of two dependent ones; -1 for a rank the lookup did not place).
 struct FfnPlan {
     int n = 0;
     long long off[16];
     FfnFill fill;  // one token, slots read on the device: the fills this launch performs
+    const int32_t *rank_slot = nullptr;  // one token, n == 0: device [k] slots by rank
 };
 
 hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, const int32_t *ids,

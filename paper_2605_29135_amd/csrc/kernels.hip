@@ -523,15 +523,26 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
             return;
         }
         if (g < k && plan.n) {
-            if (plan.off[g] < 0) return;  // a rank the host tier computes
-            blob = pool + plan.off[g];    // slots known on the host: no device lookups
+            // slots known on the host: no device lookups.  Selected with the block-uniform rank so that
+            // the offsets stay argument (scalar) loads rather than one indexed load before the weights.
+            long long off = plan.off[0];
+#pragma unroll
+            for (int j = 1; j < MOE_MAX_TOPK; ++j)
+                if (g == j) off = plan.off[j];
+            if (off < 0) return;  // a rank the host tier computes
+            blob = pool + off;
         } else if (g < k) {
-            const int e = ids[g];
-            if (e < 0 || e >= E) {
-                if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, kErrRange);
-                return;
+            int s;
+            if (plan.rank_slot) {  // the device lookup's slot for this rank (it flagged bad ids itself)
+                s = plan.rank_slot[g];
+            } else {
+                const int e = ids[g];
+                if (e < 0 || e >= E) {
+                    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, kErrRange);
+                    return;
+                }
+                s = slot_of ? slot_of[e] : e;
             }
-            const int s = slot_of ? slot_of[e] : e;
             if (s < 0) {
                 if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, kErrNotResident);
                 return;
@@ -871,8 +882,16 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
         long long off = 0;
         if (j < k) {
             if (plan.n) {
-                ok = plan.off[j] >= 0;  // (a rank the host tier computes is skipped)
-                off = ok ? plan.off[j] : 0;
+                long long o = plan.off[0];  // (argument loads, selected by lane: no indexed load)
+#pragma unroll
+                for (int jj = 1; jj < MOE_MAX_TOPK; ++jj)
+                    if (j == jj) o = plan.off[jj];
+                ok = o >= 0;  // (a rank the host tier computes is skipped)
+                off = ok ? o : 0;
+            } else if (plan.rank_slot) {
+                const int sl = plan.rank_slot[j];  // (one token: t == 0)
+                ok = sl >= 0;
+                off = ok ? (long long)sl * (long long)expert_bytes : 0;
             } else {
                 const int e = ids[t * k + j];
                 if (e >= 0 && e < E) {
@@ -1244,6 +1263,7 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
             pl1.fill = FfnFill{};  // slots known on the host: nothing left to fill
         } else {
             pl1.fill = plan->fill;
+            pl1.rank_slot = plan->rank_slot;
         }
     }
     if (pl1.fill.n) {  // fills performed by the gate/up launch

@@ -180,6 +180,8 @@ __device__ __forceinline__ void dev_lookup_body(DevLds<ROTARY, NT> &L, const Dev
             atomicOr(err, bad_sh ? kErrRange : kErrBudget);  // no state change, as the host lookup
             r.n_fill[0] = 0;                                  // nothing for the fill kernel to do
         }
+        if (slots_out)  // no rank placed: later kernels that read the slots by rank skip them all
+            for (int i = tid; i < n; i += NT) slots_out[i] = -1;
         return;
     }
     if constexpr (!FORMED) {

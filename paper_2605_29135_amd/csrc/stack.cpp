@@ -452,7 +452,10 @@ int enqueue_decode(moe_stack *s, int step, float *x, int T, const float *logit_b
         // One token with device lookups: the gate/up launch streams the lookup's misses itself (their rows
         // from the host store while the resident experts' gate/up runs), so no fill launch precedes it.
         moe::FfnPlan fplan;
-        if (fused) fplan.fill = moe::cache_ffn_fill(d.cache, (long long)moe::down_offset(d.H, d.I, d.w_dtype));
+        if (fused) {
+            fplan.fill = moe::cache_ffn_fill(d.cache, (long long)moe::down_offset(d.H, d.I, d.w_dtype));
+            fplan.rank_slot = s->dev_slots + size_t(l) * d.max_tokens * d.k;  // as the fused lookup wrote them
+        }
         // the host tier starts on its share at once; the GPU's share (every rank when no host tier, none when
         // the host computes them all and there is no shared expert) is enqueued meanwhile, so that it and the
         // fills run while the host computes

@@ -715,14 +715,17 @@ def test_device_lookup_errors_change_nothing():
     cache = moe.ExpertCache(L, E, eb, C * eb, buf.ptr, E * eb, eb, device=True)
     cache.lookup_device(0, 0, dev(np.array([1, 2, 2], np.int32)))
     moe.moe_sync_check()
-    cache.lookup_device(1, 1, dev(np.array([3, 16], np.int32)))
+    slots = dev(np.full(5, 7, np.int32))
+    cache.lookup_device(1, 1, dev(np.array([3, 16], np.int32)), slots_out=slots[:2])
     with pytest.raises(moe.MoeError) as ei:
         moe.moe_sync_check()
     assert ei.value.code == -2
-    cache.lookup_device(2, 1, dev(np.arange(5, dtype=np.int32)))
+    assert (slots.cpu().numpy()[:2] == -1).all() and slots.cpu().numpy()[2] == 7  # no rank placed
+    cache.lookup_device(2, 1, dev(np.arange(5, dtype=np.int32)), slots_out=slots)
     with pytest.raises(moe.MoeError) as ei:
         moe.moe_sync_check()
     assert ei.value.code == -4
+    assert (slots.cpu().numpy() == -1).all()
     ev = cache.trace()
     assert len(ev) == 2 and cache.stats()["misses"] == 2
     with pytest.raises(moe.MoeError):
