@@ -56,8 +56,23 @@ __device__ __forceinline__ void wave_lds_sync() {
 // take the wave maximum of the lanes' heads -- the next entry in rank order --
 // and the owning lane advances its list.  COHERENT reads logits written by
 // other workgroups of the same launch.
+// The wave's loads of the logits: lane l takes entries l, l + 64, l + 128, l + 192, every load unconditional
+// (clamped index) so that the four are in flight together; entries past E are masked by topk_wave_ranked.
 template <bool COHERENT>
-__device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wout, int *err, TopkScratch *sc) {
+__device__ __forceinline__ void topk_wave_load(const float *z, int E, float *zv) {
+    const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+    for (int m = 0; m < 4; ++m) {
+        const int e = min(lane + kWave * m, E - 1);
+        if constexpr (COHERENT)
+            zv[m] = __hip_atomic_load(z + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        else
+            zv[m] = z[e];
+    }
+}
+
+__device__ void topk_wave_ranked(const float *zv, int E, int k, int32_t *ids, float *wout, int *err,
+                                 TopkScratch *sc) {
     const int lane = threadIdx.x & (kWave - 1);
     uint64_t c[4];
     bool bad = false;
@@ -65,11 +80,7 @@ __device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wou
     for (int m = 0; m < 4; ++m) {
         const int e = lane + kWave * m;
         const bool live = e < E;
-        float v;
-        if constexpr (COHERENT)
-            v = live ? __hip_atomic_load(z + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0.f;
-        else
-            v = live ? z[e] : 0.f;
+        const float v = live ? zv[m] : 0.f;
         if (live && !isfinite(v)) bad = true;
         // a live key is at least order_key(-FLT_MAX) << 32 > 0, so 0 never outranks a live entry
         c[m] = live ? (uint64_t(order_key(v)) << 32) | uint64_t(~uint32_t(e)) : 0ull;
@@ -130,6 +141,13 @@ __device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wou
     }
 }
 
+template <bool COHERENT>
+__device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wout, int *err, TopkScratch *sc) {
+    float zv[4];
+    topk_wave_load<COHERENT>(z, E, zv);
+    topk_wave_ranked(zv, E, k, ids, wout, err, sc);
+}
+
 // One wave per token.
 // With `pub` (one token), the wave also publishes its ids to host memory: the
 // ids, then a system-scope fence, then the sequence number `seq` in pub->seq,
@@ -172,12 +190,17 @@ __global__ __launch_bounds__(NT) void topk_lookup_kernel(const float *__restrict
     __shared__ TopkScratch sc;
     __shared__ int32_t ids_l[MOE_MAX_TOPK];
     __shared__ devres::DevLds<ROTARY, NT> L;
+    float zv[4];  // wave 0: the logits, loaded before the slot state so that ranking waits for them alone
+    if (threadIdx.x < kWave) topk_wave_load<false>(logits, E, zv);
     devres::DevStaged st;
     devres::dev_stage_issue<ROTARY, NT>(r, p, st);
     if (threadIdx.x == NT - 1 && r.clk) devres::clk_fold(r.clk);  // the previous filling launch's record
     const int lane = threadIdx.x & (kWave - 1);
     if (threadIdx.x < kWave) {
-        topk_wave<false>(logits, E, k, ids, wout, err, &sc);
+        topk_wave_ranked(zv, E, k, ids, wout, err, &sc);
+        // (keeps the staging below -- it waits for the slot-state loads -- after the ranking, which needs only
+        // the logits: the compiler may otherwise hoist the staging that both branches share above it)
+        asm volatile("" ::: "memory");
         const int id = lane < k ? sc.rid[lane] : 0;  // the ranked ids (-1 if non-finite)
         if (lane < k) ids_l[lane] = id;
         devres::dev_stage_lds<ROTARY, NT>(L, p, st);  // wave 0's share (it clears the presence bits)
