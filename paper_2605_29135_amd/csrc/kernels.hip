@@ -258,7 +258,8 @@ __global__ __launch_bounds__(kBlock) void router_logits_kernel(const float *__re
 #pragma unroll
     for (int c = 0; c < NCH; ++c) {
         const int col0 = (c * kWave + lane) * EPC;
-        wv[c] = ((FULL || col0 < H) && e < E) ? load16(row + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
+        // (a wave past E reads row 0 and stores nothing: no branch, so the loads are in flight together)
+        wv[c] = (FULL || col0 < H) ? load16(row + row_bytes_of(DT, col0)) : make_uint4(0, 0, 0, 0);
     }
     if constexpr (NORM) {
         float ss = 0.f;
