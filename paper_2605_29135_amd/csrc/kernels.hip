@@ -22,6 +22,13 @@ constexpr int kDownRows = 2; // output rows per wave in the down projection (fal
 // Output rows per wave of down_combine_lds_kernel: one (two, sharing the LDS reads of the activations,
 // measured slower on config 4: 6.62 against 6.39 us).
 constexpr int kDownWaveRows = 1;
+#ifndef MOE_DOWN_BLOCK
+#define MOE_DOWN_BLOCK 512
+#endif
+// Threads per block of down_combine_lds_kernel: each block stages the token's activations once for its
+// kDownBlock / 64 output rows (512: 6.66 -> 6.33 us for config 4's bf16 down, 4.36 -> 4.10 us for config 5's
+// int4 against 256; 1024 would leave half the compute units without a block at H = 2048).
+constexpr int kDownBlock = MOE_DOWN_BLOCK;
 constexpr int kDownSlots = 4; // 16-byte chunks per lane per pass of the down projection
 constexpr float kRmsEps = 1e-6f;
 constexpr int kRouterMfmaMinTokens = 16;  // from this many tokens on, bf16 routers run on the matrix cores
@@ -858,20 +865,20 @@ __global__ __launch_bounds__(kBlock) void down_combine_kernel(
 // back without branches (an invalid chunk loads from the pool base and is
 // masked), and only then are the staged values written to LDS.
 // One output row per wave, four per block, one block per (row tile, token).
-template <int DT, int NS, int R>
-__global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
+template <int DT, int NS, int R, int BT>
+__global__ __launch_bounds__(BT) void down_combine_lds_kernel(
     int T, int H, int I, int E, int k, const int32_t *__restrict__ ids,
     const int32_t *__restrict__ slot_of, const uint8_t *__restrict__ pool, size_t expert_bytes,
     const uint8_t *__restrict__ shared_w, size_t d_off, const float *__restrict__ act,
     float *__restrict__ y, int accumulate, FfnPlan plan) {
     constexpr int EPC = Fmt<DT>::EPC;
     // int4 weights: the activations are staged as fp16 pairs (stage8_i4h), [4][chunks] words then an
-    // (exponent shift, bias term) pair per chunk; thread f of staging round m = f / 256 packs dword f % 4
-    // of chunk f / 4.  Otherwise as fp32, [(k+1) x I / 4] float4.
+    // (exponent shift, bias term) pair per chunk; thread f of staging round m = f / BT packs dword f % 4
+    // of chunk f / 4, RH rounds covering the NS * 64 chunk slots.  Otherwise as fp32, [(k+1) x I / 4]
+    // float4, SM float4 per thread: (k+1) I <= NS * 64 * EPC <= SM * 4 * BT.
     constexpr bool HALF = DT == INT4;
-    // float4 staging loads per thread: (k+1) I <= NS * 64 * EPC = SM * 4 * 256
-    constexpr int SM = (NS * EPC + 15) / 16;
-    static_assert(!HALF || SM == 2 * NS, "int4 staging: two float4 per thread per round");
+    constexpr int RH = (NS * 256 + BT - 1) / BT;
+    constexpr int SM = HALF ? 2 * RH : (NS * EPC * kWave + 4 * BT - 1) / (4 * BT);
     extern __shared__ float4 aw4[];
     const int t = blockIdx.y;
     const int NE = k + (shared_w != nullptr);
@@ -882,8 +889,8 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
     float4 stage[SM];
     if constexpr (HALF) {
 #pragma unroll
-        for (int m = 0; m < NS; ++m) {
-            const int i = 2 * (threadIdx.x + m * kBlock);  // (routed4 is even: a pair lies on one side)
+        for (int m = 0; m < RH; ++m) {
+            const int i = 2 * (threadIdx.x + m * BT);  // (routed4 is even: a pair lies on one side)
             const bool in = i < n4;
             stage[2 * m] = in ? (i < routed4 ? src_routed[i] : src_shared[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
             stage[2 * m + 1] = in ? (i < routed4 ? src_routed[i + 1] : src_shared[i + 1]) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -891,7 +898,7 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
     } else {
 #pragma unroll
         for (int m = 0; m < SM; ++m) {
-            const int i = threadIdx.x + m * kBlock;
+            const int i = threadIdx.x + m * BT;
             stage[m] = i < n4 ? (i < routed4 ? src_routed[i] : src_shared[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
     }
@@ -939,7 +946,7 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
     // go to the same XCD, so the blocks that share a cache line of int4 row scales share one L2.
     const int nb = gridDim.x;
     const int tile = (nb & 7) ? int(blockIdx.x) : int(blockIdx.x & 7) * (nb >> 3) + int(blockIdx.x >> 3);
-    const int h0 = (tile * (kBlock / kWave) + (threadIdx.x / kWave)) * R;  // the wave's first row
+    const int h0 = (tile * (BT / kWave) + (threadIdx.x / kWave)) * R;  // the wave's first row
     const size_t rb = row_bytes_of(DT, I);
     const unsigned cpr = unsigned(rb / 16);  // chunks per expert row
     const unsigned total = unsigned(NE) * cpr;
@@ -975,8 +982,8 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
     int2 *xaux = reinterpret_cast<int2 *>(xs + 4 * total);
     if constexpr (HALF) {
 #pragma unroll
-        for (int m = 0; m < NS; ++m) {
-            const unsigned f = threadIdx.x + m * kBlock, g = f >> 2, q = f & 3u;
+        for (int m = 0; m < RH; ++m) {
+            const unsigned f = threadIdx.x + m * BT, g = f >> 2, q = f & 3u;
             const float v[8] = {stage[2 * m].x, stage[2 * m].y, stage[2 * m].z, stage[2 * m].w,
                                 stage[2 * m + 1].x, stage[2 * m + 1].y, stage[2 * m + 1].z, stage[2 * m + 1].w};
             int sh;
@@ -990,7 +997,7 @@ __global__ __launch_bounds__(kBlock) void down_combine_lds_kernel(
     } else {
 #pragma unroll
         for (int m = 0; m < SM; ++m) {
-            const int i = threadIdx.x + m * kBlock;
+            const int i = threadIdx.x + m * BT;
             if (i < n4) aw4[i] = stage[m];
         }
     }
@@ -1351,11 +1358,12 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
     if (e != hipSuccess) return e;
     if (!(parts & kFfnDown)) return hipSuccess;
     if (lds_down) {
-        const dim3 grid((H + 4 * kDownWaveRows - 1) / (4 * kDownWaveRows), T);
+        constexpr int rows = kDownBlock / kWave * kDownWaveRows;  // output rows per block
+        const dim3 grid((H + rows - 1) / rows, T);
 #define DN_CASE(DT, N)                                                                               \
         if (dtype == DT && ns == N)                                                                  \
-            return launch(down_combine_lds_kernel<DT, N, kDownWaveRows>, grid, kBlock, lds, s, T, H, I, E, k, \
-                          ids, slot_of, pl, expert_bytes, sw, doff, ws.act, y, acc, pl1);
+            return launch(down_combine_lds_kernel<DT, N, kDownWaveRows, kDownBlock>, grid, kDownBlock, lds, s, T, H, \
+                          I, E, k, ids, slot_of, pl, expert_bytes, sw, doff, ws.act, y, acc, pl1);
 #define DN_ALL(N) DN_CASE(F32, N) DN_CASE(BF16, N) DN_CASE(INT4, N)
         DN_ALL(1) DN_ALL(2) DN_ALL(3) DN_ALL(4) DN_ALL(6) DN_ALL(8) DN_ALL(9) DN_ALL(12) DN_ALL(16)
 #undef DN_ALL
