@@ -219,8 +219,9 @@ def measured_traffic(cfg=4):
                 kv[key.strip()] = val.strip()
     if kv.get("kernel_source_sha256") != ffn_source_hash():
         return None, "kernel source changed since the counters were taken"
-    return {"gateup": float(kv["gateup_hbm_bytes_per_launch"]),
-            "down": float(kv["down_hbm_bytes_per_launch"])}, path[len(ROOT) + 1:]
+    return {"gateup": float(kv["gateup_hbm_bytes_per_launch"]), "down": float(kv["down_hbm_bytes_per_launch"]),
+            "gateup_alg": float(kv["gateup_algorithmic_bytes"]), "down_alg": float(kv["down_algorithmic_bytes"])}, \
+        path[len(ROOT) + 1:]
 
 
 def ffn_roofline(gu_bytes, dn_bytes, ktimes, hbm, traffic, traffic_src, replays, n_launch, label):
@@ -229,6 +230,12 @@ def ffn_roofline(gu_bytes, dn_bytes, ktimes, hbm, traffic, traffic_src, replays,
     gu_s, dn_s, ffn_s = ktimes["gateup"] * 1e-3, ktimes["down"] * 1e-3, ktimes["ffn"] * 1e-3
     ffn_bytes = gu_bytes + dn_bytes
     ach = ffn_bytes / ffn_s / 1e9
+    if traffic is not None and (abs(traffic["gateup_alg"] - gu_bytes) > 0.01 * gu_bytes or
+                                abs(traffic["down_alg"] - dn_bytes) > 0.01 * dn_bytes):
+        # the counters were taken on launches of another size (e.g. every rank on the GPU, where a host tier
+        # leaves the GPU only its share)
+        traffic, traffic_src = None, (f"counters taken on launches of {traffic['gateup_alg']:.0f} + "
+                                      f"{traffic['down_alg']:.0f} B; these move {gu_bytes:.0f} + {dn_bytes:.0f} B")
     tr = None if traffic is None else traffic["gateup"] + traffic["down"]
     sub = lambda b, t, tb: {"achieved": b / t / 1e9, "frac": b / t / 1e9 / HBM_PEAK_GBPS, "bytes_per_launch": b,
                             "mean_launch_us": t * 1e6, "traffic": tb,
