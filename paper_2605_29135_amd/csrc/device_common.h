@@ -148,13 +148,13 @@ __device__ __forceinline__ half2_t as_half2(uint32_t v) { return __builtin_bit_c
 // flipped (q + 8 as an unsigned nibble) and the result is dropped into the mantissa of 1024 (nibble at
 // bits 0-3 of a half: 1024 + q + 8) or of 64 (bits 4-7, sixteen times the weight of a mantissa step:
 // 64 + q + 8).  So every nibble is exact, and the sum carries sum_x (1032 x) over the elements at even
-// nibble positions and sum_x (72 x) over the odd ones: int4_bias_sum gives that term for the chunk,
-// which the caller subtracts once per chunk.
+// nibble positions and sum_x (72 x) over the odd ones: stage8_i4h forms that bias term for the chunk when
+// it stages the activations, and the caller subtracts it once per chunk and row.
 constexpr uint32_t kNibLo = 0x000F000Fu, kMagicLo = 0x64086408u;  // 1024 + (q ^ 8) per half
 constexpr uint32_t kNibHi = 0x00F000F0u, kMagicHi = 0x54805480u;  // 64 + (q ^ 8) per half
 constexpr float kBiasLo = 1032.f, kBiasHi = 72.f;
 
-// sum of q * x over the eight nibbles of d, added to acc (x pairs as above, unscaled by the bias).
+// sum of (q + bias) * x over the eight nibbles of d, added to acc (x pairs as above).
 __device__ __forceinline__ float dot8_i4h(uint32_t d, uint4 xq, float acc) {
     const uint32_t t = d >> 8;
     acc = __builtin_amdgcn_fdot2(as_half2((d & kNibLo) ^ kMagicLo), as_half2(xq.x), acc, false);

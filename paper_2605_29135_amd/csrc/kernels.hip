@@ -61,21 +61,13 @@ __device__ __forceinline__ void wave_lds_sync() {
 // (order key of z, then the complement of its id, so that a larger key is
 // ahead); every lane sorts its (up to 4) keys in registers, then k rounds each
 // take the wave maximum of the lanes' heads -- the next entry in rank order --
-// and the owning lane advances its list.  COHERENT reads logits written by
-// other workgroups of the same launch.
+// and the owning lane advances its list.
 // The wave's loads of the logits: lane l takes entries l, l + 64, l + 128, l + 192, every load unconditional
 // (clamped index) so that the four are in flight together; entries past E are masked by topk_wave_ranked.
-template <bool COHERENT>
 __device__ __forceinline__ void topk_wave_load(const float *z, int E, float *zv) {
     const int lane = threadIdx.x & (kWave - 1);
 #pragma unroll
-    for (int m = 0; m < 4; ++m) {
-        const int e = min(lane + kWave * m, E - 1);
-        if constexpr (COHERENT)
-            zv[m] = __hip_atomic_load(z + e, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        else
-            zv[m] = z[e];
-    }
+    for (int m = 0; m < 4; ++m) zv[m] = z[min(lane + kWave * m, E - 1)];
 }
 
 __device__ void topk_wave_ranked(const float *zv, int E, int k, int32_t *ids, float *wout, int *err,
@@ -148,10 +140,9 @@ __device__ void topk_wave_ranked(const float *zv, int E, int k, int32_t *ids, fl
     }
 }
 
-template <bool COHERENT>
 __device__ void topk_wave(const float *z, int E, int k, int32_t *ids, float *wout, int *err, TopkScratch *sc) {
     float zv[4];
-    topk_wave_load<COHERENT>(z, E, zv);
+    topk_wave_load(z, E, zv);
     topk_wave_ranked(zv, E, k, ids, wout, err, sc);
 }
 
@@ -169,7 +160,7 @@ __global__ __launch_bounds__(kBlock) void topk_softmax_kernel(const float *__res
     const int wave = threadIdx.x / kWave;
     const int t = blockIdx.x * (kBlock / kWave) + wave;
     if (t >= T) return;
-    topk_wave<false>(logits + size_t(t) * E, E, k, ids + size_t(t) * k, wout + size_t(t) * k, err, &sc[wave]);
+    topk_wave(logits + size_t(t) * E, E, k, ids + size_t(t) * k, wout + size_t(t) * k, err, &sc[wave]);
     if (pub && t == 0) {
         const int lane = threadIdx.x & (kWave - 1);
         if (lane < k) {  // this lane wrote ids[lane] and wout[lane] itself
@@ -198,7 +189,7 @@ __global__ __launch_bounds__(NT) void topk_lookup_kernel(const float *__restrict
     __shared__ int32_t ids_l[MOE_MAX_TOPK];
     __shared__ devres::DevLds<ROTARY, NT> L;
     float zv[4];  // wave 0: the logits, loaded before the slot state so that ranking waits for them alone
-    if (threadIdx.x < kWave) topk_wave_load<false>(logits, E, zv);
+    if (threadIdx.x < kWave) topk_wave_load(logits, E, zv);
     devres::DevStaged st;
     devres::dev_stage_issue<ROTARY, NT>(r, p, st);
     if (threadIdx.x == NT - 1 && r.clk) devres::clk_fold(r.clk);  // the previous filling launch's record
@@ -666,9 +657,10 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     if constexpr (STAGE_X) {
       if (first) {
         // The token row is the same for every wave of the block: it is staged in LDS once, while the
-        // weight loads are in flight, as fp16 pairs (stage8_i4h: thread f packs the eight elements of dword f % 4 of
-        // chunk slot f / 4), transposed to [chunk][dword][lane] so that each read of a dword's word is 64
-        // consecutive 16-byte words; each chunk slot's exponent shift and bias term follow.
+        // weight loads are in flight, as fp16 pairs (stage8_i4h: thread f packs the eight elements of
+        // dword f % 4 of chunk slot f / 4), transposed to [chunk][dword][lane] so that each read of a
+        // dword's word is 64 consecutive 16-byte words; each chunk slot's exponent shift and bias term
+        // follow.
         extern __shared__ uint4 xsh[];
         int2 *xaux = reinterpret_cast<int2 *>(xsh + NCH * 4 * kWave);
         wp0 = single < P ? weights[single] : 1.f;
@@ -864,7 +856,7 @@ __global__ __launch_bounds__(kBlock) void down_combine_kernel(
 // thread issues its staging loads first, then the weight loads go out back to
 // back without branches (an invalid chunk loads from the pool base and is
 // masked), and only then are the staged values written to LDS.
-// One output row per wave, four per block, one block per (row tile, token).
+// R output rows per wave, BT / 64 waves per block, one block per (row tile, token).
 template <int DT, int NS, int R, int BT>
 __global__ __launch_bounds__(BT) void down_combine_lds_kernel(
     int T, int H, int I, int E, int k, const int32_t *__restrict__ ids,
