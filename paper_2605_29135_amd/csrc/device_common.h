@@ -88,6 +88,12 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // 16-byte load with the nontemporal hint, for expert weights that are read once
 // per call: a streamed read of tens of MB then does not displace what the next
 // kernels reuse, and reaches a higher fraction of HBM bandwidth.
+// One float4 read as a native vector (a float4 copied as an aggregate can end up in private memory).
+__device__ __forceinline__ float4 load_f4(const float4 *p) {
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(p);
+    return make_float4(__uint_as_float(v.x), __uint_as_float(v.y), __uint_as_float(v.z), __uint_as_float(v.w));
+}
+
 __device__ __forceinline__ uint4 load16_stream(const uint8_t *p) {
     const u32x4 v = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(p));
     return make_uint4(v.x, v.y, v.z, v.w);

@@ -535,6 +535,14 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     const int *pairs = nullptr;
     unsigned long long *clk = nullptr;  // a filling launch: its blocks stamp the fill clock
     unsigned long long t_fill = 0;      // when this block began filling
+    int i = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
+    const int P = T * k;
+    // One token whose slots the device lookup wrote: every load that the blob's address depends on (the
+    // rank's slot, the fill count, the fill list across the wave's lanes) is issued at once, and the token's
+    // x after them, so that one wait covers the chain and x stays in flight into the weight stream.
+    int s_ld = 0, nf_ld = 0, fslot = -1;
+    long long fsrc = 0;
+    bool dev_slot = false;
     if constexpr (ONE_TOKEN) {
         clk = plan.fill.n ? plan.fill.clk : nullptr;
         if (plan.fill.n && g == int(gridDim.y) - 1) {
@@ -544,66 +552,31 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
             if (t0) devres::clk_record_fill(clk, t0, devres::clk_now());
             return;
         }
-        if (g < k && plan.n) {
-            // slots known on the host: no device lookups.  Selected with the block-uniform rank so that
-            // the offsets stay argument (scalar) loads rather than one indexed load before the weights.
-            long long off = plan.off[0];
-#pragma unroll
-            for (int j = 1; j < MOE_MAX_TOPK; ++j)
-                if (g == j) off = plan.off[j];
-            if (off < 0) return;  // a rank the host tier computes
-            blob = pool + off;
-        } else if (g < k) {
-            int s;
-            if (plan.rank_slot) {  // the device lookup's slot for this rank (it flagged bad ids itself)
-                s = plan.rank_slot[g];
-            } else {
-                const int e = ids[g];
-                if (e < 0 || e >= E) {
-                    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, kErrRange);
-                    return;
-                }
-                s = slot_of ? slot_of[e] : e;
-            }
-            if (s < 0) {
-                if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, kErrNotResident);
-                return;
-            }
-            blob = pool + size_t(s) * expert_bytes;
-            if (plan.fill.n) {
-                const int nf = min(plan.fill.n[0], MOE_MAX_TOPK);
-                for (int f = 0; f < nf; ++f)
-                    if (plan.fill.slot[f] == s) {
-                        dst = plan.fill.pool + size_t(s) * expert_bytes;
-                        blob = plan.fill.host + plan.fill.src[f];
-                        break;
-                    }
-                if (dst) {
-                    if (int(blockIdx.x) >= plan.fill.blocks) return;
-                    istride = plan.fill.blocks * (kBlock / kWave);
-                    if (clk) t_fill = devres::clk_now();
-                }
-            }
-        } else {
-            blob = shared_w;
-        }
         single = g;  // pair index: rank g, or T*k + 0 = k for the shared expert
+        dev_slot = g < k && !plan.n;
+        if (dev_slot) {
+            if (plan.fill.n) {
+                nf_ld = plan.fill.n[0];
+                if (lane < min(E, MOE_MAX_TOPK)) {  // (the fill list holds E entries)
+                    fslot = plan.fill.slot[lane];
+                    fsrc = plan.fill.src[lane];
+                }
+            }
+            s_ld = plan.rank_slot ? plan.rank_slot[g] : ids[g];
+        }
     } else {
         if (g >= groups[0]) return;
-        const int s = group_slot(groups, T, k)[g];
-        pstart = group_start(groups, T, k)[g];
-        pcount = group_count(groups, T, k)[g];
-        pairs = group_pairs(groups, T, k);
-        blob = s == -2 ? shared_w : pool + size_t(s) * expert_bytes;
     }
-    int i = blockIdx.x * (kBlock / kWave) + (threadIdx.x / kWave);
     if (!STAGE_X && i >= I) return;  // when x is staged, every wave joins the block's staging below
-    const int P = T * k;
     float xv[STAGE_X ? 1 : NCH][EPC];
     uint4 xq[STAGE_X ? NCH : 1][4];       // staged int4 path: the chunk's activations as fp16 pairs
     float xbias[NCH];                     // ... the chunk's bias term
     int xsh_[NCH];                        // ... and its exponent shift
-    float wp0;  // combine weight of the first pair (1 for the shared expert)
+    float wp0 = 1.f;  // combine weight of the first pair (1 for the shared expert)
+    if constexpr (!ONE_TOKEN) {
+        pstart = group_start(groups, T, k)[g];
+        pairs = group_pairs(groups, T, k);
+    }
     if constexpr (!STAGE_X) {
         // The first pair's activations are loaded before the weight stream: loads
         // retire in issue order, so waiting for x never waits for the weights.
@@ -633,6 +606,58 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
             xa[r][0] = in ? xt4[2 * f] : make_float4(0.f, 0.f, 0.f, 0.f);
             xa[r][1] = in ? xt4[2 * f + 1] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
+    }
+    if constexpr (ONE_TOKEN) {
+        // (the loaded values pass through an empty asm after the x loads, so that no use of them -- and no
+        // wait for them -- is scheduled before x is in flight)
+        if (dev_slot) asm volatile("" : "+v"(s_ld), "+v"(nf_ld), "+v"(fslot), "+v"(fsrc)::"memory");
+        if (g < k && plan.n) {
+            // slots known on the host: no device lookups.  Selected with the block-uniform rank so that
+            // the offsets stay argument (scalar) loads rather than one indexed load before the weights.
+            long long off = plan.off[0];
+#pragma unroll
+            for (int j = 1; j < MOE_MAX_TOPK; ++j)
+                if (g == j) off = plan.off[j];
+            if (off < 0) return;  // a rank the host tier computes
+            blob = pool + off;
+        } else if (dev_slot) {
+            int s;
+            if (plan.rank_slot) {  // the device lookup's slot for this rank (it flagged bad ids itself)
+                s = s_ld;
+            } else {
+                const int e = s_ld;
+                if (e < 0 || e >= E) {
+                    if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, kErrRange);
+                    return;
+                }
+                s = slot_of ? slot_of[e] : e;
+            }
+            if (s < 0) {
+                if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, kErrNotResident);
+                return;
+            }
+            blob = pool + size_t(s) * expert_bytes;
+            if (plan.fill.n) {
+                // the lanes holding a fill of this slot (at most one: a step fills a slot once)
+                const unsigned long long m = __ballot(lane < min(nf_ld, MOE_MAX_TOPK) && fslot == s);
+                if (m) {
+                    const int f = __ffsll((long long)m) - 1;
+                    const unsigned lo = __builtin_amdgcn_readlane(unsigned(fsrc), f);
+                    const unsigned hi = __builtin_amdgcn_readlane(unsigned((unsigned long long)fsrc >> 32), f);
+                    dst = plan.fill.pool + size_t(s) * expert_bytes;
+                    blob = plan.fill.host + (long long)(((unsigned long long)hi << 32) | lo);
+                    if (int(blockIdx.x) >= plan.fill.blocks) return;
+                    istride = plan.fill.blocks * (kBlock / kWave);
+                    if (clk) t_fill = devres::clk_now();
+                }
+            }
+        } else {
+            blob = shared_w;
+        }
+    } else {
+        const int s = group_slot(groups, T, k)[g];
+        pcount = group_count(groups, T, k)[g];
+        blob = s == -2 ? shared_w : pool + size_t(s) * expert_bytes;
     }
     const size_t rb = row_bytes_of(DT, H);
     for (bool first = true;; first = false) {
@@ -664,6 +689,15 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
         extern __shared__ uint4 xsh[];
         int2 *xaux = reinterpret_cast<int2 *>(xsh + NCH * 4 * kWave);
         wp0 = single < P ? weights[single] : 1.f;
+        // x passes through an empty asm after the weight loads: otherwise the compiler hoists the staging's
+        // first steps above the loop, and their wait for x holds the weight loads back
+#pragma unroll
+        for (int r = 0; r < NCH; ++r)
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                float &a = xa[r][h].x, &b = xa[r][h].y, &c = xa[r][h].z, &d = xa[r][h].w;
+                asm volatile("" : "+v"(a), "+v"(b), "+v"(c), "+v"(d)::"memory");
+            }
 #pragma unroll
         for (int r = 0; r < NCH; ++r) {  // NCH * 64 chunk slots x 4 dwords = NCH rounds of the block
             const int f = r * kBlock + threadIdx.x, gs = f >> 2, q = f & 3;
@@ -874,7 +908,26 @@ __global__ __launch_bounds__(BT) void down_combine_lds_kernel(
     extern __shared__ float4 aw4[];
     const int t = blockIdx.y;
     const int NE = k + (shared_w != nullptr);
-    // 1. staging loads (independent of everything else)
+    const int lane = threadIdx.x & (kWave - 1), wid = threadIdx.x / kWave;
+    // 1. where the entries live, resolved by every wave for itself (lane j < NE: entry j) into its own LDS
+    // table, so that no block barrier stands before the weight loads.  Entry j: byte offset of its blob from
+    // `pool` (the shared expert's too, so that every address derives from a kernel argument and stays a global
+    // load), or kAbsent when it contributes nothing.  Its loads go out before the staging loads, whose wait they
+    // then skip.  (Vector loads: the ids and the slot table are written by earlier kernels on the stream.)
+    __shared__ long long ent_tab[BT / kWave][MOE_MAX_TOPK + 1];
+    // Each lane loads the entry of rank min(lane, k - 1) before anything else: with host-known slots its byte
+    // offset among the kernel arguments, otherwise its slot (device lookup) or expert id from one uniformly
+    // chosen array.
+    const int jl = min(lane, k - 1);
+    long long o_ld = -1;  // with host-known slots: the rank's byte offset (-1: a rank the host tier computes)
+    int v_ld = -1;        // otherwise: the rank's slot or expert id
+    if (plan.n)
+        o_ld = plan.off[jl];
+    else
+        v_ld = (plan.rank_slot ? plan.rank_slot : ids + size_t(t) * k)[jl];
+    // 2. staging loads, unconditional (an index past the activations reads the token's first ones, which are
+    // never written to LDS: the chunks there lie past `total`), so that the wait for the entries below can
+    // count them as still in flight.  (No select on the loaded value: it would turn each load into a branch.)
     const int n4 = NE * I / 4, routed4 = k * I / 4;
     const float4 *src_routed = reinterpret_cast<const float4 *>(act) + size_t(t) * routed4;
     const float4 *src_shared = reinterpret_cast<const float4 *>(act) + (size_t(T) * k + t) * (I / 4) - routed4;
@@ -883,57 +936,41 @@ __global__ __launch_bounds__(BT) void down_combine_lds_kernel(
 #pragma unroll
         for (int m = 0; m < RH; ++m) {
             const int i = 2 * (threadIdx.x + m * BT);  // (routed4 is even: a pair lies on one side)
-            const bool in = i < n4;
-            stage[2 * m] = in ? (i < routed4 ? src_routed[i] : src_shared[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
-            stage[2 * m + 1] = in ? (i < routed4 ? src_routed[i + 1] : src_shared[i + 1]) : make_float4(0.f, 0.f, 0.f, 0.f);
+            const float4 *sp = i < n4 ? (i < routed4 ? src_routed : src_shared) + i : src_routed;
+            stage[2 * m] = load_f4(sp);
+            stage[2 * m + 1] = load_f4(sp + 1);
         }
     } else {
 #pragma unroll
         for (int m = 0; m < SM; ++m) {
             const int i = threadIdx.x + m * BT;
-            stage[m] = i < n4 ? (i < routed4 ? src_routed[i] : src_shared[i]) : make_float4(0.f, 0.f, 0.f, 0.f);
+            stage[m] = load_f4(i < n4 ? (i < routed4 ? src_routed : src_shared) + i : src_routed);
         }
     }
-    // 2. where the entries live.  Entry j: byte offset of its blob from `pool` (the shared expert's too, so
-    // that every address derives from a kernel argument and stays a global load) and whether it contributes.
-    // (Vector loads: the ids and the slot table are written by earlier kernels on the stream.)
-    __shared__ long long ent_off[MOE_MAX_TOPK + 1];
-    __shared__ int ent_ok[MOE_MAX_TOPK + 1];
-    if (threadIdx.x < NE) {
-        const int j = threadIdx.x;
-        int ok = 0;
-        long long off = 0;
-        if (j < k) {
+    // (the entries' values pass through an empty asm after the staging loads: no use of them, and no wait
+    // for them, is scheduled before those are in flight)
+    asm volatile("" : "+v"(o_ld), "+v"(v_ld)::"memory");
+    constexpr long long kAbsent = -0x7fffffffffffffffLL - 1;  // (the shared expert's offset may be negative)
+    if (lane < NE) {
+        long long off = kAbsent;
+        if (lane < k) {
             if (plan.n) {
-                long long o = plan.off[0];  // (argument loads, selected by lane: no indexed load)
-#pragma unroll
-                for (int jj = 1; jj < MOE_MAX_TOPK; ++jj)
-                    if (j == jj) o = plan.off[jj];
-                ok = o >= 0;  // (a rank the host tier computes is skipped)
-                off = ok ? o : 0;
-            } else if (plan.rank_slot) {
-                const int sl = plan.rank_slot[j];  // (one token: t == 0)
-                ok = sl >= 0;
-                off = ok ? (long long)sl * (long long)expert_bytes : 0;
+                if (o_ld >= 0) off = o_ld;
             } else {
-                const int e = ids[t * k + j];
-                if (e >= 0 && e < E) {
-                    const int sl = slot_of ? slot_of[e] : e;
-                    if (sl >= 0) {
-                        ok = 1;
-                        off = (long long)sl * (long long)expert_bytes;
-                    }
+                int sl = v_ld;
+                if (!plan.rank_slot) {  // an expert id: checked, then its slot (a dependent load, on this path only,
+                    // waited for inside it so that the common path below does not wait for the staging loads)
+                    sl = (sl >= 0 && sl < E) ? (slot_of ? slot_of[sl] : sl) : -1;
+                    asm volatile("" : "+v"(sl));
                 }
+                if (sl >= 0) off = (long long)sl * (long long)expert_bytes;
             }
         } else {
-            ok = 1;
             off = (long long)(shared_w - pool);
         }
-        ent_off[j] = off;
-        ent_ok[j] = ok;
+        ent_tab[wid][lane] = off;
     }
-    __syncthreads();
-    const int lane = threadIdx.x & (kWave - 1);
+    wave_lds_sync();
     // 3. weight loads of this wave's R output rows.  Workgroup b runs on XCD b mod 8: consecutive row tiles
     // go to the same XCD, so the blocks that share a cache line of int4 row scales share one L2.
     const int nb = gridDim.x;
@@ -949,9 +986,9 @@ __global__ __launch_bounds__(BT) void down_combine_lds_kernel(
 #pragma unroll
     for (int s = 0; s < NS; ++s) {
         const bool in = unsigned(s * kWave + lane) < total;
-        const unsigned jj = in ? j : 0u;
-        ok[s] = in && ent_ok[jj];
-        const uint8_t *blob = pool + (ok[s] ? ent_off[jj] : 0);
+        const long long o = ent_tab[wid][in ? j : 0u];
+        ok[s] = in && o != kAbsent;
+        const uint8_t *blob = pool + (ok[s] ? o : 0);
 #pragma unroll
         for (int r = 0; r < R; ++r) {
             const int h = min(h0 + r, H - 1);
