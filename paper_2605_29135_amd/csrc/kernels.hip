@@ -631,6 +631,7 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
                     return;
                 }
                 s = slot_of ? slot_of[e] : e;
+                asm volatile("" : "+v"(s));  // (the wait for this dependent load stays on this path)
             }
             if (s < 0) {
                 if (blockIdx.x == 0 && threadIdx.x == 0) atomicOr(err, kErrNotResident);
@@ -772,7 +773,7 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
         ua = wave_sum(ua);
         // the pair's combine weight is folded in here
         const float wp = q == 0 ? wp0 : (p < P ? weights[p] : 1.f);
-        if (lane == 0) act[size_t(p) * I + i] = wp * (ga / (1.f + expf(-ga)) * ua);
+        if (lane == 0) act[size_t(p) * I + i] = wp * (ga * __builtin_amdgcn_rcpf(1.f + __expf(-ga)) * ua);
     }
     if (!istride) break;  // block-uniform; no barrier follows the first pass
     i += istride;
