@@ -88,6 +88,16 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 // 16-byte load with the nontemporal hint, for expert weights that are read once
 // per call: a streamed read of tens of MB then does not displace what the next
 // kernels reuse, and reaches a higher fraction of HBM bandwidth.
+// A word that an earlier kernel on the stream wrote, loaded through a vector register even when the address is
+// uniform: the pointer passes through an empty asm (in the global address space, so the load stays a global
+// load), which keeps the compiler from issuing it through the scalar cache.
+__device__ __forceinline__ int load_stream_word(const int32_t *p) {
+    typedef const __attribute__((address_space(1))) int32_t gword;
+    gword *q = (gword *)p;
+    asm volatile("" : "+v"(q));
+    return *q;
+}
+
 // One float4 read as a native vector (a float4 copied as an aggregate can end up in private memory).
 __device__ __forceinline__ float4 load_f4(const float4 *p) {
     const u32x4 v = *reinterpret_cast<const u32x4 *>(p);

@@ -555,14 +555,15 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
         single = g;  // pair index: rank g, or T*k + 0 = k for the shared expert
         dev_slot = g < k && !plan.n;
         if (dev_slot) {
+            // (the block-uniform words go through vector loads: earlier kernels on the stream wrote them)
             if (plan.fill.n) {
-                nf_ld = plan.fill.n[0];
+                nf_ld = load_stream_word(plan.fill.n);
                 if (lane < min(E, MOE_MAX_TOPK)) {  // (the fill list holds E entries)
                     fslot = plan.fill.slot[lane];
                     fsrc = plan.fill.src[lane];
                 }
             }
-            s_ld = plan.rank_slot ? plan.rank_slot[g] : ids[g];
+            s_ld = load_stream_word((plan.rank_slot ? plan.rank_slot : ids) + g);
         }
     } else {
         if (g >= groups[0]) return;
