@@ -522,10 +522,13 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     const uint8_t *__restrict__ shared_w, const float *__restrict__ weights, int *groups,
     float *__restrict__ act, int *err, FfnPlan plan) {
     constexpr int EPC = Fmt<DT>::EPC;
-    // One int4 token: a wave streams 2 KiB of weights (two rows at H = 2048) but would read 8 KiB of
-    // x, so the block stages x in LDS once.  With bf16 or f32 weights the wave's x read is no larger
-    // than its weight stream and staging only adds a barrier.
+    // One token: the block stages x in LDS once instead of every wave reading it.  int4 (a wave streams
+    // 2 KiB of weights but would read 8 KiB of x): as fp16 pairs with per-chunk scales (STAGE_X).  bf16:
+    // as fp32, read chunk by chunk just before its products, which frees the registers that held the
+    // wave's x (STAGE_XF; config 4's gate/up 10.5 -> 9.95 us).  f32 weights keep per-wave x.
     constexpr bool STAGE_X = ONE_TOKEN && DT == INT4;
+    constexpr bool STAGE_XF = ONE_TOKEN && DT == BF16;
+    constexpr int NXF = (NCH * kWave * EPC / 4 + kBlock - 1) / kBlock;  // float4 of x per thread (STAGE_XF)
     const int lane = threadIdx.x & (kWave - 1);
     const int g = blockIdx.y;
     const uint8_t *blob;
@@ -568,8 +571,9 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     } else {
         if (g >= groups[0]) return;
     }
-    if (!STAGE_X && i >= I) return;  // when x is staged, every wave joins the block's staging below
-    float xv[STAGE_X ? 1 : NCH][EPC];
+    if (!STAGE_X && !STAGE_XF && i >= I) return;  // when x is staged, every wave joins the block's staging below
+    float xv[STAGE_X || STAGE_XF ? 1 : NCH][EPC];
+    float4 xf[STAGE_XF ? NXF : 1];  // STAGE_XF: this thread's share of x, loaded before the weight stream
     uint4 xq[STAGE_X ? NCH : 1][4];       // staged int4 path: the chunk's activations as fp16 pairs
     float xbias[NCH];                     // ... the chunk's bias term
     int xsh_[NCH];                        // ... and its exponent shift
@@ -578,7 +582,13 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
         pstart = group_start(groups, T, k)[g];
         pairs = group_pairs(groups, T, k);
     }
-    if constexpr (!STAGE_X) {
+    if constexpr (STAGE_XF) {
+        const float4 *xt4 = reinterpret_cast<const float4 *>(x);  // (one token)
+        wp0 = single < P ? weights[single] : 1.f;
+#pragma unroll
+        for (int r = 0; r < NXF; ++r) xf[r] = load_f4(xt4 + min(r * kBlock + int(threadIdx.x), H / 4 - 1));
+    }
+    if constexpr (!STAGE_X && !STAGE_XF) {
         // The first pair's activations are loaded before the weight stream: loads
         // retire in issue order, so waiting for x never waits for the weights.
         const int p0 = ONE_TOKEN ? single : pairs[pstart];
@@ -681,6 +691,16 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
             su[c] = in ? bf16_bits_to_float(sc[size_t(2 * iw + 1) * groups_per_row + col0 / 128]) : 0.f;
         }
     }
+    if constexpr (STAGE_XF) {
+      if (first) {  // x into LDS while the weight loads are in flight
+        extern __shared__ float4 xsf[];
+#pragma unroll
+        for (int r = 0; r < NXF; ++r)
+            if (r * kBlock + int(threadIdx.x) < H / 4) xsf[r * kBlock + threadIdx.x] = xf[r];
+        __syncthreads();
+        if (i >= I) return;
+      }
+    }
     if constexpr (STAGE_X) {
       if (first) {
         // The token row is the same for every wave of the block: it is staged in LDS once, while the
@@ -746,12 +766,12 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
     }
     for (int q = 0; q < pcount; ++q) {
         const int p = ONE_TOKEN ? single : pairs[pstart + q];
-        if (!STAGE_X && q > 0) {  // (a staged token is one pair)
+        if (!STAGE_X && !STAGE_XF && q > 0) {  // (a staged token is one pair)
             const float *xt = x + size_t(p < P ? p / k : p - P) * H;
 #pragma unroll
             for (int c = 0; c < NCH; ++c) {
                 const int col0 = (c * kWave + lane) * EPC;
-                if ((FULL || col0 < H)) load_x<DT>(xt, col0, xv[STAGE_X ? 0 : c]);
+                if ((FULL || col0 < H)) load_x<DT>(xt, col0, xv[STAGE_X || STAGE_XF ? 0 : c]);
             }
         }
         float ga = 0.f, ua = 0.f;
@@ -761,7 +781,23 @@ __global__ __launch_bounds__(kBlock) void gateup_kernel(
                 ga += ldexpf((chunk_dot_i4h(wg[c], xq[c]) - xbias[c]) * sg[c], xsh_[c]);
                 ua += ldexpf((chunk_dot_i4h(wu[c], xq[c]) - xbias[c]) * su[c], xsh_[c]);
             } else {
-                float dg = chunk_dot<DT>(wg[c], xv[c]), du = chunk_dot<DT>(wu[c], xv[c]);
+                float xl[EPC];  // this chunk's x: from LDS (STAGE_XF) or the wave's registers
+                if constexpr (STAGE_XF) {
+                    extern __shared__ float4 xsf[];
+                    const int col0 = (c * kWave + lane) * EPC;
+#pragma unroll
+                    for (int h = 0; h < EPC / 4; ++h) {
+                        const float4 v = (FULL || col0 < H) ? xsf[col0 / 4 + h] : make_float4(0.f, 0.f, 0.f, 0.f);
+                        xl[4 * h] = v.x;
+                        xl[4 * h + 1] = v.y;
+                        xl[4 * h + 2] = v.z;
+                        xl[4 * h + 3] = v.w;
+                    }
+                } else {
+#pragma unroll
+                    for (int h = 0; h < EPC; ++h) xl[h] = xv[STAGE_XF ? 0 : c][h];
+                }
+                float dg = chunk_dot<DT>(wg[c], xl), du = chunk_dot<DT>(wu[c], xl);
                 if constexpr (DT == INT4) {
                     dg *= sg[c];
                     du *= su[c];
@@ -1352,7 +1388,8 @@ hipError_t launch_expert_ffn(const float *x, int T, int H, int I, int E, int k, 
     const int nch = chunks_per_row(H, dtype);
     // One-token int4 x staging covers every lane's chunk slot: [nch][4][64] words of fp16 pairs, then an
     // (exponent shift, bias term) pair per slot.
-    const size_t x_lds = dtype == INT4 ? size_t(nch) * kWave * (4 * 16 + 8) : 0;
+    // (bf16: the token's x as fp32)
+    const size_t x_lds = dtype == INT4 ? size_t(nch) * kWave * (4 * 16 + 8) : dtype == BF16 ? size_t(H) * 4 : 0;
     // The down kernel: the LDS form when a token's k (+1) activation rows fit in LDS and NS chunks per lane
     // cover them, else the plain one.
     const size_t doff = down_offset(H, I, dtype);
