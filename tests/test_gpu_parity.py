@@ -193,8 +193,9 @@ def test_ffn_grouping_duplicates_slots_and_accumulate(dtype):
         check_ffn(wl, x, ids, w, ex, None, accumulate=True)
 
 
-@pytest.mark.parametrize("dtype,H", [(synth.F32, 384), (synth.BF16, 256), (synth.BF16, 640), (synth.INT4G128, 256),
-                                     (synth.INT4G128, 2176), (synth.INT4G128, 4224)])
+@pytest.mark.parametrize("dtype,H", [(synth.F32, 384), (synth.BF16, 256), (synth.BF16, 640), (synth.BF16, 3968),
+                                     (synth.BF16, 4096), (synth.INT4G128, 256), (synth.INT4G128, 2176),
+                                     (synth.INT4G128, 4224)])
 def test_ffn_one_token_partial_chunks(dtype, H):
     """One-token decode at widths where the last 64-lane chunk of a row is only partly filled."""
     wl = synth.Workload("one-token widths", H=H, E=12, k=3, I=256, dtype=dtype, router_dtype=synth.F32, shared=True,
