@@ -246,7 +246,10 @@ def ffn_roofline(gu_bytes, dn_bytes, ktimes, hbm, traffic, traffic_src, replays,
             "traffic_source": traffic_src, "bytes_per_launch": ffn_bytes, "mean_launch_us": ffn_s * 1e6,
             "timing": f"the last step's {n_launch} layers' gate/up and down launches (same arguments, every expert "
                       f"resident: the replays fill nothing, while a budgeted step's own gate/up launch also streams "
-                      f"its misses) in one HIP graph, replayed {replays}x between HIP events; per layer",
+                      f"its misses) in one HIP graph, replayed {replays}x between HIP events; per layer"
+                      + (f"; the graph repeats the layers' launches {-(-32 // n_launch)}x (at least 32 launches), "
+                         f"repeat r reading experts (e + r) mod E of the step's experts e when every expert is "
+                         f"resident" if n_launch < 32 else ""),
             "practical_ceiling_GBps": hbm["launch_GBps"], "frac_of_practical": ach / hbm["launch_GBps"],
             "gateup": sub(gu_bytes, gu_s, None if traffic is None else traffic["gateup"]),
             "down": sub(dn_bytes, dn_s, None if traffic is None else traffic["down"])}
@@ -755,6 +758,8 @@ def main():
     ktimes = {name: stack.kernel_time(w, args.replays) for w, name in enumerate(["route", "gateup", "down", "ffn"])}
     if att is not None:
         ktimes["attention"] = stack.kernel_time(4, args.replays)
+    if not budgeted and L < 32:  # the same expert FFN re-reading the step's own experts in every repeat
+        ktimes["ffn_same_experts"] = stack.kernel_time(8 + 3, args.replays)
     moe.moe_sync_check(stream)
 
     tok_s = args.steps * T / elapsed
@@ -792,6 +797,11 @@ def main():
     traffic, traffic_src = measured_traffic(4) if args.config == 4 else (None, "no counter summary")
     roof = ffn_roofline(gu_bytes, dn_bytes, ktimes, hbm, traffic, traffic_src, args.replays, L,
                         f"{synth.DTYPE_NAMES[wl.dtype]} decode, T={T}")
+    if "ffn_same_experts" in ktimes:
+        ach_same = (gu_bytes + dn_bytes) / (ktimes["ffn_same_experts"] * 1e-3) / 1e9
+        roof["same_experts_every_launch"] = {
+            "achieved": ach_same, "frac": ach_same / HBM_PEAK_GBPS, "mean_launch_us": ktimes["ffn_same_experts"] * 1e3,
+            "note": "every repeat re-reads the step's own experts, which the last-level cache may then hold"}
 
     bound = residency_bound(moe, cache, E, st1["capacity"], policy=args.policy) if budgeted and not hybrid else None
     host_tier = None

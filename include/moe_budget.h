@@ -543,8 +543,14 @@ MOE_API int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *
  * arguments, in step order, captured into one HIP graph on a private stream
  * (ordered after `stream`); the graph is replayed n times between two HIP
  * events (multi-token steps under a budget replay only the last layer, whose
- * slots are still current).  Outputs go to scratch buffers: the residual
- * stream and the residency state are untouched.  Synchronous. */
+ * slots are still current).  A graph of fewer than 32 launches repeats the
+ * sequence until it holds at least 32 (R repeats); in a stack without a budget
+ * (every expert resident) repeat r of an expert launch (which 1-3) reads
+ * experts (e + r) mod E in place of the step's experts e, so that the repeats
+ * stream many experts instead of re-reading a few from the last-level cache;
+ * which + 8 (9, 10, 11) keeps the step's own experts in every repeat.
+ * Outputs go to scratch buffers: the residual stream and the residency state
+ * are untouched.  Synchronous. */
 MOE_API int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *mean_ms);
 
 /* Offline residency bound (host call; no device work).  For a demand trace in

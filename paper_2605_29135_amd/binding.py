@@ -521,7 +521,9 @@ class MoeStack:
 
     def kernel_time(self, which: int, n: int = 200, stream=None) -> float:
         """Mean ms of one launch of kernel `which` (0 route, 1 gate/up, 2 down, 3 the whole expert FFN as
-        the decode step issues it), each layer's launch of the last step replayed n times from a graph."""
+        the decode step issues it, 4 attention), each layer's launch of the last step replayed n times from a
+        graph (repeated to at least 32 launches; a stack without a budget rotates the repeats' experts unless
+        8 is added to `which`)."""
         ms = C.c_double()
         _check(lib().moe_stack_kernel_time(self._h, which, n, _stream(stream), C.byref(ms)), "moe_stack_kernel_time")
         return ms.value

@@ -619,7 +619,9 @@ int moe_stack_prefill(moe_stack *s, int step, float *x, int T, int32_t *ids_out,
 }
 
 int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *mean_ms) {
-    if (!s || !mean_ms || which < 0 || which > 4 || n < 1)
+    const bool same_set = which >= 8;  // flag: a preloaded stack's repeats keep the step's own experts
+    if (same_set) which -= 8;
+    if (!s || !mean_ms || which < 0 || which > 4 || n < 1 || (same_set && (which < 1 || which > 3)))
         return moe::fail(MOE_ERR_INVALID_ARG, "kernel_time: bad argument");
     if (which == 4 && (!s->attn || s->last_attn_pos < 0))
         return moe::fail(MOE_ERR_INVALID_ARG, "kernel_time: no attention block, or no decode step yet");
@@ -653,17 +655,53 @@ int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *
     // graph on a private stream (so that host launch overhead does not starve
     // the device) and replayed n times.  The last layer's normalised input
     // feeds every launch; results go to scratch.
+    // Multi-token steps under a budget read the device slot table, where an
+    // earlier layer's experts may have been evicted since: replay only the
+    // last layer then (T == 1 steps carry their slots with them).
+    const int l0 = (s->budgeted && T > 1) ? L - 1 : 0;
+    // A graph of a few launches would time the graph launch, not the kernels:
+    // each layer's launch is repeated until the graph holds at least 32.  In a
+    // preloaded stack every expert of a layer is resident, so repeat r of an
+    // expert launch reads experts (e + r) mod E of the step's experts e: the
+    // launches then stream an E-expert working set (beyond the last-level
+    // cache for the large layers) instead of re-reading the same few experts.
+    const int reps = (32 + (L - l0) - 1) / (L - l0);
+    const bool rotate = !s->budgeted && !same_set && which >= 1 && which <= 3 && reps > 1;
+    std::vector<int32_t> rot_host;
+    int32_t *rot_dev = nullptr;
+    hipError_t e = hipSuccess;
+    if (rotate) {
+        // [rep][layer][T * k]
+        const size_t nid = size_t(T) * d.k, nl = size_t(L - l0);
+        rot_host.resize(nid * nl * size_t(reps));
+        e = hipStreamSynchronize(strm);
+        for (size_t l = 0; l < nl && e == hipSuccess; ++l)
+            e = hipMemcpy(rot_host.data() + l * nid, s->last[size_t(l0) + l].ids, sizeof(int32_t) * nid,
+                          hipMemcpyDeviceToHost);
+        for (int r = 1; r < reps && e == hipSuccess; ++r)
+            for (size_t j = 0; j < nl * nid; ++j) {
+                const int32_t id = rot_host[j];  // invalid ids (outside [0, E)) stay as they are
+                rot_host[size_t(r) * nl * nid + j] = id >= 0 && id < d.E ? (id + r) % d.E : id;
+            }
+        if (e == hipSuccess) e = hipMalloc(&rot_dev, sizeof(int32_t) * rot_host.size());
+        if (e == hipSuccess)
+            e = hipMemcpy(rot_dev, rot_host.data(), sizeof(int32_t) * rot_host.size(), hipMemcpyHostToDevice);
+        if (e != hipSuccess) {
+            if (rot_dev) (void)hipFree(rot_dev);
+            return moe::fail_hip(e, "kernel_time: rotated expert sets");
+        }
+    }
     hipStream_t cs = nullptr;
     hipGraph_t graph = nullptr;
     hipGraphExec_t exec = nullptr;
     hipEvent_t a = nullptr, b = nullptr;
-    hipError_t e = hipMemcpyAsync(s->scratch_x, s->h, sizeof(float) * T * d.H, hipMemcpyDeviceToDevice, strm);
+    e = hipMemcpyAsync(s->scratch_x, s->h, sizeof(float) * T * d.H, hipMemcpyDeviceToDevice, strm);
     if (e == hipSuccess) e = hipEventCreate(&a);
     if (e == hipSuccess) e = hipEventCreate(&b);
     if (e == hipSuccess) e = hipStreamCreateWithFlags(&cs, hipStreamNonBlocking);
     if (e == hipSuccess) e = hipEventRecord(a, strm);
     if (e == hipSuccess) e = hipStreamWaitEvent(cs, a, 0);
-    auto enqueue = [&](const LastLayer &ll) -> hipError_t {
+    auto enqueue = [&](const LastLayer &ll, int r) -> hipError_t {
         const int l = ll.layer;
         if (which == 4)
             return moe::launch_attention_decode(s->scratch_x, d.H, s->ad.n_heads, s->ad.n_kv, s->ad.head_dim,
@@ -676,19 +714,17 @@ int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *
             return r == hipSuccess ? moe::launch_topk_softmax(s->logits, T, d.E, d.k, s->ids, s->weights, eflags, cs)
                                    : r;
         }
-        return moe::launch_expert_ffn(s->scratch_x, T, d.H, d.I, d.E, d.k, ll.ids, ll.weights, ll.slot_of, ll.pool,
+        const int32_t *ids = rotate ? rot_dev + (size_t(r) * (L - l0) + size_t(l - l0)) * T * d.k : ll.ids;
+        return moe::launch_expert_ffn(s->scratch_x, T, d.H, d.I, d.E, d.k, ids, ll.weights, ll.slot_of, ll.pool,
                                       s->expert_bytes, d.w_dtype, s->shared_w.empty() ? nullptr : s->shared_w[l],
                                       s->scratch_y, false, ws, eflags, cs,
                                       plans[size_t(l)].n ? &plans[size_t(l)] : nullptr,
                                       which == 1 ? moe::kFfnGateUp : which == 2 ? moe::kFfnDown : moe::kFfnBoth);
     };
-    // Multi-token steps under a budget read the device slot table, where an
-    // earlier layer's experts may have been evicted since: replay only the
-    // last layer then (T == 1 steps carry their slots with them).
-    const int l0 = (s->budgeted && T > 1) ? L - 1 : 0;
     if (e == hipSuccess) e = hipStreamBeginCapture(cs, hipStreamCaptureModeThreadLocal);
     if (e == hipSuccess) {
-        for (int l = l0; l < L && e == hipSuccess; ++l) e = enqueue(s->last[l]);
+        for (int r = 0; r < reps && e == hipSuccess; ++r)
+            for (int l = l0; l < L && e == hipSuccess; ++l) e = enqueue(s->last[l], r);
         hipError_t e2 = hipStreamEndCapture(cs, &graph);
         if (e == hipSuccess) e = e2;
     }
@@ -706,8 +742,9 @@ int moe_stack_kernel_time(moe_stack *s, int which, int n, void *stream, double *
     if (cs) (void)hipStreamDestroy(cs);
     if (a) (void)hipEventDestroy(a);
     if (b) (void)hipEventDestroy(b);
+    if (rot_dev) (void)hipFree(rot_dev);
     if (e != hipSuccess) return moe::fail_hip(e, "kernel_time");
-    *mean_ms = double(ms) / (double(n) * (L - l0));
+    *mean_ms = double(ms) / (double(n) * reps * (L - l0));
     moe::clear_error();
     return MOE_OK;
 }

@@ -552,6 +552,44 @@ def test_host_tier_stack_rejects_what_it_cannot_run():
     buf.close()
 
 
+def test_preloaded_stack_kernel_time_repeats():
+    """Timing re-launches on a preloaded stack (every expert resident): a two-layer graph repeats its launches,
+    the repeats read rotated expert sets (or, with the flag, the step's own), and the stack's state is left alone,
+    so the next step equals a twin stack's bit for bit.  Timing a route launch with the flag is rejected."""
+    wl = synth.Workload("preloaded timing", H=512, E=16, k=2, I=128, L=2, dtype=synth.BF16, shared=True,
+                        routing="zipf_overlap", cfg_id=171)
+    eb = wl.expert_bytes
+    buf = _pinned_store(wl)
+    routers = [dev(synth.router_weights(wl, l)) for l in range(wl.L)]
+    shared = [dev(synth.expert_blob(wl, l, None)) for l in range(wl.L)]
+    caches = [moe.ExpertCache(wl.L, wl.E, eb, (wl.L * wl.E + wl.L) * eb, buf.ptr, wl.E * eb, eb,
+                              reserved_bytes=wl.L * eb, preload=True) for _ in range(2)]
+    stacks = [moe.MoeStack(c, wl.H, wl.I, wl.E, wl.k, wl.dtype, wl.router_dtype, routers, shared) for c in caches]
+    sets = synth.routing_sets(wl, steps=2)
+    for t in range(2):
+        x0 = dev(synth.hidden_states(wl, t))
+        bias = dev(np.stack([synth.mask_logits(wl, sets[t, l]) for l in range(wl.L)]))
+        outs = []
+        for st in stacks:
+            x = x0.clone()
+            ids = torch.empty((wl.L, 1, wl.k), dtype=torch.int32, device=DEV)
+            st.decode_step(t, x, bias, ids)
+            outs.append((x, ids))
+        moe.moe_sync_check()
+        assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1]), t
+        if t == 0:
+            for which in (0, 1, 2, 3, 9, 10, 11):
+                assert stacks[1].kernel_time(which, 2) > 0, which
+            with pytest.raises(moe.MoeError):
+                stacks[1].kernel_time(8, 1)
+            moe.moe_sync_check()
+    assert caches[1].stats()["misses"] == caches[0].stats()["misses"] == 0
+    for s_, c in zip(stacks, caches):
+        s_.close()
+        c.close()
+    buf.close()
+
+
 @pytest.mark.parametrize("device", [False, True])
 def test_budgeted_stack_full_size_config4_sampled(device):
     """The benchmark's configuration (40 layers, 6 GiB budget -> 682 slots), layers aliasing one host copy."""
