@@ -324,8 +324,10 @@ __device__ __forceinline__ void split3(const float *v, rbf16x8 &t1, rbf16x8 &t2,
     t3 = __builtin_bit_cast(rbf16x8, make_uint4(c[0], c[1], c[2], c[3]));
 }
 
-constexpr int kRouterTileT = 64;  // tokens per block (16 per wave)
-constexpr int kRouterTileE = 32;  // experts per block (two 16-column MFMA blocks)
+constexpr int kRouterTileT = 16;   // tokens per block (one MFMA row block)
+constexpr int kRouterTileE = 32;   // experts per block (two 16-column MFMA blocks)
+constexpr int kRouterKWaves = 8;   // waves per block, each over its own slice of the H range
+constexpr int kRouterRound = 8;    // 32-wide k steps whose loads a wave issues together
 
 // h = x / sqrt(mean(x^2) + eps), one wave per token.
 __global__ __launch_bounds__(kBlock) void rmsnorm_rows_kernel(const float *__restrict__ x, int T, int H,
@@ -348,44 +350,80 @@ __global__ __launch_bounds__(kBlock) void rmsnorm_rows_kernel(const float *__res
 }
 
 // logits[t, e] = sum_i W[e, i] x[t, i] (+ bias[t, e]); W bf16 [E x H], H % 32 == 0.
-// Wave w of a block takes tokens t0 + 16w .. +15; lane (lr = l % 16, lg = l / 16)
-// supplies x[t0 + 16w + lr][k + 8lg .. +7] and W[e0 + 16j + lr][k + 8lg .. +7].
-__global__ __launch_bounds__(kBlock) void router_mfma_kernel(const float *__restrict__ x,
-                                                             const uint16_t *__restrict__ w, int T, int H,
-                                                             int E, const float *__restrict__ bias,
-                                                             float *__restrict__ logits) {
+// A block takes 16 tokens x 32 experts; its 8 waves split the H range into
+// contiguous slices of 32-wide k steps, each wave issuing the loads of up to 8
+// steps before its first product (lane (lr = l % 16, lg = l / 16) supplies
+// x[t0 + lr][k + 8lg .. +7] and W[e0 + 16j + lr][k + 8lg .. +7]), and the
+// waves' partial tiles are summed through LDS in wave order.
+__global__ __launch_bounds__(kRouterKWaves * kWave) void router_mfma_kernel(const float *__restrict__ x,
+                                                                           const uint16_t *__restrict__ w, int T,
+                                                                           int H, int E,
+                                                                           const float *__restrict__ bias,
+                                                                           float *__restrict__ logits) {
+    __shared__ float red[kRouterKWaves][2 * 4 * kWave];
     const int lane = threadIdx.x & (kWave - 1), wave = threadIdx.x / kWave;
     const int lr = lane % 16, lg = lane / 16;
-    const int t0 = blockIdx.y * kRouterTileT + wave * 16, e0 = blockIdx.x * kRouterTileE;
+    const int t0 = blockIdx.y * kRouterTileT, e0 = blockIdx.x * kRouterTileE;
     const float *xr = x + size_t(min(t0 + lr, T - 1)) * H + 8 * lg;
     const uint16_t *wr0 = w + size_t(min(e0 + lr, E - 1)) * H + 8 * lg;
     const uint16_t *wr1 = w + size_t(min(e0 + 16 + lr, E - 1)) * H + 8 * lg;
+    const int nk = H / 32;                                     // k steps in all
+    const int ns = (nk + kRouterKWaves - 1) / kRouterKWaves;   // steps per wave
+    const int s_lo = wave * ns, s_hi = min(nk, s_lo + ns);     // this wave's steps (wave-uniform)
     rfloatx4 acc0 = {0.f, 0.f, 0.f, 0.f}, acc1 = {0.f, 0.f, 0.f, 0.f};
-    for (int k = 0; k < H; k += 32) {
-        const float4 xa = *reinterpret_cast<const float4 *>(xr + k);
-        const float4 xb = *reinterpret_cast<const float4 *>(xr + k + 4);
-        const rbf16x8 b0 = __builtin_bit_cast(rbf16x8, *reinterpret_cast<const uint4 *>(wr0 + k));
-        const rbf16x8 b1 = __builtin_bit_cast(rbf16x8, *reinterpret_cast<const uint4 *>(wr1 + k));
-        const float v[8] = {xa.x, xa.y, xa.z, xa.w, xb.x, xb.y, xb.z, xb.w};
-        rbf16x8 a1, a2, a3;
-        split3(v, a1, a2, a3);
-        // smallest terms first
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, b0, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, b1, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b0, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b1, acc1, 0, 0, 0);
-        acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b0, acc0, 0, 0, 0);
-        acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc1, 0, 0, 0);
+    static_assert(kRouterRound == 8, "the load fence below names eight steps");
+    for (int r0 = s_lo; r0 < s_hi; r0 += kRouterRound) {
+        u32x4 xa[kRouterRound], xb[kRouterRound], wa[kRouterRound], wb[kRouterRound];
+#pragma unroll
+        for (int r = 0; r < kRouterRound; ++r) {  // every load issued (step clamped), products only for live steps
+            const int k = 32 * min(r0 + r, nk - 1);
+            xa[r] = *reinterpret_cast<const u32x4 *>(xr + k);
+            xb[r] = *reinterpret_cast<const u32x4 *>(xr + k + 4);
+            wa[r] = *reinterpret_cast<const u32x4 *>(wr0 + k);
+            wb[r] = *reinterpret_cast<const u32x4 *>(wr1 + k);
+        }
+        // One fence over every loaded register: the compiler cannot move a load past it, so the round's loads
+        // are in flight together and the wave waits once (left to itself it interleaves each step's loads with
+        // the previous step's products, one load latency per step).
+#define RFENCE(r) "+v"(xa[r]), "+v"(xb[r]), "+v"(wa[r]), "+v"(wb[r])
+        asm volatile("" : RFENCE(0), RFENCE(1), RFENCE(2), RFENCE(3), RFENCE(4), RFENCE(5), RFENCE(6), RFENCE(7));
+#undef RFENCE
+#pragma unroll
+        for (int r = 0; r < kRouterRound; ++r) {
+            // a step past the wave's slice multiplies zero weights (no branch around the products)
+            const bool live = r0 + r < s_hi;
+            const float v[8] = {__uint_as_float(xa[r].x), __uint_as_float(xa[r].y), __uint_as_float(xa[r].z),
+                                __uint_as_float(xa[r].w), __uint_as_float(xb[r].x), __uint_as_float(xb[r].y),
+                                __uint_as_float(xb[r].z), __uint_as_float(xb[r].w)};
+            const u32x4 z4 = {0u, 0u, 0u, 0u};
+            const rbf16x8 b0 = __builtin_bit_cast(rbf16x8, live ? wa[r] : z4);
+            const rbf16x8 b1 = __builtin_bit_cast(rbf16x8, live ? wb[r] : z4);
+            rbf16x8 a1, a2, a3;
+            split3(v, a1, a2, a3);
+            // smallest terms first
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, b0, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a3, b1, acc1, 0, 0, 0);
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b0, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a2, b1, acc1, 0, 0, 0);
+            acc0 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b0, acc0, 0, 0, 0);
+            acc1 = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, b1, acc1, 0, 0, 0);
+        }
     }
-    // lane holds C[t = t0 + 4lg + q][e = e0 + 16j + lr]
+    // lane holds C[t = t0 + 4lg + q][e = e0 + 16j + lr] in acc_j[q]; entry (j, q, lane) of the tile is
+    // red[.][(j * 4 + q) * 64 + lane]
 #pragma unroll
     for (int q = 0; q < 4; ++q) {
-        const int t = t0 + 4 * lg + q;
-        if (t >= T) continue;
-        const int ea = e0 + lr, eb = e0 + 16 + lr;
-        if (ea < E) logits[size_t(t) * E + ea] = acc0[q] + (bias ? bias[size_t(t) * E + ea] : 0.f);
-        if (eb < E) logits[size_t(t) * E + eb] = acc1[q] + (bias ? bias[size_t(t) * E + eb] : 0.f);
+        red[wave][q * kWave + lane] = acc0[q];
+        red[wave][(4 + q) * kWave + lane] = acc1[q];
     }
+    __syncthreads();
+    const int i = threadIdx.x;  // one tile entry per thread: 8 x 64 entries, 512 threads
+    float v = 0.f;
+#pragma unroll
+    for (int wv = 0; wv < kRouterKWaves; ++wv) v += red[wv][i];
+    const int j = i / (4 * kWave), q = (i / kWave) % 4, l = i % kWave;
+    const int t = t0 + 4 * (l / 16) + q, e = e0 + 16 * j + l % 16;
+    if (t < T && e < E) logits[size_t(t) * E + e] = v + (bias ? bias[size_t(t) * E + e] : 0.f);
 }
 
 // ------------------------------------------------------------- grouping ---
@@ -1288,7 +1326,8 @@ hipError_t launch_router_logits(const float *x, const void *w, int w_dtype, int 
             src = h_out;
         }
         const dim3 g((E + kRouterTileE - 1) / kRouterTileE, (T + kRouterTileT - 1) / kRouterTileT);
-        router_mfma_kernel<<<g, kBlock, 0, s>>>(src, static_cast<const uint16_t *>(w), T, H, E, bias, logits);
+        router_mfma_kernel<<<g, kRouterKWaves * kWave, 0, s>>>(src, static_cast<const uint16_t *>(w), T, H, E, bias,
+                                                               logits);
         return hipGetLastError();
     }
     const dim3 grid((E + 3) / 4, T);

@@ -74,8 +74,9 @@ def test_route_parity_configs(cfg, T, norm):
 
 @pytest.mark.parametrize("norm", [False, True])
 def test_route_prefill_chunk_and_ragged_tiles(norm):
-    """Many-token routing (the matrix-core router): config 5's 2048-token chunk over 256 experts, and a
-    ragged 70 x 130 case whose last token and expert tiles are partial."""
+    """Many-token routing (the matrix-core router): config 5's 2048-token chunk over 256 experts, a ragged
+    70 x 130 case whose last token and expert tiles are partial, and hidden sizes that give a block's waves
+    several rounds of loads or nothing to do."""
     wl = synth.workload(5, L=1)
     check_route(synth.prefill_states(wl), synth.router_weights(wl, 0), wl.router_dtype, wl.k, norm=norm)
     rng = np.random.default_rng(130)
@@ -83,6 +84,12 @@ def test_route_prefill_chunk_and_ragged_tiles(norm):
     wr = synth.bf16_bits(rng.standard_normal((130, 384)).astype(np.float32) * 0.05)
     bias = rng.standard_normal((70, 130)).astype(np.float32)
     check_route(x, wr, synth.BF16, 5, bias, norm=norm)
+    # the H range split over a block's waves: two rounds of loads per wave (H 4096), and fewer k steps than
+    # waves (H 128: half the waves add nothing)
+    for T_, H_, E_ in ((20, 4096, 48), (17, 128, 40)):
+        x = (rng.standard_normal((T_, H_)) * 2.0).astype(np.float32)
+        wr = synth.bf16_bits(rng.standard_normal((E_, H_)).astype(np.float32) * 0.05)
+        check_route(x, wr, synth.BF16, 4, norm=norm)
 
 
 def test_route_with_mask_bias_selects_the_drawn_sets():
