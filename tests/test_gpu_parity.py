@@ -200,6 +200,21 @@ def test_ffn_grouping_duplicates_slots_and_accumulate(dtype):
         check_ffn(wl, x, ids, w, ex, None, accumulate=True)
 
 
+@pytest.mark.parametrize("dtype", [synth.F32, synth.BF16, synth.INT4G128])
+def test_ffn_groups_of_many_tokens(dtype):
+    """Groups holding more tokens than one LDS chunk of token rows (8 rows at H 2048): full and ragged last
+    chunks, and a shared expert that every token uses."""
+    wl = synth.Workload("many tokens", H=2048, E=12, k=4, I=256, dtype=dtype, router_dtype=synth.F32, shared=True,
+                        cfg_id=120 + dtype)
+    ex, sh = _experts(wl)
+    rng = np.random.default_rng(120 + dtype)
+    for T in (9, 13, 16):  # (at most 16 tokens per call)
+        x = rng.standard_normal((T, wl.H)).astype(np.float32)
+        ids = np.stack([rng.choice(5, size=4, replace=False) for _ in range(T)]).astype(np.int32)
+        w = rng.random((T, 4)).astype(np.float32)
+        check_ffn(wl, x, ids, w, ex, sh, slot_perm=rng.permutation(wl.E))
+
+
 @pytest.mark.parametrize("dtype,H", [(synth.F32, 384), (synth.BF16, 256), (synth.BF16, 640), (synth.BF16, 3968),
                                      (synth.BF16, 4096), (synth.INT4G128, 256), (synth.INT4G128, 2176),
                                      (synth.INT4G128, 4224)])
