@@ -428,6 +428,7 @@ def run_stack_and_check(wl, steps, capacity, layers_alias=False, check_steps=Non
     s = cache.stats()
     assert s["occupancy"] <= capacity and s["misses"] == o.stats()["misses"]
     if capacity * eb <= 64 << 20:  # every resident expert's slot holds its whole blob, byte for byte
+        torch.cuda.synchronize()  # (the cache's copy stream too: prefetches fill there)
         table_p, pool_p = cache.slot_table()
         table = _d2h(table_p, 4 * wl.L * wl.E).view(np.int32)
         pool = _d2h(pool_p, capacity * eb).reshape(capacity, eb)
